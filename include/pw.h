@@ -1,0 +1,201 @@
+/*
+ * pw.h -- C ABI of libpagedweight.so: the paged mixed-bitwidth MoE expert
+ * forward and runtime requantization of PagedWeight (arXiv 2607.16184),
+ * written for AMD Instinct MI355X (gfx950).
+ *
+ * Model (Sec. 3.1): the routed experts' weights live as pages in one device
+ * pool. A page is one row-block of one projection of one expert: R rows of
+ * gate [F,H], up [F,H] or down [H,F] (row-major, a row is an output feature,
+ * the reduction dimension K is contiguous). A page table holds one entry per
+ * (expert, projection, row-block) with the page's committed bitwidth (16, 8
+ * or 4; the paper's q_i) and its byte offsets in the pool. The kernels read
+ * every block at its committed bitwidth (Sec. 3.3). Lowering a block's
+ * bitwidth frees pool bytes Delta = M^b - M^b' (Eq. 3) that the caller can
+ * hand to its KV cache; the lower bitwidth is committed before the old pages
+ * are retired (Sec. 3.1 offload order; Sec. 3.3 safe boundaries).
+ *
+ * Page formats (the build's reading; the paper's own format is Any-Precision
+ * bit-planes, which it pairs with per-bitwidth LUTs):
+ *   16-bit: R*K values of the activation dtype, row-major.
+ *   8/4-bit: asymmetric group-wise round-to-nearest along K, group size G,
+ *     one (scale, zero) pair of dtype sdt per (row, group); weight = z + c*s.
+ *     Code block: each row's K codes in blocks of 128; a block holds 16 runs
+ *     of 8 codes; run rho (codes [8 rho, 8 rho + 8) of the block) is stored at
+ *     run position p with rho = 4*(p mod 4) + p div 4. An 8-bit run is 8 bytes;
+ *     a 4-bit run is one little-endian 32-bit word with code 2t at bits
+ *     [4t, 4t+4) and code 2t+1 at bits [16+4t, 20+4t).
+ *     Scale/zero block (right after the codes): pair index g*R + r holds
+ *     (scale, zero) of row r, group g, as two 16-bit values.
+ *   Bytes: M16 = 2RK, M8 = RK + 4R(K/G), M4 = RK/2 + 4R(K/G).
+ *   Quantizer: z = largest sdt value <= min(v); r = fl32(max(v) - z);
+ *   r == 0 -> s = +0 and all codes 0; else s = smallest sdt value >= fl32(r/Q),
+ *   one sdt step higher if fl32(s*Q) < r; c = clamp(rint(fl32(fl32(v-z)/s)),0,Q)
+ *   with Q = 2^bits - 1; a zero result of a directed rounding is +0.
+ *   A requantization 8 -> 4 starts from fl32(z + c*s).
+ *
+ * Memory ownership: the caller allocates every device buffer (pool, device
+ * page table, workspaces, activations, outputs, routing arrays) and owns the
+ * HIP streams. The library never allocates or frees device memory. It owns the
+ * host mirror of the page table, the slot allocator inside the caller's pool
+ * and the HIP events it creates.
+ *
+ * Errors: every call returns pw_status and never throws across the ABI. A
+ * failing call leaves the table, pool and free lists unchanged; pw_last_error()
+ * returns a message for the calling thread. Asynchronous HIP errors surface as
+ * PW_EHIP on a later call. A layer handle is not thread-safe.
+ *
+ * Streams: `stream` arguments are hipStream_t handles passed as void*; NULL
+ * is the null stream. Outputs are valid once the stream reaches the work.
+ */
+#ifndef PAGEDWEIGHT_PW_H
+#define PAGEDWEIGHT_PW_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    PW_OK = 0,
+    PW_EINVAL = 1,        /* bad argument, shape or size                      */
+    PW_ENOMEM = 2,        /* pool or workspace too small                      */
+    PW_EBUSY = 3,         /* the block already has a requantization pending   */
+    PW_EUNSUPPORTED = 4,  /* e.g. raising a bitwidth (needs a reload)         */
+    PW_EHIP = 5,          /* a HIP runtime call failed                        */
+    PW_ESTATE = 6         /* layer not ready (a page is missing)              */
+} pw_status;
+
+typedef enum { PW_F16 = 0, PW_BF16 = 1 } pw_dtype;
+typedef enum { PW_GATE = 0, PW_UP = 1, PW_DOWN = 2 } pw_proj;
+
+/* Page states (Sec. 3.1 page state; only GPU-resident states exist here). */
+enum { PW_PAGE_ABSENT = 0, PW_PAGE_RESIDENT = 1, PW_PAGE_REQUANT_PENDING = 2 };
+
+/* One page-table entry (device array and host mirror). 24 bytes. */
+typedef struct {
+    uint64_t data_off;  /* byte offset of the page (values or code block) in the pool */
+    uint64_t sz_off;    /* byte offset of the scale/zero block; 0 for 16-bit pages    */
+    uint8_t bits;       /* committed bitwidth q_i: 16, 8, 4; 0 = absent               */
+    uint8_t state;      /* PW_PAGE_*                                                  */
+    uint16_t rsv;
+    uint32_t gen;       /* bumped at every commit                                     */
+} pw_page_entry;
+
+/* Layer shape. act is the activation dtype (and the dtype of 16-bit pages);
+ * sdt the dtype of scales and zeros. Constraints: R a multiple of 64;
+ * F and H multiples of R and of 128; G a multiple of 32 dividing 128 or a
+ * multiple of 128, and dividing F and H.                                   */
+typedef struct {
+    int E, H, F, R, G;
+    int act;
+    int sdt;
+} pw_layer_desc;
+
+typedef struct pw_layer pw_layer;
+
+/* Number of entries of the device page table: E * 3 * max(F, H) / R.
+ * Entry (e, proj, rb) is at index (e*3 + proj) * (max(F,H)/R) + rb.        */
+size_t pw_table_entries(const pw_layer_desc* desc);
+
+/* Bytes of one page of projection `proj` at `bits` (Eq. 3's M_i^b). */
+pw_status pw_page_bytes(const pw_layer_desc* desc, int proj, int bits, size_t* bytes);
+
+/* Create a layer over a caller-owned pool [pool_dev, pool_dev + pool_bytes)
+ * (256-byte aligned) and device table table_dev (pw_table_entries entries).
+ * The table is cleared to absent entries on the null stream.              */
+pw_status pw_layer_create(const pw_layer_desc* desc, void* pool_dev, size_t pool_bytes,
+                          pw_page_entry* table_dev, pw_layer** out);
+
+/* Destroy the handle (waits for the library's events). */
+pw_status pw_layer_destroy(pw_layer* layer);
+
+/* Place page (e, proj, rb) into a fresh pool slot at `bits`: rows16_dev holds
+ * the page's R x K 16-bit values (act dtype, row-major, device memory, read
+ * on `stream`). 16 -> copied; 8/4 -> quantized on the GPU. The table entry is
+ * written on `stream` after the data. The page must be absent.             */
+pw_status pw_layer_load_page(pw_layer* layer, int e, int proj, int rb, int bits,
+                             const void* rows16_dev, void* stream);
+
+/* Router (Sec. 2.1 top-K routing) and token permutation (Sec. 3.3 dispatch).
+ *   logits   [T,E] fp32 device, row-major
+ *   topk_ids [T,K] int32 out: per token the K largest logits, ties to the
+ *            lower expert index, in decreasing order
+ *   topk_w   [T,K] fp32 out: renorm=1 softmax over the selected K logits;
+ *            renorm=0 the full softmax probability of each selected expert
+ *   offsets  [E+1] int32 out: exclusive scan of per-expert slot counts
+ *   sorted_slot [T*K] int32 out: slots s = t*K + k grouped by expert, in
+ *            increasing s within an expert
+ *   slot_pos [T*K] int32 out: inverse permutation of sorted_slot
+ * Constraints: 1 <= K <= E <= 1024, K <= 16, T*K < 2^31.                   */
+pw_status pw_route_topk(const float* logits, int T, int E, int K, int renorm,
+                        int32_t* topk_ids, float* topk_w, int32_t* offsets,
+                        int32_t* sorted_slot, int32_t* slot_pos, void* stream);
+
+/* Workspace bytes pw_moe_paged_gemm needs for T tokens with top-K. */
+pw_status pw_workspace_bytes(const pw_layer* layer, int T, int K, size_t* gemm_ws);
+
+/* Paged expert forward and combine (Sec. 3.3): for each routed slot (t,k)
+ * with expert e, o = W_down[e] (silu(W_gate[e] x_t) * W_up[e] x_t), each
+ * block read at its committed bitwidth; y[t] = sum_k topk_w[t,k] * o, k
+ * ascending, fp32 accumulation. The SwiGLU output is rounded to `act`
+ * before the down projection.
+ *   x [T,H] act device; y [T,H] act, or fp32 if out_fp32 != 0.
+ *   topk_w, offsets, sorted_slot, slot_pos: as produced by pw_route_topk.
+ *   ws: device workspace of at least pw_workspace_bytes bytes.
+ * Requires every page of the layer to be present (PW_ESTATE otherwise).
+ * Deterministic: no floating-point atomics; a fixed summation order.      */
+pw_status pw_moe_paged_gemm(const pw_layer* layer, const void* x, int T, int K,
+                            const float* topk_w, const int32_t* offsets,
+                            const int32_t* sorted_slot, const int32_t* slot_pos,
+                            void* y, int out_fp32, void* ws, size_t ws_bytes, void* stream);
+
+/* Runtime downshift of one block (Sec. 3.1 offload; Sec. 3.3 asynchronous
+ * page movement): requantize page (e, proj, rb) from its committed bitwidth
+ * b to new_bits < b into a fresh slot on `side_stream`. The committed entry
+ * is unchanged until pw_commit. *delta_bytes receives Eq. 3's M^b - M^b'.
+ *   new_bits == b: PW_OK, delta 0, no work.
+ *   new_bits > b: PW_EUNSUPPORTED.  pending already: PW_EBUSY.
+ *   no free slot: PW_ENOMEM.                                              */
+pw_status pw_requant_block(pw_layer* layer, int e, int proj, int rb, int new_bits,
+                           void* side_stream, size_t* delta_bytes);
+
+/* Batched form of pw_requant_block over n blocks (one kernel launch per 64
+ * blocks). On error no block of the batch is left pending.               */
+pw_status pw_requant_blocks(pw_layer* layer, int n, const int* e, const int* proj,
+                            const int* rb, const int* new_bits, void* side_stream,
+                            size_t* delta_bytes_total);
+
+/* Publish every pending requantization, ordered on main_stream after its
+ * requant finished: the device entries are rewritten by a kernel on
+ * main_stream, the host mirror updated, and the old slots retired until
+ * main_stream passes the commit. *n_committed may be NULL.               */
+pw_status pw_commit(pw_layer* layer, void* main_stream, int* n_committed);
+
+/* Return retired slots whose commit has completed to the pool's free list.
+ * *bytes_freed (may be NULL) receives the bytes returned by this call.    */
+pw_status pw_reclaim(pw_layer* layer, size_t* bytes_freed);
+
+/* Host-mirror view of one entry. */
+pw_status pw_page_info(const pw_layer* layer, int e, int proj, int rb, pw_page_entry* out);
+
+/* Pool occupancy: bytes in slots, free bytes, largest free range. */
+pw_status pw_pool_stats(const pw_layer* layer, size_t* used, size_t* free_bytes,
+                        size_t* largest_free);
+
+/* Per-kernel timing with HIP events recorded on the kernels' own streams.
+ * Phases: 0 gate/up GEMM, 1 down GEMM, 2 combine, 3 requant.
+ * pw_profile_read waits for the recorded events and returns the summed
+ * milliseconds and launch counts per phase; reset != 0 clears them.        */
+enum { PW_PH_GATEUP = 0, PW_PH_DOWN = 1, PW_PH_COMBINE = 2, PW_PH_REQUANT = 3, PW_NPHASE = 4 };
+pw_status pw_profile_enable(pw_layer* layer, int on);
+pw_status pw_profile_read(pw_layer* layer, double* total_ms, int64_t* count, int reset);
+
+const char* pw_last_error(void);
+const char* pw_status_str(pw_status s);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* PAGEDWEIGHT_PW_H */

@@ -1,0 +1,514 @@
+// C ABI of libpagedweight.so (declared in include/pw.h).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstring>
+#include <set>
+#include <string>
+#include <vector>
+
+#include "pw.h"
+#include "pw_internal.hpp"
+#include "pw_state.hpp"
+
+namespace {
+
+thread_local std::string g_err;
+
+pw_status fail(pw_status s, const std::string& msg) {
+  g_err = msg;
+  return s;
+}
+
+pw_status hip_fail(hipError_t e, const char* what) {
+  return fail(PW_EHIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+struct HipEvents : pw::EventOps {
+  void* create() override {
+    hipEvent_t ev = nullptr;
+    if (hipEventCreateWithFlags(&ev, hipEventDisableTiming) != hipSuccess) return nullptr;
+    return ev;
+  }
+  void destroy(void* ev) override { (void)hipEventDestroy(static_cast<hipEvent_t>(ev)); }
+  bool done(void* ev) override { return hipEventQuery(static_cast<hipEvent_t>(ev)) == hipSuccess; }
+};
+
+struct ProfRec {
+  int phase;
+  hipEvent_t a, b;
+};
+
+}  // namespace
+
+struct pw_layer {
+  HipEvents evops;
+  pw::LayerState st;
+  uint8_t* pool;
+  pw_page_entry* table;
+  bool prof = false;
+  std::vector<ProfRec> recs;
+  double tot_ms[PW_NPHASE] = {0, 0, 0, 0};
+  int64_t cnt[PW_NPHASE] = {0, 0, 0, 0};
+
+  pw_layer(const pw_layer_desc& d, void* p, size_t bytes, pw_page_entry* t)
+      : st(d, bytes, &evops), pool(static_cast<uint8_t*>(p)), table(t) {}
+};
+
+namespace {
+
+// Records a timing event pair around one launch when profiling is enabled.
+struct ProfScope {
+  pw_layer* L;
+  int phase;
+  hipStream_t st;
+  hipEvent_t a = nullptr, b = nullptr;
+  ProfScope(pw_layer* l, int ph, hipStream_t s) : L(l), phase(ph), st(s) {
+    if (L && L->prof && hipEventCreate(&a) == hipSuccess && hipEventCreate(&b) == hipSuccess)
+      (void)hipEventRecord(a, st);
+  }
+  ~ProfScope() {
+    if (a && b) {
+      (void)hipEventRecord(b, st);
+      L->recs.push_back(ProfRec{phase, a, b});
+    }
+  }
+};
+
+bool mult_of_256(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 255u) == 0; }
+
+// Device workspace layout of pw_moe_paged_gemm.
+struct WsLayout {
+  size_t h_off, h_bytes, op_off, op_bytes, total;
+  int nsplit, kb_per_split, mtb;
+};
+
+WsLayout ws_layout(const pw_layer_desc& d, int T, int K) {
+  WsLayout w{};
+  const size_t S = static_cast<size_t>(T) * K;
+  const int nkbF = d.F / 128;
+  const int expect = static_cast<int>((S + d.E - 1) / d.E);
+  // Split the down projection's K = F when too few (expert, row-block) units
+  // exist to fill the chip; deterministic in (desc, T, K).
+  int nsplit = 1;
+  if (S <= 4096) {
+    const size_t active = std::min<size_t>(d.E, S);
+    const size_t units = active * (d.H / 64);
+    nsplit = static_cast<int>(std::max<size_t>(1, std::min<size_t>(8, 2048 / std::max<size_t>(units, 1))));
+  }
+  nsplit = std::min(nsplit, nkbF);
+  w.kb_per_split = (nkbF + nsplit - 1) / nsplit;
+  w.nsplit = (nkbF + w.kb_per_split - 1) / w.kb_per_split;
+  w.mtb = expect <= 12 ? 1 : expect <= 24 ? 2 : 4;
+  auto al = [](size_t b) { return (b + 255) / 256 * 256; };
+  w.h_off = 0;
+  w.h_bytes = al(S * d.F * 2);
+  w.op_off = w.h_bytes;
+  w.op_bytes = al(static_cast<size_t>(w.nsplit) * S * d.H * 4);
+  w.total = w.h_bytes + w.op_bytes;
+  return w;
+}
+
+pw_status check_hip_last(const char* what) {
+  hipError_t e = hipGetLastError();
+  return e == hipSuccess ? PW_OK : hip_fail(e, what);
+}
+
+// Launch quantize / requant jobs that all share one projection kind.
+pw_status run_qjobs(pw_layer* L, const std::vector<pw::QJob>& jobs, int proj, hipStream_t st) {
+  const pw_layer_desc& d = L->st.desc;
+  const int K = L->st.kdim(proj);
+  for (size_t base = 0; base < jobs.size(); base += pw::kMaxQJobs) {
+    pw::QJobBatch b{};
+    b.n_jobs = static_cast<int>(std::min<size_t>(pw::kMaxQJobs, jobs.size() - base));
+    b.R = d.R;
+    b.K = K;
+    b.G = d.G;
+    b.act = d.act;
+    b.sdt = d.sdt;
+    b.items_per_job = static_cast<uint32_t>(d.R) * ((K + 511) / 512);
+    b.total_items = b.items_per_job * b.n_jobs;
+    for (int j = 0; j < b.n_jobs; ++j) {
+      b.job[j] = jobs[base + j];
+      b.job[j].item_base = b.items_per_job * j;
+    }
+    ProfScope ps(L, PW_PH_REQUANT, st);
+    hipError_t e = pw::launch_qjobs(b, st);
+    if (e != hipSuccess) return hip_fail(e, "requant launch");
+  }
+  return PW_OK;
+}
+
+pw_status write_entries(pw_layer* L, const std::vector<std::pair<size_t, pw_page_entry>>& w,
+                        hipStream_t st) {
+  for (size_t base = 0; base < w.size(); base += pw::kMaxEntryWrites) {
+    pw::EntryWrites ew{};
+    ew.n = static_cast<int>(std::min<size_t>(pw::kMaxEntryWrites, w.size() - base));
+    for (int i = 0; i < ew.n; ++i) {
+      ew.idx[i] = static_cast<uint32_t>(w[base + i].first);
+      ew.ent[i] = w[base + i].second;
+    }
+    hipError_t e = pw::launch_entry_writes(L->table, ew, st);
+    if (e != hipSuccess) return hip_fail(e, "page-table write");
+  }
+  return PW_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* pw_last_error(void) { return g_err.c_str(); }
+
+const char* pw_status_str(pw_status s) {
+  switch (s) {
+    case PW_OK: return "PW_OK";
+    case PW_EINVAL: return "PW_EINVAL";
+    case PW_ENOMEM: return "PW_ENOMEM";
+    case PW_EBUSY: return "PW_EBUSY";
+    case PW_EUNSUPPORTED: return "PW_EUNSUPPORTED";
+    case PW_EHIP: return "PW_EHIP";
+    case PW_ESTATE: return "PW_ESTATE";
+  }
+  return "unknown";
+}
+
+size_t pw_table_entries(const pw_layer_desc* d) {
+  if (!d || d->R <= 0) return 0;
+  return static_cast<size_t>(d->E) * 3 * (std::max(d->F, d->H) / d->R);
+}
+
+pw_status pw_page_bytes(const pw_layer_desc* d, int proj, int bits, size_t* bytes) {
+  std::string err;
+  if (!d || !bytes) return fail(PW_EINVAL, "null argument");
+  if (!pw::LayerState::valid_desc(*d, &err)) return fail(PW_EINVAL, err);
+  if (proj < 0 || proj > 2) return fail(PW_EINVAL, "bad projection");
+  if (bits != 16 && bits != 8 && bits != 4) return fail(PW_EINVAL, "bits must be 16, 8 or 4");
+  const uint64_t K = proj == PW_DOWN ? d->F : d->H;
+  const uint64_t rk = static_cast<uint64_t>(d->R) * K;
+  *bytes = bits == 16 ? 2 * rk : (bits == 8 ? rk : rk / 2) + 4ull * d->R * (K / d->G);
+  return PW_OK;
+}
+
+pw_status pw_layer_create(const pw_layer_desc* d, void* pool_dev, size_t pool_bytes,
+                          pw_page_entry* table_dev, pw_layer** out) {
+  std::string err;
+  if (!d || !out || !pool_dev || !table_dev) return fail(PW_EINVAL, "null argument");
+  *out = nullptr;
+  if (!pw::LayerState::valid_desc(*d, &err)) return fail(PW_EINVAL, err);
+  if (d->G > 512 || (d->G % 64)) return fail(PW_EUNSUPPORTED, "G must be 64, 128, 256 or 512");
+  if (!mult_of_256(pool_dev)) return fail(PW_EINVAL, "pool must be 256-byte aligned");
+  if (reinterpret_cast<uintptr_t>(table_dev) & 7u) return fail(PW_EINVAL, "table must be 8-byte aligned");
+  pw_layer* L = new pw_layer(*d, pool_dev, pool_bytes, table_dev);
+  hipError_t e = pw::launch_clear_table(table_dev, L->st.n_entries, nullptr);
+  if (e == hipSuccess) e = hipStreamSynchronize(nullptr);
+  if (e != hipSuccess) {
+    delete L;
+    return hip_fail(e, "clearing the page table");
+  }
+  *out = L;
+  return PW_OK;
+}
+
+pw_status pw_layer_destroy(pw_layer* L) {
+  if (!L) return PW_OK;
+  for (auto& r : L->recs) {
+    (void)hipEventSynchronize(r.b);
+    (void)hipEventDestroy(r.a);
+    (void)hipEventDestroy(r.b);
+  }
+  delete L;
+  return PW_OK;
+}
+
+pw_status pw_layer_load_page(pw_layer* L, int e, int proj, int rb, int bits, const void* rows16,
+                             void* stream) {
+  if (!L || !rows16) return fail(PW_EINVAL, "null argument");
+  std::string err;
+  pw_page_entry ent{};
+  pw_status s = L->st.plan_load(e, proj, rb, bits, &ent, &err);
+  if (s != PW_OK) return fail(s, err);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int K = L->st.kdim(proj);
+  hipError_t he = hipSuccess;
+  if (bits == 16) {
+    he = hipMemcpyAsync(L->pool + ent.data_off, rows16, static_cast<size_t>(L->st.desc.R) * K * 2,
+                        hipMemcpyDeviceToDevice, st);
+    if (he != hipSuccess) {
+      L->st.abort_slot(ent, proj);
+      return hip_fail(he, "page copy");
+    }
+  } else {
+    pw::QJob j{};
+    j.src = static_cast<const uint8_t*>(rows16);
+    j.src_sz = nullptr;
+    j.dst = L->pool + ent.data_off;
+    j.dst_sz = L->pool + ent.sz_off;
+    j.src_bits = 16;
+    j.dst_bits = static_cast<uint16_t>(bits);
+    s = run_qjobs(L, {j}, proj, st);
+    if (s != PW_OK) {
+      L->st.abort_slot(ent, proj);
+      return s;
+    }
+  }
+  s = write_entries(L, {{L->st.index(e, proj, rb), ent}}, st);
+  if (s != PW_OK) {
+    L->st.abort_slot(ent, proj);
+    return s;
+  }
+  L->st.finish_load(e, proj, rb, ent);
+  return PW_OK;
+}
+
+pw_status pw_route_topk(const float* logits, int T, int E, int K, int renorm, int32_t* ids,
+                        float* w, int32_t* offsets, int32_t* sorted_slot, int32_t* slot_pos,
+                        void* stream) {
+  if (T < 0 || E < 1 || K < 1 || K > E || K > 16 || E > 256)
+    return fail(PW_EINVAL, "need 1 <= K <= E <= 256, K <= 16, T >= 0");
+  if (static_cast<int64_t>(T) * K >= (int64_t(1) << 31)) return fail(PW_EINVAL, "T*K too large");
+  if (!offsets || (T > 0 && (!logits || !ids || !w || !sorted_slot || !slot_pos)))
+    return fail(PW_EINVAL, "null argument");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t e = pw::launch_route_topk(logits, T, E, K, renorm, ids, w, st);
+  if (e != hipSuccess) return hip_fail(e, "router launch");
+  e = pw::launch_permute(ids, T, K, E, offsets, sorted_slot, slot_pos, st);
+  if (e != hipSuccess) return hip_fail(e, "permute launch");
+  return PW_OK;
+}
+
+pw_status pw_workspace_bytes(const pw_layer* L, int T, int K, size_t* gemm_ws) {
+  if (!L || !gemm_ws || T < 0 || K < 1) return fail(PW_EINVAL, "bad argument");
+  *gemm_ws = ws_layout(L->st.desc, T, K).total;
+  return PW_OK;
+}
+
+pw_status pw_moe_paged_gemm(const pw_layer* Lc, const void* x, int T, int K, const float* topk_w,
+                            const int32_t* offsets, const int32_t* sorted_slot,
+                            const int32_t* slot_pos, void* y, int out_fp32, void* ws,
+                            size_t ws_bytes, void* stream) {
+  pw_layer* L = const_cast<pw_layer*>(Lc);
+  if (!L) return fail(PW_EINVAL, "null layer");
+  if (T < 0 || K < 1 || K > L->st.desc.E) return fail(PW_EINVAL, "need T >= 0 and 1 <= K <= E");
+  if (T == 0) return PW_OK;
+  if (!x || !topk_w || !offsets || !sorted_slot || !slot_pos || !y || !ws)
+    return fail(PW_EINVAL, "null argument");
+  if (!L->st.all_present()) return fail(PW_ESTATE, "every page of the layer must be loaded");
+  if (static_cast<int64_t>(T) * K >= (int64_t(1) << 31)) return fail(PW_EINVAL, "T*K too large");
+  const WsLayout wl = ws_layout(L->st.desc, T, K);
+  if (ws_bytes < wl.total) return fail(PW_ENOMEM, "workspace smaller than pw_workspace_bytes");
+  if (!mult_of_256(ws)) return fail(PW_EINVAL, "workspace must be 256-byte aligned");
+  if ((reinterpret_cast<uintptr_t>(x) & 15u) || (reinterpret_cast<uintptr_t>(y) & 15u))
+    return fail(PW_EINVAL, "x and y must be 16-byte aligned");
+  const pw_layer_desc& d = L->st.desc;
+  pw::GemmArgs a{};
+  a.pool = L->pool;
+  a.table = L->table;
+  a.x = static_cast<const uint16_t*>(x);
+  a.offsets = offsets;
+  a.sorted_slot = sorted_slot;
+  a.slot_pos = slot_pos;
+  a.topk_w = topk_w;
+  a.h = reinterpret_cast<uint16_t*>(static_cast<uint8_t*>(ws) + wl.h_off);
+  a.opart = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + wl.op_off);
+  a.y = y;
+  a.E = d.E;
+  a.H = d.H;
+  a.F = d.F;
+  a.R = d.R;
+  a.G = d.G;
+  a.nrb_max = L->st.nrb_max;
+  a.topk = K;
+  a.T = T;
+  a.S = T * K;
+  a.nsplit = wl.nsplit;
+  a.kb_per_split = wl.kb_per_split;
+  a.out_fp32 = out_fp32 ? 1 : 0;
+  a.act = d.act;
+  a.sdt = d.sdt;
+  a.mtb = wl.mtb;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t e;
+  {
+    ProfScope ps(L, PW_PH_GATEUP, st);
+    e = pw::launch_gateup(a, st);
+  }
+  if (e != hipSuccess) return hip_fail(e, "gate/up launch");
+  {
+    ProfScope ps(L, PW_PH_DOWN, st);
+    e = pw::launch_down(a, st);
+  }
+  if (e != hipSuccess) return hip_fail(e, "down launch");
+  {
+    ProfScope ps(L, PW_PH_COMBINE, st);
+    e = pw::launch_combine(a, st);
+  }
+  if (e != hipSuccess) return hip_fail(e, "combine launch");
+  return PW_OK;
+}
+
+pw_status pw_requant_blocks(pw_layer* L, int n, const int* e, const int* proj, const int* rb,
+                            const int* new_bits, void* side_stream, size_t* delta_total) {
+  if (!L || n < 0 || (n > 0 && (!e || !proj || !rb || !new_bits)))
+    return fail(PW_EINVAL, "bad argument");
+  if (delta_total) *delta_total = 0;
+  std::string err;
+  struct Planned {
+    int e, proj, rb;
+    pw_page_entry src, dst;
+  };
+  std::vector<Planned> plan;
+  std::set<size_t> seen;
+  uint64_t delta_sum = 0;
+  auto rollback = [&]() {
+    for (const Planned& p : plan) L->st.abort_slot(p.dst, p.proj);
+  };
+  for (int i = 0; i < n; ++i) {
+    Planned p{e[i], proj[i], rb[i], {}, {}};
+    uint64_t delta = 0;
+    std::string e2;
+    if (!L->st.check_block(p.e, p.proj, p.rb, &e2)) {
+      rollback();
+      return fail(PW_EINVAL, e2);
+    }
+    if (!seen.insert(L->st.index(p.e, p.proj, p.rb)).second) {
+      rollback();
+      return fail(PW_EINVAL, "a block appears twice in the batch");
+    }
+    pw_status s = L->st.plan_requant(p.e, p.proj, p.rb, new_bits[i], &p.src, &p.dst, &delta, &err);
+    if (s != PW_OK) {
+      rollback();
+      return fail(s, err);
+    }
+    if (delta == 0 && p.dst.bits == 0) continue;   // same bitwidth: nothing to do
+    delta_sum += delta;
+    plan.push_back(p);
+  }
+  if (plan.empty()) return PW_OK;
+  hipStream_t st = static_cast<hipStream_t>(side_stream);
+  for (int kind = 0; kind < 2; ++kind) {   // 0: gate/up (K = H), 1: down (K = F)
+    std::vector<pw::QJob> jobs;
+    for (const Planned& p : plan) {
+      if ((p.proj == PW_DOWN) != (kind == 1)) continue;
+      pw::QJob j{};
+      j.src = L->pool + p.src.data_off;
+      j.src_sz = p.src.bits == 16 ? nullptr : L->pool + p.src.sz_off;
+      j.dst = L->pool + p.dst.data_off;
+      j.dst_sz = L->pool + p.dst.sz_off;
+      j.src_bits = p.src.bits;
+      j.dst_bits = p.dst.bits;
+      jobs.push_back(j);
+    }
+    if (jobs.empty()) continue;
+    pw_status s = run_qjobs(L, jobs, kind == 1 ? PW_DOWN : PW_GATE, st);
+    if (s != PW_OK) {
+      rollback();
+      return s;
+    }
+  }
+  void* ev = L->evops.create();
+  if (!ev) {
+    rollback();
+    return fail(PW_EHIP, "hipEventCreate failed");
+  }
+  hipError_t he = hipEventRecord(static_cast<hipEvent_t>(ev), st);
+  if (he != hipSuccess) {
+    L->evops.destroy(ev);
+    rollback();
+    return hip_fail(he, "hipEventRecord");
+  }
+  L->st.ref_event(ev);   // hold while the batch is registered
+  for (const Planned& p : plan) L->st.add_pending(p.e, p.proj, p.rb, p.dst, ev);
+  L->st.unref_event(ev);
+  if (delta_total) *delta_total = delta_sum;
+  return PW_OK;
+}
+
+pw_status pw_requant_block(pw_layer* L, int e, int proj, int rb, int new_bits, void* side_stream,
+                           size_t* delta_bytes) {
+  return pw_requant_blocks(L, 1, &e, &proj, &rb, &new_bits, side_stream, delta_bytes);
+}
+
+pw_status pw_commit(pw_layer* L, void* main_stream, int* n_committed) {
+  if (!L) return fail(PW_EINVAL, "null layer");
+  if (n_committed) *n_committed = 0;
+  const auto& pend = L->st.pending();
+  if (pend.empty()) return PW_OK;
+  hipStream_t st = static_cast<hipStream_t>(main_stream);
+  std::set<void*> evs;
+  for (const auto& p : pend) evs.insert(p.ev);
+  for (void* ev : evs) {
+    hipError_t he = hipStreamWaitEvent(st, static_cast<hipEvent_t>(ev), 0);
+    if (he != hipSuccess) return hip_fail(he, "hipStreamWaitEvent");
+  }
+  std::vector<std::pair<size_t, pw_page_entry>> w;
+  for (const auto& p : pend) w.push_back({p.idx, p.next});
+  pw_status s = write_entries(L, w, st);
+  if (s != PW_OK) return s;
+  void* cev = L->evops.create();
+  if (!cev) return fail(PW_EHIP, "hipEventCreate failed");
+  hipError_t he = hipEventRecord(static_cast<hipEvent_t>(cev), st);
+  if (he != hipSuccess) {
+    L->evops.destroy(cev);
+    return hip_fail(he, "hipEventRecord");
+  }
+  const int n = static_cast<int>(pend.size());
+  L->st.committed(cev);
+  if (n_committed) *n_committed = n;
+  return PW_OK;
+}
+
+pw_status pw_reclaim(pw_layer* L, size_t* bytes_freed) {
+  if (!L) return fail(PW_EINVAL, "null layer");
+  const uint64_t f = L->st.reclaim();
+  if (bytes_freed) *bytes_freed = f;
+  return PW_OK;
+}
+
+pw_status pw_page_info(const pw_layer* L, int e, int proj, int rb, pw_page_entry* out) {
+  std::string err;
+  if (!L || !out) return fail(PW_EINVAL, "null argument");
+  if (!L->st.check_block(e, proj, rb, &err)) return fail(PW_EINVAL, err);
+  *out = L->st.mirror[L->st.index(e, proj, rb)];
+  return PW_OK;
+}
+
+pw_status pw_pool_stats(const pw_layer* L, size_t* used, size_t* free_bytes, size_t* largest) {
+  if (!L) return fail(PW_EINVAL, "null layer");
+  if (used) *used = L->st.alloc.used();
+  if (free_bytes) *free_bytes = L->st.alloc.free_bytes();
+  if (largest) *largest = L->st.alloc.largest_free();
+  return PW_OK;
+}
+
+pw_status pw_profile_enable(pw_layer* L, int on) {
+  if (!L) return fail(PW_EINVAL, "null layer");
+  L->prof = on != 0;
+  return PW_OK;
+}
+
+pw_status pw_profile_read(pw_layer* L, double* total_ms, int64_t* count, int reset) {
+  if (!L) return fail(PW_EINVAL, "null layer");
+  for (auto& r : L->recs) {
+    hipError_t he = hipEventSynchronize(r.b);
+    float ms = 0.f;
+    if (he == hipSuccess) he = hipEventElapsedTime(&ms, r.a, r.b);
+    if (he != hipSuccess) return hip_fail(he, "profile event");
+    L->tot_ms[r.phase] += ms;
+    L->cnt[r.phase] += 1;
+    (void)hipEventDestroy(r.a);
+    (void)hipEventDestroy(r.b);
+  }
+  L->recs.clear();
+  for (int i = 0; i < PW_NPHASE; ++i) {
+    if (total_ms) total_ms[i] = L->tot_ms[i];
+    if (count) count[i] = L->cnt[i];
+    if (reset) {
+      L->tot_ms[i] = 0;
+      L->cnt[i] = 0;
+    }
+  }
+  return PW_OK;
+}
+
+}  // extern "C"

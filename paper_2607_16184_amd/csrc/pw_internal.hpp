@@ -1,0 +1,69 @@
+// Kernel argument blocks and launchers shared by the C ABI (pw_api.cpp) and
+// the HIP kernels (pw_kernels.hip). Internal to libpagedweight.so.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <cstdint>
+
+#include "pw.h"
+
+namespace pw {
+
+// One page transformation for the quantize / requant kernel.
+struct QJob {
+  const uint8_t* src;      // source values (16-bit) or code block
+  const uint8_t* src_sz;   // source scale/zero block (quantized sources)
+  uint8_t* dst;            // destination code block
+  uint8_t* dst_sz;         // destination scale/zero block
+  uint32_t item_base;      // first work item of this job
+  uint16_t src_bits, dst_bits;
+};
+constexpr int kMaxQJobs = 32;
+struct QJobBatch {
+  QJob job[kMaxQJobs];
+  int n_jobs;
+  int R, K, G;             // rows, reduction length, group size (same for the batch)
+  int act, sdt;
+  uint32_t items_per_job;  // rows * chunks
+  uint32_t total_items;
+};
+
+// Page-table writes performed by a kernel on the caller's stream.
+constexpr int kMaxEntryWrites = 64;
+struct EntryWrites {
+  pw_page_entry ent[kMaxEntryWrites];
+  uint32_t idx[kMaxEntryWrites];
+  int n;
+};
+
+struct GemmArgs {
+  const uint8_t* pool;
+  const pw_page_entry* table;
+  const uint16_t* x;          // [T,H] act
+  const int32_t* offsets;     // [E+1]
+  const int32_t* sorted_slot; // [S]
+  const int32_t* slot_pos;    // [S]
+  const float* topk_w;        // [T,K]
+  uint16_t* h;                // [S,F] act, rows in sorted order
+  float* opart;               // [nsplit][S][H] fp32 partial down outputs
+  void* y;                    // [T,H] act or fp32
+  int E, H, F, R, G, nrb_max;
+  int topk, T, S;
+  int nsplit, kb_per_split;   // down projection split over K = F (in 128-blocks)
+  int out_fp32;
+  int act, sdt;
+  int mtb;                    // M tiles (of 16 slots) per pass
+};
+
+hipError_t launch_route_topk(const float* logits, int T, int E, int K, int renorm,
+                             int32_t* ids, float* w, hipStream_t st);
+hipError_t launch_permute(const int32_t* ids, int T, int K, int E, int32_t* offsets,
+                          int32_t* sorted_slot, int32_t* slot_pos, hipStream_t st);
+hipError_t launch_qjobs(const QJobBatch& b, hipStream_t st);
+hipError_t launch_entry_writes(pw_page_entry* table, const EntryWrites& w, hipStream_t st);
+hipError_t launch_clear_table(pw_page_entry* table, size_t n, hipStream_t st);
+hipError_t launch_gateup(const GemmArgs& a, hipStream_t st);
+hipError_t launch_down(const GemmArgs& a, hipStream_t st);
+hipError_t launch_combine(const GemmArgs& a, hipStream_t st);
+
+}  // namespace pw

@@ -1,0 +1,794 @@
+// HIP kernels for gfx950 (CDNA4): router, token permutation, group-wise RTN
+// quantize / requantize, the paged gate/up and down GEMMs and the combine.
+//
+// GEMM layout. Each wave computes D[n][m] = sum_k W[n][k] * X[m][k] for 16
+// weight rows n (the MFMA A operand) and 16 routed slots m (the B operand)
+// with v_mfma_f32_16x16x32_{bf16,f16}. K is walked in blocks of 128; a block
+// is four MFMA k-steps, and in k-step i lane group j (lanes 16j..16j+15)
+// supplies k = 32i + 8j .. 32i + 8j + 7 of both operands. The page format
+// stores the codes of a lane group's four k-steps contiguously (run rho at
+// position 4*(rho mod 4) + rho div 4), so every weight fragment is one or more
+// 16-byte loads per lane.
+//
+// Quantized pages run in the code domain: the A operand is the code c itself
+// as an exact 16-bit float (int8 codes through an exact conversion; int4
+// codes, and int8 codes with fp16 activations, OR-ed into the mantissa of a
+// constant OFF, giving OFF + c exactly). Per group of G along K the MFMA gives
+// P = sum (c + OFF) x and a second MFMA with an all-ones A operand gives
+// X = sum x; the group's scale s and zero z are then applied in fp32 on the
+// accumulator: acc += s * P + (z - OFF * s) * X, which is sum (z + c s) x.
+// Weights are never rounded: the dequantized value z + c*s enters exactly.
+#include <algorithm>
+
+#include "pw_internal.hpp"
+
+namespace pw {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+// ---------------------------------------------------------------------------
+// 16-bit float helpers
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ float bf16_val(uint32_t h) { return __uint_as_float(h << 16); }
+__device__ __forceinline__ float f16_val(uint32_t h) {
+  return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(h)));
+}
+__device__ __forceinline__ float val16(uint32_t h, int fmt) {
+  return fmt == PW_BF16 ? bf16_val(h & 0xFFFFu) : f16_val(h & 0xFFFFu);
+}
+// round to nearest even (finite inputs)
+__device__ __forceinline__ uint32_t bf16_rne(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+__device__ __forceinline__ uint32_t f16_rne(float f) {
+  return __builtin_bit_cast(uint16_t, static_cast<_Float16>(f));
+}
+__device__ __forceinline__ uint32_t rne16(float f, int fmt) {
+  return fmt == PW_BF16 ? bf16_rne(f) : f16_rne(f);
+}
+
+// Directed rounding of an fp32 value to bf16: truncation moves toward zero,
+// so it rounds down for positive inputs and up for negative ones.
+__device__ __forceinline__ uint32_t bf16_down(float x) {
+  if (x == 0.0f) return 0u;
+  const uint32_t u = __float_as_uint(x), t = u >> 16;
+  if ((u & 0xFFFFu) == 0u) return t;
+  return (u >> 31) ? t + 1u : t;
+}
+__device__ __forceinline__ uint32_t bf16_up(float x) {
+  if (x == 0.0f) return 0u;
+  const uint32_t u = __float_as_uint(x), t = u >> 16;
+  if ((u & 0xFFFFu) == 0u) return t;
+  const uint32_t r = (u >> 31) ? t : t + 1u;
+  return r == 0x8000u ? 0u : r;
+}
+// fp16: convert to nearest, then step one ulp if it landed on the wrong side.
+__device__ __forceinline__ uint32_t f16_step(uint32_t h, bool up) {
+  if ((h & 0x7FFFu) == 0u) return up ? 0x0001u : 0x8001u;
+  const bool neg = (h >> 15) != 0;
+  return (neg != up) ? h + 1u : h - 1u;
+}
+__device__ __forceinline__ uint32_t f16_down(float x) {
+  if (x == 0.0f) return 0u;
+  uint32_t h = f16_rne(x);
+  if (f16_val(h) > x) h = f16_step(h, false);
+  return (h & 0x7FFFu) == 0u ? 0u : h;
+}
+__device__ __forceinline__ uint32_t f16_up(float x) {
+  if (x == 0.0f) return 0u;
+  uint32_t h = f16_rne(x);
+  if (f16_val(h) < x) h = f16_step(h, true);
+  return (h & 0x7FFFu) == 0u ? 0u : h;
+}
+__device__ __forceinline__ uint32_t round_down16(float x, int fmt) {
+  return fmt == PW_BF16 ? bf16_down(x) : f16_down(x);
+}
+__device__ __forceinline__ uint32_t round_up16(float x, int fmt) {
+  return fmt == PW_BF16 ? bf16_up(x) : f16_up(x);
+}
+
+__device__ __forceinline__ int lane_id() {
+  return __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+}
+
+// ---------------------------------------------------------------------------
+// Router: top-K per token (ties to the lower index) and routing weights
+// ---------------------------------------------------------------------------
+
+constexpr int kMaxTopK = 16;
+
+__global__ __launch_bounds__(256) void k_route_topk(const float* __restrict__ logits, int T, int E,
+                                                    int K, int renorm, int32_t* __restrict__ ids,
+                                                    float* __restrict__ w) {
+  const int t = blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= T) return;
+  const float* l = logits + static_cast<size_t>(t) * E;
+  float sv[kMaxTopK];
+  int se[kMaxTopK];
+  float pv = __builtin_inff();
+  int pe = -1;
+  for (int k = 0; k < K; ++k) {
+    float bv = 0.0f;
+    int be = -1;
+    for (int e = 0; e < E; ++e) {
+      const float v = l[e];
+      const bool after = (v < pv) || (v == pv && e > pe);   // later in (value desc, index asc)
+      if (after && (be < 0 || v > bv)) {
+        bv = v;
+        be = e;
+      }
+    }
+    sv[k] = bv;
+    se[k] = be;
+    pv = bv;
+    pe = be;
+  }
+  const float m = sv[0];
+  float sum = 0.0f;
+  if (renorm) {
+    for (int k = 0; k < K; ++k) sum += expf(sv[k] - m);
+  } else {
+    for (int e = 0; e < E; ++e) sum += expf(l[e] - m);
+  }
+  for (int k = 0; k < K; ++k) {
+    ids[static_cast<size_t>(t) * K + k] = se[k];
+    w[static_cast<size_t>(t) * K + k] = expf(sv[k] - m) / sum;
+  }
+}
+
+// Token permutation in one workgroup: per-expert counts, exclusive scan, and a
+// stable expert-major placement. Within a wave, lanes holding the same expert
+// are matched with ballots; a per-wave count table gives cross-wave ranks.
+constexpr int kPermThreads = 1024;
+constexpr int kPermWaves = kPermThreads / 64;
+constexpr int kMaxExperts = 256;
+
+__global__ __launch_bounds__(kPermThreads) void k_permute(const int32_t* __restrict__ ids, int S,
+                                                          int E, int32_t* __restrict__ offsets,
+                                                          int32_t* __restrict__ sorted_slot,
+                                                          int32_t* __restrict__ slot_pos) {
+  __shared__ int cnt[kMaxExperts];
+  __shared__ int off[kMaxExperts];
+  __shared__ int run[kMaxExperts];
+  __shared__ int wcnt[kPermWaves][kMaxExperts];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = lane_id();
+  for (int e = tid; e < E; e += kPermThreads) {
+    cnt[e] = 0;
+    run[e] = 0;
+  }
+  __syncthreads();
+  for (int s = tid; s < S; s += kPermThreads) {
+    const int id = ids[s];
+    if (id >= 0 && id < E) atomicAdd(&cnt[id], 1);
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int acc = 0;
+    for (int e = 0; e < E; ++e) {
+      off[e] = acc;
+      offsets[e] = acc;
+      acc += cnt[e];
+    }
+    offsets[E] = acc;
+  }
+  __syncthreads();
+  for (int base = 0; base < S; base += kPermThreads) {
+    for (int i = tid; i < kPermWaves * E; i += kPermThreads) wcnt[i / E][i % E] = 0;
+    __syncthreads();
+    const int s = base + tid;
+    int id = -1;
+    if (s < S) {
+      id = ids[s];
+      if (id < 0 || id >= E) id = -1;
+    }
+    unsigned long long todo = __ballot(id >= 0);
+    int rank = 0;
+    while (todo) {
+      const int leader = __builtin_ctzll(todo);
+      const int lid = __shfl(id, leader);
+      const unsigned long long m = __ballot(id == lid);
+      if (id == lid)
+        rank = __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(m >> 32),
+                                         __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(m), 0u));
+      if (lane == leader) wcnt[wave][lid] = __popcll(m);
+      todo &= ~m;
+    }
+    __syncthreads();
+    if (id >= 0) {
+      int pos = off[id] + run[id] + rank;
+      for (int w = 0; w < wave; ++w) pos += wcnt[w][id];
+      sorted_slot[pos] = s;
+      slot_pos[s] = pos;
+    }
+    __syncthreads();
+    for (int e = tid; e < E; e += kPermThreads) {
+      int add = 0;
+      for (int w = 0; w < kPermWaves; ++w) add += wcnt[w][e];
+      run[e] += add;
+    }
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Group-wise RTN quantize / requantize (one wave per row x 512 codes)
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(256) void k_qjobs(const QJobBatch b) {
+  const uint32_t item = blockIdx.x * 4u + (threadIdx.x >> 6);
+  if (item >= b.total_items) return;
+  const int lane = lane_id();
+  const int K = b.K, R = b.R, G = b.G;
+  const int nchunk = (K + 511) / 512;
+  const int j = static_cast<int>(item / b.items_per_job);
+  const int rem = static_cast<int>(item % b.items_per_job);
+  const int row = rem / nchunk, chunk = rem % nchunk;
+  const QJob& job = b.job[j];
+  const int k0 = chunk * 512 + 8 * lane;
+  const bool valid = k0 < K;
+  const int blk = k0 >> 7, rho = (k0 & 127) >> 3, pos = 4 * (rho & 3) + (rho >> 2);
+  const int g = k0 / G;
+
+  float v[8];
+  for (int q = 0; q < 8; ++q) v[q] = 0.0f;
+  if (valid) {
+    if (job.src_bits == 16) {
+      const u32x4 d = *reinterpret_cast<const u32x4*>(job.src + (static_cast<size_t>(row) * K + k0) * 2);
+      for (int q = 0; q < 4; ++q) {
+        v[2 * q] = val16(d[q], b.act);
+        v[2 * q + 1] = val16(d[q] >> 16, b.act);
+      }
+    } else {
+      const uint32_t szw = *reinterpret_cast<const uint32_t*>(job.src_sz + (static_cast<size_t>(g) * R + row) * 4);
+      const float s = val16(szw, b.sdt), z = val16(szw >> 16, b.sdt);
+      uint32_t c[8];
+      if (job.src_bits == 8) {
+        const u32x2 d = *reinterpret_cast<const u32x2*>(job.src + static_cast<size_t>(row) * K + blk * 128 + 8 * pos);
+        for (int q = 0; q < 4; ++q) {
+          c[q] = (d[0] >> (8 * q)) & 0xFFu;
+          c[4 + q] = (d[1] >> (8 * q)) & 0xFFu;
+        }
+      } else {
+        const uint32_t w = *reinterpret_cast<const uint32_t*>(job.src + static_cast<size_t>(row) * (K / 2) + blk * 64 + 4 * pos);
+        for (int t = 0; t < 4; ++t) {
+          c[2 * t] = (w >> (4 * t)) & 15u;
+          c[2 * t + 1] = (w >> (16 + 4 * t)) & 15u;
+        }
+      }
+      for (int q = 0; q < 8; ++q) v[q] = z + static_cast<float>(c[q]) * s;   // c*s exact
+    }
+  }
+  float lo = v[0], hi = v[0];
+  for (int q = 1; q < 8; ++q) {
+    lo = fminf(lo, v[q]);
+    hi = fmaxf(hi, v[q]);
+  }
+  for (int m = 1; m < G / 8; m <<= 1) {
+    lo = fminf(lo, __shfl_xor(lo, m));
+    hi = fmaxf(hi, __shfl_xor(hi, m));
+  }
+  if (!valid) return;
+  const int Q = (1 << job.dst_bits) - 1;
+  const uint32_t zb = round_down16(lo, b.sdt);
+  const float z = val16(zb, b.sdt);
+  const float r = hi - z;
+  uint32_t sb = 0u;
+  uint32_t c[8];
+  if (r == 0.0f) {
+    for (int q = 0; q < 8; ++q) c[q] = 0u;
+  } else {
+    const float s0 = r / static_cast<float>(Q);
+    sb = round_up16(s0, b.sdt);
+    float s = val16(sb, b.sdt);
+    if (s * static_cast<float>(Q) < r) {
+      sb += 1u;                       // s > 0: next representable value up
+      s = val16(sb, b.sdt);
+    }
+    for (int q = 0; q < 8; ++q) {
+      const float d = v[q] - z;
+      float cq = rintf(d / s);
+      cq = fminf(fmaxf(cq, 0.0f), static_cast<float>(Q));
+      c[q] = static_cast<uint32_t>(cq);
+    }
+  }
+  if (job.dst_bits == 8) {
+    u32x2 o;
+    o[0] = c[0] | (c[1] << 8) | (c[2] << 16) | (c[3] << 24);
+    o[1] = c[4] | (c[5] << 8) | (c[6] << 16) | (c[7] << 24);
+    *reinterpret_cast<u32x2*>(job.dst + static_cast<size_t>(row) * K + blk * 128 + 8 * pos) = o;
+  } else {
+    uint32_t w = 0u;
+    for (int t = 0; t < 4; ++t) w |= (c[2 * t] << (4 * t)) | (c[2 * t + 1] << (16 + 4 * t));
+    *reinterpret_cast<uint32_t*>(job.dst + static_cast<size_t>(row) * (K / 2) + blk * 64 + 4 * pos) = w;
+  }
+  if ((lane % (G / 8)) == 0)
+    *reinterpret_cast<uint32_t*>(job.dst_sz + (static_cast<size_t>(g) * R + row) * 4) = sb | (zb << 16);
+}
+
+__global__ void k_entry_writes(pw_page_entry* table, const EntryWrites w) {
+  const int i = threadIdx.x;
+  if (i < w.n) table[w.idx[i]] = w.ent[i];
+}
+
+__global__ void k_clear_table(pw_page_entry* table, size_t n) {
+  for (size_t i = blockIdx.x * static_cast<size_t>(blockDim.x) + threadIdx.x; i < n;
+       i += static_cast<size_t>(gridDim.x) * blockDim.x)
+    table[i] = pw_page_entry{0, 0, 0, PW_PAGE_ABSENT, 0, 0};
+}
+
+// ---------------------------------------------------------------------------
+// Paged GEMM building blocks
+// ---------------------------------------------------------------------------
+
+template <int ACT>
+__device__ __forceinline__ f32x4 mma(u32x4 a, u32x4 b, f32x4 c) {
+  if constexpr (ACT == PW_BF16)
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                   __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+  else
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a),
+                                                  __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
+}
+
+template <int ACT>
+__device__ __forceinline__ u32x4 ones_op() {
+  const uint32_t one = ACT == PW_BF16 ? 0x3F803F80u : 0x3C003C00u;
+  return u32x4{one, one, one, one};
+}
+
+// Code-domain offset of a page format (see the file comment).
+template <int ACT, int B>
+struct CodeOff {
+  static constexpr float value = (B == 16) ? 0.0f : (ACT == PW_BF16 ? (B == 4 ? 128.0f : 0.0f) : 1024.0f);
+};
+
+template <int B> constexpr int row_bytes(int K) { return B == 16 ? 2 * K : B == 8 ? K : K / 2; }
+template <int B> struct WF;
+template <> struct WF<16> { u32x4 v[4]; };
+template <> struct WF<8> { u32x4 v[2]; };
+template <> struct WF<4> { u32x4 v[1]; };
+
+__device__ __forceinline__ u32x4 ld16(const uint8_t* p) { return *reinterpret_cast<const u32x4*>(p); }
+
+// Lane group lg's share of one 128-code block of its row.
+template <int B>
+__device__ __forceinline__ void wf_load(WF<B>& f, const uint8_t* rowp, int blk, int lg) {
+  if constexpr (B == 16) {
+    const uint8_t* p = rowp + blk * 256 + 16 * lg;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) f.v[i] = ld16(p + 64 * i);
+  } else if constexpr (B == 8) {
+    const uint8_t* p = rowp + blk * 128 + 32 * lg;
+    f.v[0] = ld16(p);
+    f.v[1] = ld16(p + 16);
+  } else {
+    f.v[0] = ld16(rowp + blk * 64 + 16 * lg);
+  }
+}
+
+// A operand of k-step i: eight 16-bit values (weights, or codes as floats).
+template <int ACT, int B>
+__device__ __forceinline__ u32x4 wf_op(const WF<B>& f, int i) {
+  if constexpr (B == 16) {
+    return f.v[i];
+  } else if constexpr (B == 8) {
+    const uint32_t d0 = f.v[i >> 1][(i & 1) * 2], d1 = f.v[i >> 1][(i & 1) * 2 + 1];
+    u32x4 o;
+    if constexpr (ACT == PW_BF16) {
+      // bytes -> exact fp32 -> upper halves are the exact bf16 values
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        const uint32_t d = q ? d1 : d0;
+        const float c0 = static_cast<float>(d & 0xFFu), c1 = static_cast<float>((d >> 8) & 0xFFu);
+        const float c2 = static_cast<float>((d >> 16) & 0xFFu), c3 = static_cast<float>(d >> 24);
+        o[2 * q] = __builtin_amdgcn_perm(__float_as_uint(c1), __float_as_uint(c0), 0x07060302u);
+        o[2 * q + 1] = __builtin_amdgcn_perm(__float_as_uint(c3), __float_as_uint(c2), 0x07060302u);
+      }
+    } else {
+      // 0x64 high byte: fp16 1024 + c
+      o[0] = __builtin_amdgcn_perm(0x64646464u, d0, 0x05010400u);
+      o[1] = __builtin_amdgcn_perm(0x64646464u, d0, 0x05030402u);
+      o[2] = __builtin_amdgcn_perm(0x64646464u, d1, 0x05010400u);
+      o[3] = __builtin_amdgcn_perm(0x64646464u, d1, 0x05030402u);
+    }
+    return o;
+  } else {
+    const uint32_t w = f.v[0][i];
+    const uint32_t magic = ACT == PW_BF16 ? 0x43004300u : 0x64006400u;   // 128 / 1024
+    u32x4 o;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) o[q] = ((w >> (4 * q)) & 0x000F000Fu) | magic;
+    return o;
+  }
+}
+
+// acc += s * P + (z - OFF s) * X for the lane's four rows; P is cleared.
+template <int ACT, int B, int MTB>
+__device__ __forceinline__ void group_fix(f32x4 (&acc)[MTB], f32x4 (&p)[MTB], const f32x4 (&xs)[MTB],
+                                          u32x4 sz, int sdt, int ntile) {
+  constexpr float off = CodeOff<ACT, B>::value;
+  float s[4], zp[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    s[r] = val16(sz[r], sdt);
+    zp[r] = val16(sz[r] >> 16, sdt) - off * s[r];
+  }
+#pragma unroll
+  for (int t = 0; t < MTB; ++t) {
+    if (t < ntile) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[t][r] += s[r] * p[t][r] + zp[r] * xs[t][r];
+    }
+    p[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+}
+
+__device__ __forceinline__ int clampi(int v, int lo, int hi) { return v < lo ? lo : (v > hi ? hi : v); }
+
+// Scale/zero block: 16 bytes = (s, z) of the lane's four output rows.
+__device__ __forceinline__ u32x4 sz_load(const uint8_t* szrow, int g, int R) {
+  return ld16(szrow + static_cast<size_t>(g) * R * 4);
+}
+
+template <int B>
+struct Proj {
+  WF<B> w;
+  u32x4 sz[2];
+};
+
+// ---------------------------------------------------------------------------
+// gate/up GEMM + SwiGLU (one wave: 16 rows of gate and of up, all K = H)
+// ---------------------------------------------------------------------------
+
+template <int ACT, int BG, int BU, int MTB>
+__device__ void gateup_body(const GemmArgs& a, int off_e, int n_e, int f0, int lr0,
+                            const pw_page_entry& eg, const pw_page_entry& eu) {
+  const int lane = lane_id(), lc = lane & 15, lg = lane >> 4;
+  const int H = a.H, G = a.G, R = a.R;
+  const int nkb = H / 128;
+  const uint8_t* wg_row = a.pool + eg.data_off + static_cast<size_t>(lr0 + lc) * row_bytes<BG>(H);
+  const uint8_t* wu_row = a.pool + eu.data_off + static_cast<size_t>(lr0 + lc) * row_bytes<BU>(H);
+  const uint8_t* szg_row = a.pool + eg.sz_off + static_cast<size_t>(lr0 + 4 * lg) * 4;
+  const uint8_t* szu_row = a.pool + eu.sz_off + static_cast<size_t>(lr0 + 4 * lg) * 4;
+  constexpr bool kQuant = (BG != 16) || (BU != 16);
+
+  for (int mb = 0; mb < n_e; mb += MTB * 16) {
+    const int ntile = min(MTB, (n_e - mb + 15) / 16);
+    const uint8_t* xrow[MTB];
+#pragma unroll
+    for (int t = 0; t < MTB; ++t) {
+      const int m = clampi(mb + 16 * t + lc, 0, n_e - 1);
+      const int slot = clampi(a.sorted_slot[off_e + m], 0, a.S - 1);
+      const int tok = slot / a.topk;
+      xrow[t] = reinterpret_cast<const uint8_t*>(a.x + static_cast<size_t>(tok) * H) + 16 * lg;
+    }
+    f32x4 accg[MTB], accu[MTB], pg[MTB], pu[MTB], xs[MTB];
+#pragma unroll
+    for (int t = 0; t < MTB; ++t) {
+      accg[t] = accu[t] = pg[t] = pu[t] = xs[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    struct Frag {
+      Proj<BG> g;
+      Proj<BU> u;
+      u32x4 xb[MTB][4];
+    };
+    auto load = [&](Frag& f, int blk) {
+      wf_load<BG>(f.g.w, wg_row, blk, lg);
+      wf_load<BU>(f.u.w, wu_row, blk, lg);
+#pragma unroll
+      for (int t = 0; t < MTB; ++t) {
+        if (t < ntile) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) f.xb[t][i] = ld16(xrow[t] + (blk * 128 + 32 * i) * 2);
+        }
+      }
+      if (G == 64) {
+        if constexpr (BG != 16) { f.g.sz[0] = sz_load(szg_row, 2 * blk, R); f.g.sz[1] = sz_load(szg_row, 2 * blk + 1, R); }
+        if constexpr (BU != 16) { f.u.sz[0] = sz_load(szu_row, 2 * blk, R); f.u.sz[1] = sz_load(szu_row, 2 * blk + 1, R); }
+      } else if (((blk + 1) * 128) % G == 0) {
+        const int gi = (blk * 128) / G;
+        if constexpr (BG != 16) f.g.sz[0] = sz_load(szg_row, gi, R);
+        if constexpr (BU != 16) f.u.sz[0] = sz_load(szu_row, gi, R);
+      }
+    };
+    Frag cur, nxt;
+    load(cur, 0);
+    for (int blk = 0; blk < nkb; ++blk) {
+      if (blk + 1 < nkb) load(nxt, blk + 1);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const u32x4 ag = wf_op<ACT, BG>(cur.g.w, i);
+        const u32x4 au = wf_op<ACT, BU>(cur.u.w, i);
+#pragma unroll
+        for (int t = 0; t < MTB; ++t) {
+          if (t < ntile) {
+            const u32x4 bx = cur.xb[t][i];
+            if constexpr (BG == 16) accg[t] = mma<ACT>(ag, bx, accg[t]); else pg[t] = mma<ACT>(ag, bx, pg[t]);
+            if constexpr (BU == 16) accu[t] = mma<ACT>(au, bx, accu[t]); else pu[t] = mma<ACT>(au, bx, pu[t]);
+            if constexpr (kQuant) xs[t] = mma<ACT>(ones_op<ACT>(), bx, xs[t]);
+          }
+        }
+        if constexpr (kQuant) {
+          const bool gend = (G == 64) ? ((i & 1) == 1) : (i == 3 && ((blk + 1) * 128) % G == 0);
+          if (gend) {
+            const int si = (G == 64) ? (i >> 1) : 0;
+            if constexpr (BG != 16) group_fix<ACT, BG, MTB>(accg, pg, xs, cur.g.sz[si], a.sdt, ntile);
+            if constexpr (BU != 16) group_fix<ACT, BU, MTB>(accu, pu, xs, cur.u.sz[si], a.sdt, ntile);
+#pragma unroll
+            for (int t = 0; t < MTB; ++t) xs[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+          }
+        }
+      }
+      cur = nxt;
+    }
+    // SwiGLU epilogue: h = silu(g) * u, rounded to the activation dtype
+#pragma unroll
+    for (int t = 0; t < MTB; ++t) {
+      const int m = mb + 16 * t + lc;
+      if (t < ntile && m < n_e) {
+        uint32_t hv[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float gv = accg[t][r];
+          const float hval = gv / (1.0f + expf(-gv)) * accu[t][r];
+          hv[r] = rne16(hval, ACT);
+        }
+        u32x2 o;
+        o[0] = hv[0] | (hv[1] << 16);
+        o[1] = hv[2] | (hv[3] << 16);
+        *reinterpret_cast<u32x2*>(a.h + static_cast<size_t>(off_e + m) * a.F + f0 + 4 * lg) = o;
+      }
+    }
+  }
+}
+
+template <int ACT, int MTB>
+__global__ __launch_bounds__(256) void k_gateup(const GemmArgs a) {
+  const int upe = a.F / 64;
+  const int e = blockIdx.x / upe, r64 = blockIdx.x % upe;
+  const int off_e = clampi(a.offsets[e], 0, a.S);
+  const int n_e = clampi(a.offsets[e + 1], off_e, a.S) - off_e;
+  if (n_e <= 0) return;
+  const int wave = threadIdx.x >> 6;
+  const int f0 = r64 * 64 + wave * 16;
+  const int rb = f0 / a.R, lr0 = f0 - rb * a.R;
+  const pw_page_entry eg = a.table[(static_cast<size_t>(e) * 3 + PW_GATE) * a.nrb_max + rb];
+  const pw_page_entry eu = a.table[(static_cast<size_t>(e) * 3 + PW_UP) * a.nrb_max + rb];
+  const int cg = eg.bits == 16 ? 0 : eg.bits == 8 ? 1 : eg.bits == 4 ? 2 : -1;
+  const int cu = eu.bits == 16 ? 0 : eu.bits == 8 ? 1 : eu.bits == 4 ? 2 : -1;
+  if (cg < 0 || cu < 0) return;
+  switch (cg * 3 + cu) {
+    case 0: gateup_body<ACT, 16, 16, MTB>(a, off_e, n_e, f0, lr0, eg, eu); break;
+    case 1: gateup_body<ACT, 16, 8, MTB>(a, off_e, n_e, f0, lr0, eg, eu); break;
+    case 2: gateup_body<ACT, 16, 4, MTB>(a, off_e, n_e, f0, lr0, eg, eu); break;
+    case 3: gateup_body<ACT, 8, 16, MTB>(a, off_e, n_e, f0, lr0, eg, eu); break;
+    case 4: gateup_body<ACT, 8, 8, MTB>(a, off_e, n_e, f0, lr0, eg, eu); break;
+    case 5: gateup_body<ACT, 8, 4, MTB>(a, off_e, n_e, f0, lr0, eg, eu); break;
+    case 6: gateup_body<ACT, 4, 16, MTB>(a, off_e, n_e, f0, lr0, eg, eu); break;
+    case 7: gateup_body<ACT, 4, 8, MTB>(a, off_e, n_e, f0, lr0, eg, eu); break;
+    default: gateup_body<ACT, 4, 4, MTB>(a, off_e, n_e, f0, lr0, eg, eu); break;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// down GEMM (one wave: 16 rows of down over one K split of F); fp32 partials
+// ---------------------------------------------------------------------------
+
+template <int ACT, int BD, int MTB>
+__device__ void down_body(const GemmArgs& a, int off_e, int n_e, int n0, int lr0, int split,
+                          const pw_page_entry& ed) {
+  const int lane = lane_id(), lc = lane & 15, lg = lane >> 4;
+  const int F = a.F, G = a.G, R = a.R;
+  const int kb0 = split * a.kb_per_split;
+  const int kb1 = min(F / 128, kb0 + a.kb_per_split);
+  if (kb0 >= kb1) return;
+  const uint8_t* w_row = a.pool + ed.data_off + static_cast<size_t>(lr0 + lc) * row_bytes<BD>(F);
+  const uint8_t* sz_row = a.pool + ed.sz_off + static_cast<size_t>(lr0 + 4 * lg) * 4;
+  constexpr bool kQuant = BD != 16;
+
+  for (int mb = 0; mb < n_e; mb += MTB * 16) {
+    const int ntile = min(MTB, (n_e - mb + 15) / 16);
+    const uint8_t* hrow[MTB];
+#pragma unroll
+    for (int t = 0; t < MTB; ++t) {
+      const int m = clampi(mb + 16 * t + lc, 0, n_e - 1);
+      hrow[t] = reinterpret_cast<const uint8_t*>(a.h + static_cast<size_t>(off_e + m) * F) + 16 * lg;
+    }
+    f32x4 acc[MTB], p[MTB], xs[MTB];
+#pragma unroll
+    for (int t = 0; t < MTB; ++t) acc[t] = p[t] = xs[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    struct Frag {
+      Proj<BD> d;
+      u32x4 xb[MTB][4];
+    };
+    auto load = [&](Frag& f, int blk) {
+      wf_load<BD>(f.d.w, w_row, blk, lg);
+#pragma unroll
+      for (int t = 0; t < MTB; ++t) {
+        if (t < ntile) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) f.xb[t][i] = ld16(hrow[t] + (blk * 128 + 32 * i) * 2);
+        }
+      }
+      if constexpr (kQuant) {
+        if (G == 64) {
+          f.d.sz[0] = sz_load(sz_row, 2 * blk, R);
+          f.d.sz[1] = sz_load(sz_row, 2 * blk + 1, R);
+        } else if (((blk + 1) * 128) % G == 0) {
+          f.d.sz[0] = sz_load(sz_row, (blk * 128) / G, R);
+        }
+      }
+    };
+    Frag cur, nxt;
+    load(cur, kb0);
+    for (int blk = kb0; blk < kb1; ++blk) {
+      if (blk + 1 < kb1) load(nxt, blk + 1);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const u32x4 ad = wf_op<ACT, BD>(cur.d.w, i);
+#pragma unroll
+        for (int t = 0; t < MTB; ++t) {
+          if (t < ntile) {
+            const u32x4 bx = cur.xb[t][i];
+            if constexpr (BD == 16) {
+              acc[t] = mma<ACT>(ad, bx, acc[t]);
+            } else {
+              p[t] = mma<ACT>(ad, bx, p[t]);
+              xs[t] = mma<ACT>(ones_op<ACT>(), bx, xs[t]);
+            }
+          }
+        }
+        if constexpr (kQuant) {
+          const bool gend = (G == 64) ? ((i & 1) == 1) : (i == 3 && ((blk + 1) * 128) % G == 0);
+          if (gend) {
+            group_fix<ACT, BD, MTB>(acc, p, xs, cur.d.sz[(G == 64) ? (i >> 1) : 0], a.sdt, ntile);
+#pragma unroll
+            for (int t = 0; t < MTB; ++t) xs[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+          }
+        }
+      }
+      cur = nxt;
+    }
+#pragma unroll
+    for (int t = 0; t < MTB; ++t) {
+      const int m = mb + 16 * t + lc;
+      if (t < ntile && m < n_e) {
+        float* dst = a.opart + (static_cast<size_t>(split) * a.S + off_e + m) * a.H + n0 + 4 * lg;
+        *reinterpret_cast<f32x4*>(dst) = acc[t];
+      }
+    }
+  }
+}
+
+template <int ACT, int MTB>
+__global__ __launch_bounds__(256) void k_down(const GemmArgs a) {
+  const int upe = a.H / 64;
+  const int split = blockIdx.x % a.nsplit;
+  const int rest = blockIdx.x / a.nsplit;
+  const int e = rest / upe, r64 = rest % upe;
+  const int off_e = clampi(a.offsets[e], 0, a.S);
+  const int n_e = clampi(a.offsets[e + 1], off_e, a.S) - off_e;
+  if (n_e <= 0) return;
+  const int wave = threadIdx.x >> 6;
+  const int n0 = r64 * 64 + wave * 16;
+  const int rb = n0 / a.R, lr0 = n0 - rb * a.R;
+  const pw_page_entry ed = a.table[(static_cast<size_t>(e) * 3 + PW_DOWN) * a.nrb_max + rb];
+  switch (ed.bits) {
+    case 16: down_body<ACT, 16, MTB>(a, off_e, n_e, n0, lr0, split, ed); break;
+    case 8: down_body<ACT, 8, MTB>(a, off_e, n_e, n0, lr0, split, ed); break;
+    case 4: down_body<ACT, 4, MTB>(a, off_e, n_e, n0, lr0, split, ed); break;
+    default: break;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// combine: y[t] = sum_k w[t,k] * sum_split opart[split][slot_pos[t,k]]
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(256) void k_combine(const GemmArgs a) {
+  const int t = blockIdx.x;
+  const int n = (blockIdx.y * 256 + threadIdx.x) * 4;
+  if (n >= a.H) return;
+  f32x4 y = {0.f, 0.f, 0.f, 0.f};
+  for (int k = 0; k < a.topk; ++k) {
+    const int pos = clampi(a.slot_pos[static_cast<size_t>(t) * a.topk + k], 0, a.S - 1);
+    f32x4 o = {0.f, 0.f, 0.f, 0.f};
+    for (int sp = 0; sp < a.nsplit; ++sp)
+      o += *reinterpret_cast<const f32x4*>(a.opart + (static_cast<size_t>(sp) * a.S + pos) * a.H + n);
+    const float wk = a.topk_w[static_cast<size_t>(t) * a.topk + k];
+    y += wk * o;
+  }
+  if (a.out_fp32) {
+    *reinterpret_cast<f32x4*>(static_cast<float*>(a.y) + static_cast<size_t>(t) * a.H + n) = y;
+  } else {
+    u32x2 o;
+    o[0] = rne16(y[0], a.act) | (rne16(y[1], a.act) << 16);
+    o[1] = rne16(y[2], a.act) | (rne16(y[3], a.act) << 16);
+    *reinterpret_cast<u32x2*>(static_cast<uint16_t*>(a.y) + static_cast<size_t>(t) * a.H + n) = o;
+  }
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// launchers
+// ---------------------------------------------------------------------------
+
+hipError_t launch_route_topk(const float* logits, int T, int E, int K, int renorm, int32_t* ids,
+                             float* w, hipStream_t st) {
+  if (T <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_route_topk, dim3((T + 255) / 256), dim3(256), 0, st, logits, T, E, K, renorm, ids, w);
+  return hipGetLastError();
+}
+
+hipError_t launch_permute(const int32_t* ids, int T, int K, int E, int32_t* offsets,
+                          int32_t* sorted_slot, int32_t* slot_pos, hipStream_t st) {
+  hipLaunchKernelGGL(k_permute, dim3(1), dim3(kPermThreads), 0, st, ids, T * K, E, offsets,
+                     sorted_slot, slot_pos);
+  return hipGetLastError();
+}
+
+hipError_t launch_qjobs(const QJobBatch& b, hipStream_t st) {
+  if (b.total_items == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_qjobs, dim3((b.total_items + 3) / 4), dim3(256), 0, st, b);
+  return hipGetLastError();
+}
+
+hipError_t launch_entry_writes(pw_page_entry* table, const EntryWrites& w, hipStream_t st) {
+  if (w.n == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_entry_writes, dim3(1), dim3(kMaxEntryWrites), 0, st, table, w);
+  return hipGetLastError();
+}
+
+hipError_t launch_clear_table(pw_page_entry* table, size_t n, hipStream_t st) {
+  if (n == 0) return hipSuccess;
+  const unsigned blocks = static_cast<unsigned>(std::min<size_t>((n + 255) / 256, 1024));
+  hipLaunchKernelGGL(k_clear_table, dim3(blocks), dim3(256), 0, st, table, n);
+  return hipGetLastError();
+}
+
+template <int ACT>
+static hipError_t gateup_act(const GemmArgs& a, hipStream_t st) {
+  const dim3 grid(a.E * (a.F / 64)), block(256);
+  switch (a.mtb) {
+    case 1: hipLaunchKernelGGL((k_gateup<ACT, 1>), grid, block, 0, st, a); break;
+    case 2: hipLaunchKernelGGL((k_gateup<ACT, 2>), grid, block, 0, st, a); break;
+    default: hipLaunchKernelGGL((k_gateup<ACT, 4>), grid, block, 0, st, a); break;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_gateup(const GemmArgs& a, hipStream_t st) {
+  return a.act == PW_BF16 ? gateup_act<PW_BF16>(a, st) : gateup_act<PW_F16>(a, st);
+}
+
+template <int ACT>
+static hipError_t down_act(const GemmArgs& a, hipStream_t st) {
+  const dim3 grid(a.E * (a.H / 64) * a.nsplit), block(256);
+  switch (a.mtb) {
+    case 1: hipLaunchKernelGGL((k_down<ACT, 1>), grid, block, 0, st, a); break;
+    case 2: hipLaunchKernelGGL((k_down<ACT, 2>), grid, block, 0, st, a); break;
+    default: hipLaunchKernelGGL((k_down<ACT, 4>), grid, block, 0, st, a); break;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_down(const GemmArgs& a, hipStream_t st) {
+  return a.act == PW_BF16 ? down_act<PW_BF16>(a, st) : down_act<PW_F16>(a, st);
+}
+
+hipError_t launch_combine(const GemmArgs& a, hipStream_t st) {
+  if (a.T <= 0) return hipSuccess;
+  const dim3 grid(a.T, (a.H / 4 + 255) / 256), block(256);
+  hipLaunchKernelGGL(k_combine, grid, block, 0, st, a);
+  return hipGetLastError();
+}
+
+}  // namespace pw

@@ -1,0 +1,191 @@
+// Host-side slot allocator and page-table protocol (see pw_state.hpp).
+#include "pw_state.hpp"
+
+#include <algorithm>
+
+namespace pw {
+
+SlotAllocator::SlotAllocator(uint64_t capacity) : cap_(capacity / kSlotAlign * kSlotAlign) {
+  if (cap_) free_[0] = cap_;
+}
+
+bool SlotAllocator::alloc(uint64_t bytes, uint64_t* off) {
+  const uint64_t need = round_up(bytes);
+  if (need == 0) return false;
+  for (auto it = free_.begin(); it != free_.end(); ++it) {
+    if (it->second >= need) {
+      *off = it->first;
+      const uint64_t rest = it->second - need;
+      const uint64_t start = it->first + need;
+      free_.erase(it);
+      if (rest) free_[start] = rest;
+      used_ += need;
+      return true;
+    }
+  }
+  return false;
+}
+
+void SlotAllocator::release(uint64_t off, uint64_t bytes) {
+  const uint64_t len = round_up(bytes);
+  used_ -= len;
+  auto next = free_.lower_bound(off);
+  uint64_t start = off, end = off + len;
+  if (next != free_.end() && next->first == end) {
+    end += next->second;
+    next = free_.erase(next);
+  }
+  if (next != free_.begin()) {
+    auto prev = std::prev(next);
+    if (prev->first + prev->second == start) {
+      start = prev->first;
+      free_.erase(prev);
+    }
+  }
+  free_[start] = end - start;
+}
+
+uint64_t SlotAllocator::largest_free() const {
+  uint64_t m = 0;
+  for (const auto& kv : free_) m = std::max(m, kv.second);
+  return m;
+}
+
+bool LayerState::valid_desc(const pw_layer_desc& d, std::string* err) {
+  auto bad = [&](const char* m) { *err = m; return false; };
+  if (d.E <= 0 || d.H <= 0 || d.F <= 0 || d.R <= 0 || d.G <= 0) return bad("non-positive layer dimension");
+  if (d.act != PW_F16 && d.act != PW_BF16) return bad("act must be PW_F16 or PW_BF16");
+  if (d.sdt != PW_F16 && d.sdt != PW_BF16) return bad("sdt must be PW_F16 or PW_BF16");
+  if (d.R % 64) return bad("R must be a multiple of 64");
+  if (d.F % d.R || d.H % d.R) return bad("F and H must be multiples of R");
+  if (d.F % 128 || d.H % 128) return bad("F and H must be multiples of 128");
+  if (d.G % 32) return bad("G must be a multiple of 32");
+  if (128 % d.G && d.G % 128) return bad("G must divide 128 or be a multiple of 128");
+  if (d.F % d.G || d.H % d.G) return bad("G must divide F and H");
+  if (static_cast<int64_t>(d.F) * d.H >= (int64_t(1) << 31)) return bad("F*H too large");
+  return true;
+}
+
+LayerState::LayerState(const pw_layer_desc& d, uint64_t pool_bytes, EventOps* ev)
+    : desc(d), alloc(pool_bytes), evops_(ev) {
+  nrb_max = std::max(d.F, d.H) / d.R;
+  n_entries = static_cast<size_t>(d.E) * 3 * nrb_max;
+  mirror.assign(n_entries, pw_page_entry{0, 0, 0, PW_PAGE_ABSENT, 0, 0});
+  n_pages = static_cast<size_t>(d.E) * (2 * (d.F / d.R) + d.H / d.R);
+}
+
+LayerState::~LayerState() {
+  for (auto& kv : refs_) evops_->destroy(kv.first);
+}
+
+uint64_t LayerState::code_bytes(int proj, int bits) const {
+  const uint64_t rk = static_cast<uint64_t>(desc.R) * kdim(proj);
+  return bits == 16 ? 2 * rk : bits == 8 ? rk : rk / 2;
+}
+
+uint64_t LayerState::page_bytes(int proj, int bits) const {
+  const uint64_t sz = bits == 16 ? 0 : 4ull * desc.R * (kdim(proj) / desc.G);
+  return code_bytes(proj, bits) + sz;
+}
+
+bool LayerState::check_block(int e, int proj, int rb, std::string* err) const {
+  if (e < 0 || e >= desc.E) { *err = "expert index out of range"; return false; }
+  if (proj < 0 || proj > 2) { *err = "projection must be PW_GATE, PW_UP or PW_DOWN"; return false; }
+  if (rb < 0 || rb >= nrb(proj)) { *err = "row-block index out of range"; return false; }
+  return true;
+}
+
+pw_status LayerState::plan_load(int e, int proj, int rb, int bits, pw_page_entry* ent,
+                                std::string* err) {
+  if (!check_block(e, proj, rb, err)) return PW_EINVAL;
+  if (bits != 16 && bits != 8 && bits != 4) { *err = "bits must be 16, 8 or 4"; return PW_EINVAL; }
+  if (mirror[index(e, proj, rb)].bits != 0) { *err = "page already present"; return PW_EBUSY; }
+  uint64_t off = 0;
+  if (!alloc.alloc(page_bytes(proj, bits), &off)) { *err = "pool exhausted"; return PW_ENOMEM; }
+  ent->data_off = off;
+  ent->sz_off = bits == 16 ? 0 : off + code_bytes(proj, bits);
+  ent->bits = static_cast<uint8_t>(bits);
+  ent->state = PW_PAGE_RESIDENT;
+  ent->rsv = 0;
+  ent->gen = 1;
+  return PW_OK;
+}
+
+void LayerState::finish_load(int e, int proj, int rb, const pw_page_entry& ent) {
+  mirror[index(e, proj, rb)] = ent;
+  ++n_present;
+}
+
+void LayerState::abort_slot(const pw_page_entry& ent, int proj) {
+  alloc.release(ent.data_off, page_bytes(proj, ent.bits));
+}
+
+pw_status LayerState::plan_requant(int e, int proj, int rb, int new_bits, pw_page_entry* src,
+                                   pw_page_entry* dst, uint64_t* delta, std::string* err) {
+  *delta = 0;
+  if (!check_block(e, proj, rb, err)) return PW_EINVAL;
+  if (new_bits != 16 && new_bits != 8 && new_bits != 4) { *err = "bits must be 16, 8 or 4"; return PW_EINVAL; }
+  const pw_page_entry& cur = mirror[index(e, proj, rb)];
+  if (cur.bits == 0) { *err = "page not present"; return PW_ESTATE; }
+  if (cur.state == PW_PAGE_REQUANT_PENDING) { *err = "a requantization of this block is pending"; return PW_EBUSY; }
+  if (new_bits == cur.bits) return PW_OK;
+  if (new_bits > cur.bits) { *err = "raising a bitwidth needs a reload from host memory"; return PW_EUNSUPPORTED; }
+  uint64_t off = 0;
+  if (!alloc.alloc(page_bytes(proj, new_bits), &off)) { *err = "pool exhausted"; return PW_ENOMEM; }
+  *src = cur;
+  dst->data_off = off;
+  dst->sz_off = off + code_bytes(proj, new_bits);
+  dst->bits = static_cast<uint8_t>(new_bits);
+  dst->state = PW_PAGE_RESIDENT;
+  dst->rsv = 0;
+  dst->gen = cur.gen + 1;
+  *delta = page_bytes(proj, cur.bits) - page_bytes(proj, new_bits);
+  return PW_OK;
+}
+
+void LayerState::ref_event(void* ev) { ++refs_[ev]; }
+
+void LayerState::unref_event(void* ev) {
+  auto it = refs_.find(ev);
+  if (it == refs_.end()) return;
+  if (--it->second == 0) {
+    evops_->destroy(ev);
+    refs_.erase(it);
+  }
+}
+
+void LayerState::add_pending(int e, int proj, int rb, const pw_page_entry& dst, void* ev) {
+  const size_t idx = index(e, proj, rb);
+  mirror[idx].state = PW_PAGE_REQUANT_PENDING;
+  pending_.push_back(Pending{idx, proj, dst, ev});
+  ref_event(ev);
+}
+
+void LayerState::committed(void* commit_ev) {
+  for (const Pending& p : pending_) {
+    pw_page_entry& cur = mirror[p.idx];
+    retired_.push_back(Retired{cur.data_off, page_bytes(p.proj, cur.bits), commit_ev});
+    ref_event(commit_ev);
+    cur = p.next;
+    unref_event(p.ev);
+  }
+  pending_.clear();
+}
+
+uint64_t LayerState::reclaim() {
+  uint64_t freed = 0;
+  std::vector<Retired> keep;
+  for (const Retired& r : retired_) {
+    if (evops_->done(r.ev)) {
+      alloc.release(r.off, r.bytes);
+      freed += SlotAllocator::round_up(r.bytes);
+      unref_event(r.ev);
+    } else {
+      keep.push_back(r);
+    }
+  }
+  retired_.swap(keep);
+  return freed;
+}
+
+}  // namespace pw

@@ -1,0 +1,120 @@
+// Host-side state of a paged layer: the slot allocator inside the caller's
+// pool, the host mirror of the page table and the requant / commit / reclaim
+// protocol. Plain C++ with no HIP dependency: events are reached through the
+// EventOps interface, which the library backs with HIP events and the CPU
+// tests back with a simulated clock.
+//
+// Protocol (Sec. 3.1 offload order, Sec. 3.3 asynchronous page movement):
+//   requant   -> a fresh slot is allocated and filled on a side stream; the
+//                committed entry is unchanged (state REQUANT_PENDING);
+//   commit    -> after the requant's event, the new entry is published on the
+//                main stream; the old slot is retired, tagged with the commit
+//                event (its last possible reader precedes that event);
+//   reclaim   -> retired slots whose commit event completed go back to the
+//                free list, so the bytes Delta = M^b - M^b' (Eq. 3) become
+//                available to the caller (e.g. for KV-cache blocks).
+#pragma once
+
+#include <cstdint>
+#include <map>
+#include <string>
+#include <vector>
+
+#include "pw.h"
+
+namespace pw {
+
+constexpr uint64_t kSlotAlign = 256;
+
+// First-fit allocator over byte offsets [0, capacity), 256-byte granules,
+// coalescing neighbours on release.
+class SlotAllocator {
+ public:
+  explicit SlotAllocator(uint64_t capacity);
+  bool alloc(uint64_t bytes, uint64_t* off);
+  void release(uint64_t off, uint64_t bytes);
+  uint64_t capacity() const { return cap_; }
+  uint64_t used() const { return used_; }
+  uint64_t free_bytes() const { return cap_ - used_; }
+  uint64_t largest_free() const;
+  static uint64_t round_up(uint64_t b) { return (b + kSlotAlign - 1) / kSlotAlign * kSlotAlign; }
+
+ private:
+  std::map<uint64_t, uint64_t> free_;  // offset -> length
+  uint64_t cap_;
+  uint64_t used_ = 0;
+};
+
+struct EventOps {
+  virtual ~EventOps() {}
+  virtual void* create() = 0;          // nullptr on failure
+  virtual void destroy(void* ev) = 0;
+  virtual bool done(void* ev) = 0;     // true once the recorded work completed
+};
+
+class LayerState {
+ public:
+  LayerState(const pw_layer_desc& d, uint64_t pool_bytes, EventOps* ev);
+  ~LayerState();
+
+  static bool valid_desc(const pw_layer_desc& d, std::string* err);
+
+  const pw_layer_desc desc;
+  int nrb_max;
+  size_t n_entries;
+
+  size_t index(int e, int proj, int rb) const {
+    return (static_cast<size_t>(e) * 3 + proj) * nrb_max + rb;
+  }
+  int kdim(int proj) const { return proj == PW_DOWN ? desc.F : desc.H; }
+  int rows(int proj) const { return proj == PW_DOWN ? desc.H : desc.F; }
+  int nrb(int proj) const { return rows(proj) / desc.R; }
+  uint64_t code_bytes(int proj, int bits) const;   // bytes of values / codes
+  uint64_t page_bytes(int proj, int bits) const;   // Eq. 3's M^b
+
+  bool check_block(int e, int proj, int rb, std::string* err) const;
+  bool all_present() const { return n_present == n_pages; }
+
+  // Loading an absent page: reserve a slot and describe the new entry.
+  pw_status plan_load(int e, int proj, int rb, int bits, pw_page_entry* ent, std::string* err);
+  void finish_load(int e, int proj, int rb, const pw_page_entry& ent);
+  void abort_slot(const pw_page_entry& ent, int proj);
+
+  // Requantization to a lower bitwidth into a fresh slot.
+  pw_status plan_requant(int e, int proj, int rb, int new_bits, pw_page_entry* src,
+                         pw_page_entry* dst, uint64_t* delta, std::string* err);
+  void add_pending(int e, int proj, int rb, const pw_page_entry& dst, void* ev);
+
+  struct Pending {
+    size_t idx;
+    int proj;
+    pw_page_entry next;
+    void* ev;   // requant-done event (shared by a batch; reference counted)
+  };
+  struct Retired {
+    uint64_t off, bytes;
+    void* ev;   // commit event (shared; reference counted)
+  };
+
+  const std::vector<Pending>& pending() const { return pending_; }
+  // Publish all pending entries in the mirror; old slots retire on commit_ev.
+  void committed(void* commit_ev);
+  // Free retired slots whose event completed; returns bytes freed.
+  uint64_t reclaim();
+
+  void ref_event(void* ev);
+  void unref_event(void* ev);
+
+  std::vector<pw_page_entry> mirror;
+  SlotAllocator alloc;
+  size_t n_pages = 0;
+  size_t n_present = 0;
+
+ private:
+  EventOps* evops_;
+  std::vector<Pending> pending_;
+  std::vector<Retired> retired_;
+  std::map<void*, int> refs_;
+};
+
+}  // namespace pw

@@ -1,0 +1,150 @@
+"""Device buffers around the C ABI: a paged layer held in torch memory.
+
+PyTorch supplies device memory and streams only. Every computation (quantize,
+route, GEMM, combine, requant, commit) is a call into libpagedweight.so.
+"""
+from __future__ import annotations
+
+from typing import Dict, Iterable, List, Optional, Sequence, Tuple
+
+import numpy as np
+import torch
+
+from . import pw
+from .synth import DOWN, GATE, UP, LayerConfig
+
+ENTRY_BYTES = 24
+
+
+def _stream(s: Optional[torch.cuda.Stream] = None) -> int:
+    return (s or torch.cuda.current_stream()).cuda_stream
+
+
+def _aligned_empty(nbytes: int, device, align: int = 256) -> Tuple[torch.Tensor, int]:
+    """A uint8 device buffer and the first address in it aligned to ``align``."""
+    t = torch.empty(nbytes + align, dtype=torch.uint8, device=device)
+    p = t.data_ptr()
+    return t, (p + align - 1) // align * align
+
+
+class PagedLayer:
+    """One MoE layer whose expert weights live as pages in a device pool."""
+
+    def __init__(self, cfg: LayerConfig, pool_bytes: int, device="cuda"):
+        self.cfg = cfg
+        self.device = torch.device(device)
+        self.desc = pw.pw_layer_desc(cfg.E, cfg.H, cfg.F, cfg.R, cfg.G, cfg.act, cfg.sdt)
+        self.pool_bytes = int(pool_bytes)
+        self._pool_t, self.pool_ptr = _aligned_empty(self.pool_bytes, self.device)
+        self.n_entries = pw.pw_table_entries(self.desc)
+        self._table_t, self.table_ptr = _aligned_empty(self.n_entries * ENTRY_BYTES, self.device)
+        torch.cuda.synchronize(self.device)
+        self.handle = pw.pw_layer_create(self.desc, self.pool_ptr, self.pool_bytes, self.table_ptr)
+        self._ws = None
+        self._ws_ptr = 0
+        self._ws_bytes = 0
+
+    # -- construction ------------------------------------------------------
+    @staticmethod
+    def pool_bytes_for(cfg: LayerConfig, bits: Sequence[np.ndarray], slack: float = 0.0) -> int:
+        tot = 0
+        for p in (GATE, UP, DOWN):
+            for b in np.asarray(bits[p]).ravel():
+                tot += (pw.pw_page_bytes(cfg, p, int(b)) + 255) // 256 * 256
+        return int(tot * (1.0 + slack)) + 256
+
+    def load_pages(self, w16: Sequence[np.ndarray], bits: Sequence[np.ndarray],
+                   order: Iterable[Tuple[int, int, int]], stream=None):
+        """Upload the 16-bit weights and place every page at its bitwidth.
+
+        ``w16[p]`` is the [E, rows, cols] uint16 array of projection p; pages
+        are placed in ``order`` (which fixes their pool addresses).
+        """
+        st = _stream(stream)
+        cfg = self.cfg
+        dev = []
+        for p in (GATE, UP, DOWN):
+            dev.append(torch.from_numpy(np.ascontiguousarray(w16[p]).view(np.int16)).to(self.device))
+        for (e, p, rb) in order:
+            rows, cols = w16[p].shape[1:]
+            off = ((e * rows + rb * cfg.R) * cols) * 2
+            pw.pw_layer_load_page(self.handle, e, p, rb, int(bits[p][e, rb]), dev[p].data_ptr() + off, st)
+        torch.cuda.current_stream().synchronize() if stream is None else stream.synchronize()
+        del dev
+
+    # -- hot path ------------------------------------------------------------
+    def route(self, logits: torch.Tensor, K: int, renorm: int = 1, stream=None):
+        T, E = logits.shape
+        dev = logits.device
+        ids = torch.empty((T, K), dtype=torch.int32, device=dev)
+        w = torch.empty((T, K), dtype=torch.float32, device=dev)
+        offsets = torch.empty(E + 1, dtype=torch.int32, device=dev)
+        ss = torch.empty(max(T * K, 1), dtype=torch.int32, device=dev)
+        sp = torch.empty(max(T * K, 1), dtype=torch.int32, device=dev)
+        pw.pw_route_topk(logits.data_ptr(), T, E, K, renorm, ids.data_ptr(), w.data_ptr(),
+                         offsets.data_ptr(), ss.data_ptr(), sp.data_ptr(), _stream(stream))
+        return ids, w, offsets, ss, sp
+
+    def workspace(self, T: int, K: int) -> Tuple[int, int]:
+        need = pw.pw_workspace_bytes(self.handle, T, K)
+        if need > self._ws_bytes:
+            self._ws, self._ws_ptr = _aligned_empty(need, self.device)
+            self._ws_bytes = need
+        return self._ws_ptr, self._ws_bytes
+
+    def forward(self, x: torch.Tensor, routing, out_fp32: bool = False, y: torch.Tensor = None,
+                stream=None) -> torch.Tensor:
+        ids, w, offsets, ss, sp = routing
+        T, K = ids.shape
+        if y is None:
+            y = torch.empty((T, self.cfg.H), dtype=torch.float32 if out_fp32 else torch.int16,
+                            device=x.device)
+        ws_ptr, ws_bytes = self.workspace(T, K)
+        pw.pw_moe_paged_gemm(self.handle, x.data_ptr(), T, K, w.data_ptr(), offsets.data_ptr(),
+                             ss.data_ptr(), sp.data_ptr(), y.data_ptr(), int(out_fp32),
+                             ws_ptr, ws_bytes, _stream(stream))
+        return y
+
+    # -- runtime downshift -------------------------------------------------
+    def requant(self, blocks: Sequence[Tuple[int, int, int]], new_bits: int, stream=None) -> int:
+        if not blocks:
+            return 0
+        es, ps, rbs = zip(*blocks)
+        return pw.pw_requant_blocks(self.handle, list(es), list(ps), list(rbs),
+                                    [new_bits] * len(blocks), _stream(stream))
+
+    def commit(self, stream=None) -> int:
+        return pw.pw_commit(self.handle, _stream(stream))
+
+    def reclaim(self) -> int:
+        return pw.pw_reclaim(self.handle)
+
+    # -- inspection --------------------------------------------------------
+    def entry(self, e: int, p: int, rb: int) -> pw.pw_page_entry:
+        return pw.pw_page_info(self.handle, e, p, rb)
+
+    def page_image(self, e: int, p: int, rb: int) -> np.ndarray:
+        """The page's bytes as stored in the pool (host copy)."""
+        ent = self.entry(e, p, rb)
+        n = pw.pw_page_bytes(self.desc, p, int(ent.bits))
+        base = self.pool_ptr - self._pool_t.data_ptr() + ent.data_off
+        return self._pool_t[base:base + n].cpu().numpy()
+
+    def device_table(self) -> np.ndarray:
+        off = self.table_ptr - self._table_t.data_ptr()
+        return self._table_t[off:off + self.n_entries * ENTRY_BYTES].cpu().numpy()
+
+    def stats(self):
+        return pw.pw_pool_stats(self.handle)
+
+    def close(self):
+        if self.handle:
+            torch.cuda.synchronize(self.device)
+            pw.pw_layer_destroy(self.handle)
+            self.handle = 0
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,181 @@
+"""GPU parity against the CPU oracle, through the C ABI.
+
+Bit-exact: quantized codes, scales and zeros (as pool bytes), routing ids,
+offsets, sorted slots and slot positions. Tolerance: routing weights 1e-6
+absolute; layer output max|y - r| / max|r| <= 2e-2 for the 16-bit output
+against the oracle (fp64, unrounded SwiGLU output) and <= 1e-3 for the fp32
+output against the oracle with the SwiGLU output rounded to the activation
+dtype (the kernel's own rounding point).
+"""
+import numpy as np
+import pytest
+
+import oracle
+from helpers import case, gpu_layer, oracle_layer, rel_err, say, to_dev, to_dev16, y16_values
+from paper_2607_16184_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+TOL16 = 2e-2
+TOL32 = 1e-3
+WTOL = 1e-6
+
+
+def _route_check(logits, K, renorm=1):
+    import torch
+    from paper_2607_16184_amd import pw
+    from paper_2607_16184_amd.layer import PagedLayer
+    T, E = logits.shape
+    lg = to_dev(logits)
+    ids = torch.empty((T, K), dtype=torch.int32, device="cuda")
+    w = torch.empty((T, K), dtype=torch.float32, device="cuda")
+    off = torch.empty(E + 1, dtype=torch.int32, device="cuda")
+    ss = torch.empty(max(T * K, 1), dtype=torch.int32, device="cuda")
+    sp = torch.empty(max(T * K, 1), dtype=torch.int32, device="cuda")
+    pw.pw_route_topk(lg.data_ptr(), T, E, K, renorm, ids.data_ptr(), w.data_ptr(), off.data_ptr(),
+                     ss.data_ptr(), sp.data_ptr(), torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    oid, ow = oracle.route(logits, K, renorm)
+    cnt, ooff, oss, osp = oracle.permute(oid, E)
+    assert np.array_equal(ids.cpu().numpy(), oid)
+    assert np.abs(w.cpu().numpy() - ow).max() <= WTOL
+    assert np.array_equal(off.cpu().numpy(), ooff)
+    assert np.array_equal(ss.cpu().numpy()[:T * K], oss)
+    assert np.array_equal(sp.cpu().numpy()[:T * K], osp)
+
+
+@pytest.mark.parametrize("name", ["tiny", "mixtral_decode", "mixtral_prefill", "finegrained"])
+def test_route_bit_exact(name):
+    cfg = synth.CONFIGS[name]
+    say("route %s T=%d E=%d K=%d" % (name, cfg.T, cfg.E, cfg.K))
+    _route_check(synth.logits(cfg), cfg.K)
+
+
+def test_route_edge_cases():
+    rng = np.random.default_rng(5)
+    say("route edge cases")
+    lg = rng.standard_normal((300, 8)).astype(np.float32)
+    lg[:100, :4] = 0.25                         # ties go to the lower index
+    _route_check(lg, 2)
+    _route_check(lg, 8)                         # K = E
+    _route_check(lg, 2, renorm=0)
+    _route_check(np.zeros((5, 16), np.float32), 3)
+    _route_check(rng.standard_normal((1, 64)).astype(np.float32), 6)
+    _route_check(rng.standard_normal((3000, 256)).astype(np.float32), 16)   # several permute chunks
+
+
+def _check_pages(L, O, pages):
+    for (e, p, rb) in pages:
+        got = L.page_image(e, p, rb)
+        want = O.page_image(p, e, rb)
+        assert got.size == want.size
+        if not np.array_equal(got, want):
+            b = int(O.bits[p][e, rb])
+            R, K = O.R, O.w16[p].shape[2]
+            gc, gs, gz = oracle.decode_page(got, R, K, O.G, b)
+            _, wc, ws, wz = O.page(p, e, rb)
+            raise AssertionError("page %s bits %d: codes %d, scales %d, zeros %d mismatches" % (
+                (e, p, rb), b, (gc != wc).sum(), (gs != ws).sum(), (gz != wz).sum()))
+
+
+def test_tiny_quantized_pages_bit_exact():
+    cfg, w16, bits, order = case("tiny")
+    say("tiny: load %d pages" % len(order))
+    L = gpu_layer(cfg, w16, bits, order)
+    O = oracle_layer(cfg, w16, bits)
+    _check_pages(L, O, order)
+    L.close()
+
+
+@pytest.mark.parametrize("src,dst", [(16, 8), (16, 4), (8, 4)])
+def test_tiny_requant_bit_exact(src, dst):
+    import torch
+    cfg, w16, _, order = case("tiny")
+    bits = [np.full((cfg.E, cfg.nrb(p)), src, np.int32) for p in range(3)]
+    say("tiny requant %d->%d" % (src, dst))
+    L = gpu_layer(cfg, w16, bits, order, slack=1.0)
+    O = oracle_layer(cfg, w16, bits)
+    blocks = [pg for i, pg in enumerate(order) if i % 3 == 0]
+    side = torch.cuda.Stream()
+    delta = L.requant(blocks, dst, stream=side)
+    want = 0
+    for (e, p, rb) in blocks:
+        want += O.requant(p, e, rb, dst)
+    assert delta == want
+    assert L.commit() == len(blocks)
+    torch.cuda.synchronize()
+    _check_pages(L, O, order)
+    assert L.reclaim() > 0
+    L.close()
+
+
+def _forward_parity(cfg, L, O, x16, logits, tokens=None):
+    import torch
+    routing = L.route(to_dev(logits), cfg.K)
+    x = to_dev16(x16)
+    y16 = L.forward(x, routing)
+    y32 = L.forward(x, routing, out_fp32=True)
+    torch.cuda.synchronize()
+    ids, w = oracle.route(logits, cfg.K)
+    r1 = O.forward(x16, ids, w, h_round=False, tokens=tokens)
+    r2 = O.forward(x16, ids, w, h_round=True, tokens=tokens)
+    sel = slice(None) if tokens is None else list(tokens)
+    e16 = rel_err(y16_values(y16, cfg.act)[sel], r1[sel])
+    e32 = rel_err(y32.cpu().numpy()[sel], r2[sel])
+    return e16, e32, y16, y32
+
+
+def test_tiny_forward_parity():
+    cfg, w16, bits, order = case("tiny")
+    say("tiny forward")
+    L = gpu_layer(cfg, w16, bits, order)
+    O = oracle_layer(cfg, w16, bits)
+    e16, e32, y16, y32 = _forward_parity(cfg, L, O, synth.activations(cfg), synth.logits(cfg))
+    assert e16 <= TOL16, e16
+    assert e32 <= TOL32, e32
+    L.close()
+
+
+@pytest.mark.parametrize("b", [16, 8, 4])
+def test_tiny_uniform_bitwidth(b):
+    """Every block at one bitwidth: the same kernel, a uniform configuration."""
+    cfg, w16, _, order = case("tiny")
+    bits = [np.full((cfg.E, cfg.nrb(p)), b, np.int32) for p in range(3)]
+    say("tiny uniform %d" % b)
+    L = gpu_layer(cfg, w16, bits, order)
+    O = oracle_layer(cfg, w16, bits)
+    e16, e32, _, _ = _forward_parity(cfg, L, O, synth.activations(cfg), synth.logits(cfg))
+    assert e16 <= TOL16 and e32 <= TOL32, (e16, e32)
+    L.close()
+
+
+def test_tiny_deterministic_and_pool_order_invariant():
+    import torch
+    cfg, w16, bits, order = case("tiny")
+    say("tiny determinism / pool order")
+    L1 = gpu_layer(cfg, w16, bits, order)
+    L2 = gpu_layer(cfg, w16, bits, list(reversed(order)))
+    x = to_dev16(synth.activations(cfg))
+    r1 = L1.route(to_dev(synth.logits(cfg)), cfg.K)
+    a = L1.forward(x, r1, out_fp32=True).clone()
+    b = L1.forward(x, r1, out_fp32=True).clone()
+    c = L2.forward(x, r1, out_fp32=True).clone()
+    torch.cuda.synchronize()
+    assert torch.equal(a, b) and torch.equal(a, c)
+    assert L1.entry(0, 0, 0).data_off != L2.entry(0, 0, 0).data_off or \
+        L1.entry(cfg.E - 1, 2, 0).data_off != L2.entry(cfg.E - 1, 2, 0).data_off
+    L1.close()
+    L2.close()
+
+
+def test_zero_up_projection_gives_zero():
+    import torch
+    cfg, w16, bits, order = case("tiny")
+    w16 = list(w16)
+    w16[1] = np.zeros_like(w16[1])
+    say("tiny zero up")
+    L = gpu_layer(cfg, w16, [np.full_like(b, 16) for b in bits], order)
+    y = L.forward(to_dev16(synth.activations(cfg)), L.route(to_dev(synth.logits(cfg)), cfg.K), out_fp32=True)
+    torch.cuda.synchronize()
+    assert not y.cpu().numpy().any()
+    L.close()

@@ -1,0 +1,200 @@
+"""Host-side protocol on the CPU: slot allocator, page-table mirror and the
+requant -> commit -> reclaim order (Sec. 3.1 offload: the lower bitwidth is
+committed before the old pages are freed; Sec. 3.3: commits at safe
+boundaries), driven by a simulated event clock. Errors leave state unchanged.
+"""
+import ctypes
+import os
+
+import pytest
+
+import oracle
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIBP = os.path.join(os.path.dirname(HERE), "paper_2607_16184_amd", "libpw_hosttest.so")
+
+
+class Entry(ctypes.Structure):
+    _fields_ = [("data_off", ctypes.c_uint64), ("sz_off", ctypes.c_uint64), ("bits", ctypes.c_uint8),
+                ("state", ctypes.c_uint8), ("rsv", ctypes.c_uint16), ("gen", ctypes.c_uint32)]
+
+
+class Desc(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int) for n in ("E", "H", "F", "R", "G", "act", "sdt")]
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(LIBP):
+        from paper_2607_16184_amd import build
+        build.build_hosttest()
+    lib = ctypes.CDLL(LIBP)
+    lib.pwt_create.restype = ctypes.c_void_p
+    lib.pwt_create.argtypes = [ctypes.POINTER(Desc), ctypes.c_uint64]
+    lib.pwt_destroy.argtypes = [ctypes.c_void_p]
+    lib.pwt_load.argtypes = [ctypes.c_void_p] + [ctypes.c_int] * 4
+    ip = ctypes.POINTER(ctypes.c_int)
+    lib.pwt_requant.argtypes = [ctypes.c_void_p, ctypes.c_int, ip, ip, ip, ip,
+                                ctypes.POINTER(ctypes.c_uint64), ctypes.POINTER(ctypes.c_uint64)]
+    lib.pwt_commit.restype = ctypes.c_uint64
+    lib.pwt_commit.argtypes = [ctypes.c_void_p, ip]
+    lib.pwt_complete.argtypes = [ctypes.c_void_p, ctypes.c_uint64]
+    lib.pwt_reclaim.restype = ctypes.c_uint64
+    lib.pwt_reclaim.argtypes = [ctypes.c_void_p]
+    lib.pwt_entry.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.POINTER(Entry)]
+    u64p = ctypes.POINTER(ctypes.c_uint64)
+    lib.pwt_stats.argtypes = [ctypes.c_void_p, u64p, u64p, u64p, u64p]
+    lib.pwt_all_present.argtypes = [ctypes.c_void_p]
+    lib.pwt_last_error.restype = ctypes.c_char_p
+    return lib
+
+
+R, G, E, H, F = 64, 64, 2, 256, 512
+
+
+class Layer:
+    def __init__(self, lib, pool_bytes):
+        self.lib = lib
+        self.h = lib.pwt_create(ctypes.byref(Desc(E, H, F, R, G, 1, 1)), pool_bytes)
+        assert self.h
+
+    def load(self, e, p, rb, b):
+        return self.lib.pwt_load(self.h, e, p, rb, b)
+
+    def requant(self, blocks, nb):
+        n = len(blocks)
+        arr = ctypes.c_int * max(n, 1)
+        es, ps, rbs = (zip(*blocks) if n else ((), (), ()))
+        d, ev = ctypes.c_uint64(), ctypes.c_uint64()
+        st = self.lib.pwt_requant(self.h, n, arr(*es), arr(*ps), arr(*rbs), arr(*([nb] * n)),
+                                  ctypes.byref(d), ctypes.byref(ev))
+        return st, d.value, ev.value
+
+    def commit(self):
+        n = ctypes.c_int()
+        ev = self.lib.pwt_commit(self.h, ctypes.byref(n))
+        return n.value, ev
+
+    def entry(self, e, p, rb):
+        x = Entry()
+        assert self.lib.pwt_entry(self.h, e, p, rb, ctypes.byref(x)) == 0
+        return x
+
+    def stats(self):
+        v = [ctypes.c_uint64() for _ in range(4)]
+        self.lib.pwt_stats(self.h, *[ctypes.byref(x) for x in v])
+        return [x.value for x in v]
+
+    def close(self):
+        self.lib.pwt_destroy(self.h)
+
+
+def pages():
+    return [(e, p, rb) for e in range(E) for p in range(3) for rb in range((F if p < 2 else H) // R)]
+
+
+def _load_all(Lx, bits=16):
+    for (e, p, rb) in pages():
+        assert Lx.load(e, p, rb, bits) == 0
+
+
+def test_allocator_and_load(L):
+    need = sum(oracle.page_bytes(R, H if p < 2 else F, G, 16) for (_, p, _) in pages())
+    Lx = Layer(L, need)
+    _load_all(Lx)
+    assert L.pwt_all_present(Lx.h) == 1
+    used, free, largest, _ = Lx.stats()
+    assert used == need and free == 0
+    assert Lx.load(0, 0, 0, 16) == 3          # PW_EBUSY: already present
+    offs = sorted((Lx.entry(*pg).data_off, oracle.page_bytes(R, H if pg[1] < 2 else F, G, 16))
+                  for pg in pages())
+    for (a, n), (b, _) in zip(offs, offs[1:]):
+        assert a + n <= b                     # slots never overlap
+    Lx.close()
+
+
+def test_pool_exhaustion_leaves_state_unchanged(L):
+    Lx = Layer(L, 4 * 65536)
+    assert Lx.load(0, 0, 0, 16) == 0          # 32 KiB
+    before = Lx.stats()
+    st, d, ev = Lx.requant([(0, 0, 0)], 8)
+    assert st == 0
+    Lx2 = Layer(L, oracle.page_bytes(R, H, G, 16))
+    assert Lx2.load(0, 0, 0, 16) == 0
+    assert Lx2.load(0, 0, 1, 4) == 2          # PW_ENOMEM
+    st, d, ev = Lx2.requant([(0, 0, 0)], 4)
+    assert st == 2 and Lx2.entry(0, 0, 0).bits == 16 and Lx2.entry(0, 0, 0).state == 1
+    Lx.close()
+    Lx2.close()
+
+
+def test_requant_commit_reclaim_order(L):
+    need = sum(oracle.page_bytes(R, H if p < 2 else F, G, 16) for (_, p, _) in pages())
+    Lx = Layer(L, 2 * need)
+    _load_all(Lx)
+    old = Lx.entry(1, 2, 3)
+    free0 = Lx.stats()[1]
+    st, delta, ev = Lx.requant([(1, 2, 3)], 4)
+    assert st == 0 and delta == oracle.delta_bytes(R, F, G, 16, 4)
+    cur = Lx.entry(1, 2, 3)
+    # offload: nothing is published before the commit
+    assert (cur.bits, cur.data_off, cur.state) == (16, old.data_off, 2)
+    assert Lx.requant([(1, 2, 3)], 8)[0] == 3  # PW_EBUSY while pending
+    n, cev = Lx.commit()
+    assert n == 1 and cev != 0
+    cur = Lx.entry(1, 2, 3)
+    assert cur.bits == 4 and cur.gen == old.gen + 1 and cur.data_off != old.data_off and cur.state == 1
+    # the old slot is retired, not freed, until the commit has completed
+    assert L.pwt_reclaim(Lx.h) == 0
+    L.pwt_complete(Lx.h, cev)
+    assert L.pwt_reclaim(Lx.h) == oracle.page_bytes(R, F, G, 16)
+    assert Lx.stats()[1] - free0 == delta      # Eq. 3: the pool gained exactly Delta
+    assert Lx.stats()[3] == 0                  # every event released
+    Lx.close()
+
+
+def test_requant_rules(L):
+    need = sum(oracle.page_bytes(R, H if p < 2 else F, G, 16) for (_, p, _) in pages())
+    Lx = Layer(L, 2 * need)
+    _load_all(Lx, bits=8)
+    st, d, ev = Lx.requant([(0, 0, 0)], 8)     # same bits: no-op
+    assert st == 0 and d == 0 and ev == 0 and Lx.commit()[0] == 0
+    assert Lx.requant([(0, 0, 0)], 16)[0] == 4  # raising: PW_EUNSUPPORTED
+    assert Lx.requant([(0, 0, 0)], 5)[0] == 1
+    assert Lx.requant([(0, 0, 0), (0, 0, 0)], 4)[0] == 1   # duplicate in a batch
+    assert Lx.requant([(0, 0, 99)], 4)[0] == 1
+    free0 = Lx.stats()[1]
+    # a failing batch rolls back the slots of the earlier blocks
+    assert Lx.requant([(0, 0, 0), (0, 1, 0), (5, 0, 0)], 4)[0] == 1
+    assert Lx.stats()[1] == free0 and Lx.entry(0, 0, 0).state == 1
+    st, d, ev = Lx.requant([(0, 0, 0), (1, 2, 0)], 4)
+    assert st == 0 and d == oracle.delta_bytes(R, H, G, 8, 4) + oracle.delta_bytes(R, F, G, 8, 4)
+    n, cev = Lx.commit()
+    assert n == 2
+    L.pwt_complete(Lx.h, cev)
+    assert L.pwt_reclaim(Lx.h) == oracle.page_bytes(R, H, G, 8) + oracle.page_bytes(R, F, G, 8)
+    assert Lx.stats()[1] - free0 == d
+    Lx.close()
+
+
+def test_allocator_coalesces(L):
+    one = oracle.page_bytes(R, H, G, 16)
+    Lx = Layer(L, 3 * one)
+    for rb in range(3):
+        assert Lx.load(0, 0, rb, 16) == 0
+    for rb in range(3):
+        st, _, _ = Lx.requant([(0, 0, rb)], 4)
+        assert st == 2                          # pool full: ENOMEM, nothing changed
+    Lx.close()
+    Lx = Layer(L, 4 * one)
+    for rb in range(3):
+        assert Lx.load(0, 0, rb, 16) == 0
+    for rb in (0, 2, 1):
+        assert Lx.requant([(0, 0, rb)], 4)[0] == 0
+        n, cev = Lx.commit()
+        L.pwt_complete(Lx.h, cev)
+        Lx.reclaim = L.pwt_reclaim(Lx.h)
+    used, free, largest, _ = Lx.stats()
+    assert used == 3 * ((oracle.page_bytes(R, H, G, 4) + 255) // 256 * 256)
+    assert largest >= 2 * one                  # freed neighbours merged
+    Lx.close()
