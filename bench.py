@@ -1,0 +1,226 @@
+"""Benchmark of the paged mixed-bitwidth MoE layer on one MI355X.
+
+A step is one pass of the whole hot path over one batch: route (top-K and
+token permutation), paged gate/up GEMM + SwiGLU, paged down GEMM, combine.
+Inputs are seeded synthetic tensors already resident in HBM.
+
+Default workload: the Mixtral-shaped decode layer (8 experts, top-2,
+H=4096, F=14336, 64 tokens bf16, 128-row pages with 50% 16-bit / 25% int8 /
+25% int4, group 128, pool order shuffled). The metric is weight-read HBM
+GB/s: bytes of every page (codes plus scale/zero) of the experts with routed
+tokens, per step, divided by the step time.
+
+One JSON line is printed on stdout. ``--gpus`` above 1 is refused: this build
+runs on one GPU.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "paged mixed-bit MoE layer: weight-read HBM GB/s (decode), MFMA % (prefill)"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+MFMA_PEAK_BF16 = 2.5166e15     # dense bf16 MFMA, flop/s (256 CU x 2.4 GHz x 4096)
+KERNEL_SRC = os.path.join(ROOT, "paper_2607_16184_amd", "csrc", "pw_kernels.hip")
+
+
+def log(msg):
+    sys.stderr.write("[bench] %s\n" % msg)
+    sys.stderr.flush()
+
+
+def kernel_hash():
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def describe(cfg):
+    mix = "iid{16,8,4}" if cfg.mix is None else "%d/%d/%d%% 16-bit/int8/int4" % tuple(round(100 * m) for m in cfg.mix)
+    return ("%s: %d experts top-%d, H=%d, F=%d, %d tokens %s, %d-row pages %s, G=%d, shuffled pool"
+            % (cfg.name, cfg.E, cfg.K, cfg.H, cfg.F, cfg.T, "bf16" if cfg.act else "fp16", cfg.R, mix, cfg.G))
+
+
+def page_bytes_active(cfg, bits, counts):
+    from paper_2607_16184_amd import pw
+    per = {}
+    for p in range(3):
+        tot = 0
+        for e in range(cfg.E):
+            if counts[e] == 0:
+                continue
+            for b in bits[p][e]:
+                tot += pw.pw_page_bytes(cfg, p, int(b))
+        per[p] = tot
+    return per
+
+
+def build_layer(cfg):
+    import numpy as np
+    from paper_2607_16184_amd import synth
+    from paper_2607_16184_amd.layer import PagedLayer
+    t0 = time.time()
+    w16 = [synth.expert_weights(cfg, p) for p in range(3)]
+    bits = synth.bitmap(cfg)
+    L = PagedLayer(cfg, PagedLayer.pool_bytes_for(cfg, bits, slack=0.0))
+    L.load_pages(w16, bits, synth.pool_order(cfg))
+    log("%s: weights generated and paged in %.1f s" % (cfg.name, time.time() - t0))
+    return L, w16, bits
+
+
+def time_steps(L, cfg, x, logits, steps, warmup):
+    """Warm up, then time exactly `steps` steps; per-kernel HIP-event times."""
+    import torch
+    from paper_2607_16184_amd import pw
+    from paper_2607_16184_amd.layer import PagedLayer
+    rbuf = PagedLayer.routing_buffers(cfg.T, cfg.E, cfg.K)
+    y = torch.empty((cfg.T, cfg.H), dtype=torch.int16, device="cuda")
+
+    def step():
+        routing = L.route(logits, cfg.K, out=rbuf)
+        L.forward(x, routing, y=y)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    pw.pw_profile_read(L.handle, reset=True)
+    pw.pw_profile_enable(L.handle, True)
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record()
+    for _ in range(steps):
+        step()
+    ev1.record()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    pw.pw_profile_enable(L.handle, False)
+    ms, cnt = pw.pw_profile_read(L.handle, reset=True)
+    per_kernel = {name: (ms[i] / cnt[i] if cnt[i] else None)
+                  for i, name in enumerate(("gateup", "down", "combine", "requant"))}
+    counts = (rbuf[2][1:] - rbuf[2][:-1]).cpu().numpy()
+    return {"wall_ms": (t1 - t0) * 1e3 / steps, "event_ms": ev0.elapsed_time(ev1) / steps,
+            "kernel_ms": per_kernel, "counts": counts}
+
+
+def traffic_for(kernel, workload, algo_bytes):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if they were
+    taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", "traffic_%s_%s.json" % (kernel, workload))
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("kernel_sha256_16") != kernel_hash():
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def cpu_baseline(cfg, w16, bits, logits_np, x16, weight_bytes, budget_s=20.0):
+    """The oracle, timed on this host on a bounded sample of the step's tokens."""
+    import numpy as np
+    import oracle
+    t0 = time.time()
+    O = oracle.OracleLayer(cfg.E, cfg.H, cfg.F, cfg.R, cfg.G, cfg.act, cfg.sdt, w16, bits)
+    log("oracle layer built in %.1f s" % (time.time() - t0))
+    ids, w = oracle.route(logits_np, cfg.K)
+    done, spent = 0, 0.0
+    chunk = 1
+    while done < cfg.T and spent < budget_s:
+        toks = list(range(done, min(cfg.T, done + chunk)))
+        t = time.perf_counter()
+        O.forward(x16, ids, w, tokens=toks)
+        spent += time.perf_counter() - t
+        done += len(toks)
+        chunk = min(chunk * 2, 8)
+    step_s = spent * cfg.T / done
+    return {"value": weight_bytes / step_s / 1e9, "unit": "GB/s", "cores": oracle.threads(),
+            "kind": "oracle",
+            "sample": "oracle forward (fp64, OpenMP) of %d of the %d tokens of one step, scaled to "
+                      "the full step (%.2f s measured, %.1f s per step)" % (done, cfg.T, spent, step_s)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="mixtral_decode")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        sys.stderr.write("bench.py runs on one GPU only: the paged MoE hot path here is a "
+                         "single-GPU build (no collectives); --gpus %d is not supported.\n" % args.gpus)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2607_16184_amd import synth
+
+    if not torch.cuda.is_available():
+        sys.stderr.write("bench.py needs a GPU\n")
+        sys.exit(1)
+    cfg = synth.CONFIGS[args.workload]
+    L, w16, bits = build_layer(cfg)
+    logits_np = synth.logits(cfg)
+    x16 = synth.activations(cfg)
+    logits = torch.from_numpy(logits_np).cuda()
+    x = torch.from_numpy(x16.view(np.int16)).cuda()
+    r = time_steps(L, cfg, x, logits, args.steps, args.warmup)
+    per = page_bytes_active(cfg, bits, r["counts"])
+    wbytes = per[0] + per[1] + per[2]
+    ms = r["event_ms"]
+    value = wbytes / (ms * 1e-3) / 1e9
+    S = cfg.T * cfg.K
+    # dominant kernel: the gate/up GEMM. Algorithmic bytes per launch: its pages
+    # (codes + scale/zero) of active experts, the activations read and the
+    # SwiGLU output written.
+    gu_ms = r["kernel_ms"]["gateup"]
+    gu_bytes = per[0] + per[1] + cfg.T * cfg.H * 2 + S * cfg.F * 2
+    achieved = gu_bytes / (gu_ms * 1e-3) / 1e9
+    dn_ms = r["kernel_ms"]["down"]
+    dn_bytes = per[2] + S * cfg.F * 2 + S * cfg.H * 4
+    flops = 6.0 * S * cfg.H * cfg.F
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if cfg.act else "f16",
+        "data": "synthetic",
+        "config": {"workload": describe(cfg), "tokens": cfg.T, "experts": cfg.E, "top_k": cfg.K,
+                   "hidden": cfg.H, "ffn": cfg.F, "page_rows": cfg.R, "group": cfg.G,
+                   "weight_bytes_per_step": int(wbytes)},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": traffic_for("gateup", cfg.name, gu_bytes),
+                     "kernel": "k_gateup (paged gate/up GEMM + SwiGLU)",
+                     "algorithmic_bytes_per_launch": int(gu_bytes), "avg_launch_ms": round(gu_ms, 4)},
+        "kernels": {
+            "gateup_ms": round(gu_ms, 4), "down_ms": round(dn_ms, 4),
+            "combine_ms": round(r["kernel_ms"]["combine"], 4),
+            "down_GBps": round(dn_bytes / (dn_ms * 1e-3) / 1e9, 1),
+            "gemm_weight_GBps": round((per[0] + per[1] + per[2]) / ((gu_ms + dn_ms) * 1e-3) / 1e9, 1),
+            "mfma_frac": round(flops / ((gu_ms + dn_ms) * 1e-3) / MFMA_PEAK_BF16, 5),
+            "wall_ms_per_step": round(r["wall_ms"], 4),
+        },
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(cfg, w16, bits, logits_np, x16, wbytes)
+    L.close()
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

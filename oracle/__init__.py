@@ -82,6 +82,7 @@ def lib():
         [_c_u16p] + [ctypes.c_int] * 9 + [_c_i32p, _c_f64p]
         + [_c_u16p, _c_i32p, _c_u8p, _c_u16p, _c_u16p] * 3
         + [ctypes.c_int, _c_i32p, ctypes.c_int, _c_f64p])
+    L.or_threads.restype = ctypes.c_int
     L.or_init()
     _lib = L
     return L
@@ -233,6 +234,11 @@ def permute(ids: np.ndarray, E: int):
     sp = np.zeros(S, np.int32)
     lib().or_permute(ids, T, K, E, counts, offsets, ss, sp)
     return counts, offsets, ss, sp
+
+
+def threads() -> int:
+    """OpenMP threads the oracle's parallel loops use."""
+    return int(lib().or_threads())
 
 
 def routing_mass(ids: np.ndarray, w: np.ndarray, E: int) -> np.ndarray:

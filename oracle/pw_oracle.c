@@ -29,6 +29,9 @@
  * Build: gcc -O2 -std=c11 -fPIC -shared -fopenmp -ffp-contract=off
  */
 #include <math.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -144,6 +147,15 @@ uint16_t or_round_nearest16(double x, int fmt) {
     if (db < da) return g_tab[fmt][i + 1].bits;
     /* exact tie: the pattern with an even last fraction bit */
     return (g_tab[fmt][i].bits & 1) ? g_tab[fmt][i + 1].bits : g_tab[fmt][i].bits;
+}
+
+/* Threads an OpenMP region of the oracle uses (1 without OpenMP). */
+int or_threads(void) {
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
 }
 
 /* Build the lookup tables of both formats (call once before any threads). */

@@ -73,14 +73,18 @@ class PagedLayer:
         del dev
 
     # -- hot path ------------------------------------------------------------
-    def route(self, logits: torch.Tensor, K: int, renorm: int = 1, stream=None):
+    @staticmethod
+    def routing_buffers(T: int, E: int, K: int, device="cuda"):
+        """(ids [T,K], w [T,K], offsets [E+1], sorted_slot [S], slot_pos [S])."""
+        return (torch.empty((T, K), dtype=torch.int32, device=device),
+                torch.empty((T, K), dtype=torch.float32, device=device),
+                torch.empty(E + 1, dtype=torch.int32, device=device),
+                torch.empty(max(T * K, 1), dtype=torch.int32, device=device),
+                torch.empty(max(T * K, 1), dtype=torch.int32, device=device))
+
+    def route(self, logits: torch.Tensor, K: int, renorm: int = 1, stream=None, out=None):
         T, E = logits.shape
-        dev = logits.device
-        ids = torch.empty((T, K), dtype=torch.int32, device=dev)
-        w = torch.empty((T, K), dtype=torch.float32, device=dev)
-        offsets = torch.empty(E + 1, dtype=torch.int32, device=dev)
-        ss = torch.empty(max(T * K, 1), dtype=torch.int32, device=dev)
-        sp = torch.empty(max(T * K, 1), dtype=torch.int32, device=dev)
+        ids, w, offsets, ss, sp = out if out is not None else self.routing_buffers(T, E, K, logits.device)
         pw.pw_route_topk(logits.data_ptr(), T, E, K, renorm, ids.data_ptr(), w.data_ptr(),
                          offsets.data_ptr(), ss.data_ptr(), sp.data_ptr(), _stream(stream))
         return ids, w, offsets, ss, sp
