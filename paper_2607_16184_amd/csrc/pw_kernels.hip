@@ -437,238 +437,298 @@ __device__ __forceinline__ u32x4 sz_load(const uint8_t* szrow, int g, int R) {
   return ld16(szrow + static_cast<size_t>(g) * R * 4);
 }
 
-template <int B>
-struct Proj {
+// ---------------------------------------------------------------------------
+// Paged GEMM core: one wave streams 16 rows of one page over a K range.
+//
+// K is processed in chunks of kCK 128-blocks. The activation tile of a chunk
+// (NT*16 slots x kCK*128 values) is staged by the whole workgroup into one of
+// two LDS buffers; the MFMA B operand is read from LDS. Each wave keeps its
+// page's weights for the next chunk in flight in registers while it computes
+// the current one, so the only vector-memory traffic in the loop is the
+// weight stream plus one activation chunk; every wait count is static.
+// Per chunk c:  issue x(c+1) | issue w(c+1) | compute c | LDS <- x(c+1) | barrier
+// ---------------------------------------------------------------------------
+
+constexpr int kCK = 2;                            // 128-blocks per chunk
+constexpr int kXRow = kCK * 128 * 2 + 16;         // LDS bytes per staged activation row
+
+template <int NT>
+constexpr int lds_x_bytes() { return 2 * NT * 16 * kXRow; }
+
+// Rolling register window of a wave's page: slot j holds one 128-block's
+// weights (and its scale/zero pairs for quantized pages).
+template <int B, int GPK>
+struct Slot {
   WF<B> w;
-  u32x4 sz[2];
+  u32x4 sz[GPK];
+};
+template <int GPK>
+struct Slot<16, GPK> {
+  WF<16> w;
+};
+// Blocks kept in flight per wave: about 8-16 KiB of weights for every format.
+template <int B> constexpr int window() { return B == 4 ? 8 : 4; }
+
+template <int B, int GPK>
+__device__ __forceinline__ void load_slot(Slot<B, GPK>& sl, const uint8_t* wrow, const uint8_t* szrow,
+                                          int b, int lg, int G, int R) {
+  wf_load<B>(sl.w, wrow, b, lg);
+  if constexpr (B != 16) {
+#pragma unroll
+    for (int q = 0; q < GPK; ++q) sl.sz[q] = sz_load(szrow, GPK == 2 ? 2 * b + q : (b * 128) / G, R);
+  }
+}
+
+// The workgroup's activation rows for one chunk (NT*16 rows x kCK*128
+// values): thread tid stages the 16-byte pieces q = tid + 256 j, i.e. row
+// q / kPieces, piece q % kPieces. rowoff[j] are byte offsets of its rows.
+constexpr int kPieces = kCK * 128 / 8;            // 16-byte pieces per row
+constexpr int kRowsPerPass = 256 / kPieces;
+template <int NT> constexpr int x_passes() { return NT * 16 / kRowsPerPass; }
+__device__ __forceinline__ int x_row(int j) { return static_cast<int>(threadIdx.x) / kPieces + kRowsPerPass * j; }
+
+template <int NT>
+struct XStage {
+  u32x4 v[x_passes<NT>()];
 };
 
-// ---------------------------------------------------------------------------
-// gate/up GEMM + SwiGLU (one wave: 16 rows of gate and of up, all K = H)
-// ---------------------------------------------------------------------------
+template <int NT>
+__device__ __forceinline__ void x_fetch(XStage<NT>& s, const uint8_t* base, const uint32_t (&rowoff)[x_passes<NT>()],
+                                        int kel, int K) {
+  const int col = (threadIdx.x % kPieces) * 8;
+  const int k = min(kel + col, K - 8);
+#pragma unroll
+  for (int j = 0; j < x_passes<NT>(); ++j) s.v[j] = ld16(base + rowoff[j] + static_cast<size_t>(k) * 2);
+}
 
-template <int ACT, int BG, int BU, int MTB>
-__device__ void gateup_body(const GemmArgs& a, int off_e, int n_e, int f0, int lr0,
-                            const pw_page_entry& eg, const pw_page_entry& eu) {
+template <int NT>
+__device__ __forceinline__ void x_store(const XStage<NT>& s, uint8_t* buf) {
+  const int col = threadIdx.x % kPieces;
+#pragma unroll
+  for (int j = 0; j < x_passes<NT>(); ++j)
+    *reinterpret_cast<u32x4*>(buf + x_row(j) * kXRow + col * 16) = s.v[j];
+}
+
+// LDS stores of this wave complete, then a workgroup barrier (no memory fence:
+// weight loads stay in flight across it).
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
+  __builtin_amdgcn_s_barrier();
+}
+
+__device__ __forceinline__ bool group_end_g(int GPK, int G, int kb, int i) {
+  return GPK == 2 ? ((i & 1) == 1) : (i == 3 && ((kb + 1) * 128) % G == 0);
+}
+
+// Four k-steps of one 128-block (absolute block index kb); xrow points at the
+// block's 128 values inside the staged chunk.
+template <int ACT, int B, int NT, int GPK>
+__device__ __forceinline__ void compute_block(const Slot<B, GPK>& sl, const uint8_t* xblk, int kb, int G, int sdt,
+                                              f32x4 (&acc)[NT], f32x4 (&p)[NT], f32x4 (&xs)[NT]) {
   const int lane = lane_id(), lc = lane & 15, lg = lane >> 4;
-  const int H = a.H, G = a.G, R = a.R;
-  const int nkb = H / 128;
-  const uint8_t* wg_row = a.pool + eg.data_off + static_cast<size_t>(lr0 + lc) * row_bytes<BG>(H);
-  const uint8_t* wu_row = a.pool + eu.data_off + static_cast<size_t>(lr0 + lc) * row_bytes<BU>(H);
-  const uint8_t* szg_row = a.pool + eg.sz_off + static_cast<size_t>(lr0 + 4 * lg) * 4;
-  const uint8_t* szu_row = a.pool + eu.sz_off + static_cast<size_t>(lr0 + 4 * lg) * 4;
-  constexpr bool kQuant = (BG != 16) || (BU != 16);
-
-  for (int mb = 0; mb < n_e; mb += MTB * 16) {
-    const int ntile = min(MTB, (n_e - mb + 15) / 16);
-    const uint8_t* xrow[MTB];
 #pragma unroll
-    for (int t = 0; t < MTB; ++t) {
-      const int m = clampi(mb + 16 * t + lc, 0, n_e - 1);
-      const int slot = clampi(a.sorted_slot[off_e + m], 0, a.S - 1);
-      const int tok = slot / a.topk;
-      xrow[t] = reinterpret_cast<const uint8_t*>(a.x + static_cast<size_t>(tok) * H) + 16 * lg;
-    }
-    f32x4 accg[MTB], accu[MTB], pg[MTB], pu[MTB], xs[MTB];
+  for (int i = 0; i < 4; ++i) {
+    const u32x4 aw = wf_op<ACT, B>(sl.w, i);
 #pragma unroll
-    for (int t = 0; t < MTB; ++t) {
-      accg[t] = accu[t] = pg[t] = pu[t] = xs[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-    }
-    struct Frag {
-      Proj<BG> g;
-      Proj<BU> u;
-      u32x4 xb[MTB][4];
-    };
-    auto load = [&](Frag& f, int blk) {
-      wf_load<BG>(f.g.w, wg_row, blk, lg);
-      wf_load<BU>(f.u.w, wu_row, blk, lg);
-#pragma unroll
-      for (int t = 0; t < MTB; ++t) {
-        if (t < ntile) {
-#pragma unroll
-          for (int i = 0; i < 4; ++i) f.xb[t][i] = ld16(xrow[t] + (blk * 128 + 32 * i) * 2);
-        }
+    for (int t = 0; t < NT; ++t) {
+      const u32x4 bx = *reinterpret_cast<const u32x4*>(xblk + (t * 16 + lc) * kXRow + (32 * i + 8 * lg) * 2);
+      if constexpr (B == 16) {
+        acc[t] = mma<ACT>(aw, bx, acc[t]);
+      } else {
+        p[t] = mma<ACT>(aw, bx, p[t]);
+        xs[t] = mma<ACT>(ones_op<ACT>(), bx, xs[t]);
       }
-      if (G == 64) {
-        if constexpr (BG != 16) { f.g.sz[0] = sz_load(szg_row, 2 * blk, R); f.g.sz[1] = sz_load(szg_row, 2 * blk + 1, R); }
-        if constexpr (BU != 16) { f.u.sz[0] = sz_load(szu_row, 2 * blk, R); f.u.sz[1] = sz_load(szu_row, 2 * blk + 1, R); }
-      } else if (((blk + 1) * 128) % G == 0) {
-        const int gi = (blk * 128) / G;
-        if constexpr (BG != 16) f.g.sz[0] = sz_load(szg_row, gi, R);
-        if constexpr (BU != 16) f.u.sz[0] = sz_load(szu_row, gi, R);
-      }
-    };
-    Frag cur, nxt;
-    load(cur, 0);
-    for (int blk = 0; blk < nkb; ++blk) {
-      if (blk + 1 < nkb) load(nxt, blk + 1);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const u32x4 ag = wf_op<ACT, BG>(cur.g.w, i);
-        const u32x4 au = wf_op<ACT, BU>(cur.u.w, i);
-#pragma unroll
-        for (int t = 0; t < MTB; ++t) {
-          if (t < ntile) {
-            const u32x4 bx = cur.xb[t][i];
-            if constexpr (BG == 16) accg[t] = mma<ACT>(ag, bx, accg[t]); else pg[t] = mma<ACT>(ag, bx, pg[t]);
-            if constexpr (BU == 16) accu[t] = mma<ACT>(au, bx, accu[t]); else pu[t] = mma<ACT>(au, bx, pu[t]);
-            if constexpr (kQuant) xs[t] = mma<ACT>(ones_op<ACT>(), bx, xs[t]);
-          }
-        }
-        if constexpr (kQuant) {
-          const bool gend = (G == 64) ? ((i & 1) == 1) : (i == 3 && ((blk + 1) * 128) % G == 0);
-          if (gend) {
-            const int si = (G == 64) ? (i >> 1) : 0;
-            if constexpr (BG != 16) group_fix<ACT, BG, MTB>(accg, pg, xs, cur.g.sz[si], a.sdt, ntile);
-            if constexpr (BU != 16) group_fix<ACT, BU, MTB>(accu, pu, xs, cur.u.sz[si], a.sdt, ntile);
-#pragma unroll
-            for (int t = 0; t < MTB; ++t) xs[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-          }
-        }
-      }
-      cur = nxt;
     }
-    // SwiGLU epilogue: h = silu(g) * u, rounded to the activation dtype
+    if constexpr (B != 16) {
+      if (group_end_g(GPK, G, kb, i)) {
+        group_fix<ACT, B, NT>(acc, p, xs, sl.sz[GPK == 2 ? (i >> 1) : 0], sdt, NT);
 #pragma unroll
-    for (int t = 0; t < MTB; ++t) {
-      const int m = mb + 16 * t + lc;
-      if (t < ntile && m < n_e) {
-        uint32_t hv[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float gv = accg[t][r];
-          const float hval = gv / (1.0f + expf(-gv)) * accu[t][r];
-          hv[r] = rne16(hval, ACT);
-        }
-        u32x2 o;
-        o[0] = hv[0] | (hv[1] << 16);
-        o[1] = hv[2] | (hv[3] << 16);
-        *reinterpret_cast<u32x2*>(a.h + static_cast<size_t>(off_e + m) * a.F + f0 + 4 * lg) = o;
+        for (int t = 0; t < NT; ++t) xs[t] = f32x4{0.f, 0.f, 0.f, 0.f};
       }
     }
   }
 }
 
-template <int ACT, int MTB>
+// One wave: acc[t] = W[16 rows] . X[16 slots of tile t]^T over 128-blocks
+// [kb0, kb1). Block b's weights are loaded window() blocks ahead into slot
+// b mod window(); the activation chunk (kCK blocks) of chunk c sits in LDS
+// buffer c mod 2. Per chunk c: fetch x(c+1) | compute and refill | LDS <- x(c+1)
+// | barrier. Every load is unconditional (addresses clamped to the range), so
+// all wait counts are static; the workgroup passes nchunk - 1 barriers here.
+template <int ACT, int B, int NT, int GPK>
+__device__ void wave_gemm(const GemmArgs& a, uint8_t* lds, const uint8_t* xbase, const uint32_t (&rowoff)[x_passes<NT>()],
+                          int K, const uint8_t* wrow, const uint8_t* szrow, int kb0, int kb1, f32x4 (&acc)[NT]) {
+  constexpr int W = window<B>();
+  static_assert(W % kCK == 0, "window must cover whole chunks");
+  const int lg = lane_id() >> 4;
+  const int nkb = kb1 - kb0, kmax = kb1 - 1;
+  const int nchunk = (nkb + kCK - 1) / kCK;
+  f32x4 p[NT], xs[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) acc[t] = p[t] = xs[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  Slot<B, GPK> win[W];
+  XStage<NT> xr;
+  x_fetch<NT>(xr, xbase, rowoff, kb0 * 128, K);
+#pragma unroll
+  for (int j = 0; j < W; ++j) load_slot<B, GPK>(win[j], wrow, szrow, min(kb0 + j, kmax), lg, a.G, a.R);
+  x_store<NT>(xr, lds);
+  lds_barrier();
+  for (int base = 0; base < nkb; base += W) {
+#pragma unroll
+    for (int j = 0; j < W; ++j) {
+      const int b = base + j;                       // block index within the range
+      const int c = b / kCK;                        // chunk
+      uint8_t* buf = lds + (c & 1) * (NT * 16 * kXRow);
+      if (j % kCK == 0) x_fetch<NT>(xr, xbase, rowoff, (kb0 + (c + 1) * kCK) * 128, K);
+      if (b < nkb) compute_block<ACT, B, NT, GPK>(win[j], buf + (b % kCK) * 256, kb0 + b, a.G, a.sdt, acc, p, xs);
+      load_slot<B, GPK>(win[j], wrow, szrow, min(kb0 + b + W, kmax), lg, a.G, a.R);
+      if (j % kCK == kCK - 1 && c + 1 < nchunk) {
+        x_store<NT>(xr, lds + ((c + 1) & 1) * (NT * 16 * kXRow));
+        lds_barrier();
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+}
+
+__device__ __forceinline__ int fmt_code(uint8_t bits) {
+  return bits == 16 ? 0 : bits == 8 ? 1 : bits == 4 ? 2 : -1;
+}
+
+// ---------------------------------------------------------------------------
+// gate/up: a workgroup covers 32 rows of gate and the same 32 rows of up for
+// one expert; waves 0-1 stream gate, waves 2-3 stream up (each in its own
+// page format); the SwiGLU output h = silu(g) * u meets through LDS.
+// ---------------------------------------------------------------------------
+
+template <int ACT, int NT, int GPK>
+__device__ void gateup_unit(const GemmArgs& a, uint8_t* lds, int e, int off_e, int n_e, int r32) {
+  const int tid = threadIdx.x, wave = tid >> 6, lane = lane_id(), lc = lane & 15, lg = lane >> 4;
+  const int proj = wave >> 1, wsub = wave & 1;
+  const int f0 = r32 * 32 + 16 * wsub;
+  const int rb = f0 / a.R, lr0 = f0 - rb * a.R;
+  const pw_page_entry ent = a.table[(static_cast<size_t>(e) * 3 + proj) * a.nrb_max + rb];
+  const int code = fmt_code(ent.bits);
+  const int H = a.H;
+  float* xch = reinterpret_cast<float*>(lds + lds_x_bytes<NT>());   // [2 waves][NT][64 lanes][4]
+  for (int mb = 0; mb < n_e; mb += NT * 16) {
+    const uint8_t* xbase = reinterpret_cast<const uint8_t*>(a.x);
+    uint32_t rowoff[x_passes<NT>()];
+#pragma unroll
+    for (int j = 0; j < x_passes<NT>(); ++j) {
+      const int m = clampi(mb + x_row(j), 0, n_e - 1);
+      const int slot = clampi(a.sorted_slot[off_e + m], 0, a.S - 1);
+      rowoff[j] = static_cast<uint32_t>(slot / a.topk) * static_cast<uint32_t>(H * 2);
+    }
+    f32x4 acc[NT];
+    const int nkb = H / 128;
+    if (code == 0) {
+      const uint8_t* wrow = a.pool + ent.data_off + static_cast<size_t>(lr0 + lc) * row_bytes<16>(H);
+      wave_gemm<ACT, 16, NT, GPK>(a, lds, xbase, rowoff, H, wrow, nullptr, 0, nkb, acc);
+    } else if (code == 1) {
+      const uint8_t* wrow = a.pool + ent.data_off + static_cast<size_t>(lr0 + lc) * row_bytes<8>(H);
+      const uint8_t* szrow = a.pool + ent.sz_off + static_cast<size_t>(lr0 + 4 * lg) * 4;
+      wave_gemm<ACT, 8, NT, GPK>(a, lds, xbase, rowoff, H, wrow, szrow, 0, nkb, acc);
+    } else {
+      const uint8_t* wrow = a.pool + ent.data_off + static_cast<size_t>(lr0 + lc) * row_bytes<4>(H);
+      const uint8_t* szrow = a.pool + ent.sz_off + static_cast<size_t>(lr0 + 4 * lg) * 4;
+      wave_gemm<ACT, 4, NT, GPK>(a, lds, xbase, rowoff, H, wrow, szrow, 0, nkb, acc);
+    }
+    if (proj == 0) {
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+        *reinterpret_cast<f32x4*>(xch + ((wsub * NT + t) * 64 + lane) * 4) = acc[t];
+    }
+    lds_barrier();
+    if (proj == 1) {
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        const int m = mb + 16 * t + lc;
+        if (m < n_e) {
+          const f32x4 g = *reinterpret_cast<const f32x4*>(xch + ((wsub * NT + t) * 64 + lane) * 4);
+          uint32_t hv[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) hv[r] = rne16(g[r] / (1.0f + expf(-g[r])) * acc[t][r], ACT);
+          u32x2 o;
+          o[0] = hv[0] | (hv[1] << 16);
+          o[1] = hv[2] | (hv[3] << 16);
+          *reinterpret_cast<u32x2*>(a.h + static_cast<size_t>(off_e + m) * a.F + f0 + 4 * lg) = o;
+        }
+      }
+    }
+    lds_barrier();
+  }
+}
+
+template <int ACT, int NTMAX, int GPK>
 __global__ __launch_bounds__(256) void k_gateup(const GemmArgs a) {
-  const int upe = a.F / 64;
-  const int e = blockIdx.x / upe, r64 = blockIdx.x % upe;
+  __shared__ __attribute__((aligned(16))) uint8_t lds[lds_x_bytes<NTMAX>() + 2 * NTMAX * 64 * 16];
+  const int upe = a.F / 32;
+  const int e = blockIdx.x / upe, r32 = blockIdx.x % upe;
   const int off_e = clampi(a.offsets[e], 0, a.S);
   const int n_e = clampi(a.offsets[e + 1], off_e, a.S) - off_e;
   if (n_e <= 0) return;
-  const int wave = threadIdx.x >> 6;
-  const int f0 = r64 * 64 + wave * 16;
-  const int rb = f0 / a.R, lr0 = f0 - rb * a.R;
-  const pw_page_entry eg = a.table[(static_cast<size_t>(e) * 3 + PW_GATE) * a.nrb_max + rb];
-  const pw_page_entry eu = a.table[(static_cast<size_t>(e) * 3 + PW_UP) * a.nrb_max + rb];
-  const int cg = eg.bits == 16 ? 0 : eg.bits == 8 ? 1 : eg.bits == 4 ? 2 : -1;
-  const int cu = eu.bits == 16 ? 0 : eu.bits == 8 ? 1 : eu.bits == 4 ? 2 : -1;
-  if (cg < 0 || cu < 0) return;
-  switch (cg * 3 + cu) {
-    case 0: gateup_body<ACT, 16, 16, MTB>(a, off_e, n_e, f0, lr0, eg, eu); break;
-    case 1: gateup_body<ACT, 16, 8, MTB>(a, off_e, n_e, f0, lr0, eg, eu); break;
-    case 2: gateup_body<ACT, 16, 4, MTB>(a, off_e, n_e, f0, lr0, eg, eu); break;
-    case 3: gateup_body<ACT, 8, 16, MTB>(a, off_e, n_e, f0, lr0, eg, eu); break;
-    case 4: gateup_body<ACT, 8, 8, MTB>(a, off_e, n_e, f0, lr0, eg, eu); break;
-    case 5: gateup_body<ACT, 8, 4, MTB>(a, off_e, n_e, f0, lr0, eg, eu); break;
-    case 6: gateup_body<ACT, 4, 16, MTB>(a, off_e, n_e, f0, lr0, eg, eu); break;
-    case 7: gateup_body<ACT, 4, 8, MTB>(a, off_e, n_e, f0, lr0, eg, eu); break;
-    default: gateup_body<ACT, 4, 4, MTB>(a, off_e, n_e, f0, lr0, eg, eu); break;
-  }
+  // every page of the unit must be present; otherwise the whole group returns
+  const int rb = (r32 * 32) / a.R;
+  for (int p = 0; p < 2; ++p)
+    if (fmt_code(a.table[(static_cast<size_t>(e) * 3 + p) * a.nrb_max + rb].bits) < 0) return;
+  if (NTMAX == 1 || n_e <= 16) gateup_unit<ACT, 1, GPK>(a, lds, e, off_e, n_e, r32);
+  else if (NTMAX == 2 || n_e <= 32) gateup_unit<ACT, (NTMAX < 2 ? NTMAX : 2), GPK>(a, lds, e, off_e, n_e, r32);
+  else gateup_unit<ACT, NTMAX, GPK>(a, lds, e, off_e, n_e, r32);
 }
 
 // ---------------------------------------------------------------------------
-// down GEMM (one wave: 16 rows of down over one K split of F); fp32 partials
+// down: a workgroup covers 64 rows of one down page over one K split of F;
+// fp32 partial sums per split, reduced by the combine.
 // ---------------------------------------------------------------------------
 
-template <int ACT, int BD, int MTB>
-__device__ void down_body(const GemmArgs& a, int off_e, int n_e, int n0, int lr0, int split,
-                          const pw_page_entry& ed) {
-  const int lane = lane_id(), lc = lane & 15, lg = lane >> 4;
-  const int F = a.F, G = a.G, R = a.R;
+template <int ACT, int NT, int GPK>
+__device__ void down_unit(const GemmArgs& a, uint8_t* lds, int e, int off_e, int n_e, int r64, int split,
+                          const pw_page_entry& ent) {
+  const int tid = threadIdx.x, wave = tid >> 6, lane = lane_id(), lc = lane & 15, lg = lane >> 4;
+  const int F = a.F;
+  const int n0 = r64 * 64 + 16 * wave;
+  const int rb = n0 / a.R, lr0 = n0 - rb * a.R;
   const int kb0 = split * a.kb_per_split;
   const int kb1 = min(F / 128, kb0 + a.kb_per_split);
   if (kb0 >= kb1) return;
-  const uint8_t* w_row = a.pool + ed.data_off + static_cast<size_t>(lr0 + lc) * row_bytes<BD>(F);
-  const uint8_t* sz_row = a.pool + ed.sz_off + static_cast<size_t>(lr0 + 4 * lg) * 4;
-  constexpr bool kQuant = BD != 16;
-
-  for (int mb = 0; mb < n_e; mb += MTB * 16) {
-    const int ntile = min(MTB, (n_e - mb + 15) / 16);
-    const uint8_t* hrow[MTB];
+  const int code = fmt_code(ent.bits);
+  for (int mb = 0; mb < n_e; mb += NT * 16) {
+    const uint8_t* xbase = reinterpret_cast<const uint8_t*>(a.h);
+    uint32_t rowoff[x_passes<NT>()];
 #pragma unroll
-    for (int t = 0; t < MTB; ++t) {
-      const int m = clampi(mb + 16 * t + lc, 0, n_e - 1);
-      hrow[t] = reinterpret_cast<const uint8_t*>(a.h + static_cast<size_t>(off_e + m) * F) + 16 * lg;
+    for (int j = 0; j < x_passes<NT>(); ++j) {
+      const int m = clampi(mb + x_row(j), 0, n_e - 1);
+      rowoff[j] = static_cast<uint32_t>(off_e + m) * static_cast<uint32_t>(F * 2);
     }
-    f32x4 acc[MTB], p[MTB], xs[MTB];
-#pragma unroll
-    for (int t = 0; t < MTB; ++t) acc[t] = p[t] = xs[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-    struct Frag {
-      Proj<BD> d;
-      u32x4 xb[MTB][4];
-    };
-    auto load = [&](Frag& f, int blk) {
-      wf_load<BD>(f.d.w, w_row, blk, lg);
-#pragma unroll
-      for (int t = 0; t < MTB; ++t) {
-        if (t < ntile) {
-#pragma unroll
-          for (int i = 0; i < 4; ++i) f.xb[t][i] = ld16(hrow[t] + (blk * 128 + 32 * i) * 2);
-        }
-      }
-      if constexpr (kQuant) {
-        if (G == 64) {
-          f.d.sz[0] = sz_load(sz_row, 2 * blk, R);
-          f.d.sz[1] = sz_load(sz_row, 2 * blk + 1, R);
-        } else if (((blk + 1) * 128) % G == 0) {
-          f.d.sz[0] = sz_load(sz_row, (blk * 128) / G, R);
-        }
-      }
-    };
-    Frag cur, nxt;
-    load(cur, kb0);
-    for (int blk = kb0; blk < kb1; ++blk) {
-      if (blk + 1 < kb1) load(nxt, blk + 1);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const u32x4 ad = wf_op<ACT, BD>(cur.d.w, i);
-#pragma unroll
-        for (int t = 0; t < MTB; ++t) {
-          if (t < ntile) {
-            const u32x4 bx = cur.xb[t][i];
-            if constexpr (BD == 16) {
-              acc[t] = mma<ACT>(ad, bx, acc[t]);
-            } else {
-              p[t] = mma<ACT>(ad, bx, p[t]);
-              xs[t] = mma<ACT>(ones_op<ACT>(), bx, xs[t]);
-            }
-          }
-        }
-        if constexpr (kQuant) {
-          const bool gend = (G == 64) ? ((i & 1) == 1) : (i == 3 && ((blk + 1) * 128) % G == 0);
-          if (gend) {
-            group_fix<ACT, BD, MTB>(acc, p, xs, cur.d.sz[(G == 64) ? (i >> 1) : 0], a.sdt, ntile);
-#pragma unroll
-            for (int t = 0; t < MTB; ++t) xs[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-          }
-        }
-      }
-      cur = nxt;
+    f32x4 acc[NT];
+    if (code == 0) {
+      const uint8_t* wrow = a.pool + ent.data_off + static_cast<size_t>(lr0 + lc) * row_bytes<16>(F);
+      wave_gemm<ACT, 16, NT, GPK>(a, lds, xbase, rowoff, F, wrow, nullptr, kb0, kb1, acc);
+    } else if (code == 1) {
+      const uint8_t* wrow = a.pool + ent.data_off + static_cast<size_t>(lr0 + lc) * row_bytes<8>(F);
+      const uint8_t* szrow = a.pool + ent.sz_off + static_cast<size_t>(lr0 + 4 * lg) * 4;
+      wave_gemm<ACT, 8, NT, GPK>(a, lds, xbase, rowoff, F, wrow, szrow, kb0, kb1, acc);
+    } else {
+      const uint8_t* wrow = a.pool + ent.data_off + static_cast<size_t>(lr0 + lc) * row_bytes<4>(F);
+      const uint8_t* szrow = a.pool + ent.sz_off + static_cast<size_t>(lr0 + 4 * lg) * 4;
+      wave_gemm<ACT, 4, NT, GPK>(a, lds, xbase, rowoff, F, wrow, szrow, kb0, kb1, acc);
     }
 #pragma unroll
-    for (int t = 0; t < MTB; ++t) {
+    for (int t = 0; t < NT; ++t) {
       const int m = mb + 16 * t + lc;
-      if (t < ntile && m < n_e) {
-        float* dst = a.opart + (static_cast<size_t>(split) * a.S + off_e + m) * a.H + n0 + 4 * lg;
+      if (m < n_e) {
+        float* dst = a.opart + (static_cast<size_t>(split) * a.S + off_e + m) * a.H + r64 * 64 + 16 * wave + 4 * lg;
         *reinterpret_cast<f32x4*>(dst) = acc[t];
       }
     }
+    lds_barrier();
   }
 }
 
-template <int ACT, int MTB>
+template <int ACT, int NTMAX, int GPK>
 __global__ __launch_bounds__(256) void k_down(const GemmArgs a) {
+  __shared__ __attribute__((aligned(16))) uint8_t lds[lds_x_bytes<NTMAX>()];
   const int upe = a.H / 64;
   const int split = blockIdx.x % a.nsplit;
   const int rest = blockIdx.x / a.nsplit;
@@ -676,16 +736,12 @@ __global__ __launch_bounds__(256) void k_down(const GemmArgs a) {
   const int off_e = clampi(a.offsets[e], 0, a.S);
   const int n_e = clampi(a.offsets[e + 1], off_e, a.S) - off_e;
   if (n_e <= 0) return;
-  const int wave = threadIdx.x >> 6;
-  const int n0 = r64 * 64 + wave * 16;
-  const int rb = n0 / a.R, lr0 = n0 - rb * a.R;
-  const pw_page_entry ed = a.table[(static_cast<size_t>(e) * 3 + PW_DOWN) * a.nrb_max + rb];
-  switch (ed.bits) {
-    case 16: down_body<ACT, 16, MTB>(a, off_e, n_e, n0, lr0, split, ed); break;
-    case 8: down_body<ACT, 8, MTB>(a, off_e, n_e, n0, lr0, split, ed); break;
-    case 4: down_body<ACT, 4, MTB>(a, off_e, n_e, n0, lr0, split, ed); break;
-    default: break;
-  }
+  const int rb = (r64 * 64) / a.R;
+  const pw_page_entry ent = a.table[(static_cast<size_t>(e) * 3 + PW_DOWN) * a.nrb_max + rb];
+  if (fmt_code(ent.bits) < 0) return;
+  if (NTMAX == 1 || n_e <= 16) down_unit<ACT, 1, GPK>(a, lds, e, off_e, n_e, r64, split, ent);
+  else if (NTMAX == 2 || n_e <= 32) down_unit<ACT, (NTMAX < 2 ? NTMAX : 2), GPK>(a, lds, e, off_e, n_e, r64, split, ent);
+  else down_unit<ACT, NTMAX, GPK>(a, lds, e, off_e, n_e, r64, split, ent);
 }
 
 // ---------------------------------------------------------------------------
@@ -754,35 +810,36 @@ hipError_t launch_clear_table(pw_page_entry* table, size_t n, hipStream_t st) {
   return hipGetLastError();
 }
 
-template <int ACT>
-static hipError_t gateup_act(const GemmArgs& a, hipStream_t st) {
-  const dim3 grid(a.E * (a.F / 64)), block(256);
-  switch (a.mtb) {
-    case 1: hipLaunchKernelGGL((k_gateup<ACT, 1>), grid, block, 0, st, a); break;
-    case 2: hipLaunchKernelGGL((k_gateup<ACT, 2>), grid, block, 0, st, a); break;
-    default: hipLaunchKernelGGL((k_gateup<ACT, 4>), grid, block, 0, st, a); break;
+template <int ACT, int GPK>
+static hipError_t gemm_launch(const GemmArgs& a, bool gateup, hipStream_t st) {
+  const dim3 block(256);
+  if (gateup) {
+    const dim3 grid(a.E * (a.F / 32));
+    switch (a.mtb) {
+      case 1: hipLaunchKernelGGL((k_gateup<ACT, 1, GPK>), grid, block, 0, st, a); break;
+      case 2: hipLaunchKernelGGL((k_gateup<ACT, 2, GPK>), grid, block, 0, st, a); break;
+      default: hipLaunchKernelGGL((k_gateup<ACT, 4, GPK>), grid, block, 0, st, a); break;
+    }
+  } else {
+    const dim3 grid(a.E * (a.H / 64) * a.nsplit);
+    switch (a.mtb) {
+      case 1: hipLaunchKernelGGL((k_down<ACT, 1, GPK>), grid, block, 0, st, a); break;
+      case 2: hipLaunchKernelGGL((k_down<ACT, 2, GPK>), grid, block, 0, st, a); break;
+      default: hipLaunchKernelGGL((k_down<ACT, 4, GPK>), grid, block, 0, st, a); break;
+    }
   }
   return hipGetLastError();
 }
 
-hipError_t launch_gateup(const GemmArgs& a, hipStream_t st) {
-  return a.act == PW_BF16 ? gateup_act<PW_BF16>(a, st) : gateup_act<PW_F16>(a, st);
+static hipError_t gemm_dispatch(const GemmArgs& a, bool gateup, hipStream_t st) {
+  const bool g64 = a.G == 64;
+  if (a.act == PW_BF16) return g64 ? gemm_launch<PW_BF16, 2>(a, gateup, st) : gemm_launch<PW_BF16, 1>(a, gateup, st);
+  return g64 ? gemm_launch<PW_F16, 2>(a, gateup, st) : gemm_launch<PW_F16, 1>(a, gateup, st);
 }
 
-template <int ACT>
-static hipError_t down_act(const GemmArgs& a, hipStream_t st) {
-  const dim3 grid(a.E * (a.H / 64) * a.nsplit), block(256);
-  switch (a.mtb) {
-    case 1: hipLaunchKernelGGL((k_down<ACT, 1>), grid, block, 0, st, a); break;
-    case 2: hipLaunchKernelGGL((k_down<ACT, 2>), grid, block, 0, st, a); break;
-    default: hipLaunchKernelGGL((k_down<ACT, 4>), grid, block, 0, st, a); break;
-  }
-  return hipGetLastError();
-}
+hipError_t launch_gateup(const GemmArgs& a, hipStream_t st) { return gemm_dispatch(a, true, st); }
 
-hipError_t launch_down(const GemmArgs& a, hipStream_t st) {
-  return a.act == PW_BF16 ? down_act<PW_BF16>(a, st) : down_act<PW_F16>(a, st);
-}
+hipError_t launch_down(const GemmArgs& a, hipStream_t st) { return gemm_dispatch(a, false, st); }
 
 hipError_t launch_combine(const GemmArgs& a, hipStream_t st) {
   if (a.T <= 0) return hipSuccess;

@@ -1,0 +1,73 @@
+"""GPU parity at the full workload sizes, in the launch configuration the
+benchmark times. The oracle computes sampled tokens one by one; pages are
+compared byte for byte on a sample; routing is compared in full.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from helpers import case, gpu_layer, oracle_layer, rel_err, say, to_dev, to_dev16, y16_values
+from paper_2607_16184_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+TOL16, TOL32 = 2e-2, 1e-3
+
+
+def _sample_pages(cfg, bits, n, seed):
+    rng = np.random.default_rng(seed)
+    out = []
+    for p in range(3):
+        for b in (16, 8, 4):
+            cand = [(e, p, rb) for e in range(cfg.E) for rb in range(cfg.nrb(p)) if bits[p][e, rb] == b]
+            for i in rng.permutation(len(cand))[:n]:
+                out.append(cand[i])
+    return out
+
+
+def _full_case(name, tokens):
+    import torch
+    cfg, w16, bits, order = case(name)
+    say("%s: build GPU layer (%d pages)" % (name, len(order)))
+    L = gpu_layer(cfg, w16, bits, order)
+    O = oracle_layer(cfg, w16, bits)
+    for (e, p, rb) in _sample_pages(cfg, bits, 3, cfg.cfg_id):
+        assert np.array_equal(L.page_image(e, p, rb), O.page_image(p, e, rb)), (e, p, rb)
+    logits, x16 = synth.logits(cfg), synth.activations(cfg)
+    say("%s: forward" % name)
+    routing = L.route(to_dev(logits), cfg.K)
+    x = to_dev16(x16)
+    y16 = L.forward(x, routing)
+    y32 = L.forward(x, routing, out_fp32=True)
+    torch.cuda.synchronize()
+    ids, w = oracle.route(logits, cfg.K)
+    _, off, ss, sp = oracle.permute(ids, cfg.E)
+    assert np.array_equal(routing[0].cpu().numpy(), ids)
+    assert np.array_equal(routing[2].cpu().numpy(), off)
+    assert np.array_equal(routing[3].cpu().numpy()[:cfg.S], ss)
+    say("%s: oracle on tokens %s" % (name, list(tokens)))
+    r1 = O.forward(x16, ids, w, h_round=False, tokens=tokens)
+    r2 = O.forward(x16, ids, w, h_round=True, tokens=tokens)
+    t = list(tokens)
+    e16 = rel_err(y16_values(y16, cfg.act)[t], r1[t])
+    e32 = rel_err(y32.cpu().numpy()[t], r2[t])
+    L.close()
+    return e16, e32
+
+
+def test_mixtral_decode_full():
+    """Mixtral-shaped decode layer (the benchmark workload), 6 sampled tokens."""
+    e16, e32 = _full_case("mixtral_decode", [0, 9, 21, 33, 47, 63])
+    assert e16 <= TOL16 and e32 <= TOL32, (e16, e32)
+
+
+def test_finegrained_full():
+    """64 experts, top-6, 2048/1408, 512 tokens."""
+    e16, e32 = _full_case("finegrained", [0, 100, 255, 511])
+    assert e16 <= TOL16 and e32 <= TOL32, (e16, e32)
+
+
+def test_mixtral_prefill_full():
+    """4096 tokens with skewed routing; 4 sampled tokens."""
+    e16, e32 = _full_case("mixtral_prefill", [0, 1234, 2900, 4095])
+    assert e16 <= TOL16 and e32 <= TOL32, (e16, e32)
