@@ -75,6 +75,8 @@ def lib():
     L.or_delta_bytes.restype = ctypes.c_uint64
     L.or_encode_page.argtypes = [_c_u8p, _c_u16p, _c_u16p] + [ctypes.c_int] * 4 + [_c_u8p]
     L.or_decode_page.argtypes = [_c_u8p] + [ctypes.c_int] * 4 + [_c_u8p, _c_u16p, _c_u16p]
+    L.or_encode_page16.argtypes = [_c_u16p, ctypes.c_int, ctypes.c_int, _c_u8p]
+    L.or_decode_page16.argtypes = [_c_u8p, ctypes.c_int, ctypes.c_int, _c_u16p]
     L.or_route.argtypes = [_c_f32p] + [ctypes.c_int] * 4 + [_c_i32p, _c_f64p]
     L.or_permute.argtypes = [_c_i32p] + [ctypes.c_int] * 3 + [_c_i32p] * 4
     L.or_routing_mass.argtypes = [_c_i32p, _c_f64p] + [ctypes.c_int] * 3 + [_c_f64p]
@@ -199,6 +201,23 @@ def encode_page(codes, s, z, G: int, bits: int) -> np.ndarray:
     return out
 
 
+def encode_page16(w16) -> np.ndarray:
+    """Bytes of a 16-bit page ([R][K] values) in the tiled pool layout."""
+    w16 = np.ascontiguousarray(w16, np.uint16)
+    R, K = w16.shape
+    out = np.zeros(2 * R * K, np.uint8)
+    lib().or_encode_page16(w16, R, K, out)
+    return out
+
+
+def decode_page16(buf: np.ndarray, R: int, K: int) -> np.ndarray:
+    buf = np.ascontiguousarray(buf, np.uint8)
+    assert buf.size >= 2 * R * K
+    w = np.zeros((R, K), np.uint16)
+    lib().or_decode_page16(buf, R, K, w)
+    return w
+
+
 def decode_page(buf: np.ndarray, R: int, K: int, G: int, bits: int):
     buf = np.ascontiguousarray(buf, np.uint8)
     assert buf.size >= page_bytes(R, K, G, bits)
@@ -299,7 +318,7 @@ class OracleLayer:
         """The page's bytes in the pool format."""
         b, c, s, z = self.page(p, e, rb)
         if b == 16:
-            return np.ascontiguousarray(c).view(np.uint8).ravel()
+            return encode_page16(c)
         return encode_page(c, s, z, self.G, b)
 
     def requant(self, p, e, rb, new_bits) -> int:

@@ -257,16 +257,18 @@ void or_requant_page(const uint8_t* codes_in, const uint16_t* s_in, const uint16
 /* Page byte format (pool layout) -- encoder and decoder                      */
 /* ------------------------------------------------------------------------- */
 /*
- * 16-bit page: R*K values row-major.
- * 8/4-bit page: a code block followed by a scale/zero block.
- *   Each row's K codes are cut into blocks of 128; a block holds 16 runs of 8
- *   consecutive codes. The run covering codes [8*rho, 8*rho+8) of the block is
- *   stored at run position p, where rho = 4*(p mod 4) + p div 4.
- *   8-bit: a run is 8 bytes, code q of the run at byte q.
- *   4-bit: a run is one little-endian 32-bit word; code 2t of the run sits in
- *   bits [4t, 4t+4) and code 2t+1 in bits [16+4t, 16+4t+4), t = 0..3.
- *   Scale/zero block: for group g (K/G of them) and row r, the pair
- *   (scale, zero) as two 16-bit values at pair index g*R + r.
+ * A page of R rows x K values is cut into tiles of 16 rows x 128 values
+ * (tile (tau, beta): rows [16 tau, 16 tau + 16), values [128 beta, 128 beta +
+ * 128)), stored in the order tau-major, beta-minor. Inside a tile, value
+ * (r, k) with lc = r mod 16, i = (k mod 128) div 32, lg = (k mod 32) div 8,
+ * q = k mod 8 belongs to "lane" l = 16 lg + lc and "step" i:
+ *   16-bit: tile of 4096 bytes; value at byte 1024 i + 16 l + 2 q.
+ *   8-bit : tile of 2048 bytes; code at byte 1024 (i div 2) + 16 l + 8 (i mod 2) + q.
+ *   4-bit : tile of 1024 bytes; code in the little-endian 32-bit word at byte
+ *           16 l + 4 i, at bits [4t, 4t+4) if q = 2t and [16+4t, 20+4t) if q = 2t+1.
+ * 8/4-bit pages are followed by the scale/zero block: for group g (K/G of
+ * them) and row r, the pair (scale, zero) as two 16-bit values at pair index
+ * g R + r.
  * Page bytes: M16 = 2RK, M8 = RK + 4R(K/G), M4 = RK/2 + 4R(K/G).
  */
 
@@ -282,32 +284,57 @@ uint64_t or_delta_bytes(int R, int K, int G, int b, int bp) {
     return or_page_bytes(R, K, G, b) - or_page_bytes(R, K, G, bp);
 }
 
-static int run_of_position(int p) { return 4 * (p % 4) + p / 4; }
+/* Byte offset of value (r, k) in the code/value block, and for 4-bit codes
+ * the bit position inside the 32-bit word starting at that offset. */
+static uint64_t value_offset(int K, int bits, int r, int k, int* bitpos) {
+    int tau = r / 16, lc = r % 16, beta = k / 128;
+    int i = (k % 128) / 32, lg = (k % 32) / 8, q = k % 8, l = 16 * lg + lc;
+    uint64_t tile = (uint64_t)tau * (K / 128) + beta;
+    *bitpos = 0;
+    if (bits == 16) return tile * 4096 + 1024 * i + 16 * l + 2 * q;
+    if (bits == 8) return tile * 2048 + 1024 * (i / 2) + 16 * l + 8 * (i % 2) + q;
+    *bitpos = (q % 2) ? 16 + 4 * (q / 2) : 4 * (q / 2);
+    return tile * 1024 + 16 * l + 4 * i;
+}
+
+void or_encode_page16(const uint16_t* w16, int R, int K, uint8_t* out) {
+    int bp;
+    for (int r = 0; r < R; ++r)
+        for (int k = 0; k < K; ++k) {
+            uint64_t o = value_offset(K, 16, r, k, &bp);
+            uint16_t v = w16[(size_t)r * K + k];
+            out[o] = (uint8_t)(v & 255);
+            out[o + 1] = (uint8_t)(v >> 8);
+        }
+}
+
+void or_decode_page16(const uint8_t* in, int R, int K, uint16_t* w16) {
+    int bp;
+    for (int r = 0; r < R; ++r)
+        for (int k = 0; k < K; ++k) {
+            uint64_t o = value_offset(K, 16, r, k, &bp);
+            w16[(size_t)r * K + k] = (uint16_t)(in[o] | (in[o + 1] << 8));
+        }
+}
 
 void or_encode_page(const uint8_t* codes, const uint16_t* s, const uint16_t* z,
                     int R, int K, int G, int bits, uint8_t* out) {
-    int ng = K / G;
+    int ng = K / G, bp;
     size_t code_bytes = bits == 8 ? (size_t)R * K : (size_t)R * K / 2;
-    for (int r = 0; r < R; ++r) {
-        const uint8_t* c = codes + (size_t)r * K;
-        for (int blk = 0; blk < K / 128; ++blk) {
-            for (int p = 0; p < 16; ++p) {
-                int k0 = blk * 128 + 8 * run_of_position(p);
-                if (bits == 8) {
-                    uint8_t* dst = out + (size_t)r * K + blk * 128 + 8 * p;
-                    for (int q = 0; q < 8; ++q) dst[q] = c[k0 + q];
-                } else {
-                    uint32_t w = 0;
-                    for (int t = 0; t < 4; ++t) {
-                        w |= (uint32_t)(c[k0 + 2 * t] & 15) << (4 * t);
-                        w |= (uint32_t)(c[k0 + 2 * t + 1] & 15) << (16 + 4 * t);
-                    }
-                    uint8_t* dst = out + (size_t)r * (K / 2) + blk * 64 + 4 * p;
-                    for (int q = 0; q < 4; ++q) dst[q] = (uint8_t)(w >> (8 * q));
-                }
+    memset(out, 0, code_bytes);
+    for (int r = 0; r < R; ++r)
+        for (int k = 0; k < K; ++k) {
+            uint64_t o = value_offset(K, bits, r, k, &bp);
+            uint8_t c = codes[(size_t)r * K + k];
+            if (bits == 8) {
+                out[o] = c;
+            } else {
+                uint32_t w = (uint32_t)out[o] | ((uint32_t)out[o + 1] << 8) |
+                             ((uint32_t)out[o + 2] << 16) | ((uint32_t)out[o + 3] << 24);
+                w |= (uint32_t)(c & 15) << bp;
+                for (int b = 0; b < 4; ++b) out[o + b] = (uint8_t)(w >> (8 * b));
             }
         }
-    }
     uint8_t* szp = out + code_bytes;
     for (int g = 0; g < ng; ++g)
         for (int r = 0; r < R; ++r) {
@@ -322,28 +349,21 @@ void or_encode_page(const uint8_t* codes, const uint16_t* s, const uint16_t* z,
 
 void or_decode_page(const uint8_t* in, int R, int K, int G, int bits,
                     uint8_t* codes, uint16_t* s, uint16_t* z) {
-    int ng = K / G;
+    int ng = K / G, bp;
     size_t code_bytes = bits == 8 ? (size_t)R * K : (size_t)R * K / 2;
-    for (int r = 0; r < R; ++r) {
-        uint8_t* c = codes + (size_t)r * K;
-        for (int blk = 0; blk < K / 128; ++blk) {
-            for (int p = 0; p < 16; ++p) {
-                int k0 = blk * 128 + 8 * run_of_position(p);
-                if (bits == 8) {
-                    const uint8_t* src = in + (size_t)r * K + blk * 128 + 8 * p;
-                    for (int q = 0; q < 8; ++q) c[k0 + q] = src[q];
-                } else {
-                    const uint8_t* src = in + (size_t)r * (K / 2) + blk * 64 + 4 * p;
-                    uint32_t w = (uint32_t)src[0] | ((uint32_t)src[1] << 8) |
-                                 ((uint32_t)src[2] << 16) | ((uint32_t)src[3] << 24);
-                    for (int t = 0; t < 4; ++t) {
-                        c[k0 + 2 * t] = (uint8_t)((w >> (4 * t)) & 15);
-                        c[k0 + 2 * t + 1] = (uint8_t)((w >> (16 + 4 * t)) & 15);
-                    }
-                }
+    for (int r = 0; r < R; ++r)
+        for (int k = 0; k < K; ++k) {
+            uint64_t o = value_offset(K, bits, r, k, &bp);
+            uint8_t c;
+            if (bits == 8) {
+                c = in[o];
+            } else {
+                uint32_t w = (uint32_t)in[o] | ((uint32_t)in[o + 1] << 8) |
+                             ((uint32_t)in[o + 2] << 16) | ((uint32_t)in[o + 3] << 24);
+                c = (uint8_t)((w >> bp) & 15);
             }
+            codes[(size_t)r * K + k] = c;
         }
-    }
     const uint8_t* szp = in + code_bytes;
     for (int g = 0; g < ng; ++g)
         for (int r = 0; r < R; ++r) {

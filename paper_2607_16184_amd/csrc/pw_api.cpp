@@ -126,7 +126,8 @@ pw_status run_qjobs(pw_layer* L, const std::vector<pw::QJob>& jobs, int proj, hi
     b.G = d.G;
     b.act = d.act;
     b.sdt = d.sdt;
-    b.items_per_job = static_cast<uint32_t>(d.R) * ((K + 511) / 512);
+    const int span = d.G > 128 ? d.G / 128 : 1;
+    b.items_per_job = static_cast<uint32_t>(d.R / 16) * static_cast<uint32_t>((K / 128) / span);
     b.total_items = b.items_per_job * b.n_jobs;
     for (int j = 0; j < b.n_jobs; ++j) {
       b.job[j] = jobs[base + j];
@@ -230,27 +231,20 @@ pw_status pw_layer_load_page(pw_layer* L, int e, int proj, int rb, int bits, con
   if (s != PW_OK) return fail(s, err);
   hipStream_t st = static_cast<hipStream_t>(stream);
   const int K = L->st.kdim(proj);
-  hipError_t he = hipSuccess;
-  if (bits == 16) {
-    he = hipMemcpyAsync(L->pool + ent.data_off, rows16, static_cast<size_t>(L->st.desc.R) * K * 2,
-                        hipMemcpyDeviceToDevice, st);
-    if (he != hipSuccess) {
-      L->st.abort_slot(ent, proj);
-      return hip_fail(he, "page copy");
-    }
-  } else {
-    pw::QJob j{};
-    j.src = static_cast<const uint8_t*>(rows16);
-    j.src_sz = nullptr;
-    j.dst = L->pool + ent.data_off;
-    j.dst_sz = L->pool + ent.sz_off;
-    j.src_bits = 16;
-    j.dst_bits = static_cast<uint16_t>(bits);
-    s = run_qjobs(L, {j}, proj, st);
-    if (s != PW_OK) {
-      L->st.abort_slot(ent, proj);
-      return s;
-    }
+  (void)K;
+  // 16-bit: the rows are laid out as tiles; 8/4-bit: quantized into tiles
+  pw::QJob j{};
+  j.src = static_cast<const uint8_t*>(rows16);
+  j.src_sz = nullptr;
+  j.dst = L->pool + ent.data_off;
+  j.dst_sz = bits == 16 ? nullptr : L->pool + ent.sz_off;
+  j.src_bits = 16;
+  j.dst_bits = static_cast<uint8_t>(bits);
+  j.src_plain = 1;
+  s = run_qjobs(L, {j}, proj, st);
+  if (s != PW_OK) {
+    L->st.abort_slot(ent, proj);
+    return s;
   }
   s = write_entries(L, {{L->st.index(e, proj, rb), ent}}, st);
   if (s != PW_OK) {
@@ -397,6 +391,7 @@ pw_status pw_requant_blocks(pw_layer* L, int n, const int* e, const int* proj, c
       j.dst_sz = L->pool + p.dst.sz_off;
       j.src_bits = p.src.bits;
       j.dst_bits = p.dst.bits;
+      j.src_plain = 0;
       jobs.push_back(j);
     }
     if (jobs.empty()) continue;

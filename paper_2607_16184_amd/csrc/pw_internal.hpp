@@ -16,7 +16,9 @@ struct QJob {
   uint8_t* dst;            // destination code block
   uint8_t* dst_sz;         // destination scale/zero block
   uint32_t item_base;      // first work item of this job
-  uint16_t src_bits, dst_bits;
+  uint8_t src_bits, dst_bits;
+  uint8_t src_plain;       // 1: src is R x K row-major 16-bit values (not a pool page)
+  uint8_t rsv;
 };
 constexpr int kMaxQJobs = 32;
 struct QJobBatch {
@@ -24,7 +26,7 @@ struct QJobBatch {
   int n_jobs;
   int R, K, G;             // rows, reduction length, group size (same for the batch)
   int act, sdt;
-  uint32_t items_per_job;  // rows * chunks
+  uint32_t items_per_job;  // (R / 16) tiles x K-spans
   uint32_t total_items;
 };
 

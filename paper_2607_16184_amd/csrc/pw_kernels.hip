@@ -218,98 +218,186 @@ __global__ __launch_bounds__(kPermThreads) void k_permute(const int32_t* __restr
 }
 
 // ---------------------------------------------------------------------------
-// Group-wise RTN quantize / requantize (one wave per row x 512 codes)
+// Group-wise RTN quantize / requantize / 16-bit layout transform.
+//
+// Page layout: tiles of 16 rows x 128 values stored tile after tile (row tile
+// major); inside a tile, lane l = 16 lg + lc (row lc, k-run lg) of k-step i
+// owns 16 contiguous bytes: 16-bit values at 1024 i + 16 l, 8-bit codes of
+// steps 2u, 2u+1 at 1024 u + 16 l, the four 4-bit words at 16 l. A wave reads
+// or writes a tile as contiguous 1 KB rows. One wave handles one row tile over
+// one span of K (max(G,128) values); groups are reduced over the lane groups.
 // ---------------------------------------------------------------------------
+
+template <int B> constexpr int tile_bytes() { return B == 16 ? 4096 : B == 8 ? 2048 : 1024; }
+
+// The 32 values (k-steps i = 0..3, 8 values each) lane l holds of one block,
+// widened to fp32: from a plain row-major 16-bit source, a tiled 16-bit page,
+// or a quantized page (dequantized as fl32(z + c s)).
+__device__ __forceinline__ void q_read(const QJob& job, const QJobBatch& b, int tau, int blk, float (&v)[32]) {
+  const int lane = lane_id(), lc = lane & 15, lg = lane >> 4;
+  const int K = b.K, nkb = K / 128;
+  const size_t tile = static_cast<size_t>(tau) * nkb + blk;
+  if (job.src_bits == 16) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint8_t* src = job.src_plain
+          ? job.src + (static_cast<size_t>(tau * 16 + lc) * K + blk * 128 + 32 * i + 8 * lg) * 2
+          : job.src + tile * 4096 + 1024 * i + 16 * lane;
+      const u32x4 d = *reinterpret_cast<const u32x4*>(src);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        v[8 * i + 2 * q] = val16(d[q], b.act);
+        v[8 * i + 2 * q + 1] = val16(d[q] >> 16, b.act);
+      }
+    }
+    return;
+  }
+  uint32_t c[32];
+  if (job.src_bits == 8) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const u32x4 d = *reinterpret_cast<const u32x4*>(job.src + tile * 2048 + 1024 * u + 16 * lane);
+#pragma unroll
+      for (int w = 0; w < 4; ++w)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) c[16 * u + 4 * w + q] = (d[w] >> (8 * q)) & 0xFFu;
+    }
+  } else {
+    const u32x4 d = *reinterpret_cast<const u32x4*>(job.src + tile * 1024 + 16 * lane);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        c[8 * i + 2 * t] = (d[i] >> (4 * t)) & 15u;
+        c[8 * i + 2 * t + 1] = (d[i] >> (16 + 4 * t)) & 15u;
+      }
+  }
+  const int r = tau * 16 + lc;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int g = (blk * 128 + 32 * i) / b.G;
+    const uint32_t szw = *reinterpret_cast<const uint32_t*>(job.src_sz + (static_cast<size_t>(g) * b.R + r) * 4);
+    const float s = val16(szw, b.sdt), z = val16(szw >> 16, b.sdt);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) v[8 * i + q] = z + static_cast<float>(c[8 * i + q]) * s;   // c*s exact
+  }
+}
+
+// (scale, zero) bit patterns of a group from its extremes (the quantizer's steps).
+__device__ __forceinline__ void q_params(float lo, float hi, int Q, int sdt, uint32_t* sb, uint32_t* zb) {
+  *zb = round_down16(lo, sdt);
+  const float z = val16(*zb, sdt);
+  const float r = hi - z;
+  *sb = 0u;
+  if (r == 0.0f) return;
+  *sb = round_up16(r / static_cast<float>(Q), sdt);
+  if (val16(*sb, sdt) * static_cast<float>(Q) < r) *sb += 1u;   // s > 0: next value up
+}
+
+__device__ __forceinline__ uint32_t q_code(float v, uint32_t sb, uint32_t zb, int Q, int sdt) {
+  if (sb == 0u) return 0u;
+  const float d = v - val16(zb, sdt);
+  const float c = rintf(d / val16(sb, sdt));
+  return static_cast<uint32_t>(fminf(fmaxf(c, 0.0f), static_cast<float>(Q)));
+}
 
 __global__ __launch_bounds__(256) void k_qjobs(const QJobBatch b) {
   const uint32_t item = blockIdx.x * 4u + (threadIdx.x >> 6);
   if (item >= b.total_items) return;
-  const int lane = lane_id();
-  const int K = b.K, R = b.R, G = b.G;
-  const int nchunk = (K + 511) / 512;
+  const int lane = lane_id(), lc = lane & 15, lg = lane >> 4;
+  const int K = b.K, R = b.R, G = b.G, nkb = K / 128;
+  const int span = G > 128 ? G / 128 : 1;          // blocks per item
+  const int nspan = nkb / span;
   const int j = static_cast<int>(item / b.items_per_job);
   const int rem = static_cast<int>(item % b.items_per_job);
-  const int row = rem / nchunk, chunk = rem % nchunk;
+  const int tau = rem / nspan, sp = rem % nspan;
   const QJob& job = b.job[j];
-  const int k0 = chunk * 512 + 8 * lane;
-  const bool valid = k0 < K;
-  const int blk = k0 >> 7, rho = (k0 & 127) >> 3, pos = 4 * (rho & 3) + (rho >> 2);
-  const int g = k0 / G;
-
-  float v[8];
-  for (int q = 0; q < 8; ++q) v[q] = 0.0f;
-  if (valid) {
-    if (job.src_bits == 16) {
-      const u32x4 d = *reinterpret_cast<const u32x4*>(job.src + (static_cast<size_t>(row) * K + k0) * 2);
-      for (int q = 0; q < 4; ++q) {
-        v[2 * q] = val16(d[q], b.act);
-        v[2 * q + 1] = val16(d[q] >> 16, b.act);
+  const int r = tau * 16 + lc;
+  float v[32];
+  if (job.dst_bits == 16) {          // layout transform of a 16-bit page
+    for (int blk = sp * span; blk < (sp + 1) * span; ++blk) {
+      q_read(job, b, tau, blk, v);
+      const size_t tile = static_cast<size_t>(tau) * nkb + blk;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        u32x4 o;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) o[q] = rne16(v[8 * i + 2 * q], b.act) | (rne16(v[8 * i + 2 * q + 1], b.act) << 16);
+        *reinterpret_cast<u32x4*>(job.dst + tile * 4096 + 1024 * i + 16 * lane) = o;
+      }
+    }
+    return;
+  }
+  // pass 1: extremes of each group this item touches (one group, or two for G = 64)
+  float lo0 = __builtin_inff(), hi0 = -__builtin_inff(), lo1 = lo0, hi1 = hi0;
+  for (int blk = sp * span; blk < (sp + 1) * span; ++blk) {
+    q_read(job, b, tau, blk, v);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        if (G == 64 && i >= 2) {
+          lo1 = fminf(lo1, v[8 * i + q]);
+          hi1 = fmaxf(hi1, v[8 * i + q]);
+        } else {
+          lo0 = fminf(lo0, v[8 * i + q]);
+          hi0 = fmaxf(hi0, v[8 * i + q]);
+        }
+      }
+  }
+  // the row's other values sit in lanes lc + 16, lc + 32, lc + 48
+  lo0 = fminf(lo0, __shfl_xor(lo0, 16));
+  hi0 = fmaxf(hi0, __shfl_xor(hi0, 16));
+  lo1 = fminf(lo1, __shfl_xor(lo1, 16));
+  hi1 = fmaxf(hi1, __shfl_xor(hi1, 16));
+  lo0 = fminf(lo0, __shfl_xor(lo0, 32));
+  hi0 = fmaxf(hi0, __shfl_xor(hi0, 32));
+  lo1 = fminf(lo1, __shfl_xor(lo1, 32));
+  hi1 = fmaxf(hi1, __shfl_xor(hi1, 32));
+  const int Q = (1 << job.dst_bits) - 1;
+  uint32_t sb0, zb0, sb1 = 0u, zb1 = 0u;
+  q_params(lo0, hi0, Q, b.sdt, &sb0, &zb0);
+  if (G == 64) q_params(lo1, hi1, Q, b.sdt, &sb1, &zb1);
+  // pass 2: codes
+  for (int blk = sp * span; blk < (sp + 1) * span; ++blk) {
+    q_read(job, b, tau, blk, v);
+    uint32_t c[32];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const bool second = G == 64 && i >= 2;
+#pragma unroll
+      for (int q = 0; q < 8; ++q)
+        c[8 * i + q] = q_code(v[8 * i + q], second ? sb1 : sb0, second ? zb1 : zb0, Q, b.sdt);
+    }
+    const size_t tile = static_cast<size_t>(tau) * nkb + blk;
+    if (job.dst_bits == 8) {
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        u32x4 o;
+#pragma unroll
+        for (int w = 0; w < 4; ++w)
+          o[w] = c[16 * u + 4 * w] | (c[16 * u + 4 * w + 1] << 8) | (c[16 * u + 4 * w + 2] << 16) |
+                 (c[16 * u + 4 * w + 3] << 24);
+        *reinterpret_cast<u32x4*>(job.dst + tile * 2048 + 1024 * u + 16 * lane) = o;
       }
     } else {
-      const uint32_t szw = *reinterpret_cast<const uint32_t*>(job.src_sz + (static_cast<size_t>(g) * R + row) * 4);
-      const float s = val16(szw, b.sdt), z = val16(szw >> 16, b.sdt);
-      uint32_t c[8];
-      if (job.src_bits == 8) {
-        const u32x2 d = *reinterpret_cast<const u32x2*>(job.src + static_cast<size_t>(row) * K + blk * 128 + 8 * pos);
-        for (int q = 0; q < 4; ++q) {
-          c[q] = (d[0] >> (8 * q)) & 0xFFu;
-          c[4 + q] = (d[1] >> (8 * q)) & 0xFFu;
-        }
-      } else {
-        const uint32_t w = *reinterpret_cast<const uint32_t*>(job.src + static_cast<size_t>(row) * (K / 2) + blk * 64 + 4 * pos);
-        for (int t = 0; t < 4; ++t) {
-          c[2 * t] = (w >> (4 * t)) & 15u;
-          c[2 * t + 1] = (w >> (16 + 4 * t)) & 15u;
-        }
+      u32x4 o;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        uint32_t w = 0u;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) w |= (c[8 * i + 2 * t] << (4 * t)) | (c[8 * i + 2 * t + 1] << (16 + 4 * t));
+        o[i] = w;
       }
-      for (int q = 0; q < 8; ++q) v[q] = z + static_cast<float>(c[q]) * s;   // c*s exact
+      *reinterpret_cast<u32x4*>(job.dst + tile * 1024 + 16 * lane) = o;
     }
   }
-  float lo = v[0], hi = v[0];
-  for (int q = 1; q < 8; ++q) {
-    lo = fminf(lo, v[q]);
-    hi = fmaxf(hi, v[q]);
+  if (lg == 0) {
+    const int g0 = G == 64 ? 2 * sp : sp;
+    *reinterpret_cast<uint32_t*>(job.dst_sz + (static_cast<size_t>(g0) * R + r) * 4) = sb0 | (zb0 << 16);
+    if (G == 64)
+      *reinterpret_cast<uint32_t*>(job.dst_sz + (static_cast<size_t>(g0 + 1) * R + r) * 4) = sb1 | (zb1 << 16);
   }
-  for (int m = 1; m < G / 8; m <<= 1) {
-    lo = fminf(lo, __shfl_xor(lo, m));
-    hi = fmaxf(hi, __shfl_xor(hi, m));
-  }
-  if (!valid) return;
-  const int Q = (1 << job.dst_bits) - 1;
-  const uint32_t zb = round_down16(lo, b.sdt);
-  const float z = val16(zb, b.sdt);
-  const float r = hi - z;
-  uint32_t sb = 0u;
-  uint32_t c[8];
-  if (r == 0.0f) {
-    for (int q = 0; q < 8; ++q) c[q] = 0u;
-  } else {
-    const float s0 = r / static_cast<float>(Q);
-    sb = round_up16(s0, b.sdt);
-    float s = val16(sb, b.sdt);
-    if (s * static_cast<float>(Q) < r) {
-      sb += 1u;                       // s > 0: next representable value up
-      s = val16(sb, b.sdt);
-    }
-    for (int q = 0; q < 8; ++q) {
-      const float d = v[q] - z;
-      float cq = rintf(d / s);
-      cq = fminf(fmaxf(cq, 0.0f), static_cast<float>(Q));
-      c[q] = static_cast<uint32_t>(cq);
-    }
-  }
-  if (job.dst_bits == 8) {
-    u32x2 o;
-    o[0] = c[0] | (c[1] << 8) | (c[2] << 16) | (c[3] << 24);
-    o[1] = c[4] | (c[5] << 8) | (c[6] << 16) | (c[7] << 24);
-    *reinterpret_cast<u32x2*>(job.dst + static_cast<size_t>(row) * K + blk * 128 + 8 * pos) = o;
-  } else {
-    uint32_t w = 0u;
-    for (int t = 0; t < 4; ++t) w |= (c[2 * t] << (4 * t)) | (c[2 * t + 1] << (16 + 4 * t));
-    *reinterpret_cast<uint32_t*>(job.dst + static_cast<size_t>(row) * (K / 2) + blk * 64 + 4 * pos) = w;
-  }
-  if ((lane % (G / 8)) == 0)
-    *reinterpret_cast<uint32_t*>(job.dst_sz + (static_cast<size_t>(g) * R + row) * 4) = sb | (zb << 16);
 }
 
 __global__ void k_entry_writes(pw_page_entry* table, const EntryWrites w) {
@@ -349,28 +437,24 @@ struct CodeOff {
   static constexpr float value = (B == 16) ? 0.0f : (ACT == PW_BF16 ? (B == 4 ? 128.0f : 0.0f) : 1024.0f);
 };
 
-template <int B> constexpr int row_bytes(int K) { return B == 16 ? 2 * K : B == 8 ? K : K / 2; }
 template <int B> struct WF;
 template <> struct WF<16> { u32x4 v[4]; };
 template <> struct WF<8> { u32x4 v[2]; };
 template <> struct WF<4> { u32x4 v[1]; };
 
 __device__ __forceinline__ u32x4 ld16(const uint8_t* p) { return *reinterpret_cast<const u32x4*>(p); }
+// Weights are streamed once: nontemporal loads.
+__device__ __forceinline__ u32x4 ld16_nt(const uint8_t* p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+}
 
-// Lane group lg's share of one 128-code block of its row.
+// The lane's 16-byte pieces of 128-block blk of its row tile; `tile0` is the
+// tile row's first tile plus 16 * lane.
 template <int B>
-__device__ __forceinline__ void wf_load(WF<B>& f, const uint8_t* rowp, int blk, int lg) {
-  if constexpr (B == 16) {
-    const uint8_t* p = rowp + blk * 256 + 16 * lg;
+__device__ __forceinline__ void wf_load(WF<B>& f, const uint8_t* tile0, int blk) {
+  const uint8_t* p = tile0 + static_cast<size_t>(blk) * tile_bytes<B>();
 #pragma unroll
-    for (int i = 0; i < 4; ++i) f.v[i] = ld16(p + 64 * i);
-  } else if constexpr (B == 8) {
-    const uint8_t* p = rowp + blk * 128 + 32 * lg;
-    f.v[0] = ld16(p);
-    f.v[1] = ld16(p + 16);
-  } else {
-    f.v[0] = ld16(rowp + blk * 64 + 16 * lg);
-  }
+  for (int i = 0; i < tile_bytes<B>() / 1024; ++i) f.v[i] = ld16_nt(p + 1024 * i);
 }
 
 // A operand of k-step i: eight 16-bit values (weights, or codes as floats).
@@ -410,9 +494,10 @@ __device__ __forceinline__ u32x4 wf_op(const WF<B>& f, int i) {
 }
 
 // acc += s * P + (z - OFF s) * X for the lane's four rows; P is cleared.
-template <int ACT, int B, int MTB>
-__device__ __forceinline__ void group_fix(f32x4 (&acc)[MTB], f32x4 (&p)[MTB], const f32x4 (&xs)[MTB],
-                                          u32x4 sz, int sdt, int ntile) {
+// X[t] is the group's activation sum for this lane's slot (tile t).
+template <int ACT, int B, int NT>
+__device__ __forceinline__ void group_fix(f32x4 (&acc)[NT], f32x4 (&p)[NT], const float (&xs)[NT], u32x4 sz,
+                                          int sdt) {
   constexpr float off = CodeOff<ACT, B>::value;
   float s[4], zp[4];
 #pragma unroll
@@ -421,11 +506,9 @@ __device__ __forceinline__ void group_fix(f32x4 (&acc)[MTB], f32x4 (&p)[MTB], co
     zp[r] = val16(sz[r] >> 16, sdt) - off * s[r];
   }
 #pragma unroll
-  for (int t = 0; t < MTB; ++t) {
-    if (t < ntile) {
+  for (int t = 0; t < NT; ++t) {
 #pragma unroll
-      for (int r = 0; r < 4; ++r) acc[t][r] += s[r] * p[t][r] + zp[r] * xs[t][r];
-    }
+    for (int r = 0; r < 4; ++r) acc[t][r] += s[r] * p[t][r] + zp[r] * xs[t];
     p[t] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 }
@@ -452,8 +535,12 @@ __device__ __forceinline__ u32x4 sz_load(const uint8_t* szrow, int g, int R) {
 constexpr int kCK = 2;                            // 128-blocks per chunk
 constexpr int kXRow = kCK * 128 * 2 + 16;         // LDS bytes per staged activation row
 
+// Per chunk buffer: NT*16 staged rows, then NT*16 x (2 kCK) fp32 sums of
+// 64-value half blocks (the code-domain X of each quantization group).
 template <int NT>
-constexpr int lds_x_bytes() { return 2 * NT * 16 * kXRow; }
+constexpr int xbuf_bytes() { return NT * 16 * kXRow + NT * 16 * 2 * kCK * 4; }
+template <int NT>
+constexpr int lds_x_bytes() { return 2 * xbuf_bytes<NT>(); }
 
 // Rolling register window of a wave's page: slot j holds one 128-block's
 // weights (and its scale/zero pairs for quantized pages).
@@ -472,7 +559,7 @@ template <int B> constexpr int window() { return B == 4 ? 8 : 4; }
 template <int B, int GPK>
 __device__ __forceinline__ void load_slot(Slot<B, GPK>& sl, const uint8_t* wrow, const uint8_t* szrow,
                                           int b, int lg, int G, int R) {
-  wf_load<B>(sl.w, wrow, b, lg);
+  wf_load<B>(sl.w, wrow, b);
   if constexpr (B != 16) {
 #pragma unroll
     for (int q = 0; q < GPK; ++q) sl.sz[q] = sz_load(szrow, GPK == 2 ? 2 * b + q : (b * 128) / G, R);
@@ -501,12 +588,23 @@ __device__ __forceinline__ void x_fetch(XStage<NT>& s, const uint8_t* base, cons
   for (int j = 0; j < x_passes<NT>(); ++j) s.v[j] = ld16(base + rowoff[j] + static_cast<size_t>(k) * 2);
 }
 
-template <int NT>
+// Writes the staged rows and, per row, the sums of each 64-value half block
+// (8 consecutive pieces held by 8 consecutive lanes).
+template <int ACT, int NT>
 __device__ __forceinline__ void x_store(const XStage<NT>& s, uint8_t* buf) {
   const int col = threadIdx.x % kPieces;
+  float* sums = reinterpret_cast<float*>(buf + NT * 16 * kXRow);
 #pragma unroll
-  for (int j = 0; j < x_passes<NT>(); ++j)
+  for (int j = 0; j < x_passes<NT>(); ++j) {
     *reinterpret_cast<u32x4*>(buf + x_row(j) * kXRow + col * 16) = s.v[j];
+    float acc = 0.0f;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) acc += val16(s.v[j][q], ACT) + val16(s.v[j][q] >> 16, ACT);
+    acc += __shfl_xor(acc, 1);
+    acc += __shfl_xor(acc, 2);
+    acc += __shfl_xor(acc, 4);
+    if ((col & 7) == 0) sums[x_row(j) * (2 * kCK) + (col >> 3)] = acc;
+  }
 }
 
 // LDS stores of this wave complete, then a workgroup barrier (no memory fence:
@@ -520,11 +618,13 @@ __device__ __forceinline__ bool group_end_g(int GPK, int G, int kb, int i) {
   return GPK == 2 ? ((i & 1) == 1) : (i == 3 && ((kb + 1) * 128) % G == 0);
 }
 
-// Four k-steps of one 128-block (absolute block index kb); xrow points at the
-// block's 128 values inside the staged chunk.
+// Four k-steps of one 128-block (absolute block index kb). xblk points at the
+// block's 128 values inside the staged chunk; hsum at the chunk's half-block
+// sums and hb0 is this block's first half block.
 template <int ACT, int B, int NT, int GPK>
-__device__ __forceinline__ void compute_block(const Slot<B, GPK>& sl, const uint8_t* xblk, int kb, int G, int sdt,
-                                              f32x4 (&acc)[NT], f32x4 (&p)[NT], f32x4 (&xs)[NT]) {
+__device__ __forceinline__ void compute_block(const Slot<B, GPK>& sl, const uint8_t* xblk, const float* hsum, int hb0,
+                                              int kb, int G, int sdt, f32x4 (&acc)[NT], f32x4 (&p)[NT],
+                                              float (&xs)[NT]) {
   const int lane = lane_id(), lc = lane & 15, lg = lane >> 4;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -532,18 +632,25 @@ __device__ __forceinline__ void compute_block(const Slot<B, GPK>& sl, const uint
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
       const u32x4 bx = *reinterpret_cast<const u32x4*>(xblk + (t * 16 + lc) * kXRow + (32 * i + 8 * lg) * 2);
-      if constexpr (B == 16) {
-        acc[t] = mma<ACT>(aw, bx, acc[t]);
-      } else {
-        p[t] = mma<ACT>(aw, bx, p[t]);
-        xs[t] = mma<ACT>(ones_op<ACT>(), bx, xs[t]);
-      }
+      if constexpr (B == 16) acc[t] = mma<ACT>(aw, bx, acc[t]);
+      else p[t] = mma<ACT>(aw, bx, p[t]);
     }
     if constexpr (B != 16) {
-      if (group_end_g(GPK, G, kb, i)) {
-        group_fix<ACT, B, NT>(acc, p, xs, sl.sz[GPK == 2 ? (i >> 1) : 0], sdt, NT);
+      if constexpr (GPK == 2) {
+        if (i & 1) {
 #pragma unroll
-        for (int t = 0; t < NT; ++t) xs[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+          for (int t = 0; t < NT; ++t) xs[t] = hsum[(t * 16 + lc) * (2 * kCK) + hb0 + (i >> 1)];
+          group_fix<ACT, B, NT>(acc, p, xs, sl.sz[i >> 1], sdt);
+        }
+      } else if (i == 3) {
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+          xs[t] += hsum[(t * 16 + lc) * (2 * kCK) + hb0] + hsum[(t * 16 + lc) * (2 * kCK) + hb0 + 1];
+        if (((kb + 1) * 128) % G == 0) {
+          group_fix<ACT, B, NT>(acc, p, xs, sl.sz[0], sdt);
+#pragma unroll
+          for (int t = 0; t < NT; ++t) xs[t] = 0.0f;
+        }
       }
     }
   }
@@ -563,27 +670,34 @@ __device__ void wave_gemm(const GemmArgs& a, uint8_t* lds, const uint8_t* xbase,
   const int lg = lane_id() >> 4;
   const int nkb = kb1 - kb0, kmax = kb1 - 1;
   const int nchunk = (nkb + kCK - 1) / kCK;
-  f32x4 p[NT], xs[NT];
+  f32x4 p[NT];
+  float xs[NT];
 #pragma unroll
-  for (int t = 0; t < NT; ++t) acc[t] = p[t] = xs[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int t = 0; t < NT; ++t) {
+    acc[t] = p[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    xs[t] = 0.0f;
+  }
   Slot<B, GPK> win[W];
   XStage<NT> xr;
   x_fetch<NT>(xr, xbase, rowoff, kb0 * 128, K);
 #pragma unroll
   for (int j = 0; j < W; ++j) load_slot<B, GPK>(win[j], wrow, szrow, min(kb0 + j, kmax), lg, a.G, a.R);
-  x_store<NT>(xr, lds);
+  x_store<ACT, NT>(xr, lds);
   lds_barrier();
   for (int base = 0; base < nkb; base += W) {
 #pragma unroll
     for (int j = 0; j < W; ++j) {
       const int b = base + j;                       // block index within the range
       const int c = b / kCK;                        // chunk
-      uint8_t* buf = lds + (c & 1) * (NT * 16 * kXRow);
+      uint8_t* buf = lds + (c & 1) * xbuf_bytes<NT>();
       if (j % kCK == 0) x_fetch<NT>(xr, xbase, rowoff, (kb0 + (c + 1) * kCK) * 128, K);
-      if (b < nkb) compute_block<ACT, B, NT, GPK>(win[j], buf + (b % kCK) * 256, kb0 + b, a.G, a.sdt, acc, p, xs);
+      if (b < nkb)
+        compute_block<ACT, B, NT, GPK>(win[j], buf + (b % kCK) * 256,
+                                       reinterpret_cast<const float*>(buf + NT * 16 * kXRow), 2 * (b % kCK),
+                                       kb0 + b, a.G, a.sdt, acc, p, xs);
       load_slot<B, GPK>(win[j], wrow, szrow, min(kb0 + b + W, kmax), lg, a.G, a.R);
       if (j % kCK == kCK - 1 && c + 1 < nchunk) {
-        x_store<NT>(xr, lds + ((c + 1) & 1) * (NT * 16 * kXRow));
+        x_store<ACT, NT>(xr, lds + ((c + 1) & 1) * xbuf_bytes<NT>());
         lds_barrier();
       }
       __builtin_amdgcn_sched_barrier(0);
@@ -623,14 +737,14 @@ __device__ void gateup_unit(const GemmArgs& a, uint8_t* lds, int e, int off_e, i
     f32x4 acc[NT];
     const int nkb = H / 128;
     if (code == 0) {
-      const uint8_t* wrow = a.pool + ent.data_off + static_cast<size_t>(lr0 + lc) * row_bytes<16>(H);
+      const uint8_t* wrow = a.pool + ent.data_off + static_cast<size_t>(lr0 / 16) * (H / 128) * tile_bytes<16>() + 16 * lane;
       wave_gemm<ACT, 16, NT, GPK>(a, lds, xbase, rowoff, H, wrow, nullptr, 0, nkb, acc);
     } else if (code == 1) {
-      const uint8_t* wrow = a.pool + ent.data_off + static_cast<size_t>(lr0 + lc) * row_bytes<8>(H);
+      const uint8_t* wrow = a.pool + ent.data_off + static_cast<size_t>(lr0 / 16) * (H / 128) * tile_bytes<8>() + 16 * lane;
       const uint8_t* szrow = a.pool + ent.sz_off + static_cast<size_t>(lr0 + 4 * lg) * 4;
       wave_gemm<ACT, 8, NT, GPK>(a, lds, xbase, rowoff, H, wrow, szrow, 0, nkb, acc);
     } else {
-      const uint8_t* wrow = a.pool + ent.data_off + static_cast<size_t>(lr0 + lc) * row_bytes<4>(H);
+      const uint8_t* wrow = a.pool + ent.data_off + static_cast<size_t>(lr0 / 16) * (H / 128) * tile_bytes<4>() + 16 * lane;
       const uint8_t* szrow = a.pool + ent.sz_off + static_cast<size_t>(lr0 + 4 * lg) * 4;
       wave_gemm<ACT, 4, NT, GPK>(a, lds, xbase, rowoff, H, wrow, szrow, 0, nkb, acc);
     }
@@ -703,14 +817,14 @@ __device__ void down_unit(const GemmArgs& a, uint8_t* lds, int e, int off_e, int
     }
     f32x4 acc[NT];
     if (code == 0) {
-      const uint8_t* wrow = a.pool + ent.data_off + static_cast<size_t>(lr0 + lc) * row_bytes<16>(F);
+      const uint8_t* wrow = a.pool + ent.data_off + static_cast<size_t>(lr0 / 16) * (F / 128) * tile_bytes<16>() + 16 * lane;
       wave_gemm<ACT, 16, NT, GPK>(a, lds, xbase, rowoff, F, wrow, nullptr, kb0, kb1, acc);
     } else if (code == 1) {
-      const uint8_t* wrow = a.pool + ent.data_off + static_cast<size_t>(lr0 + lc) * row_bytes<8>(F);
+      const uint8_t* wrow = a.pool + ent.data_off + static_cast<size_t>(lr0 / 16) * (F / 128) * tile_bytes<8>() + 16 * lane;
       const uint8_t* szrow = a.pool + ent.sz_off + static_cast<size_t>(lr0 + 4 * lg) * 4;
       wave_gemm<ACT, 8, NT, GPK>(a, lds, xbase, rowoff, F, wrow, szrow, kb0, kb1, acc);
     } else {
-      const uint8_t* wrow = a.pool + ent.data_off + static_cast<size_t>(lr0 + lc) * row_bytes<4>(F);
+      const uint8_t* wrow = a.pool + ent.data_off + static_cast<size_t>(lr0 / 16) * (F / 128) * tile_bytes<4>() + 16 * lane;
       const uint8_t* szrow = a.pool + ent.sz_off + static_cast<size_t>(lr0 + 4 * lg) * 4;
       wave_gemm<ACT, 4, NT, GPK>(a, lds, xbase, rowoff, F, wrow, szrow, kb0, kb1, acc);
     }

@@ -14,22 +14,31 @@ import oracle
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
 
+def _lane_step(r, k):
+    """(tile index pieces, lane, step, position in run) of value (r, k)."""
+    tau, lc = divmod(r, 16)
+    beta, within = divmod(k, 128)
+    i, rest = divmod(within, 32)
+    lg, q = divmod(rest, 8)
+    return tau, beta, 16 * lg + lc, i, q
+
+
 def _scatter_encode(codes, s, z, G, bits):
     """Place each code directly at its byte/bit position (forward construction)."""
     R, K = codes.shape
+    nkb = K // 128
     code_bytes = R * K if bits == 8 else R * K // 2
     out = np.zeros(code_bytes + 4 * R * (K // G), np.uint8)
     for r in range(R):
         for k in range(K):
-            blk, within = divmod(k, 128)
-            rho, q = divmod(within, 8)
-            p = 4 * (rho % 4) + rho // 4            # run position of run rho
+            tau, beta, l, i, q = _lane_step(r, k)
+            tile = tau * nkb + beta
             if bits == 8:
-                out[r * K + blk * 128 + 8 * p + q] = codes[r, k]
+                out[tile * 2048 + 1024 * (i // 2) + 16 * l + 8 * (i % 2) + q] = codes[r, k]
             else:
                 t, hi = divmod(q, 2)
                 bit = 4 * t + 16 * hi
-                word = r * (K // 2) + blk * 64 + 4 * p
+                word = tile * 1024 + 16 * l + 4 * i
                 out[word + bit // 8] |= (int(codes[r, k]) & 15) << (bit % 8)
     for r in range(R):
         for g in range(K // G):
@@ -39,8 +48,20 @@ def _scatter_encode(codes, s, z, G, bits):
     return out
 
 
+def _scatter_encode16(w):
+    R, K = w.shape
+    nkb = K // 128
+    out = np.zeros(2 * R * K, np.uint8)
+    for r in range(R):
+        for k in range(K):
+            tau, beta, l, i, q = _lane_step(r, k)
+            o = (tau * nkb + beta) * 4096 + 1024 * i + 16 * l + 2 * q
+            out[o:o + 2] = np.array([w[r, k]], np.uint16).view(np.uint8)
+    return out
+
+
 @pytest.mark.parametrize("bits", [8, 4])
-@pytest.mark.parametrize("R,K,G", [(2, 128, 64), (3, 256, 128), (1, 384, 128)])
+@pytest.mark.parametrize("R,K,G", [(16, 128, 64), (32, 256, 128), (48, 384, 128)])
 def test_encoder_matches_scatter_construction(bits, R, K, G):
     rng = np.random.default_rng(R * K + bits)
     codes = rng.integers(0, 1 << bits, size=(R, K)).astype(np.uint8)
@@ -50,6 +71,14 @@ def test_encoder_matches_scatter_construction(bits, R, K, G):
     assert np.array_equal(enc, _scatter_encode(codes, s, z, G, bits))
     c2, s2, z2 = oracle.decode_page(enc, R, K, G, bits)
     assert np.array_equal(c2, codes) and np.array_equal(s2, s) and np.array_equal(z2, z)
+
+
+@pytest.mark.parametrize("R,K", [(16, 128), (32, 384)])
+def test_encoder16_matches_scatter_construction(R, K):
+    w = np.random.default_rng(R + K).integers(0, 65536, size=(R, K)).astype(np.uint16)
+    enc = oracle.encode_page16(w)
+    assert np.array_equal(enc, _scatter_encode16(w))
+    assert np.array_equal(oracle.decode_page16(enc, R, K), w)
 
 
 def _read_golden(name):
@@ -63,20 +92,21 @@ def _read_golden(name):
     return vals
 
 
-def test_golden_int4_and_int8_layout():
-    """Hand-derived bytes of a one-row page with codes (k + k div 8) mod 2^bits."""
+def test_golden_tiled_layout():
+    """Hand-derived bytes of a one-tile page (16 rows x 128 values)."""
     g = _read_golden("page_format_example.txt")
-    K = 128
-    k = np.arange(K)
-    c4 = ((k + k // 8) % 16).astype(np.uint8)[None]
-    c8 = ((k + k // 8) % 256).astype(np.uint8)[None]
-    sz = np.zeros((1, 1), np.uint16)
-    e4 = oracle.encode_page(c4, sz, sz, 128, 4)
-    e8 = oracle.encode_page(c8, sz, sz, 128, 8)
-    assert e4[0:4].tobytes().hex() == g["int4_word_p0"]
-    assert e4[4:8].tobytes().hex() == g["int4_word_p1"]
-    assert e8[0:8].tobytes().hex() == g["int8_run_p0"]
-    assert e8[8:16].tobytes().hex() == g["int8_run_p1"]
+    r = np.arange(16)[:, None]
+    k = np.arange(128)[None, :]
+    sz = np.zeros((16, 1), np.uint16)
+    e4 = oracle.encode_page(((r + k) % 16).astype(np.uint8), sz, sz, 128, 4)
+    e8 = oracle.encode_page(((r + k) % 256).astype(np.uint8), sz, sz, 128, 8)
+    e16 = oracle.encode_page16((r * 256 + k).astype(np.uint16))
+    assert e4[0:4].tobytes().hex() == g["int4_lane0_step0"]
+    assert e4[16:20].tobytes().hex() == g["int4_lane1_step0"]
+    assert e4[260:264].tobytes().hex() == g["int4_lane16_step1"]
+    assert e8[24:32].tobytes().hex() == g["int8_lane1_step1"]
+    assert e8[1296:1304].tobytes().hex() == g["int8_lane17_step2"]
+    assert e16[3104:3120].tobytes().hex() == g["v16_lane2_step3"]
 
 
 def test_page_sizes_eq3_closed_form():
@@ -93,6 +123,7 @@ def test_page_sizes_eq3_closed_form():
     assert 224 * 770_048 + 32 * 2_695_168 == 258_736_128
     for b in (16, 8, 4):
         assert oracle.page_bytes(64, 512, 64, b) % 256 == 0
+    assert oracle.encode_page16(np.zeros((16, 128), np.uint16)).size == oracle.page_bytes(16, 128, 128, 16)
 
 
 def test_encoded_size_matches_page_bytes():
