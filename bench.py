@@ -152,6 +152,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="mixtral_decode")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="after the timed steps, run one device copy of this many MiB "
+                         "(a known-size kernel for scaling HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         sys.stderr.write("bench.py runs on one GPU only: the paged MoE hot path here is a "
@@ -172,6 +175,14 @@ def main():
     logits = torch.from_numpy(logits_np).cuda()
     x = torch.from_numpy(x16.view(np.int16)).cuda()
     r = time_steps(L, cfg, x, logits, args.steps, args.warmup)
+    if args.calib_copy_mib:
+        n = args.calib_copy_mib << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     per = page_bytes_active(cfg, bits, r["counts"])
     wbytes = per[0] + per[1] + per[2]
     ms = r["event_ms"]
