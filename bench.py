@@ -145,6 +145,103 @@ def cpu_baseline(cfg, w16, bits, logits_np, x16, weight_bytes, budget_s=20.0):
                       "the full step (%.2f s measured, %.1f s per step)" % (done, cfg.T, spent, step_s)}
 
 
+def leg_layer(name, steps, warmup):
+    """Time another workload's full step; GB/s of active pages and MFMA share."""
+    import numpy as np
+    import torch
+    from paper_2607_16184_amd import synth
+    cfg = synth.CONFIGS[name]
+    L, w16, bits = build_layer(cfg)
+    del w16
+    logits = torch.from_numpy(synth.logits(cfg)).cuda()
+    x = torch.from_numpy(synth.activations(cfg).view(np.int16)).cuda()
+    r = time_steps(L, cfg, x, logits, steps, warmup)
+    per = page_bytes_active(cfg, bits, r["counts"])
+    wb = per[0] + per[1] + per[2]
+    km = r["kernel_ms"]
+    gemm_ms = km["gateup"] + km["down"]
+    flops = 6.0 * cfg.T * cfg.K * cfg.H * cfg.F
+    L.close()
+    return {"workload": describe(cfg), "steps": steps, "ms_per_step": round(r["event_ms"], 4),
+            "weight_GBps_per_step": round(wb / (r["event_ms"] * 1e-3) / 1e9, 1),
+            "gateup_ms": round(km["gateup"], 4), "down_ms": round(km["down"], 4),
+            "combine_ms": round(km["combine"], 4),
+            "mfma_frac_gemm": round(flops / (gemm_ms * 1e-3) / MFMA_PEAK_BF16, 4),
+            "mfma_frac_step": round(flops / (r["event_ms"] * 1e-3) / MFMA_PEAK_BF16, 4),
+            "tflops_gemm": round(flops / (gemm_ms * 1e-3) / 1e12, 1)}
+
+
+def leg_downshift(steps_before=8, steps_after=8):
+    """Decode steps of the Mixtral-shaped layer while 8 chunks of 32 16-bit pages
+    are requantized to int4 on a side stream and committed at step boundaries."""
+    import numpy as np
+    import torch
+    from paper_2607_16184_amd import pw, synth
+    from paper_2607_16184_amd.layer import PagedLayer
+    cfg = synth.CONFIGS["downshift"]
+    t0 = time.time()
+    w16 = [synth.expert_weights(cfg, p) for p in range(3)]
+    bits = synth.bitmap(cfg)
+    L = PagedLayer(cfg, PagedLayer.pool_bytes_for(cfg, bits, slack=0.1))
+    L.load_pages(w16, bits, synth.pool_order(cfg))
+    del w16
+    plan = synth.downshift_plan(cfg, bits)
+    log("downshift layer ready in %.1f s" % (time.time() - t0))
+    nsteps = steps_before + len(plan) + steps_after
+    ins = []
+    for s in range(nsteps):
+        lg, x16 = synth.step_inputs(cfg, s)
+        ins.append((torch.from_numpy(lg).cuda(), torch.from_numpy(x16.view(np.int16)).cuda()))
+    rbuf = PagedLayer.routing_buffers(cfg.T, cfg.E, cfg.K)
+    y = torch.empty((cfg.T, cfg.H), dtype=torch.int16, device="cuda")
+    side = torch.cuda.Stream()
+    main = torch.cuda.current_stream()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(nsteps)]
+    for s in range(2):   # warm-up
+        L.forward(ins[s][1], L.route(ins[s][0], cfg.K, out=rbuf), y=y)
+    torch.cuda.synchronize()
+    free0 = L.stats()[1]
+    pw.pw_profile_read(L.handle, reset=True)
+    pw.pw_profile_enable(L.handle, True)
+    moved = 0
+    for s in range(nsteps):
+        k = s - steps_before
+        if 0 <= k < len(plan):
+            side.wait_stream(main)
+            L.requant(plan[k], 4, stream=side)
+            for (e, p, rb) in plan[k]:
+                moved += pw.pw_page_bytes(cfg, p, 16) + pw.pw_page_bytes(cfg, p, 4)
+        ev[s][0].record()
+        L.forward(ins[s][1], L.route(ins[s][0], cfg.K, out=rbuf), y=y)
+        ev[s][1].record()
+        if 0 <= k < len(plan):
+            L.commit()
+        L.reclaim()
+    torch.cuda.synchronize()
+    L.reclaim()
+    pw.pw_profile_enable(L.handle, False)
+    ms, cnt = pw.pw_profile_read(L.handle, reset=True)
+    step_ms = [a.elapsed_time(b) for a, b in ev]
+    before = float(np.median(step_ms[:steps_before]))
+    during = float(np.median(step_ms[steps_before:steps_before + len(plan)]))
+    after = float(np.median(step_ms[steps_before + len(plan):]))
+    freed = L.stats()[1] - free0
+    post = [b.copy() for b in bits]
+    for chunk in plan:
+        for (e, p, rb) in chunk:
+            post[p][e, rb] = 4
+    post_bytes = sum(pw.pw_page_bytes(cfg, p, int(b)) for p in range(3) for b in post[p].ravel())
+    L.close()
+    rq_ms = ms[pw.PW_PH_REQUANT]
+    return {"workload": "mixtral_decode layer, 64-token steps; 8 chunks of 32 16-bit pages -> int4 "
+                        "on a side stream, committed at step boundaries",
+            "step_ms_before": round(before, 4), "step_ms_during": round(during, 4),
+            "step_ms_after": round(after, 4), "decode_slowdown": round(during / before - 1.0, 4),
+            "requant_GBps": round(moved / (rq_ms * 1e-3) / 1e9, 1) if rq_ms else None,
+            "requant_ms_per_chunk": round(rq_ms / max(cnt[pw.PW_PH_REQUANT], 1), 4),
+            "bytes_freed": int(freed), "post_switch_weight_GBps": round(post_bytes / (after * 1e-3) / 1e9, 1)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -152,6 +249,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="mixtral_decode")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--extras", default="prefill,finegrained,downshift",
+                    help="comma list of extra legs on the same JSON line ('' for none)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after the timed steps, run one device copy of this many MiB "
                          "(a known-size kernel for scaling HBM byte counters)")
@@ -230,6 +329,19 @@ def main():
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, w16, bits, logits_np, x16, wbytes)
     L.close()
+    del L, w16
+    extras = {}
+    for leg in [e for e in args.extras.split(",") if e]:
+        t0 = time.time()
+        if leg == "prefill":
+            extras["prefill"] = leg_layer("mixtral_prefill", steps=5, warmup=1)
+        elif leg == "finegrained":
+            extras["finegrained"] = leg_layer("finegrained", steps=20, warmup=3)
+        elif leg == "downshift":
+            extras["downshift"] = leg_downshift()
+        log("leg %s done in %.1f s" % (leg, time.time() - t0))
+    if extras:
+        out["extras"] = extras
     print(json.dumps(out))
 
 
