@@ -83,7 +83,7 @@ def lib():
     L.or_moe_forward.argtypes = (
         [_c_u16p] + [ctypes.c_int] * 9 + [_c_i32p, _c_f64p]
         + [_c_u16p, _c_i32p, _c_u8p, _c_u16p, _c_u16p] * 3
-        + [ctypes.c_int, _c_i32p, ctypes.c_int, _c_f64p])
+        + [ctypes.c_int, ctypes.c_int, _c_i32p, ctypes.c_int, _c_f64p])
     L.or_threads.restype = ctypes.c_int
     L.or_init()
     _lib = L
@@ -339,8 +339,12 @@ class OracleLayer:
         return delta_bytes(self.R, K, self.G, b, new_bits)
 
     def forward(self, x16: np.ndarray, ids: np.ndarray, w: np.ndarray, h_round: bool = False,
-                tokens: Optional[Sequence[int]] = None) -> np.ndarray:
-        """y [T,H] float64 for the listed tokens (all by default); other rows 0."""
+                tokens: Optional[Sequence[int]] = None, w_round: bool = False) -> np.ndarray:
+        """y [T,H] float64 for the listed tokens (all by default); other rows 0.
+
+        h_round: round the SwiGLU output to the activation format before the
+        down projection. w_round: read a quantized weight as its fp32 value
+        z + c*s rounded to the activation format (16-bit pages unchanged)."""
         x16 = np.ascontiguousarray(x16, np.uint16)
         T = x16.shape[0]
         K = ids.shape[1]
@@ -351,7 +355,7 @@ class OracleLayer:
             args += [self.w16[p], self.bits[p], self.codes[p], self.s[p], self.z[p]]
         lib().or_moe_forward(x16, T, self.H, self.F, self.E, K, self.R, self.G, self.act, self.sdt,
                              np.ascontiguousarray(ids, np.int32), np.ascontiguousarray(w, np.float64),
-                             *args, int(h_round), np.ascontiguousarray(tok), int(tok.size), y)
+                             *args, int(h_round), int(w_round), np.ascontiguousarray(tok), int(tok.size), y)
         return y
 
     def active_weight_bytes(self, counts: np.ndarray) -> int:

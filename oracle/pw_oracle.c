@@ -458,9 +458,12 @@ typedef struct {
 } or_proj;
 
 /* dot(row n of expert e's projection, v) with the weight read at its page's
- * committed bitwidth: the 16-bit value, or z + c*s (exact in fp64).         */
+ * committed bitwidth: the 16-bit value, or z + c*s (exact in fp64). With
+ * w_round=1 a quantized weight is instead first rounded to fp32 and then to
+ * the activation format (round to nearest even both times): the value a
+ * kernel feeds to a 16-bit matrix unit after dequantizing in fp32.         */
 static double proj_row_dot(const or_proj* P, int e, int n, const double* v, int R, int G,
-                           const double* d16, const double* dsdt) {
+                           const double* d16, const double* dsdt, int w_round, int act) {
     int b = P->bits[(size_t)e * (P->rows / R) + n / R];
     size_t base = ((size_t)e * P->rows + n) * P->cols;
     double acc = 0.0;
@@ -474,6 +477,7 @@ static double proj_row_dot(const or_proj* P, int e, int n, const double* v, int 
         const uint16_t* z = P->z + ((size_t)e * P->rows + n) * ng;
         for (int j = 0; j < P->cols; ++j) {
             double wv = dsdt[z[j / G]] + (double)c[j] * dsdt[s[j / G]];
+            if (w_round) wv = or_decode16(or_round_nearest16((double)(float)wv, act), act);
             acc += wv * v[j];
         }
     }
@@ -483,7 +487,8 @@ static double proj_row_dot(const or_proj* P, int e, int n, const double* v, int 
 /* y[t] = sum_k w[t,k] * down_e( silu(gate_e(x_t)) * up_e(x_t) ), e = ids[t,k],
  * for the tokens listed in `tok` (n_tok of them). fp64 throughout; with
  * h_round=1 the SwiGLU output is rounded to the activation format before the
- * down projection. y is [T][H] and only the listed rows are written.       */
+ * down projection; w_round as in proj_row_dot. y is [T][H] and only the
+ * listed rows are written.                                                  */
 void or_moe_forward(const uint16_t* x16, int T, int H, int F, int E, int K, int R, int G,
                     int act, int sdt, const int32_t* ids, const double* w,
                     const uint16_t* g16, const int32_t* gbits, const uint8_t* gcodes,
@@ -492,7 +497,7 @@ void or_moe_forward(const uint16_t* x16, int T, int H, int F, int E, int K, int 
                     const uint16_t* us, const uint16_t* uz,
                     const uint16_t* d16w, const int32_t* dbits, const uint8_t* dcodes,
                     const uint16_t* ds, const uint16_t* dz,
-                    int h_round, const int32_t* tok, int n_tok, double* y) {
+                    int h_round, int w_round, const int32_t* tok, int n_tok, double* y) {
     (void)T;
     (void)E;
     or_init();
@@ -512,15 +517,15 @@ void or_moe_forward(const uint16_t* x16, int T, int H, int F, int E, int K, int 
             int e = ids[(size_t)t * K + k];
 #pragma omp parallel for schedule(static)
             for (int f = 0; f < F; ++f) {
-                double gv = proj_row_dot(&PG, e, f, xv, R, G, d16, dsdt);
-                double uv = proj_row_dot(&PU, e, f, xv, R, G, d16, dsdt);
+                double gv = proj_row_dot(&PG, e, f, xv, R, G, d16, dsdt, w_round, act);
+                double uv = proj_row_dot(&PU, e, f, xv, R, G, d16, dsdt, w_round, act);
                 double hv = gv / (1.0 + exp(-gv)) * uv;
                 if (h_round) hv = or_decode16(or_round_nearest16(hv, act), act);
                 h[f] = hv;
             }
 #pragma omp parallel for schedule(static)
             for (int n = 0; n < H; ++n)
-                o[n] = proj_row_dot(&PD, e, n, h, R, G, d16, dsdt);
+                o[n] = proj_row_dot(&PD, e, n, h, R, G, d16, dsdt, w_round, act);
             double wk = w[(size_t)t * K + k];
             for (int n = 0; n < H; ++n) y[(size_t)t * H + n] += wk * o[n];
         }

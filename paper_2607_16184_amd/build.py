@@ -37,7 +37,7 @@ def build_hip(verbose=False):
     objdir = os.path.join(HERE, "_build")
     os.makedirs(objdir, exist_ok=True)
     objs = []
-    for src in ("pw_kernels.hip", "pw_api.cpp", "pw_state.cpp"):
+    for src in ("pw_kernels.hip", "pw_tgemm.hip", "pw_api.cpp", "pw_state.cpp"):
         obj = os.path.join(objdir, src + ".o")
         extra = ["-x", "hip"] if src.endswith(".hip") else []
         out = _run([HIPCC] + HIP_FLAGS + extra + ["-c", os.path.join(CSRC, src), "-o", obj])

@@ -81,7 +81,18 @@ bool mult_of_256(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 255u)
 struct WsLayout {
   size_t h_off, h_bytes, op_off, op_bytes, total;
   int nsplit, kb_per_split, mtb;
+  bool tiled;   // large per-expert token counts: the LDS-tiled GEMM
 };
+
+// The LDS-tiled GEMM (256 x 256 tiles) pays off once an expert's slots fill
+// its tiles; it needs 64-row staging inside one page, 256-row down blocks and
+// one scale/zero group per 64-value stage.
+bool use_tiled(const pw_layer_desc& d, size_t S) {
+  const size_t expect = (S + d.E - 1) / d.E;
+  // activation row offsets are 32-bit in that kernel
+  const bool fits = S * d.F * 2 < (size_t(1) << 32) && S * d.H * 2 < (size_t(1) << 32);
+  return expect >= 128 && fits && d.G >= 64 && d.H % 256 == 0 && d.F % 128 == 0 && d.R % 64 == 0;
+}
 
 WsLayout ws_layout(const pw_layer_desc& d, int T, int K) {
   WsLayout w{};
@@ -91,7 +102,8 @@ WsLayout ws_layout(const pw_layer_desc& d, int T, int K) {
   // Split the down projection's K = F when too few (expert, row-block) units
   // exist to fill the chip; deterministic in (desc, T, K).
   int nsplit = 1;
-  if (S <= 4096) {
+  w.tiled = use_tiled(d, S);
+  if (S <= 4096 && !w.tiled) {
     const size_t active = std::min<size_t>(d.E, S);
     const size_t units = active * (d.H / 64);
     nsplit = static_cast<int>(std::max<size_t>(1, std::min<size_t>(8, 2048 / std::max<size_t>(units, 1))));
@@ -325,12 +337,12 @@ pw_status pw_moe_paged_gemm(const pw_layer* Lc, const void* x, int T, int K, con
   hipError_t e;
   {
     ProfScope ps(L, PW_PH_GATEUP, st);
-    e = pw::launch_gateup(a, st);
+    e = wl.tiled ? pw::launch_tgemm(a, true, st) : pw::launch_gateup(a, st);
   }
   if (e != hipSuccess) return hip_fail(e, "gate/up launch");
   {
     ProfScope ps(L, PW_PH_DOWN, st);
-    e = pw::launch_down(a, st);
+    e = wl.tiled ? pw::launch_tgemm(a, false, st) : pw::launch_down(a, st);
   }
   if (e != hipSuccess) return hip_fail(e, "down launch");
   {

@@ -67,5 +67,7 @@ hipError_t launch_clear_table(pw_page_entry* table, size_t n, hipStream_t st);
 hipError_t launch_gateup(const GemmArgs& a, hipStream_t st);
 hipError_t launch_down(const GemmArgs& a, hipStream_t st);
 hipError_t launch_combine(const GemmArgs& a, hipStream_t st);
+// large per-expert slot counts: LDS-tiled GEMM (256 x 256 tiles)
+hipError_t launch_tgemm(const GemmArgs& a, bool gateup, hipStream_t st);
 
 }  // namespace pw

@@ -25,7 +25,7 @@ def _sample_pages(cfg, bits, n, seed):
     return out
 
 
-def _full_case(name, tokens):
+def _full_case(name, tokens, w_round=False):
     import torch
     cfg, w16, bits, order = case(name)
     say("%s: build GPU layer (%d pages)" % (name, len(order)))
@@ -47,7 +47,7 @@ def _full_case(name, tokens):
     assert np.array_equal(routing[3].cpu().numpy()[:cfg.S], ss)
     say("%s: oracle on tokens %s" % (name, list(tokens)))
     r1 = O.forward(x16, ids, w, h_round=False, tokens=tokens)
-    r2 = O.forward(x16, ids, w, h_round=True, tokens=tokens)
+    r2 = O.forward(x16, ids, w, h_round=True, tokens=tokens, w_round=w_round)
     t = list(tokens)
     e16 = rel_err(y16_values(y16, cfg.act)[t], r1[t])
     e32 = rel_err(y32.cpu().numpy()[t], r2[t])
@@ -68,6 +68,8 @@ def test_finegrained_full():
 
 
 def test_mixtral_prefill_full():
-    """4096 tokens with skewed routing; 4 sampled tokens."""
-    e16, e32 = _full_case("mixtral_prefill", [0, 1234, 2900, 4095])
+    """4096 tokens with skewed routing; 4 sampled tokens. The LDS-tiled GEMM
+    runs here: the fp32 output is compared with the oracle reading quantized
+    weights rounded to the activation dtype (w_round)."""
+    e16, e32 = _full_case("mixtral_prefill", [0, 1234, 2900, 4095], w_round=True)
     assert e16 <= TOL16 and e32 <= TOL32, (e16, e32)

@@ -109,7 +109,7 @@ def test_tiny_requant_bit_exact(src, dst):
     L.close()
 
 
-def _forward_parity(cfg, L, O, x16, logits, tokens=None):
+def _forward_parity(cfg, L, O, x16, logits, tokens=None, w_round=False):
     import torch
     routing = L.route(to_dev(logits), cfg.K)
     x = to_dev16(x16)
@@ -118,7 +118,7 @@ def _forward_parity(cfg, L, O, x16, logits, tokens=None):
     torch.cuda.synchronize()
     ids, w = oracle.route(logits, cfg.K)
     r1 = O.forward(x16, ids, w, h_round=False, tokens=tokens)
-    r2 = O.forward(x16, ids, w, h_round=True, tokens=tokens)
+    r2 = O.forward(x16, ids, w, h_round=True, tokens=tokens, w_round=w_round)
     sel = slice(None) if tokens is None else list(tokens)
     e16 = rel_err(y16_values(y16, cfg.act)[sel], r1[sel])
     e32 = rel_err(y32.cpu().numpy()[sel], r2[sel])
@@ -178,4 +178,37 @@ def test_zero_up_projection_gives_zero():
     y = L.forward(to_dev16(synth.activations(cfg)), L.route(to_dev(synth.logits(cfg)), cfg.K), out_fp32=True)
     torch.cuda.synchronize()
     assert not y.cpu().numpy().any()
+    L.close()
+
+
+# Large per-expert slot counts (at least 128 expected per expert) take the
+# LDS-tiled GEMM, which feeds quantized weights to the MFMA as fl32(z + c*s)
+# rounded to the activation dtype: its fp32 output is compared with the oracle
+# read the same way (w_round).
+
+@pytest.mark.parametrize("T", [1000, 1531])
+def test_tiny_tiled_path_parity(T):
+    cfg, w16, bits, order = case("tiny", T=T)
+    say("tiny tiled T=%d" % T)
+    L = gpu_layer(cfg, w16, bits, order)
+    O = oracle_layer(cfg, w16, bits)
+    e16, e32, _, _ = _forward_parity(cfg, L, O, synth.activations(cfg), synth.logits(cfg), w_round=True)
+    assert e16 <= TOL16 and e32 <= TOL32, (e16, e32)
+    L.close()
+
+
+@pytest.mark.parametrize("b", [16, 8, 4])
+def test_tiny_tiled_uniform_and_empty_experts(b):
+    """Every page at one bitwidth; all slots on experts 0 and 1 (ragged tails
+    of 1100 slots, six experts with none)."""
+    cfg, w16, _, order = case("tiny", T=1100)
+    bits = [np.full((cfg.E, cfg.nrb(p)), b, np.int32) for p in range(3)]
+    lg = synth.logits(cfg).copy()
+    lg[:, :2] += 100.0
+    say("tiny tiled uniform %d, two experts" % b)
+    L = gpu_layer(cfg, w16, bits, order)
+    O = oracle_layer(cfg, w16, bits)
+    toks = list(range(0, 1100, 7)) + [1099]
+    e16, e32, _, _ = _forward_parity(cfg, L, O, synth.activations(cfg), lg, tokens=toks, w_round=True)
+    assert e16 <= TOL16 and e32 <= TOL32, (e16, e32)
     L.close()

@@ -177,6 +177,40 @@ def test_mixed_pages_equal_dense_moe_of_dequantized_weights():
     np.testing.assert_allclose(yr, refr, rtol=1e-9, atol=1e-9 * np.abs(refr).max())
 
 
+def _bf16_rne(a32):
+    """float32 -> bfloat16 value (round to nearest even), by the bit formula."""
+    u = np.asarray(a32, np.float32).view(np.uint32).astype(np.uint64)
+    r = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16) << 16
+    return r.astype(np.uint32).view(np.float32).astype(np.float64)
+
+
+@pytest.mark.parametrize("act", [F16, BF16])
+def test_w_round_equals_dense_moe_of_rounded_weights(act):
+    """w_round: a quantized weight enters as fl32(z + c*s) rounded to the
+    activation format; 16-bit pages are unchanged. Reference: numpy's own
+    float32 / float16 conversions (bfloat16 by the round-to-nearest-even bit
+    formula) applied to the dense dequantized weights."""
+    cfg = _small_cfg(E=3, H=256, F=192, T=5, act=act, sdt=act)
+    L, _ = _layer(cfg)
+    x16 = synth.activations(cfg)
+    ids, w = oracle.route(synth.logits(cfg), cfg.K)
+    dense = []
+    for p in range(3):
+        W = _dequantized_dense(L, p)
+        q = np.repeat(np.stack([np.array(L.bits[p][e]) for e in range(cfg.E)]) != 16, cfg.R, axis=1)
+        W32 = W.astype(np.float32)
+        Wr = W32.astype(np.float16).astype(np.float64) if act == F16 else _bf16_rne(W32)
+        dense.append(np.where(q[:, :, None], Wr, W))
+        assert (dense[-1] != W).any()
+    y = L.forward(x16, ids, w, w_round=True)
+    ref = _dense_moe(oracle.decode16(x16, act), *dense, ids, w)
+    np.testing.assert_allclose(y, ref, rtol=1e-12, atol=1e-12 * np.abs(ref).max())
+    # with every page at 16 bits the option changes nothing
+    bits16 = [np.full((cfg.E, cfg.nrb(p)), 16, np.int32) for p in range(3)]
+    L16, _ = _layer(cfg, bits16)
+    assert np.array_equal(L16.forward(x16, ids, w, w_round=True), L16.forward(x16, ids, w))
+
+
 def test_zero_up_projection_gives_zero_output():
     """P9: W_up = 0 -> h = 0 -> y = 0 exactly."""
     cfg = _small_cfg()
