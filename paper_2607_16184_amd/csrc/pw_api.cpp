@@ -78,20 +78,27 @@ struct ProfScope {
 bool mult_of_256(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 255u) == 0; }
 
 // Device workspace layout of pw_moe_paged_gemm.
+enum class GemmPath { kDecode, kStream, kTiled };
+
 struct WsLayout {
   size_t h_off, h_bytes, op_off, op_bytes, total;
   int nsplit, kb_per_split, mtb;
-  bool tiled;   // large per-expert token counts: the LDS-tiled GEMM
+  GemmPath path;
 };
 
-// The LDS-tiled GEMM (256 x 256 tiles) pays off once an expert's slots fill
-// its tiles; it needs 64-row staging inside one page, 256-row down blocks and
-// one scale/zero group per 64-value stage.
-bool use_tiled(const pw_layer_desc& d, size_t S) {
+// Which GEMM kernels serve a call, from the expected slots per expert
+// S / E: up to 32, the decode kernels (weights streamed in registers, exact
+// code-domain arithmetic, M tiles of 16 slots); up to 127, the streaming
+// kernel with 64-slot tiles; from 128, the LDS-tiled 256 x 256 kernel. The
+// last two need 32/64-row staging inside one page, 128-row down blocks and
+// 32-bit activation row offsets (and the tiled kernel 256-row down blocks).
+GemmPath pick_path(const pw_layer_desc& d, size_t S) {
   const size_t expect = (S + d.E - 1) / d.E;
-  // activation row offsets are 32-bit in that kernel
   const bool fits = S * d.F * 2 < (size_t(1) << 32) && S * d.H * 2 < (size_t(1) << 32);
-  return expect >= 128 && fits && d.G >= 64 && d.H % 256 == 0 && d.F % 128 == 0 && d.R % 64 == 0;
+  const bool tiles = fits && d.G >= 64 && d.R % 64 == 0 && d.F % 128 == 0;
+  if (expect >= 128 && tiles && d.H % 256 == 0) return GemmPath::kTiled;
+  if (expect > 32 && tiles && d.H % 128 == 0) return GemmPath::kStream;
+  return GemmPath::kDecode;
 }
 
 WsLayout ws_layout(const pw_layer_desc& d, int T, int K) {
@@ -99,11 +106,12 @@ WsLayout ws_layout(const pw_layer_desc& d, int T, int K) {
   const size_t S = static_cast<size_t>(T) * K;
   const int nkbF = d.F / 128;
   const int expect = static_cast<int>((S + d.E - 1) / d.E);
-  // Split the down projection's K = F when too few (expert, row-block) units
-  // exist to fill the chip; deterministic in (desc, T, K).
+  w.path = pick_path(d, S);
+  // The decode kernels split the down projection's K = F when too few
+  // (expert, row-block) units exist to fill the chip; deterministic in
+  // (desc, T, K).
   int nsplit = 1;
-  w.tiled = use_tiled(d, S);
-  if (S <= 4096 && !w.tiled) {
+  if (w.path == GemmPath::kDecode && S <= 4096) {
     const size_t active = std::min<size_t>(d.E, S);
     const size_t units = active * (d.H / 64);
     nsplit = static_cast<int>(std::max<size_t>(1, std::min<size_t>(8, 2048 / std::max<size_t>(units, 1))));
@@ -111,7 +119,7 @@ WsLayout ws_layout(const pw_layer_desc& d, int T, int K) {
   nsplit = std::min(nsplit, nkbF);
   w.kb_per_split = (nkbF + nsplit - 1) / nsplit;
   w.nsplit = (nkbF + w.kb_per_split - 1) / w.kb_per_split;
-  w.mtb = expect <= 12 ? 1 : expect <= 24 ? 2 : 4;
+  w.mtb = expect <= 12 ? 1 : 2;
   auto al = [](size_t b) { return (b + 255) / 256 * 256; };
   w.h_off = 0;
   w.h_bytes = al(S * d.F * 2);
@@ -337,12 +345,16 @@ pw_status pw_moe_paged_gemm(const pw_layer* Lc, const void* x, int T, int K, con
   hipError_t e;
   {
     ProfScope ps(L, PW_PH_GATEUP, st);
-    e = wl.tiled ? pw::launch_tgemm(a, true, st) : pw::launch_gateup(a, st);
+    e = wl.path == GemmPath::kTiled    ? pw::launch_tgemm(a, true, st)
+        : wl.path == GemmPath::kStream ? pw::launch_sgemm(a, true, st)
+                                       : pw::launch_gateup(a, st);
   }
   if (e != hipSuccess) return hip_fail(e, "gate/up launch");
   {
     ProfScope ps(L, PW_PH_DOWN, st);
-    e = wl.tiled ? pw::launch_tgemm(a, false, st) : pw::launch_down(a, st);
+    e = wl.path == GemmPath::kTiled    ? pw::launch_tgemm(a, false, st)
+        : wl.path == GemmPath::kStream ? pw::launch_sgemm(a, false, st)
+                                       : pw::launch_down(a, st);
   }
   if (e != hipSuccess) return hip_fail(e, "down launch");
   {

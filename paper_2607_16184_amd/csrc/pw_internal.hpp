@@ -69,5 +69,7 @@ hipError_t launch_down(const GemmArgs& a, hipStream_t st);
 hipError_t launch_combine(const GemmArgs& a, hipStream_t st);
 // large per-expert slot counts: LDS-tiled GEMM (256 x 256 tiles)
 hipError_t launch_tgemm(const GemmArgs& a, bool gateup, hipStream_t st);
+// small and medium slot counts: register-streamed tiles of 16/32/64 slots
+hipError_t launch_sgemm(const GemmArgs& a, bool gateup, hipStream_t st);
 
 }  // namespace pw

@@ -833,18 +833,12 @@ static hipError_t gemm_launch(const GemmArgs& a, bool gateup, hipStream_t st) {
   const dim3 block(256);
   if (gateup) {
     const dim3 grid(a.E * (a.F / 32));
-    switch (a.mtb) {
-      case 1: hipLaunchKernelGGL((k_gateup<ACT, 1, GPK>), grid, block, 0, st, a); break;
-      case 2: hipLaunchKernelGGL((k_gateup<ACT, 2, GPK>), grid, block, 0, st, a); break;
-      default: hipLaunchKernelGGL((k_gateup<ACT, 4, GPK>), grid, block, 0, st, a); break;
-    }
+    if (a.mtb == 1) hipLaunchKernelGGL((k_gateup<ACT, 1, GPK>), grid, block, 0, st, a);
+    else hipLaunchKernelGGL((k_gateup<ACT, 2, GPK>), grid, block, 0, st, a);
   } else {
     const dim3 grid(a.E * (a.H / 64) * a.nsplit);
-    switch (a.mtb) {
-      case 1: hipLaunchKernelGGL((k_down<ACT, 1, GPK>), grid, block, 0, st, a); break;
-      case 2: hipLaunchKernelGGL((k_down<ACT, 2, GPK>), grid, block, 0, st, a); break;
-      default: hipLaunchKernelGGL((k_down<ACT, 4, GPK>), grid, block, 0, st, a); break;
-    }
+    if (a.mtb == 1) hipLaunchKernelGGL((k_down<ACT, 1, GPK>), grid, block, 0, st, a);
+    else hipLaunchKernelGGL((k_down<ACT, 2, GPK>), grid, block, 0, st, a);
   }
   return hipGetLastError();
 }

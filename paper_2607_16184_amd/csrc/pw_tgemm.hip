@@ -311,6 +311,223 @@ __global__ __launch_bounds__(kThreads) void k_tgemm(const GemmArgs a, int nblk, 
   }
 }
 
+// ---------------------------------------------------------------------------
+// Streaming paged GEMM for small and medium per-expert slot counts (decode,
+// fine-grained experts): HBM-bound, so the design goal is bytes in flight.
+// A workgroup of 4 waves covers 128 weight rows (gate/up: 64 rows of gate and
+// the same 64 rows of up; down: 128 rows) and MT slots of one expert. Each wave
+// streams 32 rows of one page through a register ring of D stages (64 values
+// of K each, about 8 KiB per wave for every format) and computes them against
+// all MT slots itself, so weights never pass through LDS; the MT x 64 slice of
+// activations is staged once per stage for the four waves. Quantized weights
+// are dequantized in registers to fl32(z + c s) rounded to the activation
+// dtype, as in the large-tile kernel.
+// ---------------------------------------------------------------------------
+
+template <int B> constexpr int sg_depth() { return B == 16 ? 2 : B == 8 ? 4 : 8; }
+constexpr int kSgStagePad = 8;   // stage counts are padded to a multiple of every depth
+
+template <int MT> constexpr int sg_xbuf() { return MT * kTK * 2; }            // one activation buffer
+template <int MT> constexpr int sg_lds() { return 2 * sg_xbuf<MT>() + 4 * 1024; } // + a discard area
+
+// The loop body has no branches (every load and store is unconditional, with
+// clamped indices), so the compiler's wait counts stay static and the ring's
+// D stages really are in flight.
+template <int ACT, int SDT, int B, int MT>
+__device__ __forceinline__ void sg_loop(uint8_t* lds, const uint8_t* tile0, const uint8_t* szrow,
+                                        const uint8_t* xrow, int xf, int nkb, int R, int gshift, int wave,
+                                        f32x4 (&acc)[2][MT / 16]) {
+  constexpr int D = sg_depth<B>();
+  constexpr int XF = MT >= 32 ? MT / 32 : 1;       // activation fragments per wave
+  constexpr int XB = sg_xbuf<MT>();
+  const int lane = lane_id(), lg = lane >> 4;
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int u = 0; u < MT / 16; ++u) acc[t][u] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int nstage = nkb * 128 / kTK;
+  const int npad = (nstage + kSgStagePad - 1) / kSgStagePad * kSgStagePad;
+  auto group_of = [&](int st) { return (st * kTK) >> gshift; };
+  // waves past the tile's activation fragments write a discard area instead
+  const int xoff = xf < MT / 8 ? 1024 * xf : 2 * XB + 1024 * wave - 1024 * xf;
+  auto fetch_w = [&](WStage<B>& w, int st) {
+    const int s = min(st, nstage - 1);
+    w_fetch<B>(w, tile0, szrow, s >> 1, s & 1, group_of(s), nkb, R);
+  };
+  // activation fragment q of this wave: xf + q (slot tile (xf + q) / 2, k-step (xf + q) mod 2)
+  auto fetch_x = [&](u32x4 (&xv)[XF], int st) {
+    const int s = min(st, nstage - 1);
+#pragma unroll
+    for (int q = 0; q < XF; ++q)
+      xv[q] = ld16(xrow + static_cast<size_t>(s * kTK + 32 * ((xf + q) & 1) + 8 * lg) * 2);
+  };
+  auto store_x = [&](const u32x4 (&xv)[XF], int b) {
+    uint8_t* d = lds + (xf < MT / 8 ? b * XB : 0) + xoff + 16 * lane;
+#pragma unroll
+    for (int q = 0; q < XF; ++q) *reinterpret_cast<u32x4*>(d + 1024 * q) = xv[q];
+  };
+  WStage<B> ring[D];
+  u32x4 xv[XF];
+#pragma unroll
+  for (int j = 0; j < D; ++j) fetch_w(ring[j], j);
+  fetch_x(xv, 0);
+  store_x(xv, 0);
+  __syncthreads();
+  for (int base = 0; base < npad; base += D) {
+#pragma unroll
+    for (int j = 0; j < D; ++j) {
+      const int st = base + j;
+      const uint8_t* cur = lds + (st & 1) * XB + 16 * lane;
+      fetch_x(xv, st + 1);
+      __builtin_amdgcn_sched_barrier(0);   // issue the activation load first: its wait ends the stage
+      const bool live = st < nstage;
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        u32x4 bx[MT / 16];
+#pragma unroll
+        for (int u = 0; u < MT / 16; ++u) bx[u] = ld16(cur + 1024 * (2 * u + i));
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+          u32x4 aw = w_piece<ACT, SDT, B>(ring[j], 2 * t + i);
+          if (!live) aw = u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+          for (int u = 0; u < MT / 16; ++u) acc[t][u] = mma<ACT>(aw, bx[u], acc[t][u]);
+        }
+      }
+      fetch_w(ring[j], st + D);
+      store_x(xv, (st + 1) & 1);
+      __syncthreads();
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+}
+
+template <int ACT, int SDT, bool GATEUP, int MT>
+__global__ __launch_bounds__(256) void k_sgemm(const GemmArgs a, int nblk, int mtmax) {
+  __shared__ __attribute__((aligned(16))) uint8_t lds[sg_lds<MT>()];
+  const int per_xcd = gridDim.x / 8;
+  const int logical = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+  const int band = logical / (kGN * mtmax), inb = logical % (kGN * mtmax);
+  const int nb = band * kGN + inb % kGN, mt = inb / kGN;
+  if (nb >= nblk) return;
+  int e = 0, off_e = 0, n_e = 0, m0 = 0;
+  {
+    int rest = mt;
+    bool found = false;
+    for (int x = 0; x < a.E && !found; ++x) {
+      const int o = clampi(a.offsets[x], 0, a.S);
+      const int n = clampi(a.offsets[x + 1], o, a.S) - o;
+      const int cnt = (n + MT - 1) / MT;
+      if (rest < cnt) {
+        e = x;
+        off_e = o;
+        n_e = n;
+        m0 = rest * MT;
+        found = true;
+      } else {
+        rest -= cnt;
+      }
+    }
+    if (!found) return;
+  }
+  const int wave = threadIdx.x >> 6, lane = lane_id(), lc = lane & 15, lg = lane >> 4;
+  const int K = GATEUP ? a.H : a.F;
+  const int R = a.R;
+  int proj, grow;
+  if (GATEUP) {
+    proj = wave >> 1;                       // waves 0-1: gate; 2-3: up
+    grow = nb * 64 + 32 * (wave & 1);
+  } else {
+    proj = PW_DOWN;
+    grow = nb * 128 + 32 * wave;
+  }
+  const int rb = grow / R, lr0 = grow - rb * R;
+  const pw_page_entry ent = a.table[(static_cast<size_t>(e) * 3 + proj) * a.nrb_max + rb];
+  const int bits = ent.bits;
+  const size_t tbytes = bits == 16 ? 4096 : bits == 8 ? 2048 : 1024;
+  const uint8_t* tile0 = a.pool + ent.data_off + static_cast<size_t>(lr0 / 16) * (K / 128) * tbytes;
+  const uint8_t* szrow = a.pool + ent.sz_off + static_cast<size_t>(lr0 + lc) * 4;
+  // this wave's activation fragments start at xf = wave * XF (slot tile xf / 2)
+  constexpr int XF = MT >= 32 ? MT / 32 : 1;
+  const int xf = wave * XF;
+  const int m = clampi(m0 + (xf >> 1) * 16 + lc, 0, n_e - 1);
+  const uint8_t* xrow;
+  if (GATEUP) {
+    const int slot = clampi(a.sorted_slot[off_e + m], 0, a.S - 1);
+    xrow = reinterpret_cast<const uint8_t*>(a.x) + static_cast<size_t>(slot / a.topk) * a.H * 2;
+  } else {
+    xrow = reinterpret_cast<const uint8_t*>(a.h) + static_cast<size_t>(off_e + m) * a.F * 2;
+  }
+  // The host checks that every page is present, so bits is 16, 8 or 4 here; a
+  // wave never leaves early (the loop's barriers need all four).
+  f32x4 acc[2][MT / 16];
+  const int nkb = K / 128;
+  const int gshift = 31 - __builtin_clz(a.G);     // G is a power of two, at least 64
+  if (bits == 16) sg_loop<ACT, SDT, 16, MT>(lds, tile0, szrow, xrow, xf, nkb, R, gshift, wave, acc);
+  else if (bits == 8) sg_loop<ACT, SDT, 8, MT>(lds, tile0, szrow, xrow, xf, nkb, R, gshift, wave, acc);
+  else sg_loop<ACT, SDT, 4, MT>(lds, tile0, szrow, xrow, xf, nkb, R, gshift, wave, acc);
+
+  const int wr = wave & 1;
+  if (GATEUP) {
+    // gate waves hand their 32 x MT accumulators to the up wave of the same rows
+    float* xch = reinterpret_cast<float*>(lds) + wr * (2 * (MT / 16) * 64 * 4);
+    if (proj == PW_GATE) {
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int u = 0; u < MT / 16; ++u)
+          *reinterpret_cast<f32x4*>(xch + ((t * (MT / 16) + u) * 64 + lane) * 4) = acc[t][u];
+    }
+    __syncthreads();
+    if (proj == PW_UP) {
+#pragma unroll
+      for (int u = 0; u < MT / 16; ++u) {
+        const int mm = m0 + u * 16 + lc;
+        if (mm < n_e) {
+#pragma unroll
+          for (int t = 0; t < 2; ++t) {
+            const f32x4 g = *reinterpret_cast<const f32x4*>(xch + ((t * (MT / 16) + u) * 64 + lane) * 4);
+            uint32_t hv[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) hv[r] = rne16(g[r] / (1.0f + expf(-g[r])) * acc[t][u][r], ACT);
+            u32x2 o;
+            o[0] = hv[0] | (hv[1] << 16);
+            o[1] = hv[2] | (hv[3] << 16);
+            *reinterpret_cast<u32x2*>(a.h + static_cast<size_t>(off_e + mm) * a.F + grow + t * 16 + 4 * lg) = o;
+          }
+        }
+      }
+    }
+  } else {
+#pragma unroll
+    for (int u = 0; u < MT / 16; ++u) {
+      const int mm = m0 + u * 16 + lc;
+      if (mm < n_e) {
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+          *reinterpret_cast<f32x4*>(a.opart + static_cast<size_t>(off_e + mm) * a.H + grow + t * 16 + 4 * lg) =
+              acc[t][u];
+      }
+    }
+  }
+}
+
+template <int ACT, int SDT, int MT>
+void sgemm_go(const GemmArgs& a, bool gateup, hipStream_t st) {
+  const int nblk = gateup ? a.F / 64 : a.H / 128;
+  const int mtmax = (a.S + MT - 1) / MT + a.E;
+  const int n = ((nblk + kGN - 1) / kGN * kGN * mtmax + 7) / 8 * 8;
+  if (gateup)
+    hipLaunchKernelGGL((k_sgemm<ACT, SDT, true, MT>), dim3(n), dim3(256), 0, st, a, nblk, mtmax);
+  else
+    hipLaunchKernelGGL((k_sgemm<ACT, SDT, false, MT>), dim3(n), dim3(256), 0, st, a, nblk, mtmax);
+}
+
+template <int ACT, int SDT>
+void sgemm_mt(const GemmArgs& a, bool gateup, hipStream_t st) {
+  sgemm_go<ACT, SDT, 64>(a, gateup, st);
+}
+
 template <int ACT, int SDT>
 void tgemm_go(const GemmArgs& a, bool gateup, int n, int nblk, int mtmax, hipStream_t st) {
   if (gateup)
@@ -334,6 +551,19 @@ hipError_t launch_tgemm(const GemmArgs& a, bool gateup, hipStream_t st) {
   } else {
     if (a.sdt == PW_BF16) tgemm_go<PW_F16, PW_BF16>(a, gateup, n, nblk, mtmax, st);
     else tgemm_go<PW_F16, PW_F16>(a, gateup, n, nblk, mtmax, st);
+  }
+  return hipGetLastError();
+}
+
+// Streaming path (64-slot tiles): per-expert slot counts between the decode
+// kernels' range and the large-tile kernel's.
+hipError_t launch_sgemm(const GemmArgs& a, bool gateup, hipStream_t st) {
+  if (a.act == PW_BF16) {
+    if (a.sdt == PW_BF16) sgemm_mt<PW_BF16, PW_BF16>(a, gateup, st);
+    else sgemm_mt<PW_BF16, PW_F16>(a, gateup, st);
+  } else {
+    if (a.sdt == PW_BF16) sgemm_mt<PW_F16, PW_BF16>(a, gateup, st);
+    else sgemm_mt<PW_F16, PW_F16>(a, gateup, st);
   }
   return hipGetLastError();
 }

@@ -182,9 +182,10 @@ def test_zero_up_projection_gives_zero():
 
 
 # Large per-expert slot counts (at least 128 expected per expert) take the
-# LDS-tiled GEMM, which feeds quantized weights to the MFMA as fl32(z + c*s)
-# rounded to the activation dtype: its fp32 output is compared with the oracle
-# read the same way (w_round).
+# LDS-tiled GEMM and medium ones (33..127) the streaming GEMM with 64-slot
+# tiles; both feed quantized weights to the MFMA as fl32(z + c*s) rounded to
+# the activation dtype, so their fp32 output is compared with the oracle read
+# the same way (w_round).
 
 @pytest.mark.parametrize("T", [1000, 1531])
 def test_tiny_tiled_path_parity(T):
@@ -210,5 +211,33 @@ def test_tiny_tiled_uniform_and_empty_experts(b):
     O = oracle_layer(cfg, w16, bits)
     toks = list(range(0, 1100, 7)) + [1099]
     e16, e32, _, _ = _forward_parity(cfg, L, O, synth.activations(cfg), lg, tokens=toks, w_round=True)
+    assert e16 <= TOL16 and e32 <= TOL32, (e16, e32)
+    L.close()
+
+
+@pytest.mark.parametrize("T", [300, 211])
+def test_tiny_stream_path_parity(T):
+    """33..127 expected slots per expert: the streaming GEMM (64-slot tiles)."""
+    cfg, w16, bits, order = case("tiny", T=T)
+    say("tiny stream T=%d" % T)
+    L = gpu_layer(cfg, w16, bits, order)
+    O = oracle_layer(cfg, w16, bits)
+    e16, e32, _, _ = _forward_parity(cfg, L, O, synth.activations(cfg), synth.logits(cfg), w_round=True)
+    assert e16 <= TOL16 and e32 <= TOL32, (e16, e32)
+    L.close()
+
+
+@pytest.mark.parametrize("b", [16, 8, 4])
+def test_tiny_stream_uniform_and_empty_experts(b):
+    """Every page at one bitwidth; 150 tokens all routed to experts 3 and 5
+    (three 64-slot tiles each, the last ragged; six experts with none)."""
+    cfg, w16, _, order = case("tiny", T=150)
+    bits = [np.full((cfg.E, cfg.nrb(p)), b, np.int32) for p in range(3)]
+    lg = synth.logits(cfg).copy()
+    lg[:, [3, 5]] += 100.0
+    say("tiny stream uniform %d, two experts" % b)
+    L = gpu_layer(cfg, w16, bits, order)
+    O = oracle_layer(cfg, w16, bits)
+    e16, e32, _, _ = _forward_parity(cfg, L, O, synth.activations(cfg), lg, w_round=True)
     assert e16 <= TOL16 and e32 <= TOL32, (e16, e32)
     L.close()
