@@ -31,33 +31,60 @@ namespace {
 // ---------------------------------------------------------------------------
 
 constexpr int kMaxTopK = 16;
+constexpr int kRouteLogitsPerLane = 4;            // E <= 256
 
+// One wave per token: lane l holds logits l, l + 64, ...; K rounds of a
+// wave-wide arg-max in (value descending, index ascending) order take the
+// next expert each. The weights use the same fp32 arithmetic as a serial
+// loop: m = the largest selected logit, a_k = exp(l_k - m), w_k = a_k / sum,
+// with the sum taken in k order (renorm) or in expert order over all E.
 __global__ __launch_bounds__(256) void k_route_topk(const float* __restrict__ logits, int T, int E,
                                                     int K, int renorm, int32_t* __restrict__ ids,
                                                     float* __restrict__ w) {
-  const int t = blockIdx.x * blockDim.x + threadIdx.x;
-  if (t >= T) return;
+  const int t = blockIdx.x * 4 + static_cast<int>(threadIdx.x >> 6);
+  if (t >= T) return;   // wave-uniform
+  const int lane = lane_id();
   const float* l = logits + static_cast<size_t>(t) * E;
+  float v[kRouteLogitsPerLane];
+  bool live[kRouteLogitsPerLane];
+#pragma unroll
+  for (int q = 0; q < kRouteLogitsPerLane; ++q) {
+    const int e = lane + 64 * q;
+    live[q] = e < E;
+    v[q] = live[q] ? l[e] : 0.0f;
+  }
   float sv[kMaxTopK];
   int se[kMaxTopK];
-  float pv = __builtin_inff();
-  int pe = -1;
-  for (int k = 0; k < K; ++k) {
-    float bv = 0.0f;
-    int be = -1;
-    for (int e = 0; e < E; ++e) {
-      const float v = l[e];
-      const bool after = (v < pv) || (v == pv && e > pe);   // later in (value desc, index asc)
-      if (after && (be < 0 || v > bv)) {
-        bv = v;
-        be = e;
+#pragma unroll
+  for (int k = 0; k < kMaxTopK; ++k) {
+    if (k < K) {
+      float bv = 0.0f;
+      int be = 0x7fffffff;
+#pragma unroll
+      for (int q = 0; q < kRouteLogitsPerLane; ++q) {
+        const int e = lane + 64 * q;
+        if (live[q] && (be == 0x7fffffff || v[q] > bv || (v[q] == bv && e < be))) {
+          bv = v[q];
+          be = e;
+        }
       }
+#pragma unroll
+      for (int off = 32; off >= 1; off >>= 1) {
+        const float ov = __shfl_xor(bv, off);
+        const int oe = __shfl_xor(be, off);
+        if (oe != 0x7fffffff && (be == 0x7fffffff || ov > bv || (ov == bv && oe < be))) {
+          bv = ov;
+          be = oe;
+        }
+      }
+      sv[k] = bv;
+      se[k] = be;
+#pragma unroll
+      for (int q = 0; q < kRouteLogitsPerLane; ++q)
+        if (lane + 64 * q == be) live[q] = false;
     }
-    sv[k] = bv;
-    se[k] = be;
-    pv = bv;
-    pe = be;
   }
+  if (lane != 0) return;
   const float m = sv[0];
   float sum = 0.0f;
   if (renorm) {
@@ -65,84 +92,84 @@ __global__ __launch_bounds__(256) void k_route_topk(const float* __restrict__ lo
   } else {
     for (int e = 0; e < E; ++e) sum += expf(l[e] - m);
   }
-  for (int k = 0; k < K; ++k) {
-    ids[static_cast<size_t>(t) * K + k] = se[k];
-    w[static_cast<size_t>(t) * K + k] = expf(sv[k] - m) / sum;
+#pragma unroll
+  for (int k = 0; k < kMaxTopK; ++k) {
+    if (k < K) {
+      ids[static_cast<size_t>(t) * K + k] = se[k];
+      w[static_cast<size_t>(t) * K + k] = expf(sv[k] - m) / sum;
+    }
   }
 }
 
-// Token permutation in one workgroup: per-expert counts, exclusive scan, and a
-// stable expert-major placement. Within a wave, lanes holding the same expert
-// are matched with ballots; a per-wave count table gives cross-wave ranks.
-constexpr int kPermThreads = 1024;
-constexpr int kPermWaves = kPermThreads / 64;
+// Token permutation, one workgroup per expert e. Each workgroup builds the
+// full histogram (order-free LDS atomics on counts), so every expert's offset
+// is known everywhere; wave q then owns the q-th quarter of the slots and
+// places e's slots in it in slot order: a ballot per 64 slots gives the ranks,
+// the counts of the earlier quarters the base. No order depends on timing.
+constexpr int kPermThreads = 256;
 constexpr int kMaxExperts = 256;
+
+// Ballots of `e` over slots [q0, q1) in 8-block steps (loads in flight
+// together); calls f(s, rank within the step's block, block mask) for e's slots
+// and returns their count.
+template <class F>
+__device__ __forceinline__ int perm_scan(const int32_t* __restrict__ ids, int q0, int q1, int e, F&& f) {
+  const int lane = lane_id();
+  int c = 0;
+  for (int base = q0; base < q1; base += 8 * 64) {
+    int idb[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int s = base + 64 * q + lane;
+      idb[q] = s < q1 ? ids[s] : -1;
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const unsigned long long m = __ballot(idb[q] == e);
+      if (idb[q] == e) {
+        const int r = static_cast<int>(__builtin_amdgcn_mbcnt_hi(
+            static_cast<uint32_t>(m >> 32), __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(m), 0u)));
+        f(base + 64 * q + lane, c + r);
+      }
+      c += __popcll(m);
+    }
+  }
+  return c;
+}
 
 __global__ __launch_bounds__(kPermThreads) void k_permute(const int32_t* __restrict__ ids, int S,
                                                           int E, int32_t* __restrict__ offsets,
                                                           int32_t* __restrict__ sorted_slot,
                                                           int32_t* __restrict__ slot_pos) {
   __shared__ int cnt[kMaxExperts];
-  __shared__ int off[kMaxExperts];
-  __shared__ int run[kMaxExperts];
-  __shared__ int wcnt[kPermWaves][kMaxExperts];
-  const int tid = threadIdx.x, wave = tid >> 6, lane = lane_id();
-  for (int e = tid; e < E; e += kPermThreads) {
-    cnt[e] = 0;
-    run[e] = 0;
-  }
+  __shared__ int qcnt[4];
+  const int e = blockIdx.x, tid = threadIdx.x, wave = tid >> 6, lane = lane_id();
+  for (int i = tid; i < E; i += kPermThreads) cnt[i] = 0;
   __syncthreads();
   for (int s = tid; s < S; s += kPermThreads) {
     const int id = ids[s];
     if (id >= 0 && id < E) atomicAdd(&cnt[id], 1);
   }
+  const int per = ((S + 3) / 4 + 63) / 64 * 64;
+  const int q0 = min(S, wave * per), q1 = min(S, q0 + per);
+  const int mine = perm_scan(ids, q0, q1, e, [](int, int) {});
+  if (lane == 0) qcnt[wave] = mine;
   __syncthreads();
-  if (tid == 0) {
+  if (e == 0 && tid == 0) {
     int acc = 0;
-    for (int e = 0; e < E; ++e) {
-      off[e] = acc;
-      offsets[e] = acc;
-      acc += cnt[e];
+    for (int x = 0; x < E; ++x) {
+      offsets[x] = acc;
+      acc += cnt[x];
     }
     offsets[E] = acc;
   }
-  __syncthreads();
-  for (int base = 0; base < S; base += kPermThreads) {
-    for (int i = tid; i < kPermWaves * E; i += kPermThreads) wcnt[i / E][i % E] = 0;
-    __syncthreads();
-    const int s = base + tid;
-    int id = -1;
-    if (s < S) {
-      id = ids[s];
-      if (id < 0 || id >= E) id = -1;
-    }
-    unsigned long long todo = __ballot(id >= 0);
-    int rank = 0;
-    while (todo) {
-      const int leader = __builtin_ctzll(todo);
-      const int lid = __shfl(id, leader);
-      const unsigned long long m = __ballot(id == lid);
-      if (id == lid)
-        rank = __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(m >> 32),
-                                         __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(m), 0u));
-      if (lane == leader) wcnt[wave][lid] = __popcll(m);
-      todo &= ~m;
-    }
-    __syncthreads();
-    if (id >= 0) {
-      int pos = off[id] + run[id] + rank;
-      for (int w = 0; w < wave; ++w) pos += wcnt[w][id];
-      sorted_slot[pos] = s;
-      slot_pos[s] = pos;
-    }
-    __syncthreads();
-    for (int e = tid; e < E; e += kPermThreads) {
-      int add = 0;
-      for (int w = 0; w < kPermWaves; ++w) add += wcnt[w][e];
-      run[e] += add;
-    }
-    __syncthreads();
-  }
+  int base = 0;
+  for (int x = 0; x < e; ++x) base += cnt[x];
+  for (int w = 0; w < wave; ++w) base += qcnt[w];
+  perm_scan(ids, q0, q1, e, [&](int s, int r) {
+    sorted_slot[base + r] = s;
+    slot_pos[s] = base + r;
+  });
 }
 
 // ---------------------------------------------------------------------------
@@ -798,13 +825,13 @@ __global__ __launch_bounds__(256) void k_combine(const GemmArgs a) {
 hipError_t launch_route_topk(const float* logits, int T, int E, int K, int renorm, int32_t* ids,
                              float* w, hipStream_t st) {
   if (T <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_route_topk, dim3((T + 255) / 256), dim3(256), 0, st, logits, T, E, K, renorm, ids, w);
+  hipLaunchKernelGGL(k_route_topk, dim3((T + 3) / 4), dim3(256), 0, st, logits, T, E, K, renorm, ids, w);
   return hipGetLastError();
 }
 
 hipError_t launch_permute(const int32_t* ids, int T, int K, int E, int32_t* offsets,
                           int32_t* sorted_slot, int32_t* slot_pos, hipStream_t st) {
-  hipLaunchKernelGGL(k_permute, dim3(1), dim3(kPermThreads), 0, st, ids, T * K, E, offsets,
+  hipLaunchKernelGGL(k_permute, dim3(E), dim3(kPermThreads), 0, st, ids, T * K, E, offsets,
                      sorted_slot, slot_pos);
   return hipGetLastError();
 }
