@@ -218,10 +218,32 @@ def leg_downshift(steps_before=8, steps_after=8):
     t0 = time.time()
     w16 = [synth.expert_weights(cfg, p) for p in range(3)]
     bits = synth.bitmap(cfg)
+    plan = synth.downshift_plan(cfg, bits)
+    # requant alone: the plan's pages in a pool of their own, idle GPU
+    pages = [pg for chunk in plan for pg in chunk]
+    need = sum(pw.pw_page_bytes(cfg, p, 16) + pw.pw_page_bytes(cfg, p, 4) for (_, p, _) in pages)
+    Li = PagedLayer(cfg, int(need * 1.05) + (1 << 20))
+    Li.load_pages(w16, bits, pages)
+    torch.cuda.synchronize()
+    evi = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in plan]
+    pw.pw_profile_read(Li.handle, reset=True)
+    pw.pw_profile_enable(Li.handle, True)
+    for k, chunk in enumerate(plan):
+        evi[k][0].record()
+        Li.requant(chunk, 4)
+        evi[k][1].record()
+        Li.commit()
+        Li.reclaim()
+    torch.cuda.synchronize()
+    pw.pw_profile_enable(Li.handle, False)
+    alone_kernel_ms = pw.pw_profile_read(Li.handle, reset=True)[0][pw.PW_PH_REQUANT]
+    alone_ms = [a.elapsed_time(b) for a, b in evi]
+    alone_moved = sum(pw.pw_page_bytes(cfg, p, 16) + pw.pw_page_bytes(cfg, p, 4) for (_, p, _) in pages)
+    Li.close()
+    del Li
     L = PagedLayer(cfg, PagedLayer.pool_bytes_for(cfg, bits, slack=0.1))
     L.load_pages(w16, bits, synth.pool_order(cfg))
     del w16
-    plan = synth.downshift_plan(cfg, bits)
     log("downshift layer ready in %.1f s" % (time.time() - t0))
     nsteps = steps_before + len(plan) + steps_after
     ins = []
@@ -273,8 +295,11 @@ def leg_downshift(steps_before=8, steps_after=8):
                         "on a side stream, committed at step boundaries",
             "step_ms_before": round(before, 4), "step_ms_during": round(during, 4),
             "step_ms_after": round(after, 4), "decode_slowdown": round(during / before - 1.0, 4),
-            "requant_GBps": round(moved / (rq_ms * 1e-3) / 1e9, 1) if rq_ms else None,
-            "requant_ms_per_chunk": round(rq_ms / max(cnt[pw.PW_PH_REQUANT], 1), 4),
+            "requant_alone_GBps": round(alone_moved / (alone_kernel_ms * 1e-3) / 1e9, 1),
+            "requant_alone_kernel_ms_all_chunks": round(alone_kernel_ms, 4),
+            "requant_alone_call_ms_all_chunks": round(sum(alone_ms), 4),
+            "requant_during_decode_GBps": round(moved / (rq_ms * 1e-3) / 1e9, 1) if rq_ms else None,
+            "requant_ms_per_launch_during_decode": round(rq_ms / max(cnt[pw.PW_PH_REQUANT], 1), 4),
             "bytes_freed": int(freed), "post_switch_weight_GBps": round(post_bytes / (after * 1e-3) / 1e9, 1)}
 
 

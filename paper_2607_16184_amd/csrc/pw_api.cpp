@@ -147,7 +147,9 @@ pw_status run_qjobs(pw_layer* L, const std::vector<pw::QJob>& jobs, int proj, hi
     b.act = d.act;
     b.sdt = d.sdt;
     const int span = d.G > 128 ? d.G / 128 : 1;
-    b.items_per_job = static_cast<uint32_t>(d.R / 16) * static_cast<uint32_t>((K / 128) / span);
+    const int nkb = K / 128;
+    b.nb = 1;
+    b.items_per_job = static_cast<uint32_t>(d.R / 16) * static_cast<uint32_t>(nkb / (span * b.nb));
     b.total_items = b.items_per_job * b.n_jobs;
     for (int j = 0; j < b.n_jobs; ++j) {
       b.job[j] = jobs[base + j];

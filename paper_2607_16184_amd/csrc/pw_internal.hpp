@@ -26,7 +26,8 @@ struct QJobBatch {
   int n_jobs;
   int R, K, G;             // rows, reduction length, group size (same for the batch)
   int act, sdt;
-  uint32_t items_per_job;  // (R / 16) tiles x K-spans
+  int nb;                  // 128-blocks per item (1, 2 or 4; 1 when G > 128)
+  uint32_t items_per_job;  // (R / 16) tiles x (K / 128) / (nb x blocks per group)
   uint32_t total_items;
 };
 

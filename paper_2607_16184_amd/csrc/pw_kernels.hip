@@ -184,10 +184,15 @@ __global__ __launch_bounds__(kPermThreads) void k_permute(const int32_t* __restr
 // ---------------------------------------------------------------------------
 
 
-// The 32 values (k-steps i = 0..3, 8 values each) lane l holds of one block,
-// widened to fp32: from a plain row-major 16-bit source, a tiled 16-bit page,
-// or a quantized page (dequantized as fl32(z + c s)).
-__device__ __forceinline__ void q_read(const QJob& job, const QJobBatch& b, int tau, int blk, float (&v)[32]) {
+// The raw 16-byte pieces lane l holds of one 128-value block of a row tile,
+// for every source format (16-bit: four pieces; 8-bit: two; 4-bit: one), plus
+// the (scale, zero) word of each k-step's group for quantized sources.
+struct QRaw {
+  u32x4 w[4];
+  uint32_t sz[4];
+};
+
+__device__ __forceinline__ void q_load(const QJob& job, const QJobBatch& b, int tau, int blk, QRaw& raw) {
   const int lane = lane_id(), lc = lane & 15, lg = lane >> 4;
   const int K = b.K, nkb = K / 128;
   const size_t tile = static_cast<size_t>(tau) * nkb + blk;
@@ -197,44 +202,67 @@ __device__ __forceinline__ void q_read(const QJob& job, const QJobBatch& b, int 
       const uint8_t* src = job.src_plain
           ? job.src + (static_cast<size_t>(tau * 16 + lc) * K + blk * 128 + 32 * i + 8 * lg) * 2
           : job.src + tile * 4096 + 1024 * i + 16 * lane;
-      const u32x4 d = *reinterpret_cast<const u32x4*>(src);
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        v[8 * i + 2 * q] = val16(d[q], b.act);
-        v[8 * i + 2 * q + 1] = val16(d[q] >> 16, b.act);
-      }
+      raw.w[i] = *reinterpret_cast<const u32x4*>(src);
     }
     return;
   }
-  uint32_t c[32];
   if (job.src_bits == 8) {
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const u32x4 d = *reinterpret_cast<const u32x4*>(job.src + tile * 2048 + 1024 * u + 16 * lane);
-#pragma unroll
-      for (int w = 0; w < 4; ++w)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) c[16 * u + 4 * w + q] = (d[w] >> (8 * q)) & 0xFFu;
-    }
+    for (int u = 0; u < 2; ++u) raw.w[u] = *reinterpret_cast<const u32x4*>(job.src + tile * 2048 + 1024 * u + 16 * lane);
   } else {
-    const u32x4 d = *reinterpret_cast<const u32x4*>(job.src + tile * 1024 + 16 * lane);
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        c[8 * i + 2 * t] = (d[i] >> (4 * t)) & 15u;
-        c[8 * i + 2 * t + 1] = (d[i] >> (16 + 4 * t)) & 15u;
-      }
+    raw.w[0] = *reinterpret_cast<const u32x4*>(job.src + tile * 1024 + 16 * lane);
   }
   const int r = tau * 16 + lc;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int g = (blk * 128 + 32 * i) / b.G;
-    const uint32_t szw = *reinterpret_cast<const uint32_t*>(job.src_sz + (static_cast<size_t>(g) * b.R + r) * 4);
-    const float s = val16(szw, b.sdt), z = val16(szw >> 16, b.sdt);
+    raw.sz[i] = *reinterpret_cast<const uint32_t*>(job.src_sz + (static_cast<size_t>(g) * b.R + r) * 4);
+  }
+}
+
+// The 32 values (k-steps i = 0..3, 8 values each) lane l holds of the block,
+// widened to fp32: 16-bit values, or quantized codes dequantized as
+// fl32(z + c s) (c s is exact in fp32).
+__device__ __forceinline__ void q_widen(const QJob& job, const QJobBatch& b, const QRaw& raw, float (&v)[32]) {
+  if (job.src_bits == 16) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        v[8 * i + 2 * q] = val16(raw.w[i][q], b.act);
+        v[8 * i + 2 * q + 1] = val16(raw.w[i][q] >> 16, b.act);
+      }
+    return;
+  }
+  uint32_t c[32];
+  if (job.src_bits == 8) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int w = 0; w < 4; ++w)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) c[16 * u + 4 * w + q] = (raw.w[u][w] >> (8 * q)) & 0xFFu;
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        c[8 * i + 2 * t] = (raw.w[0][i] >> (4 * t)) & 15u;
+        c[8 * i + 2 * t + 1] = (raw.w[0][i] >> (16 + 4 * t)) & 15u;
+      }
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float s = val16(raw.sz[i], b.sdt), z = val16(raw.sz[i] >> 16, b.sdt);
 #pragma unroll
     for (int q = 0; q < 8; ++q) v[8 * i + q] = z + static_cast<float>(c[8 * i + q]) * s;   // c*s exact
   }
+}
+
+__device__ __forceinline__ void q_read(const QJob& job, const QJobBatch& b, int tau, int blk, float (&v)[32]) {
+  QRaw raw;
+  q_load(job, b, tau, blk, raw);
+  q_widen(job, b, raw, v);
 }
 
 // (scale, zero) bit patterns of a group from its extremes (the quantizer's steps).
@@ -255,20 +283,130 @@ __device__ __forceinline__ uint32_t q_code(float v, uint32_t sb, uint32_t zb, in
   return static_cast<uint32_t>(fminf(fmaxf(c, 0.0f), static_cast<float>(Q)));
 }
 
+// Codes of one block from its values and its group parameters, stored in the
+// destination page's tile layout; the (scale, zero) words are written by the
+// caller. Group g0 covers k-steps 0-3 (G >= 128) or 0-1 and g1 2-3 (G = 64).
+__device__ __forceinline__ void q_store_codes(const QJob& job, const QJobBatch& b, int tau, int blk,
+                                              const float (&v)[32], uint32_t sb0, uint32_t zb0, uint32_t sb1,
+                                              uint32_t zb1, int Q) {
+  const int lane = lane_id();
+  uint32_t c[32];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const bool second = b.G == 64 && i >= 2;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) c[8 * i + q] = q_code(v[8 * i + q], second ? sb1 : sb0, second ? zb1 : zb0, Q, b.sdt);
+  }
+  const size_t tile = static_cast<size_t>(tau) * (b.K / 128) + blk;
+  if (job.dst_bits == 8) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      u32x4 o;
+#pragma unroll
+      for (int w = 0; w < 4; ++w)
+        o[w] = c[16 * u + 4 * w] | (c[16 * u + 4 * w + 1] << 8) | (c[16 * u + 4 * w + 2] << 16) |
+               (c[16 * u + 4 * w + 3] << 24);
+      *reinterpret_cast<u32x4*>(job.dst + tile * 2048 + 1024 * u + 16 * lane) = o;
+    }
+  } else {
+    u32x4 o;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      uint32_t w = 0u;
+#pragma unroll
+      for (int t = 0; t < 4; ++t) w |= (c[8 * i + 2 * t] << (4 * t)) | (c[8 * i + 2 * t + 1] << (16 + 4 * t));
+      o[i] = w;
+    }
+    *reinterpret_cast<u32x4*>(job.dst + tile * 1024 + 16 * lane) = o;
+  }
+}
+
+// Extremes of the block's group(s) across the row's four lane groups.
+__device__ __forceinline__ void q_extremes(const float (&v)[32], int G, float& lo0, float& hi0, float& lo1,
+                                           float& hi1) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      if (G == 64 && i >= 2) {
+        lo1 = fminf(lo1, v[8 * i + q]);
+        hi1 = fmaxf(hi1, v[8 * i + q]);
+      } else {
+        lo0 = fminf(lo0, v[8 * i + q]);
+        hi0 = fmaxf(hi0, v[8 * i + q]);
+      }
+    }
+}
+
+__device__ __forceinline__ void q_rowreduce(float& lo0, float& hi0, float& lo1, float& hi1) {
+  // the row's other values sit in lanes lc + 16, lc + 32, lc + 48
+#pragma unroll
+  for (int m = 16; m <= 32; m <<= 1) {
+    lo0 = fminf(lo0, __shfl_xor(lo0, m));
+    hi0 = fmaxf(hi0, __shfl_xor(hi0, m));
+    lo1 = fminf(lo1, __shfl_xor(lo1, m));
+    hi1 = fmaxf(hi1, __shfl_xor(hi1, m));
+  }
+}
+
+// One wave per item: a 16-row tile over NB consecutive 128-blocks (G <= 128),
+// or over one span of G values (G > 128, NB = 1). With G <= 128 every group
+// lies inside one block, so all NB blocks are loaded first (their loads in
+// flight together) and each block is quantized from registers in one pass.
+template <int NB>
 __global__ __launch_bounds__(256) void k_qjobs(const QJobBatch b) {
   const uint32_t item = blockIdx.x * 4u + (threadIdx.x >> 6);
   if (item >= b.total_items) return;
   const int lane = lane_id(), lc = lane & 15, lg = lane >> 4;
   const int K = b.K, R = b.R, G = b.G, nkb = K / 128;
-  const int span = G > 128 ? G / 128 : 1;          // blocks per item
-  const int nspan = nkb / span;
+  const int span = G > 128 ? G / 128 : 1;          // blocks per group
+  const int nsp = nkb / (span * NB);
   const int j = static_cast<int>(item / b.items_per_job);
   const int rem = static_cast<int>(item % b.items_per_job);
-  const int tau = rem / nspan, sp = rem % nspan;
+  const int tau = rem / nsp, sp = rem % nsp;
   const QJob& job = b.job[j];
   const int r = tau * 16 + lc;
+  const int Q = (1 << job.dst_bits) - 1;
   float v[32];
-  if (job.dst_bits == 16) {          // layout transform of a 16-bit page
+  if (span == 1) {
+    QRaw raw[NB];
+#pragma unroll
+    for (int n = 0; n < NB; ++n) q_load(job, b, tau, sp * NB + n, raw[n]);
+#pragma unroll
+    for (int n = 0; n < NB; ++n) {
+      const int blk = sp * NB + n;
+      q_widen(job, b, raw[n], v);
+      if (job.dst_bits == 16) {      // layout transform of a 16-bit page
+        const size_t tile = static_cast<size_t>(tau) * nkb + blk;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          u32x4 o;
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            o[q] = rne16(v[8 * i + 2 * q], b.act) | (rne16(v[8 * i + 2 * q + 1], b.act) << 16);
+          *reinterpret_cast<u32x4*>(job.dst + tile * 4096 + 1024 * i + 16 * lane) = o;
+        }
+        continue;
+      }
+      float lo0 = __builtin_inff(), hi0 = -__builtin_inff(), lo1 = lo0, hi1 = hi0;
+      q_extremes(v, G, lo0, hi0, lo1, hi1);
+      q_rowreduce(lo0, hi0, lo1, hi1);
+      uint32_t sb0, zb0, sb1 = 0u, zb1 = 0u;
+      q_params(lo0, hi0, Q, b.sdt, &sb0, &zb0);
+      if (G == 64) q_params(lo1, hi1, Q, b.sdt, &sb1, &zb1);
+      q_store_codes(job, b, tau, blk, v, sb0, zb0, sb1, zb1, Q);
+      if (lg == 0) {
+        const int g0 = G == 64 ? 2 * blk : blk;
+        *reinterpret_cast<uint32_t*>(job.dst_sz + (static_cast<size_t>(g0) * R + r) * 4) = sb0 | (zb0 << 16);
+        if (G == 64)
+          *reinterpret_cast<uint32_t*>(job.dst_sz + (static_cast<size_t>(g0 + 1) * R + r) * 4) = sb1 | (zb1 << 16);
+      }
+    }
+    return;
+  }
+  // G > 128: one group spans several blocks; pass 1 finds its extremes, pass 2
+  // re-reads the blocks for the codes
+  if (job.dst_bits == 16) {
     for (int blk = sp * span; blk < (sp + 1) * span; ++blk) {
       q_read(job, b, tau, blk, v);
       const size_t tile = static_cast<size_t>(tau) * nkb + blk;
@@ -282,76 +420,19 @@ __global__ __launch_bounds__(256) void k_qjobs(const QJobBatch b) {
     }
     return;
   }
-  // pass 1: extremes of each group this item touches (one group, or two for G = 64)
   float lo0 = __builtin_inff(), hi0 = -__builtin_inff(), lo1 = lo0, hi1 = hi0;
   for (int blk = sp * span; blk < (sp + 1) * span; ++blk) {
     q_read(job, b, tau, blk, v);
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        if (G == 64 && i >= 2) {
-          lo1 = fminf(lo1, v[8 * i + q]);
-          hi1 = fmaxf(hi1, v[8 * i + q]);
-        } else {
-          lo0 = fminf(lo0, v[8 * i + q]);
-          hi0 = fmaxf(hi0, v[8 * i + q]);
-        }
-      }
+    q_extremes(v, G, lo0, hi0, lo1, hi1);
   }
-  // the row's other values sit in lanes lc + 16, lc + 32, lc + 48
-  lo0 = fminf(lo0, __shfl_xor(lo0, 16));
-  hi0 = fmaxf(hi0, __shfl_xor(hi0, 16));
-  lo1 = fminf(lo1, __shfl_xor(lo1, 16));
-  hi1 = fmaxf(hi1, __shfl_xor(hi1, 16));
-  lo0 = fminf(lo0, __shfl_xor(lo0, 32));
-  hi0 = fmaxf(hi0, __shfl_xor(hi0, 32));
-  lo1 = fminf(lo1, __shfl_xor(lo1, 32));
-  hi1 = fmaxf(hi1, __shfl_xor(hi1, 32));
-  const int Q = (1 << job.dst_bits) - 1;
-  uint32_t sb0, zb0, sb1 = 0u, zb1 = 0u;
+  q_rowreduce(lo0, hi0, lo1, hi1);
+  uint32_t sb0, zb0;
   q_params(lo0, hi0, Q, b.sdt, &sb0, &zb0);
-  if (G == 64) q_params(lo1, hi1, Q, b.sdt, &sb1, &zb1);
-  // pass 2: codes
   for (int blk = sp * span; blk < (sp + 1) * span; ++blk) {
     q_read(job, b, tau, blk, v);
-    uint32_t c[32];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const bool second = G == 64 && i >= 2;
-#pragma unroll
-      for (int q = 0; q < 8; ++q)
-        c[8 * i + q] = q_code(v[8 * i + q], second ? sb1 : sb0, second ? zb1 : zb0, Q, b.sdt);
-    }
-    const size_t tile = static_cast<size_t>(tau) * nkb + blk;
-    if (job.dst_bits == 8) {
-#pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        u32x4 o;
-#pragma unroll
-        for (int w = 0; w < 4; ++w)
-          o[w] = c[16 * u + 4 * w] | (c[16 * u + 4 * w + 1] << 8) | (c[16 * u + 4 * w + 2] << 16) |
-                 (c[16 * u + 4 * w + 3] << 24);
-        *reinterpret_cast<u32x4*>(job.dst + tile * 2048 + 1024 * u + 16 * lane) = o;
-      }
-    } else {
-      u32x4 o;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        uint32_t w = 0u;
-#pragma unroll
-        for (int t = 0; t < 4; ++t) w |= (c[8 * i + 2 * t] << (4 * t)) | (c[8 * i + 2 * t + 1] << (16 + 4 * t));
-        o[i] = w;
-      }
-      *reinterpret_cast<u32x4*>(job.dst + tile * 1024 + 16 * lane) = o;
-    }
+    q_store_codes(job, b, tau, blk, v, sb0, zb0, 0u, 0u, Q);
   }
-  if (lg == 0) {
-    const int g0 = G == 64 ? 2 * sp : sp;
-    *reinterpret_cast<uint32_t*>(job.dst_sz + (static_cast<size_t>(g0) * R + r) * 4) = sb0 | (zb0 << 16);
-    if (G == 64)
-      *reinterpret_cast<uint32_t*>(job.dst_sz + (static_cast<size_t>(g0 + 1) * R + r) * 4) = sb1 | (zb1 << 16);
-  }
+  if (lg == 0) *reinterpret_cast<uint32_t*>(job.dst_sz + (static_cast<size_t>(sp) * R + r) * 4) = sb0 | (zb0 << 16);
 }
 
 __global__ void k_entry_writes(pw_page_entry* table, const EntryWrites w) {
@@ -838,7 +919,10 @@ hipError_t launch_permute(const int32_t* ids, int T, int K, int E, int32_t* offs
 
 hipError_t launch_qjobs(const QJobBatch& b, hipStream_t st) {
   if (b.total_items == 0) return hipSuccess;
-  hipLaunchKernelGGL(k_qjobs, dim3((b.total_items + 3) / 4), dim3(256), 0, st, b);
+  const dim3 grid((b.total_items + 3) / 4), block(256);
+  if (b.nb == 4) hipLaunchKernelGGL(k_qjobs<4>, grid, block, 0, st, b);
+  else if (b.nb == 2) hipLaunchKernelGGL(k_qjobs<2>, grid, block, 0, st, b);
+  else hipLaunchKernelGGL(k_qjobs<1>, grid, block, 0, st, b);
   return hipGetLastError();
 }
 
