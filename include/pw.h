@@ -16,16 +16,22 @@
  *
  * Page formats (the build's reading; the paper's own format is Any-Precision
  * bit-planes, which it pairs with per-bitwidth LUTs):
- *   16-bit: R*K values of the activation dtype, row-major.
- *   8/4-bit: asymmetric group-wise round-to-nearest along K, group size G,
- *     one (scale, zero) pair of dtype sdt per (row, group); weight = z + c*s.
- *     Code block: each row's K codes in blocks of 128; a block holds 16 runs
- *     of 8 codes; run rho (codes [8 rho, 8 rho + 8) of the block) is stored at
- *     run position p with rho = 4*(p mod 4) + p div 4. An 8-bit run is 8 bytes;
- *     a 4-bit run is one little-endian 32-bit word with code 2t at bits
- *     [4t, 4t+4) and code 2t+1 at bits [16+4t, 20+4t).
- *     Scale/zero block (right after the codes): pair index g*R + r holds
- *     (scale, zero) of row r, group g, as two 16-bit values.
+ *   8/4-bit pages are asymmetric group-wise round-to-nearest along K, group
+ *   size G, one (scale, zero) pair of dtype sdt per (row, group); weight =
+ *   z + c*s. 16-bit pages hold values of the activation dtype.
+ *   Layout of every format: the page's R x K values are cut into tiles of 16
+ *   rows x 128 values, stored tile after tile (row-tile major: tile (tau, b)
+ *   at index tau*(K/128) + b). Inside a tile, value (r, k) with lc = r mod 16,
+ *   i = (k mod 128) div 32, lg = (k mod 32) div 8, q = k mod 8 belongs to lane
+ *   l = 16*lg + lc and step i:
+ *     16-bit: 4096-byte tile, value at byte 1024*i + 16*l + 2*q;
+ *     8-bit:  2048-byte tile, code at byte 1024*(i div 2) + 16*l + 8*(i mod 2) + q;
+ *     4-bit:  1024-byte tile, code in the little-endian 32-bit word at byte
+ *             16*l + 4*i, at bits [4t, 4t+4) for q = 2t and [16+4t, 20+4t)
+ *             for q = 2t+1.
+ *   Scale/zero block (8/4-bit, right after the codes): pair index g*R + r
+ *   holds (scale, zero) of row r, group g, as two 16-bit values (scale in the
+ *   low half of the 32-bit pair).
  *   Bytes: M16 = 2RK, M8 = RK + 4R(K/G), M4 = RK/2 + 4R(K/G).
  *   Quantizer: z = largest sdt value <= min(v); r = fl32(max(v) - z);
  *   r == 0 -> s = +0 and all codes 0; else s = smallest sdt value >= fl32(r/Q),

@@ -1,23 +1,25 @@
 // HIP kernels for gfx950 (CDNA4): router, token permutation, group-wise RTN
-// quantize / requantize, the paged gate/up and down GEMMs and the combine.
+// quantize / requantize, the decode-size paged gate/up and down GEMMs and the
+// combine. (The streaming and LDS-tiled GEMMs for larger batches are in
+// pw_tgemm.hip.)
 //
 // GEMM layout. Each wave computes D[n][m] = sum_k W[n][k] * X[m][k] for 16
 // weight rows n (the MFMA A operand) and 16 routed slots m (the B operand)
 // with v_mfma_f32_16x16x32_{bf16,f16}. K is walked in blocks of 128; a block
 // is four MFMA k-steps, and in k-step i lane group j (lanes 16j..16j+15)
 // supplies k = 32i + 8j .. 32i + 8j + 7 of both operands. The page format
-// stores the codes of a lane group's four k-steps contiguously (run rho at
-// position 4*(rho mod 4) + rho div 4), so every weight fragment is one or more
-// 16-byte loads per lane.
+// stores a 16-row x 128-value tile in exactly this lane order (16 contiguous
+// bytes per lane and k-step for 16-bit values), so every weight fragment is
+// one or more 16-byte loads per lane of a contiguous 1 KB row.
 //
 // Quantized pages run in the code domain: the A operand is the code c itself
 // as an exact 16-bit float (int8 codes through an exact conversion; int4
 // codes, and int8 codes with fp16 activations, OR-ed into the mantissa of a
 // constant OFF, giving OFF + c exactly). Per group of G along K the MFMA gives
-// P = sum (c + OFF) x and a second MFMA with an all-ones A operand gives
-// X = sum x; the group's scale s and zero z are then applied in fp32 on the
-// accumulator: acc += s * P + (z - OFF * s) * X, which is sum (z + c s) x.
-// Weights are never rounded: the dequantized value z + c*s enters exactly.
+// P = sum (c + OFF) x, and X = sum x comes from sums taken while the
+// activations are staged; the group's scale s and zero z are then applied in
+// fp32 on the accumulator: acc += s * P + (z - OFF * s) * X, which is
+// sum (z + c s) x. Weights are never rounded: z + c*s enters exactly.
 #include <algorithm>
 
 #include "pw_device.hpp"
