@@ -26,7 +26,8 @@ sys.path.insert(0, ROOT)
 METRIC = "paged mixed-bit MoE layer: weight-read HBM GB/s (decode), MFMA % (prefill)"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 MFMA_PEAK_BF16 = 2.5166e15     # dense bf16 MFMA, flop/s (256 CU x 2.4 GHz x 4096)
-KERNEL_SRC = os.path.join(ROOT, "paper_2607_16184_amd", "csrc", "pw_kernels.hip")
+# sources of the decode kernels the traffic counters describe
+KERNEL_SRC = [os.path.join(ROOT, "paper_2607_16184_amd", "csrc", f) for f in ("pw_kernels.hip", "pw_device.hpp")]
 
 
 def log(msg):
@@ -35,8 +36,11 @@ def log(msg):
 
 
 def kernel_hash():
-    with open(KERNEL_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for path in KERNEL_SRC:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def describe(cfg):
