@@ -27,7 +27,7 @@ METRIC = "paged mixed-bit MoE layer: weight-read HBM GB/s (decode), MFMA % (pref
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 MFMA_PEAK_BF16 = 2.5166e15     # dense bf16 MFMA, flop/s (256 CU x 2.4 GHz x 4096)
 # sources of the decode kernels the traffic counters describe
-KERNEL_SRC = [os.path.join(ROOT, "paper_2607_16184_amd", "csrc", f) for f in ("pw_kernels.hip", "pw_device.hpp")]
+KERNEL_SRC = [os.path.join(ROOT, "paper_2607_16184_amd", "csrc", f) for f in ("pw_decode.hip", "pw_device.hpp")]
 
 
 def log(msg):

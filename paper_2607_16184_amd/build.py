@@ -33,17 +33,39 @@ def _run(cmd):
     return out
 
 
+# Per-file device flags. The decode GEMMs keep their MFMA accumulators in
+# architectural VGPRs: each group's partial product is read back by VALU code
+# right after its last MFMA, and VGPR destinations avoid the AGPR moves.
+SOURCES = {
+    "pw_kernels.hip": [],
+    "pw_decode.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+    "pw_tgemm.hip": [],
+    "pw_api.cpp": [],
+    "pw_state.cpp": [],
+}
+
+
 def build_hip(verbose=False):
+    """Compile every source (in parallel) and link libpagedweight.so."""
     objdir = os.path.join(HERE, "_build")
     os.makedirs(objdir, exist_ok=True)
-    objs = []
-    for src in ("pw_kernels.hip", "pw_tgemm.hip", "pw_api.cpp", "pw_state.cpp"):
+    procs, objs = [], []
+    for src, flags in SOURCES.items():
         obj = os.path.join(objdir, src + ".o")
         extra = ["-x", "hip"] if src.endswith(".hip") else []
-        out = _run([HIPCC] + HIP_FLAGS + extra + ["-c", os.path.join(CSRC, src), "-o", obj])
-        if verbose and out:
-            print(out)
+        cmd = [HIPCC] + HIP_FLAGS + flags + extra + ["-c", os.path.join(CSRC, src), "-o", obj]
+        procs.append((cmd, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)))
         objs.append(obj)
+    failed = []
+    for cmd, p in procs:
+        out = "\n".join(l for l in p.communicate()[0].splitlines() if "packed-fp32-ops' is not a recognized" not in l)
+        if p.returncode != 0:
+            sys.stderr.write(out + "\n")
+            failed.append(os.path.basename(cmd[-3]))
+        elif verbose and out:
+            print(out)
+    if failed:
+        raise RuntimeError("build failed: " + ", ".join(failed))
     tmp = LIB + ".tmp%d" % os.getpid()
     _run([HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC", "-o", tmp] + objs)
     os.replace(tmp, LIB)

@@ -117,7 +117,9 @@ WsLayout ws_layout(const pw_layer_desc& d, int T, int K) {
     nsplit = static_cast<int>(std::max<size_t>(1, std::min<size_t>(8, 2048 / std::max<size_t>(units, 1))));
   }
   nsplit = std::min(nsplit, nkbF);
-  w.kb_per_split = (nkbF + nsplit - 1) / nsplit;
+  // a split holds whole quantization groups (G = 256, 512 span 2, 4 blocks)
+  const int bpg = d.G > 128 ? d.G / 128 : 1;
+  w.kb_per_split = ((nkbF + nsplit - 1) / nsplit + bpg - 1) / bpg * bpg;
   w.nsplit = (nkbF + w.kb_per_split - 1) / w.kb_per_split;
   w.mtb = expect <= 12 ? 1 : 2;
   auto al = [](size_t b) { return (b + 255) / 256 * 256; };

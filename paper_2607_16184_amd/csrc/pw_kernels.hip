@@ -1,25 +1,8 @@
 // HIP kernels for gfx950 (CDNA4): router, token permutation, group-wise RTN
-// quantize / requantize, the decode-size paged gate/up and down GEMMs and the
-// combine. (The streaming and LDS-tiled GEMMs for larger batches are in
-// pw_tgemm.hip.)
-//
-// GEMM layout. Each wave computes D[n][m] = sum_k W[n][k] * X[m][k] for 16
-// weight rows n (the MFMA A operand) and 16 routed slots m (the B operand)
-// with v_mfma_f32_16x16x32_{bf16,f16}. K is walked in blocks of 128; a block
-// is four MFMA k-steps, and in k-step i lane group j (lanes 16j..16j+15)
-// supplies k = 32i + 8j .. 32i + 8j + 7 of both operands. The page format
-// stores a 16-row x 128-value tile in exactly this lane order (16 contiguous
-// bytes per lane and k-step for 16-bit values), so every weight fragment is
-// one or more 16-byte loads per lane of a contiguous 1 KB row.
-//
-// Quantized pages run in the code domain: the A operand is the code c itself
-// as an exact 16-bit float (int8 codes through an exact conversion; int4
-// codes, and int8 codes with fp16 activations, OR-ed into the mantissa of a
-// constant OFF, giving OFF + c exactly). Per group of G along K the MFMA gives
-// P = sum (c + OFF) x, and X = sum x comes from sums taken while the
-// activations are staged; the group's scale s and zero z are then applied in
-// fp32 on the accumulator: acc += s * P + (z - OFF * s) * X, which is
-// sum (z + c s) x. Weights are never rounded: z + c*s enters exactly.
+// quantize / requantize, page-table writes and the combine. The paged GEMMs
+// are in pw_decode.hip (decode-size batches) and pw_tgemm.hip (streaming and
+// LDS-tiled GEMMs for larger batches); all three read the tiled page format
+// described in pw.h.
 #include <algorithm>
 
 #include "pw_device.hpp"
@@ -449,430 +432,6 @@ __global__ void k_clear_table(pw_page_entry* table, size_t n) {
 }
 
 // ---------------------------------------------------------------------------
-// Paged GEMM building blocks
-// ---------------------------------------------------------------------------
-
-// Code-domain offset of a page format (see the file comment).
-template <int ACT, int B>
-struct CodeOff {
-  static constexpr float value = (B == 16) ? 0.0f : (ACT == PW_BF16 ? (B == 4 ? 128.0f : 0.0f) : 1024.0f);
-};
-
-template <int B> struct WF;
-template <> struct WF<16> { u32x4 v[4]; };
-template <> struct WF<8> { u32x4 v[2]; };
-template <> struct WF<4> { u32x4 v[1]; };
-
-// The lane's 16-byte pieces of 128-block blk of its row tile; `tile0` is the
-// tile row's first tile plus 16 * lane.
-template <int B>
-__device__ __forceinline__ void wf_load(WF<B>& f, const uint8_t* tile0, int blk) {
-  const uint8_t* p = tile0 + static_cast<size_t>(blk) * tile_bytes<B>();
-#pragma unroll
-  for (int i = 0; i < tile_bytes<B>() / 1024; ++i) f.v[i] = ld16_nt(p + 1024 * i);
-}
-
-// A operand of k-step i: eight 16-bit values (weights, or codes as floats).
-template <int ACT, int B>
-__device__ __forceinline__ u32x4 wf_op(const WF<B>& f, int i) {
-  if constexpr (B == 16) {
-    return f.v[i];
-  } else if constexpr (B == 8) {
-    const uint32_t d0 = f.v[i >> 1][(i & 1) * 2], d1 = f.v[i >> 1][(i & 1) * 2 + 1];
-    u32x4 o;
-    if constexpr (ACT == PW_BF16) {
-      // bytes -> exact fp32 -> upper halves are the exact bf16 values
-#pragma unroll
-      for (int q = 0; q < 2; ++q) {
-        const uint32_t d = q ? d1 : d0;
-        const float c0 = static_cast<float>(d & 0xFFu), c1 = static_cast<float>((d >> 8) & 0xFFu);
-        const float c2 = static_cast<float>((d >> 16) & 0xFFu), c3 = static_cast<float>(d >> 24);
-        o[2 * q] = __builtin_amdgcn_perm(__float_as_uint(c1), __float_as_uint(c0), 0x07060302u);
-        o[2 * q + 1] = __builtin_amdgcn_perm(__float_as_uint(c3), __float_as_uint(c2), 0x07060302u);
-      }
-    } else {
-      // 0x64 high byte: fp16 1024 + c
-      o[0] = __builtin_amdgcn_perm(0x64646464u, d0, 0x05010400u);
-      o[1] = __builtin_amdgcn_perm(0x64646464u, d0, 0x05030402u);
-      o[2] = __builtin_amdgcn_perm(0x64646464u, d1, 0x05010400u);
-      o[3] = __builtin_amdgcn_perm(0x64646464u, d1, 0x05030402u);
-    }
-    return o;
-  } else {
-    const uint32_t w = f.v[0][i];
-    const uint32_t magic = ACT == PW_BF16 ? 0x43004300u : 0x64006400u;   // 128 / 1024
-    u32x4 o;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) o[q] = ((w >> (4 * q)) & 0x000F000Fu) | magic;
-    return o;
-  }
-}
-
-// acc += s * P + (z - OFF s) * X for the lane's four rows; P is cleared.
-// X[t] is the group's activation sum for this lane's slot (tile t).
-template <int ACT, int B, int NT>
-__device__ __forceinline__ void group_fix(f32x4 (&acc)[NT], f32x4 (&p)[NT], const float (&xs)[NT], u32x4 sz,
-                                          int sdt) {
-  constexpr float off = CodeOff<ACT, B>::value;
-  float s[4], zp[4];
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    s[r] = val16(sz[r], sdt);
-    zp[r] = val16(sz[r] >> 16, sdt) - off * s[r];
-  }
-#pragma unroll
-  for (int t = 0; t < NT; ++t) {
-#pragma unroll
-    for (int r = 0; r < 4; ++r) acc[t][r] += s[r] * p[t][r] + zp[r] * xs[t];
-    p[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-  }
-}
-
-
-// Scale/zero block: 16 bytes = (s, z) of the lane's four output rows.
-__device__ __forceinline__ u32x4 sz_load(const uint8_t* szrow, int g, int R) {
-  return ld16(szrow + static_cast<size_t>(g) * R * 4);
-}
-
-// ---------------------------------------------------------------------------
-// Paged GEMM core: one wave streams 16 rows of one page over a K range.
-//
-// K is processed in chunks of kCK 128-blocks. The activation tile of a chunk
-// (NT*16 slots x kCK*128 values) is staged by the whole workgroup into one of
-// two LDS buffers; the MFMA B operand is read from LDS. Each wave keeps its
-// page's weights for the next chunk in flight in registers while it computes
-// the current one, so the only vector-memory traffic in the loop is the
-// weight stream plus one activation chunk; every wait count is static.
-// Per chunk c:  issue x(c+1) | issue w(c+1) | compute c | LDS <- x(c+1) | barrier
-// ---------------------------------------------------------------------------
-
-constexpr int kCK = 2;                            // 128-blocks per chunk
-constexpr int kXRow = kCK * 128 * 2 + 16;         // LDS bytes per staged activation row
-
-// Per chunk buffer: NT*16 staged rows, then NT*16 x (2 kCK) fp32 sums of
-// 64-value half blocks (the code-domain X of each quantization group).
-template <int NT>
-constexpr int xbuf_bytes() { return NT * 16 * kXRow + NT * 16 * 2 * kCK * 4; }
-template <int NT>
-constexpr int lds_x_bytes() { return 2 * xbuf_bytes<NT>(); }
-
-// Rolling register window of a wave's page: slot j holds one 128-block's
-// weights (and its scale/zero pairs for quantized pages).
-template <int B, int GPK>
-struct Slot {
-  WF<B> w;
-  u32x4 sz[GPK];
-};
-template <int GPK>
-struct Slot<16, GPK> {
-  WF<16> w;
-};
-// Blocks kept in flight per wave: about 8-16 KiB of weights for every format.
-template <int B> constexpr int window() { return B == 4 ? 8 : 4; }
-
-template <int B, int GPK>
-__device__ __forceinline__ void load_slot(Slot<B, GPK>& sl, const uint8_t* wrow, const uint8_t* szrow,
-                                          int b, int lg, int G, int R) {
-  wf_load<B>(sl.w, wrow, b);
-  if constexpr (B != 16) {
-#pragma unroll
-    for (int q = 0; q < GPK; ++q) sl.sz[q] = sz_load(szrow, GPK == 2 ? 2 * b + q : (b * 128) / G, R);
-  }
-}
-
-// The workgroup's activation rows for one chunk (NT*16 rows x kCK*128
-// values): thread tid stages the 16-byte pieces q = tid + 256 j, i.e. row
-// q / kPieces, piece q % kPieces. rowoff[j] are byte offsets of its rows.
-constexpr int kPieces = kCK * 128 / 8;            // 16-byte pieces per row
-constexpr int kRowsPerPass = 256 / kPieces;
-template <int NT> constexpr int x_passes() { return NT * 16 / kRowsPerPass; }
-__device__ __forceinline__ int x_row(int j) { return static_cast<int>(threadIdx.x) / kPieces + kRowsPerPass * j; }
-
-template <int NT>
-struct XStage {
-  u32x4 v[x_passes<NT>()];
-};
-
-template <int NT>
-__device__ __forceinline__ void x_fetch(XStage<NT>& s, const uint8_t* base, const uint32_t (&rowoff)[x_passes<NT>()],
-                                        int kel, int K) {
-  const int col = (threadIdx.x % kPieces) * 8;
-  const int k = min(kel + col, K - 8);
-#pragma unroll
-  for (int j = 0; j < x_passes<NT>(); ++j) s.v[j] = ld16(base + rowoff[j] + static_cast<size_t>(k) * 2);
-}
-
-// Writes the staged rows and, per row, the sums of each 64-value half block
-// (8 consecutive pieces held by 8 consecutive lanes).
-template <int ACT, int NT>
-__device__ __forceinline__ void x_store(const XStage<NT>& s, uint8_t* buf) {
-  const int col = threadIdx.x % kPieces;
-  float* sums = reinterpret_cast<float*>(buf + NT * 16 * kXRow);
-#pragma unroll
-  for (int j = 0; j < x_passes<NT>(); ++j) {
-    *reinterpret_cast<u32x4*>(buf + x_row(j) * kXRow + col * 16) = s.v[j];
-    float acc = 0.0f;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) acc += val16(s.v[j][q], ACT) + val16(s.v[j][q] >> 16, ACT);
-    acc += __shfl_xor(acc, 1);
-    acc += __shfl_xor(acc, 2);
-    acc += __shfl_xor(acc, 4);
-    if ((col & 7) == 0) sums[x_row(j) * (2 * kCK) + (col >> 3)] = acc;
-  }
-}
-
-// LDS stores of this wave complete, then a workgroup barrier (no memory fence:
-// weight loads stay in flight across it).
-__device__ __forceinline__ void lds_barrier() {
-  __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
-  __builtin_amdgcn_s_barrier();
-}
-
-__device__ __forceinline__ bool group_end_g(int GPK, int G, int kb, int i) {
-  return GPK == 2 ? ((i & 1) == 1) : (i == 3 && ((kb + 1) * 128) % G == 0);
-}
-
-// Four k-steps of one 128-block (absolute block index kb). xblk points at the
-// block's 128 values inside the staged chunk; hsum at the chunk's half-block
-// sums and hb0 is this block's first half block.
-template <int ACT, int B, int NT, int GPK>
-__device__ __forceinline__ void compute_block(const Slot<B, GPK>& sl, const uint8_t* xblk, const float* hsum, int hb0,
-                                              int kb, int G, int sdt, f32x4 (&acc)[NT], f32x4 (&p)[NT],
-                                              float (&xs)[NT]) {
-  const int lane = lane_id(), lc = lane & 15, lg = lane >> 4;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const u32x4 aw = wf_op<ACT, B>(sl.w, i);
-#pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      const u32x4 bx = *reinterpret_cast<const u32x4*>(xblk + (t * 16 + lc) * kXRow + (32 * i + 8 * lg) * 2);
-      if constexpr (B == 16) acc[t] = mma<ACT>(aw, bx, acc[t]);
-      else p[t] = mma<ACT>(aw, bx, p[t]);
-    }
-    if constexpr (B != 16) {
-      if constexpr (GPK == 2) {
-        if (i & 1) {
-#pragma unroll
-          for (int t = 0; t < NT; ++t) xs[t] = hsum[(t * 16 + lc) * (2 * kCK) + hb0 + (i >> 1)];
-          group_fix<ACT, B, NT>(acc, p, xs, sl.sz[i >> 1], sdt);
-        }
-      } else if (i == 3) {
-#pragma unroll
-        for (int t = 0; t < NT; ++t)
-          xs[t] += hsum[(t * 16 + lc) * (2 * kCK) + hb0] + hsum[(t * 16 + lc) * (2 * kCK) + hb0 + 1];
-        if (((kb + 1) * 128) % G == 0) {
-          group_fix<ACT, B, NT>(acc, p, xs, sl.sz[0], sdt);
-#pragma unroll
-          for (int t = 0; t < NT; ++t) xs[t] = 0.0f;
-        }
-      }
-    }
-  }
-}
-
-// One wave: acc[t] = W[16 rows] . X[16 slots of tile t]^T over 128-blocks
-// [kb0, kb1). Block b's weights are loaded window() blocks ahead into slot
-// b mod window(); the activation chunk (kCK blocks) of chunk c sits in LDS
-// buffer c mod 2. Per chunk c: fetch x(c+1) | compute and refill | LDS <- x(c+1)
-// | barrier. Every load is unconditional (addresses clamped to the range), so
-// all wait counts are static; the workgroup passes nchunk - 1 barriers here.
-template <int ACT, int B, int NT, int GPK>
-__device__ void wave_gemm(const GemmArgs& a, uint8_t* lds, const uint8_t* xbase, const uint32_t (&rowoff)[x_passes<NT>()],
-                          int K, const uint8_t* wrow, const uint8_t* szrow, int kb0, int kb1, f32x4 (&acc)[NT]) {
-  constexpr int W = window<B>();
-  static_assert(W % kCK == 0, "window must cover whole chunks");
-  const int lg = lane_id() >> 4;
-  const int nkb = kb1 - kb0, kmax = kb1 - 1;
-  const int nchunk = (nkb + kCK - 1) / kCK;
-  f32x4 p[NT];
-  float xs[NT];
-#pragma unroll
-  for (int t = 0; t < NT; ++t) {
-    acc[t] = p[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-    xs[t] = 0.0f;
-  }
-  Slot<B, GPK> win[W];
-  XStage<NT> xr;
-  x_fetch<NT>(xr, xbase, rowoff, kb0 * 128, K);
-#pragma unroll
-  for (int j = 0; j < W; ++j) load_slot<B, GPK>(win[j], wrow, szrow, min(kb0 + j, kmax), lg, a.G, a.R);
-  x_store<ACT, NT>(xr, lds);
-  lds_barrier();
-  for (int base = 0; base < nkb; base += W) {
-#pragma unroll
-    for (int j = 0; j < W; ++j) {
-      const int b = base + j;                       // block index within the range
-      const int c = b / kCK;                        // chunk
-      uint8_t* buf = lds + (c & 1) * xbuf_bytes<NT>();
-      if (j % kCK == 0) x_fetch<NT>(xr, xbase, rowoff, (kb0 + (c + 1) * kCK) * 128, K);
-      if (b < nkb)
-        compute_block<ACT, B, NT, GPK>(win[j], buf + (b % kCK) * 256,
-                                       reinterpret_cast<const float*>(buf + NT * 16 * kXRow), 2 * (b % kCK),
-                                       kb0 + b, a.G, a.sdt, acc, p, xs);
-      load_slot<B, GPK>(win[j], wrow, szrow, min(kb0 + b + W, kmax), lg, a.G, a.R);
-      if (j % kCK == kCK - 1 && c + 1 < nchunk) {
-        x_store<ACT, NT>(xr, lds + ((c + 1) & 1) * xbuf_bytes<NT>());
-        lds_barrier();
-      }
-      __builtin_amdgcn_sched_barrier(0);
-    }
-  }
-}
-
-__device__ __forceinline__ int fmt_code(uint8_t bits) {
-  return bits == 16 ? 0 : bits == 8 ? 1 : bits == 4 ? 2 : -1;
-}
-
-// ---------------------------------------------------------------------------
-// gate/up: a workgroup covers 32 rows of gate and the same 32 rows of up for
-// one expert; waves 0-1 stream gate, waves 2-3 stream up (each in its own
-// page format); the SwiGLU output h = silu(g) * u meets through LDS.
-// ---------------------------------------------------------------------------
-
-template <int ACT, int NT, int GPK>
-__device__ void gateup_unit(const GemmArgs& a, uint8_t* lds, int e, int off_e, int n_e, int r32) {
-  const int tid = threadIdx.x, wave = tid >> 6, lane = lane_id(), lc = lane & 15, lg = lane >> 4;
-  const int proj = wave >> 1, wsub = wave & 1;
-  const int f0 = r32 * 32 + 16 * wsub;
-  const int rb = f0 / a.R, lr0 = f0 - rb * a.R;
-  const pw_page_entry ent = a.table[(static_cast<size_t>(e) * 3 + proj) * a.nrb_max + rb];
-  const int code = fmt_code(ent.bits);
-  const int H = a.H;
-  float* xch = reinterpret_cast<float*>(lds + lds_x_bytes<NT>());   // [2 waves][NT][64 lanes][4]
-  for (int mb = 0; mb < n_e; mb += NT * 16) {
-    const uint8_t* xbase = reinterpret_cast<const uint8_t*>(a.x);
-    uint32_t rowoff[x_passes<NT>()];
-#pragma unroll
-    for (int j = 0; j < x_passes<NT>(); ++j) {
-      const int m = clampi(mb + x_row(j), 0, n_e - 1);
-      const int slot = clampi(a.sorted_slot[off_e + m], 0, a.S - 1);
-      rowoff[j] = static_cast<uint32_t>(slot / a.topk) * static_cast<uint32_t>(H * 2);
-    }
-    f32x4 acc[NT];
-    const int nkb = H / 128;
-    if (code == 0) {
-      const uint8_t* wrow = a.pool + ent.data_off + static_cast<size_t>(lr0 / 16) * (H / 128) * tile_bytes<16>() + 16 * lane;
-      wave_gemm<ACT, 16, NT, GPK>(a, lds, xbase, rowoff, H, wrow, nullptr, 0, nkb, acc);
-    } else if (code == 1) {
-      const uint8_t* wrow = a.pool + ent.data_off + static_cast<size_t>(lr0 / 16) * (H / 128) * tile_bytes<8>() + 16 * lane;
-      const uint8_t* szrow = a.pool + ent.sz_off + static_cast<size_t>(lr0 + 4 * lg) * 4;
-      wave_gemm<ACT, 8, NT, GPK>(a, lds, xbase, rowoff, H, wrow, szrow, 0, nkb, acc);
-    } else {
-      const uint8_t* wrow = a.pool + ent.data_off + static_cast<size_t>(lr0 / 16) * (H / 128) * tile_bytes<4>() + 16 * lane;
-      const uint8_t* szrow = a.pool + ent.sz_off + static_cast<size_t>(lr0 + 4 * lg) * 4;
-      wave_gemm<ACT, 4, NT, GPK>(a, lds, xbase, rowoff, H, wrow, szrow, 0, nkb, acc);
-    }
-    if (proj == 0) {
-#pragma unroll
-      for (int t = 0; t < NT; ++t)
-        *reinterpret_cast<f32x4*>(xch + ((wsub * NT + t) * 64 + lane) * 4) = acc[t];
-    }
-    lds_barrier();
-    if (proj == 1) {
-#pragma unroll
-      for (int t = 0; t < NT; ++t) {
-        const int m = mb + 16 * t + lc;
-        if (m < n_e) {
-          const f32x4 g = *reinterpret_cast<const f32x4*>(xch + ((wsub * NT + t) * 64 + lane) * 4);
-          uint32_t hv[4];
-#pragma unroll
-          for (int r = 0; r < 4; ++r) hv[r] = rne16(g[r] / (1.0f + expf(-g[r])) * acc[t][r], ACT);
-          u32x2 o;
-          o[0] = hv[0] | (hv[1] << 16);
-          o[1] = hv[2] | (hv[3] << 16);
-          *reinterpret_cast<u32x2*>(a.h + static_cast<size_t>(off_e + m) * a.F + f0 + 4 * lg) = o;
-        }
-      }
-    }
-    lds_barrier();
-  }
-}
-
-template <int ACT, int NTMAX, int GPK>
-__global__ __launch_bounds__(256) void k_gateup(const GemmArgs a) {
-  __shared__ __attribute__((aligned(16))) uint8_t lds[lds_x_bytes<NTMAX>() + 2 * NTMAX * 64 * 16];
-  const int upe = a.F / 32;
-  const int e = blockIdx.x / upe, r32 = blockIdx.x % upe;
-  const int off_e = clampi(a.offsets[e], 0, a.S);
-  const int n_e = clampi(a.offsets[e + 1], off_e, a.S) - off_e;
-  if (n_e <= 0) return;
-  // every page of the unit must be present; otherwise the whole group returns
-  const int rb = (r32 * 32) / a.R;
-  for (int p = 0; p < 2; ++p)
-    if (fmt_code(a.table[(static_cast<size_t>(e) * 3 + p) * a.nrb_max + rb].bits) < 0) return;
-  if (NTMAX == 1 || n_e <= 16) gateup_unit<ACT, 1, GPK>(a, lds, e, off_e, n_e, r32);
-  else if (NTMAX == 2 || n_e <= 32) gateup_unit<ACT, (NTMAX < 2 ? NTMAX : 2), GPK>(a, lds, e, off_e, n_e, r32);
-  else gateup_unit<ACT, NTMAX, GPK>(a, lds, e, off_e, n_e, r32);
-}
-
-// ---------------------------------------------------------------------------
-// down: a workgroup covers 64 rows of one down page over one K split of F;
-// fp32 partial sums per split, reduced by the combine.
-// ---------------------------------------------------------------------------
-
-template <int ACT, int NT, int GPK>
-__device__ void down_unit(const GemmArgs& a, uint8_t* lds, int e, int off_e, int n_e, int r64, int split,
-                          const pw_page_entry& ent) {
-  const int tid = threadIdx.x, wave = tid >> 6, lane = lane_id(), lc = lane & 15, lg = lane >> 4;
-  const int F = a.F;
-  const int n0 = r64 * 64 + 16 * wave;
-  const int rb = n0 / a.R, lr0 = n0 - rb * a.R;
-  const int kb0 = split * a.kb_per_split;
-  const int kb1 = min(F / 128, kb0 + a.kb_per_split);
-  if (kb0 >= kb1) return;
-  const int code = fmt_code(ent.bits);
-  for (int mb = 0; mb < n_e; mb += NT * 16) {
-    const uint8_t* xbase = reinterpret_cast<const uint8_t*>(a.h);
-    uint32_t rowoff[x_passes<NT>()];
-#pragma unroll
-    for (int j = 0; j < x_passes<NT>(); ++j) {
-      const int m = clampi(mb + x_row(j), 0, n_e - 1);
-      rowoff[j] = static_cast<uint32_t>(off_e + m) * static_cast<uint32_t>(F * 2);
-    }
-    f32x4 acc[NT];
-    if (code == 0) {
-      const uint8_t* wrow = a.pool + ent.data_off + static_cast<size_t>(lr0 / 16) * (F / 128) * tile_bytes<16>() + 16 * lane;
-      wave_gemm<ACT, 16, NT, GPK>(a, lds, xbase, rowoff, F, wrow, nullptr, kb0, kb1, acc);
-    } else if (code == 1) {
-      const uint8_t* wrow = a.pool + ent.data_off + static_cast<size_t>(lr0 / 16) * (F / 128) * tile_bytes<8>() + 16 * lane;
-      const uint8_t* szrow = a.pool + ent.sz_off + static_cast<size_t>(lr0 + 4 * lg) * 4;
-      wave_gemm<ACT, 8, NT, GPK>(a, lds, xbase, rowoff, F, wrow, szrow, kb0, kb1, acc);
-    } else {
-      const uint8_t* wrow = a.pool + ent.data_off + static_cast<size_t>(lr0 / 16) * (F / 128) * tile_bytes<4>() + 16 * lane;
-      const uint8_t* szrow = a.pool + ent.sz_off + static_cast<size_t>(lr0 + 4 * lg) * 4;
-      wave_gemm<ACT, 4, NT, GPK>(a, lds, xbase, rowoff, F, wrow, szrow, kb0, kb1, acc);
-    }
-#pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      const int m = mb + 16 * t + lc;
-      if (m < n_e) {
-        float* dst = a.opart + (static_cast<size_t>(split) * a.S + off_e + m) * a.H + r64 * 64 + 16 * wave + 4 * lg;
-        *reinterpret_cast<f32x4*>(dst) = acc[t];
-      }
-    }
-    lds_barrier();
-  }
-}
-
-template <int ACT, int NTMAX, int GPK>
-__global__ __launch_bounds__(256) void k_down(const GemmArgs a) {
-  __shared__ __attribute__((aligned(16))) uint8_t lds[lds_x_bytes<NTMAX>()];
-  const int upe = a.H / 64;
-  const int split = blockIdx.x % a.nsplit;
-  const int rest = blockIdx.x / a.nsplit;
-  const int e = rest / upe, r64 = rest % upe;
-  const int off_e = clampi(a.offsets[e], 0, a.S);
-  const int n_e = clampi(a.offsets[e + 1], off_e, a.S) - off_e;
-  if (n_e <= 0) return;
-  const int rb = (r64 * 64) / a.R;
-  const pw_page_entry ent = a.table[(static_cast<size_t>(e) * 3 + PW_DOWN) * a.nrb_max + rb];
-  if (fmt_code(ent.bits) < 0) return;
-  if (NTMAX == 1 || n_e <= 16) down_unit<ACT, 1, GPK>(a, lds, e, off_e, n_e, r64, split, ent);
-  else if (NTMAX == 2 || n_e <= 32) down_unit<ACT, (NTMAX < 2 ? NTMAX : 2), GPK>(a, lds, e, off_e, n_e, r64, split, ent);
-  else down_unit<ACT, NTMAX, GPK>(a, lds, e, off_e, n_e, r64, split, ent);
-}
-
-// ---------------------------------------------------------------------------
 // combine: y[t] = sum_k w[t,k] * sum_split opart[split][slot_pos[t,k]]
 // ---------------------------------------------------------------------------
 
@@ -940,31 +499,6 @@ hipError_t launch_clear_table(pw_page_entry* table, size_t n, hipStream_t st) {
   hipLaunchKernelGGL(k_clear_table, dim3(blocks), dim3(256), 0, st, table, n);
   return hipGetLastError();
 }
-
-template <int ACT, int GPK>
-static hipError_t gemm_launch(const GemmArgs& a, bool gateup, hipStream_t st) {
-  const dim3 block(256);
-  if (gateup) {
-    const dim3 grid(a.E * (a.F / 32));
-    if (a.mtb == 1) hipLaunchKernelGGL((k_gateup<ACT, 1, GPK>), grid, block, 0, st, a);
-    else hipLaunchKernelGGL((k_gateup<ACT, 2, GPK>), grid, block, 0, st, a);
-  } else {
-    const dim3 grid(a.E * (a.H / 64) * a.nsplit);
-    if (a.mtb == 1) hipLaunchKernelGGL((k_down<ACT, 1, GPK>), grid, block, 0, st, a);
-    else hipLaunchKernelGGL((k_down<ACT, 2, GPK>), grid, block, 0, st, a);
-  }
-  return hipGetLastError();
-}
-
-static hipError_t gemm_dispatch(const GemmArgs& a, bool gateup, hipStream_t st) {
-  const bool g64 = a.G == 64;
-  if (a.act == PW_BF16) return g64 ? gemm_launch<PW_BF16, 2>(a, gateup, st) : gemm_launch<PW_BF16, 1>(a, gateup, st);
-  return g64 ? gemm_launch<PW_F16, 2>(a, gateup, st) : gemm_launch<PW_F16, 1>(a, gateup, st);
-}
-
-hipError_t launch_gateup(const GemmArgs& a, hipStream_t st) { return gemm_dispatch(a, true, st); }
-
-hipError_t launch_down(const GemmArgs& a, hipStream_t st) { return gemm_dispatch(a, false, st); }
 
 hipError_t launch_combine(const GemmArgs& a, hipStream_t st) {
   if (a.T <= 0) return hipSuccess;

@@ -241,3 +241,27 @@ def test_tiny_stream_uniform_and_empty_experts(b):
     e16, e32, _, _ = _forward_parity(cfg, L, O, synth.activations(cfg), lg, w_round=True)
     assert e16 <= TOL16 and e32 <= TOL32, (e16, e32)
     L.close()
+
+
+# Group sizes above 128 (a group spans 2 or 4 128-blocks; on the decode path
+# the down projection's K splits must hold whole groups) and scale/zero dtypes
+# other than the activation dtype, on each of the three GEMM paths: 16 tokens
+# (4 expected slots per expert) decode, 300 the streaming GEMM, 1000 the tiled.
+@pytest.mark.parametrize("act,sdt,G,H,F,T", [
+    (synth.BF16, synth.F16, 256, 256, 512, 16),
+    (synth.F16, synth.BF16, 512, 512, 1024, 16),
+    (synth.BF16, synth.F16, 128, 256, 512, 16),
+    (synth.F16, synth.BF16, 128, 256, 512, 16),
+    (synth.F16, synth.BF16, 256, 256, 512, 300),
+    (synth.BF16, synth.F16, 512, 512, 1024, 1000),
+])
+def test_tiny_group_sizes_and_scale_dtypes(act, sdt, G, H, F, T):
+    cfg, w16, bits, order = case("tiny", act=act, sdt=sdt, G=G, H=H, F=F, T=T)
+    say("tiny act=%d sdt=%d G=%d H=%d F=%d T=%d" % (act, sdt, G, H, F, T))
+    L = gpu_layer(cfg, w16, bits, order)
+    O = oracle_layer(cfg, w16, bits)
+    toks = None if T <= 16 else list(range(0, T, 9)) + [T - 1]
+    e16, e32, _, _ = _forward_parity(cfg, L, O, synth.activations(cfg), synth.logits(cfg), tokens=toks,
+                                     w_round=T > 16)
+    assert e16 <= TOL16 and e32 <= TOL32, (e16, e32)
+    L.close()
