@@ -156,8 +156,10 @@ template <int GK>
 struct Slot<16, GK> {
   WF<16> w;
 };
-// Blocks kept in flight per wave: about 8-16 KiB of weights for every format.
-template <int B> constexpr int window() { return B == 4 ? 8 : 4; }
+// Blocks kept in flight per wave: 4-8 KiB of weights. Small windows keep the
+// kernel near 160 VGPRs (three waves per SIMD), which hides more latency than
+// deeper per-wave prefetch.
+template <int B> constexpr int window() { return B == 4 ? 4 : 2; }
 
 // Where a wave's page rows live: wave-uniform bases plus per-lane offsets.
 struct PageRows {
