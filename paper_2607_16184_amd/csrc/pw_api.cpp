@@ -137,26 +137,24 @@ pw_status check_hip_last(const char* what) {
 }
 
 // Launch quantize / requant jobs that all share one projection kind.
-pw_status run_qjobs(pw_layer* L, const std::vector<pw::QJob>& jobs, int proj, hipStream_t st) {
+// Quantize / requantize jobs (each with its own K), up to kMaxQJobs per launch.
+pw_status run_qjobs(pw_layer* L, const std::vector<pw::QJob>& jobs, hipStream_t st) {
   const pw_layer_desc& d = L->st.desc;
-  const int K = L->st.kdim(proj);
+  const int span = d.G > 128 ? d.G / 128 : 1;
   for (size_t base = 0; base < jobs.size(); base += pw::kMaxQJobs) {
     pw::QJobBatch b{};
     b.n_jobs = static_cast<int>(std::min<size_t>(pw::kMaxQJobs, jobs.size() - base));
     b.R = d.R;
-    b.K = K;
     b.G = d.G;
     b.act = d.act;
     b.sdt = d.sdt;
-    const int span = d.G > 128 ? d.G / 128 : 1;
-    const int nkb = K / 128;
-    b.nb = 1;
-    b.items_per_job = static_cast<uint32_t>(d.R / 16) * static_cast<uint32_t>(nkb / (span * b.nb));
-    b.total_items = b.items_per_job * b.n_jobs;
+    uint32_t items = 0;
     for (int j = 0; j < b.n_jobs; ++j) {
       b.job[j] = jobs[base + j];
-      b.job[j].item_base = b.items_per_job * j;
+      b.job[j].item_base = items;
+      items += static_cast<uint32_t>(d.R / 16) * static_cast<uint32_t>((b.job[j].K / 128) / span);
     }
+    b.total_items = items;
     ProfScope ps(L, PW_PH_REQUANT, st);
     hipError_t e = pw::launch_qjobs(b, st);
     if (e != hipSuccess) return hip_fail(e, "requant launch");
@@ -254,10 +252,9 @@ pw_status pw_layer_load_page(pw_layer* L, int e, int proj, int rb, int bits, con
   pw_status s = L->st.plan_load(e, proj, rb, bits, &ent, &err);
   if (s != PW_OK) return fail(s, err);
   hipStream_t st = static_cast<hipStream_t>(stream);
-  const int K = L->st.kdim(proj);
-  (void)K;
   // 16-bit: the rows are laid out as tiles; 8/4-bit: quantized into tiles
   pw::QJob j{};
+  j.K = L->st.kdim(proj);
   j.src = static_cast<const uint8_t*>(rows16);
   j.src_sz = nullptr;
   j.dst = L->pool + ent.data_off;
@@ -265,7 +262,7 @@ pw_status pw_layer_load_page(pw_layer* L, int e, int proj, int rb, int bits, con
   j.src_bits = 16;
   j.dst_bits = static_cast<uint8_t>(bits);
   j.src_plain = 1;
-  s = run_qjobs(L, {j}, proj, st);
+  s = run_qjobs(L, {j}, st);
   if (s != PW_OK) {
     L->st.abort_slot(ent, proj);
     return s;
@@ -408,26 +405,24 @@ pw_status pw_requant_blocks(pw_layer* L, int n, const int* e, const int* proj, c
   }
   if (plan.empty()) return PW_OK;
   hipStream_t st = static_cast<hipStream_t>(side_stream);
-  for (int kind = 0; kind < 2; ++kind) {   // 0: gate/up (K = H), 1: down (K = F)
-    std::vector<pw::QJob> jobs;
-    for (const Planned& p : plan) {
-      if ((p.proj == PW_DOWN) != (kind == 1)) continue;
-      pw::QJob j{};
-      j.src = L->pool + p.src.data_off;
-      j.src_sz = p.src.bits == 16 ? nullptr : L->pool + p.src.sz_off;
-      j.dst = L->pool + p.dst.data_off;
-      j.dst_sz = L->pool + p.dst.sz_off;
-      j.src_bits = p.src.bits;
-      j.dst_bits = p.dst.bits;
-      j.src_plain = 0;
-      jobs.push_back(j);
-    }
-    if (jobs.empty()) continue;
-    pw_status s = run_qjobs(L, jobs, kind == 1 ? PW_DOWN : PW_GATE, st);
-    if (s != PW_OK) {
-      rollback();
-      return s;
-    }
+  // one launch for the whole plan (jobs of every projection, each with its K)
+  std::vector<pw::QJob> jobs;
+  for (const Planned& p : plan) {
+    pw::QJob j{};
+    j.src = L->pool + p.src.data_off;
+    j.src_sz = p.src.bits == 16 ? nullptr : L->pool + p.src.sz_off;
+    j.dst = L->pool + p.dst.data_off;
+    j.dst_sz = L->pool + p.dst.sz_off;
+    j.K = L->st.kdim(p.proj);
+    j.src_bits = p.src.bits;
+    j.dst_bits = p.dst.bits;
+    j.src_plain = 0;
+    jobs.push_back(j);
+  }
+  pw_status rs = run_qjobs(L, jobs, st);
+  if (rs != PW_OK) {
+    rollback();
+    return rs;
   }
   void* ev = L->evops.create();
   if (!ev) {

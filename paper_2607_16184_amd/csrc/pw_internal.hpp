@@ -16,18 +16,19 @@ struct QJob {
   uint8_t* dst;            // destination code block
   uint8_t* dst_sz;         // destination scale/zero block
   uint32_t item_base;      // first work item of this job
+  int K;                   // reduction length of the page's rows (H or F)
   uint8_t src_bits, dst_bits;
   uint8_t src_plain;       // 1: src is R x K row-major 16-bit values (not a pool page)
   uint8_t rsv;
 };
 constexpr int kMaxQJobs = 32;
+// A job has (R / 16) tiles x (K / max(G, 128)) work items; job j's items
+// start at job[j].item_base (increasing).
 struct QJobBatch {
   QJob job[kMaxQJobs];
   int n_jobs;
-  int R, K, G;             // rows, reduction length, group size (same for the batch)
+  int R, G;                // rows, group size (same for the batch)
   int act, sdt;
-  int nb;                  // 128-blocks per item (1, 2 or 4; 1 when G > 128)
-  uint32_t items_per_job;  // (R / 16) tiles x (K / 128) / (nb x blocks per group)
   uint32_t total_items;
 };
 

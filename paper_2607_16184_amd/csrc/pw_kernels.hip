@@ -169,6 +169,12 @@ __global__ __launch_bounds__(kPermThreads) void k_permute(const int32_t* __restr
 // ---------------------------------------------------------------------------
 
 
+// Group layout along K: G = 64 (two groups per 128-block), G = 128 (one),
+// G = 256 or 512 (one group spans 2 or 4 blocks). The activation dtype ACT,
+// the scale dtype SDT and the group layout GK are template parameters of the
+// kernel; source and destination bitwidths vary per job.
+enum { kQG64 = 0, kQG128 = 1, kQGBig = 2 };
+
 // The raw 16-byte pieces lane l holds of one 128-value block of a row tile,
 // for every source format (16-bit: four pieces; 8-bit: two; 4-bit: one), plus
 // the (scale, zero) word of each k-step's group for quantized sources.
@@ -177,9 +183,10 @@ struct QRaw {
   uint32_t sz[4];
 };
 
+template <int GK>
 __device__ __forceinline__ void q_load(const QJob& job, const QJobBatch& b, int tau, int blk, QRaw& raw) {
   const int lane = lane_id(), lc = lane & 15, lg = lane >> 4;
-  const int K = b.K, nkb = K / 128;
+  const int K = job.K, nkb = K / 128;
   const size_t tile = static_cast<size_t>(tau) * nkb + blk;
   if (job.src_bits == 16) {
 #pragma unroll
@@ -200,7 +207,7 @@ __device__ __forceinline__ void q_load(const QJob& job, const QJobBatch& b, int 
   const int r = tau * 16 + lc;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const int g = (blk * 128 + 32 * i) / b.G;
+    const int g = GK == kQG64 ? 2 * blk + (i >> 1) : GK == kQG128 ? blk : (blk * 128) / b.G;
     raw.sz[i] = *reinterpret_cast<const uint32_t*>(job.src_sz + (static_cast<size_t>(g) * b.R + r) * 4);
   }
 }
@@ -208,14 +215,15 @@ __device__ __forceinline__ void q_load(const QJob& job, const QJobBatch& b, int 
 // The 32 values (k-steps i = 0..3, 8 values each) lane l holds of the block,
 // widened to fp32: 16-bit values, or quantized codes dequantized as
 // fl32(z + c s) (c s is exact in fp32).
-__device__ __forceinline__ void q_widen(const QJob& job, const QJobBatch& b, const QRaw& raw, float (&v)[32]) {
+template <int ACT, int SDT>
+__device__ __forceinline__ void q_widen(const QJob& job, const QRaw& raw, float (&v)[32]) {
   if (job.src_bits == 16) {
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        v[8 * i + 2 * q] = val16(raw.w[i][q], b.act);
-        v[8 * i + 2 * q + 1] = val16(raw.w[i][q] >> 16, b.act);
+        v[8 * i + 2 * q] = val16(raw.w[i][q], ACT);
+        v[8 * i + 2 * q + 1] = val16(raw.w[i][q] >> 16, ACT);
       }
     return;
   }
@@ -238,51 +246,78 @@ __device__ __forceinline__ void q_widen(const QJob& job, const QJobBatch& b, con
   }
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const float s = val16(raw.sz[i], b.sdt), z = val16(raw.sz[i] >> 16, b.sdt);
+    const float s = val16(raw.sz[i], SDT), z = val16(raw.sz[i] >> 16, SDT);
 #pragma unroll
     for (int q = 0; q < 8; ++q) v[8 * i + q] = z + static_cast<float>(c[8 * i + q]) * s;   // c*s exact
   }
 }
 
+template <int ACT, int SDT, int GK>
 __device__ __forceinline__ void q_read(const QJob& job, const QJobBatch& b, int tau, int blk, float (&v)[32]) {
   QRaw raw;
-  q_load(job, b, tau, blk, raw);
-  q_widen(job, b, raw, v);
+  q_load<GK>(job, b, tau, blk, raw);
+  q_widen<ACT, SDT>(job, raw, v);
 }
 
 // (scale, zero) bit patterns of a group from its extremes (the quantizer's steps).
-__device__ __forceinline__ void q_params(float lo, float hi, int Q, int sdt, uint32_t* sb, uint32_t* zb) {
-  *zb = round_down16(lo, sdt);
-  const float z = val16(*zb, sdt);
+template <int SDT>
+__device__ __forceinline__ void q_params(float lo, float hi, int Q, uint32_t* sb, uint32_t* zb) {
+  *zb = round_down16(lo, SDT);
+  const float z = val16(*zb, SDT);
   const float r = hi - z;
   *sb = 0u;
   if (r == 0.0f) return;
-  *sb = round_up16(r / static_cast<float>(Q), sdt);
-  if (val16(*sb, sdt) * static_cast<float>(Q) < r) *sb += 1u;   // s > 0: next value up
+  *sb = round_up16(r / static_cast<float>(Q), SDT);
+  if (val16(*sb, SDT) * static_cast<float>(Q) < r) *sb += 1u;   // s > 0: next value up
 }
 
-__device__ __forceinline__ uint32_t q_code(float v, uint32_t sb, uint32_t zb, int Q, int sdt) {
-  if (sb == 0u) return 0u;
-  const float d = v - val16(zb, sdt);
-  const float c = rintf(d / val16(sb, sdt));
-  return static_cast<uint32_t>(fminf(fmaxf(c, 0.0f), static_cast<float>(Q)));
+// One group's (scale, zero) as the code computation uses them. A zero scale
+// (every code 0) takes rs = 0, so the fast quotient below is 0.
+struct QGroup {
+  float z, s, rs;   // zero, scale, approximate 1 / s
+  bool fast;        // d * rs decides the code (s far from the fp32 range limits, or s = 0)
+};
+template <int SDT>
+__device__ __forceinline__ QGroup q_group(uint32_t sb, uint32_t zb) {
+  QGroup g;
+  g.z = val16(zb, SDT);
+  g.s = val16(sb, SDT);
+  const bool zero = sb == 0u;
+  g.rs = zero ? 0.0f : __builtin_amdgcn_rcpf(g.s);
+  g.fast = zero || (g.s >= 0x1p-100f && g.s <= 0x1p100f);
+  return g;
+}
+
+// c = clamp(rint(fl32(d / s)), 0, Q) with d = fl32(v - z), d / s in [0, Q]
+// up to rounding. The quotient is first taken as d * rcp(s), within a few
+// fp32 ulp (below 2^-14 for quotients up to 256) of the correctly rounded
+// one, so it decides rint unless it lies within 2^-12 of a half-integer;
+// there, and for extreme scales, the correctly rounded division decides.
+// Either way the code equals the one of the plain definition.
+__device__ __forceinline__ uint32_t q_code(float v, const QGroup& g, int Q) {
+  const float d = v - g.z;
+  const float qa = d * g.rs;
+  float c = rintf(qa);
+  if (!g.fast || fabsf(qa - c) > 0.5f - 0x1p-12f) c = rintf(d / g.s);
+  return static_cast<uint32_t>(__builtin_amdgcn_fmed3f(c, 0.0f, static_cast<float>(Q)));
 }
 
 // Codes of one block from its values and its group parameters, stored in the
 // destination page's tile layout; the (scale, zero) words are written by the
 // caller. Group g0 covers k-steps 0-3 (G >= 128) or 0-1 and g1 2-3 (G = 64).
-__device__ __forceinline__ void q_store_codes(const QJob& job, const QJobBatch& b, int tau, int blk,
-                                              const float (&v)[32], uint32_t sb0, uint32_t zb0, uint32_t sb1,
-                                              uint32_t zb1, int Q) {
+template <int SDT, int GK>
+__device__ __forceinline__ void q_store_codes(const QJob& job, int tau, int blk, const float (&v)[32], uint32_t sb0,
+                                              uint32_t zb0, uint32_t sb1, uint32_t zb1, int Q) {
   const int lane = lane_id();
+  const QGroup g0 = q_group<SDT>(sb0, zb0), g1 = q_group<SDT>(sb1, zb1);
   uint32_t c[32];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const bool second = b.G == 64 && i >= 2;
+    const bool second = GK == kQG64 && i >= 2;
 #pragma unroll
-    for (int q = 0; q < 8; ++q) c[8 * i + q] = q_code(v[8 * i + q], second ? sb1 : sb0, second ? zb1 : zb0, Q, b.sdt);
+    for (int q = 0; q < 8; ++q) c[8 * i + q] = q_code(v[8 * i + q], second ? g1 : g0, Q);
   }
-  const size_t tile = static_cast<size_t>(tau) * (b.K / 128) + blk;
+  const size_t tile = static_cast<size_t>(tau) * (job.K / 128) + blk;
   if (job.dst_bits == 8) {
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
@@ -306,14 +341,29 @@ __device__ __forceinline__ void q_store_codes(const QJob& job, const QJobBatch& 
   }
 }
 
+// 16-bit destination: the block's values rounded to the activation dtype, in
+// tile layout (a layout transform of a plain 16-bit source).
+template <int ACT>
+__device__ __forceinline__ void q_store16(const QJob& job, int tau, int blk, const float (&v)[32]) {
+  const int lane = lane_id();
+  const size_t tile = static_cast<size_t>(tau) * (job.K / 128) + blk;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    u32x4 o;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) o[q] = rne16(v[8 * i + 2 * q], ACT) | (rne16(v[8 * i + 2 * q + 1], ACT) << 16);
+    *reinterpret_cast<u32x4*>(job.dst + tile * 4096 + 1024 * i + 16 * lane) = o;
+  }
+}
+
 // Extremes of the block's group(s) across the row's four lane groups.
-__device__ __forceinline__ void q_extremes(const float (&v)[32], int G, float& lo0, float& hi0, float& lo1,
-                                           float& hi1) {
+template <int GK>
+__device__ __forceinline__ void q_extremes(const float (&v)[32], float& lo0, float& hi0, float& lo1, float& hi1) {
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
-      if (G == 64 && i >= 2) {
+      if (GK == kQG64 && i >= 2) {
         lo1 = fminf(lo1, v[8 * i + q]);
         hi1 = fmaxf(hi1, v[8 * i + q]);
       } else {
@@ -334,90 +384,81 @@ __device__ __forceinline__ void q_rowreduce(float& lo0, float& hi0, float& lo1, 
   }
 }
 
-// One wave per item: a 16-row tile over NB consecutive 128-blocks (G <= 128),
-// or over one span of G values (G > 128, NB = 1). With G <= 128 every group
-// lies inside one block, so all NB blocks are loaded first (their loads in
-// flight together) and each block is quantized from registers in one pass.
-template <int NB>
+// Work item -> (job j, 16-row tile tau, span sp of max(G, 128) values); job
+// j's items start at job[j].item_base.
+struct QItem {
+  int j, tau, sp;
+};
+__device__ __forceinline__ QItem q_item(const QJobBatch& b, uint32_t item, int span) {
+  QItem it;
+  int j = 0;
+  while (j + 1 < b.n_jobs && item >= b.job[j + 1].item_base) ++j;   // wave-uniform
+  const int nsp = (b.job[j].K / 128) / span;
+  const int rem = static_cast<int>(item - b.job[j].item_base);
+  it.j = j;
+  it.tau = rem / nsp;
+  it.sp = rem % nsp;
+  return it;
+}
+
+// One wave per item: a 16-row tile over one span of K. G <= 128 (every group
+// inside one block): one block, quantized from registers in one pass. G > 128:
+// G / 128 blocks, two passes (the group's extremes, then the codes).
+template <int ACT, int SDT, int GK>
 __global__ __launch_bounds__(256) void k_qjobs(const QJobBatch b) {
   const uint32_t item = blockIdx.x * 4u + (threadIdx.x >> 6);
   if (item >= b.total_items) return;
   const int lane = lane_id(), lc = lane & 15, lg = lane >> 4;
-  const int K = b.K, R = b.R, G = b.G, nkb = K / 128;
-  const int span = G > 128 ? G / 128 : 1;          // blocks per group
-  const int nsp = nkb / (span * NB);
-  const int j = static_cast<int>(item / b.items_per_job);
-  const int rem = static_cast<int>(item % b.items_per_job);
-  const int tau = rem / nsp, sp = rem % nsp;
-  const QJob& job = b.job[j];
+  const int R = b.R;
+  const int span = GK == kQGBig ? b.G / 128 : 1;    // blocks per item
+  const QItem it = q_item(b, item, span);
+  const QJob& job = b.job[it.j];
+  const int tau = it.tau, sp = it.sp;
   const int r = tau * 16 + lc;
   const int Q = (1 << job.dst_bits) - 1;
   float v[32];
-  if (span == 1) {
-    QRaw raw[NB];
-#pragma unroll
-    for (int n = 0; n < NB; ++n) q_load(job, b, tau, sp * NB + n, raw[n]);
-#pragma unroll
-    for (int n = 0; n < NB; ++n) {
-      const int blk = sp * NB + n;
-      q_widen(job, b, raw[n], v);
-      if (job.dst_bits == 16) {      // layout transform of a 16-bit page
-        const size_t tile = static_cast<size_t>(tau) * nkb + blk;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          u32x4 o;
-#pragma unroll
-          for (int q = 0; q < 4; ++q)
-            o[q] = rne16(v[8 * i + 2 * q], b.act) | (rne16(v[8 * i + 2 * q + 1], b.act) << 16);
-          *reinterpret_cast<u32x4*>(job.dst + tile * 4096 + 1024 * i + 16 * lane) = o;
-        }
-        continue;
-      }
-      float lo0 = __builtin_inff(), hi0 = -__builtin_inff(), lo1 = lo0, hi1 = hi0;
-      q_extremes(v, G, lo0, hi0, lo1, hi1);
-      q_rowreduce(lo0, hi0, lo1, hi1);
-      uint32_t sb0, zb0, sb1 = 0u, zb1 = 0u;
-      q_params(lo0, hi0, Q, b.sdt, &sb0, &zb0);
-      if (G == 64) q_params(lo1, hi1, Q, b.sdt, &sb1, &zb1);
-      q_store_codes(job, b, tau, blk, v, sb0, zb0, sb1, zb1, Q);
-      if (lg == 0) {
-        const int g0 = G == 64 ? 2 * blk : blk;
-        *reinterpret_cast<uint32_t*>(job.dst_sz + (static_cast<size_t>(g0) * R + r) * 4) = sb0 | (zb0 << 16);
-        if (G == 64)
-          *reinterpret_cast<uint32_t*>(job.dst_sz + (static_cast<size_t>(g0 + 1) * R + r) * 4) = sb1 | (zb1 << 16);
-      }
+  if constexpr (GK != kQGBig) {
+    const int blk = sp;
+    q_read<ACT, SDT, GK>(job, b, tau, blk, v);
+    if (job.dst_bits == 16) {      // layout transform of a 16-bit page
+      q_store16<ACT>(job, tau, blk, v);
+      return;
     }
-    return;
-  }
-  // G > 128: one group spans several blocks; pass 1 finds its extremes, pass 2
-  // re-reads the blocks for the codes
-  if (job.dst_bits == 16) {
+    float lo0 = __builtin_inff(), hi0 = -__builtin_inff(), lo1 = lo0, hi1 = hi0;
+    q_extremes<GK>(v, lo0, hi0, lo1, hi1);
+    q_rowreduce(lo0, hi0, lo1, hi1);
+    uint32_t sb0, zb0, sb1 = 0u, zb1 = 0u;
+    q_params<SDT>(lo0, hi0, Q, &sb0, &zb0);
+    if (GK == kQG64) q_params<SDT>(lo1, hi1, Q, &sb1, &zb1);
+    q_store_codes<SDT, GK>(job, tau, blk, v, sb0, zb0, sb1, zb1, Q);
+    if (lg == 0) {
+      const int g0 = GK == kQG64 ? 2 * blk : blk;
+      *reinterpret_cast<uint32_t*>(job.dst_sz + (static_cast<size_t>(g0) * R + r) * 4) = sb0 | (zb0 << 16);
+      if (GK == kQG64)
+        *reinterpret_cast<uint32_t*>(job.dst_sz + (static_cast<size_t>(g0 + 1) * R + r) * 4) = sb1 | (zb1 << 16);
+    }
+  } else {
+    if (job.dst_bits == 16) {
+      for (int blk = sp * span; blk < (sp + 1) * span; ++blk) {
+        q_read<ACT, SDT, GK>(job, b, tau, blk, v);
+        q_store16<ACT>(job, tau, blk, v);
+      }
+      return;
+    }
+    float lo0 = __builtin_inff(), hi0 = -__builtin_inff(), lo1 = lo0, hi1 = hi0;
     for (int blk = sp * span; blk < (sp + 1) * span; ++blk) {
-      q_read(job, b, tau, blk, v);
-      const size_t tile = static_cast<size_t>(tau) * nkb + blk;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        u32x4 o;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) o[q] = rne16(v[8 * i + 2 * q], b.act) | (rne16(v[8 * i + 2 * q + 1], b.act) << 16);
-        *reinterpret_cast<u32x4*>(job.dst + tile * 4096 + 1024 * i + 16 * lane) = o;
-      }
+      q_read<ACT, SDT, GK>(job, b, tau, blk, v);
+      q_extremes<GK>(v, lo0, hi0, lo1, hi1);
     }
-    return;
+    q_rowreduce(lo0, hi0, lo1, hi1);
+    uint32_t sb0, zb0;
+    q_params<SDT>(lo0, hi0, Q, &sb0, &zb0);
+    for (int blk = sp * span; blk < (sp + 1) * span; ++blk) {
+      q_read<ACT, SDT, GK>(job, b, tau, blk, v);
+      q_store_codes<SDT, GK>(job, tau, blk, v, sb0, zb0, 0u, 0u, Q);
+    }
+    if (lg == 0) *reinterpret_cast<uint32_t*>(job.dst_sz + (static_cast<size_t>(sp) * R + r) * 4) = sb0 | (zb0 << 16);
   }
-  float lo0 = __builtin_inff(), hi0 = -__builtin_inff(), lo1 = lo0, hi1 = hi0;
-  for (int blk = sp * span; blk < (sp + 1) * span; ++blk) {
-    q_read(job, b, tau, blk, v);
-    q_extremes(v, G, lo0, hi0, lo1, hi1);
-  }
-  q_rowreduce(lo0, hi0, lo1, hi1);
-  uint32_t sb0, zb0;
-  q_params(lo0, hi0, Q, b.sdt, &sb0, &zb0);
-  for (int blk = sp * span; blk < (sp + 1) * span; ++blk) {
-    q_read(job, b, tau, blk, v);
-    q_store_codes(job, b, tau, blk, v, sb0, zb0, 0u, 0u, Q);
-  }
-  if (lg == 0) *reinterpret_cast<uint32_t*>(job.dst_sz + (static_cast<size_t>(sp) * R + r) * 4) = sb0 | (zb0 << 16);
 }
 
 __global__ void k_entry_writes(pw_page_entry* table, const EntryWrites w) {
@@ -478,12 +519,23 @@ hipError_t launch_permute(const int32_t* ids, int T, int K, int E, int32_t* offs
   return hipGetLastError();
 }
 
+template <int ACT, int SDT>
+static void qjobs_go(const QJobBatch& b, hipStream_t st) {
+  const dim3 grid((b.total_items + 3) / 4), block(256);
+  if (b.G == 64) hipLaunchKernelGGL((k_qjobs<ACT, SDT, kQG64>), grid, block, 0, st, b);
+  else if (b.G == 128) hipLaunchKernelGGL((k_qjobs<ACT, SDT, kQG128>), grid, block, 0, st, b);
+  else hipLaunchKernelGGL((k_qjobs<ACT, SDT, kQGBig>), grid, block, 0, st, b);
+}
+
 hipError_t launch_qjobs(const QJobBatch& b, hipStream_t st) {
   if (b.total_items == 0) return hipSuccess;
-  const dim3 grid((b.total_items + 3) / 4), block(256);
-  if (b.nb == 4) hipLaunchKernelGGL(k_qjobs<4>, grid, block, 0, st, b);
-  else if (b.nb == 2) hipLaunchKernelGGL(k_qjobs<2>, grid, block, 0, st, b);
-  else hipLaunchKernelGGL(k_qjobs<1>, grid, block, 0, st, b);
+  if (b.act == PW_BF16) {
+    if (b.sdt == PW_BF16) qjobs_go<PW_BF16, PW_BF16>(b, st);
+    else qjobs_go<PW_BF16, PW_F16>(b, st);
+  } else {
+    if (b.sdt == PW_BF16) qjobs_go<PW_F16, PW_BF16>(b, st);
+    else qjobs_go<PW_F16, PW_F16>(b, st);
+  }
   return hipGetLastError();
 }
 
