@@ -87,17 +87,18 @@ struct WsLayout {
 };
 
 // Which GEMM kernels serve a call, from the expected slots per expert
-// S / E: up to 32, the decode kernels (weights streamed in registers, exact
-// code-domain arithmetic, M tiles of 16 slots); up to 127, the streaming
-// kernel with 64-slot tiles; from 128, the LDS-tiled 256 x 256 kernel. The
-// last two need 32/64-row staging inside one page, 128-row down blocks and
-// 32-bit activation row offsets (and the tiled kernel 256-row down blocks).
+// S / E: up to 48, the decode kernels (weights streamed in registers, exact
+// code-domain arithmetic, up to four 16-slot tiles per pass); up to 127, the
+// streaming kernel with 64-slot tiles; from 128, the LDS-tiled 256 x 256
+// kernel. The last two need 32/64-row staging inside one page, 128-row down
+// blocks and 32-bit activation row offsets (and the tiled kernel 256-row down
+// blocks).
 GemmPath pick_path(const pw_layer_desc& d, size_t S) {
   const size_t expect = (S + d.E - 1) / d.E;
   const bool fits = S * d.F * 2 < (size_t(1) << 32) && S * d.H * 2 < (size_t(1) << 32);
   const bool tiles = fits && d.G >= 64 && d.R % 64 == 0 && d.F % 128 == 0;
   if (expect >= 128 && tiles && d.H % 256 == 0) return GemmPath::kTiled;
-  if (expect > 32 && tiles && d.H % 128 == 0) return GemmPath::kStream;
+  if (expect > 48 && tiles && d.H % 128 == 0) return GemmPath::kStream;
   return GemmPath::kDecode;
 }
 
@@ -121,7 +122,9 @@ WsLayout ws_layout(const pw_layer_desc& d, int T, int K) {
   const int bpg = d.G > 128 ? d.G / 128 : 1;
   w.kb_per_split = ((nkbF + nsplit - 1) / nsplit + bpg - 1) / bpg * bpg;
   w.nsplit = (nkbF + w.kb_per_split - 1) / w.kb_per_split;
-  w.mtb = expect <= 12 ? 1 : 2;
+  // slot tiles per pass of the decode kernels: 1, 2 or 4 (with 4, a wave
+  // streams two 16-row weight tiles)
+  w.mtb = expect <= 12 ? 1 : expect <= 20 ? 2 : 4;
   auto al = [](size_t b) { return (b + 255) / 256 * 256; };
   w.h_off = 0;
   w.h_bytes = al(S * d.F * 2);

@@ -2,9 +2,10 @@
 // and down with fp32 partial sums per K split. Used while an expert holds at
 // most a few 16-slot tiles; larger batches go to pw_tgemm.hip.
 //
-// GEMM layout. Each wave computes D[n][m] = sum_k W[n][k] * X[m][k] for 16
-// weight rows n (the MFMA A operand) and 16 routed slots m (the B operand)
-// with v_mfma_f32_16x16x32_{bf16,f16}. K is walked in blocks of 128; a block
+// GEMM layout. Each wave computes D[n][m] = sum_k W[n][k] * X[m][k] for RT
+// tiles of 16 weight rows n (the MFMA A operand) against tiles of 16 routed
+// slots m (the B operand) with v_mfma_f32_16x16x32_{bf16,f16}; each B fragment
+// read from LDS feeds the RT row tiles. K is walked in blocks of 128; a block
 // is four MFMA k-steps, and in k-step i lane group j (lanes 16j..16j+15)
 // supplies k = 32i + 8j .. 32i + 8j + 7 of both operands. The page format
 // stores a 16-row x 128-value tile in exactly this lane order (16 contiguous
@@ -145,40 +146,51 @@ constexpr int xbuf_bytes() { return NT * 16 * kXRow + NT * 16 * 2 * kCK * 4; }
 template <int NT>
 constexpr int lds_x_bytes() { return 2 * xbuf_bytes<NT>(); }
 
-// Rolling register window of a wave's page: slot j holds one 128-block's
-// weights (and its scale/zero pairs for quantized pages).
-template <int B, int GK>
+// A wave streams RT 16-row weight tiles: each B fragment read from LDS feeds
+// RT MFMAs. RT = 1 for up to two slot tiles per expert (decode), RT = 2 for
+// four (the LDS operand traffic per weight byte halves).
+template <int NTMAX> constexpr int row_tiles() { return NTMAX >= 4 ? 2 : 1; }
+
+// Rolling register window of a wave's page: slot j holds one 128-block of the
+// wave's RT row tiles (and their scale/zero pairs for quantized pages).
+template <int B, int GK, int RT>
 struct Slot {
-  WF<B> w;
-  u32x4 sz[groups_per_block<GK>()];
+  WF<B> w[RT];
+  u32x4 sz[RT][groups_per_block<GK>()];
 };
-template <int GK>
-struct Slot<16, GK> {
-  WF<16> w;
+template <int GK, int RT>
+struct Slot<16, GK, RT> {
+  WF<16> w[RT];
 };
-// Blocks kept in flight per wave: 4-8 KiB of weights. Small windows keep the
-// kernel near 160 VGPRs (three waves per SIMD), which hides more latency than
-// deeper per-wave prefetch.
-template <int B> constexpr int window() { return B == 4 ? 4 : 2; }
+// Blocks kept in flight per wave: 4-16 KiB of weights. Small windows keep the
+// kernels at three (RT = 1) or two (RT = 2) waves per SIMD, which hides more
+// latency than deeper per-wave prefetch.
+template <int B, int RT> constexpr int window() { return RT == 1 && B == 4 ? 4 : 2; }
 
 // Where a wave's page rows live: wave-uniform bases plus per-lane offsets.
+// Row tile rt of the wave starts rt * tstride bytes after `tiles` and its
+// scale/zero pairs 64 * rt bytes after `sz`.
 struct PageRows {
-  const uint8_t* tiles;    // first tile of the wave's 16-row tile row
-  const uint8_t* sz;       // scale/zero pair of the tile row's first row, group 0
+  const uint8_t* tiles;    // first tile of the wave's first 16-row tile row
+  const uint8_t* sz;       // scale/zero pair of the wave's first row, group 0
+  size_t tstride;          // bytes of one tile row: (K / 128) tiles
   uint32_t wlo, szlo;      // lane offsets: 16 * lane, 16 * (lane / 16)
   int R;                   // rows per page (pair stride between groups)
   int gshift;              // log2(G / 128) for G >= 128
 };
 
-template <int B, int GK>
-__device__ __forceinline__ void load_slot(Slot<B, GK>& sl, const PageRows& pr, int b) {
-  wf_load<B>(sl.w, pr.tiles, pr.wlo, b);
+template <int B, int GK, int RT>
+__device__ __forceinline__ void load_slot(Slot<B, GK, RT>& sl, const PageRows& pr, int b) {
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) wf_load<B>(sl.w[rt], pr.tiles + rt * pr.tstride, pr.wlo, b);
   if constexpr (B != 16) {
 #pragma unroll
-    for (int q = 0; q < groups_per_block<GK>(); ++q) {
-      const int g = GK == kG64 ? 2 * b + q : GK == kG128 ? b : (b >> pr.gshift);
-      sl.sz[q] = ld16(pr.sz + static_cast<size_t>(g) * pr.R * 4 + pr.szlo);
-    }
+    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+      for (int q = 0; q < groups_per_block<GK>(); ++q) {
+        const int g = GK == kG64 ? 2 * b + q : GK == kG128 ? b : (b >> pr.gshift);
+        sl.sz[rt][q] = ld16(pr.sz + static_cast<size_t>(g) * pr.R * 4 + 64 * rt + pr.szlo);
+      }
   }
 }
 
@@ -269,64 +281,73 @@ __device__ __forceinline__ void lds_barrier() {
 // the staged chunk; hsum at the chunk's half-block sums and hb0 is this
 // block's first half block. gend: a G > 128 group ends with this block.
 // A group's P starts from a zero accumulator in its first k-step.
-template <int ACT, int SDT, int B, int NT, int GK>
-__device__ __forceinline__ void compute_block(const Slot<B, GK>& sl, const uint8_t* xblk, const float* hsum, int hb0,
-                                              bool gend, uint32_t magic, f32x4 (&acc)[NT], f32x4 (&p)[NT],
-                                              float (&xs)[NT]) {
+template <int ACT, int SDT, int B, int NT, int GK, int RT>
+__device__ __forceinline__ void compute_block(const Slot<B, GK, RT>& sl, const uint8_t* xblk, const float* hsum,
+                                              int hb0, bool gend, uint32_t magic, f32x4 (&acc)[RT][NT],
+                                              f32x4 (&p)[RT][NT], float (&xs)[NT]) {
   const int lane = lane_id(), lc = lane & 15, lg = lane >> 4;
   const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const u32x4 aw = wf_op<ACT, B>(sl.w, i, magic);
+    u32x4 aw[RT];
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) aw[rt] = wf_op<ACT, B>(sl.w[rt], i, magic);
     const bool fresh = (GK == kG128 && i == 0) || (GK == kG64 && (i & 1) == 0);
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
       const u32x4 bx = *reinterpret_cast<const u32x4*>(xblk + (t * 16 + lc) * kXRow + (32 * i + 8 * lg) * 2);
-      if constexpr (B == 16) acc[t] = mma<ACT>(aw, bx, acc[t]);
-      else p[t] = mma<ACT>(aw, bx, fresh ? zero : p[t]);
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) {
+        if constexpr (B == 16) acc[rt][t] = mma<ACT>(aw[rt], bx, acc[rt][t]);
+        else p[rt][t] = mma<ACT>(aw[rt], bx, fresh ? zero : p[rt][t]);
+      }
     }
     if constexpr (B != 16) {
       if constexpr (GK == kG64) {
         if (i & 1) {
 #pragma unroll
           for (int t = 0; t < NT; ++t) xs[t] = hsum[(t * 16 + lc) * (2 * kCK) + hb0 + (i >> 1)];
-          group_fix<ACT, SDT, B, NT>(acc, p, xs, sl.sz[i >> 1]);
+#pragma unroll
+          for (int rt = 0; rt < RT; ++rt) group_fix<ACT, SDT, B, NT>(acc[rt], p[rt], xs, sl.sz[rt][i >> 1]);
         }
       } else if constexpr (GK == kG128) {
         if (i == 3) {
 #pragma unroll
           for (int t = 0; t < NT; ++t)
             xs[t] = hsum[(t * 16 + lc) * (2 * kCK) + hb0] + hsum[(t * 16 + lc) * (2 * kCK) + hb0 + 1];
-          group_fix<ACT, SDT, B, NT>(acc, p, xs, sl.sz[0]);
+#pragma unroll
+          for (int rt = 0; rt < RT; ++rt) group_fix<ACT, SDT, B, NT>(acc[rt], p[rt], xs, sl.sz[rt][0]);
         }
       } else if (i == 3) {
 #pragma unroll
         for (int t = 0; t < NT; ++t)
           xs[t] += hsum[(t * 16 + lc) * (2 * kCK) + hb0] + hsum[(t * 16 + lc) * (2 * kCK) + hb0 + 1];
         if (gend) {
-          group_fix<ACT, SDT, B, NT>(acc, p, xs, sl.sz[0]);
 #pragma unroll
-          for (int t = 0; t < NT; ++t) {
-            p[t] = zero;
-            xs[t] = 0.0f;
+          for (int rt = 0; rt < RT; ++rt) {
+            group_fix<ACT, SDT, B, NT>(acc[rt], p[rt], xs, sl.sz[rt][0]);
+#pragma unroll
+            for (int t = 0; t < NT; ++t) p[rt][t] = zero;
           }
+#pragma unroll
+          for (int t = 0; t < NT; ++t) xs[t] = 0.0f;
         }
       }
     }
   }
 }
 
-// One wave: acc[t] = W[16 rows] . X[16 slots of tile t]^T over 128-blocks
+// One wave: acc[rt][t] = W[16 rows of tile rt] . X[16 slots of tile t]^T over 128-blocks
 // [kb0, kb1). Block b's weights are loaded window() blocks ahead into slot
 // b mod window(); the activation chunk (kCK blocks) of chunk c sits in LDS
 // buffer c mod 2. Per chunk c: fetch x(c+1) | compute and refill | LDS <- x(c+1)
 // | barrier. Every load is unconditional (addresses clamped to the range), so
 // all wait counts are static; the workgroup passes nchunk - 1 barriers here.
 // `sums`: some wave of the workgroup reads a quantized page (workgroup-uniform).
-template <int ACT, int SDT, int B, int NT, int GK>
+template <int ACT, int SDT, int B, int NT, int GK, int RT>
 __device__ void wave_gemm(uint8_t* lds, const uint8_t* xbase, const uint32_t (&rowoff)[x_passes<NT>()], int K,
-                          const PageRows& pr, int kb0, int kb1, bool sums, f32x4 (&acc)[NT]) {
-  constexpr int W = window<B>();
+                          const PageRows& pr, int kb0, int kb1, bool sums, f32x4 (&acc)[RT][NT]) {
+  constexpr int W = window<B, RT>();
   static_assert(W % kCK == 0, "window must cover whole chunks");
   const int nkb = kb1 - kb0, kmax = kb1 - 1;
   const int nchunk = (nkb + kCK - 1) / kCK;
@@ -334,18 +355,19 @@ __device__ void wave_gemm(uint8_t* lds, const uint8_t* xbase, const uint32_t (&r
   // OFF in a register: keeps the unpack's constant out of the instruction
   uint32_t magic = code_magic<ACT>();
   asm volatile("" : "+v"(magic));
-  f32x4 p[NT];
+  f32x4 p[RT][NT];
   float xs[NT];
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
-    acc[t] = p[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) acc[rt][t] = p[rt][t] = f32x4{0.f, 0.f, 0.f, 0.f};
     xs[t] = 0.0f;
   }
-  Slot<B, GK> win[W];
+  Slot<B, GK, RT> win[W];
   XStage<NT> xr;
   x_fetch<NT>(xr, xbase, rowoff, kb0 * 128, K);
 #pragma unroll
-  for (int j = 0; j < W; ++j) load_slot<B, GK>(win[j], pr, min(kb0 + j, kmax));
+  for (int j = 0; j < W; ++j) load_slot<B, GK, RT>(win[j], pr, min(kb0 + j, kmax));
   x_store<ACT, NT>(xr, lds, sums);
   lds_barrier();
   for (int base = 0; base < nkb; base += W) {
@@ -356,10 +378,10 @@ __device__ void wave_gemm(uint8_t* lds, const uint8_t* xbase, const uint32_t (&r
       uint8_t* buf = lds + (c & 1) * xbuf_bytes<NT>();
       if (j % kCK == 0) x_fetch<NT>(xr, xbase, rowoff, (kb0 + (c + 1) * kCK) * 128, K);
       if (b < nkb)
-        compute_block<ACT, SDT, B, NT, GK>(win[j], buf + (b % kCK) * 256,
+        compute_block<ACT, SDT, B, NT, GK, RT>(win[j], buf + (b % kCK) * 256,
                                            reinterpret_cast<const float*>(buf + NT * 16 * kXRow), 2 * (b % kCK),
                                            ((kb0 + b + 1) & gmask) == 0, magic, acc, p, xs);
-      load_slot<B, GK>(win[j], pr, min(kb0 + b + W, kmax));
+      load_slot<B, GK, RT>(win[j], pr, min(kb0 + b + W, kmax));
       if (j % kCK == kCK - 1 && c + 1 < nchunk) {
         x_store<ACT, NT>(xr, lds + ((c + 1) & 1) * xbuf_bytes<NT>(), sums);
         lds_barrier();
@@ -373,12 +395,14 @@ __device__ __forceinline__ int fmt_code(uint8_t bits) {
   return bits == 16 ? 0 : bits == 8 ? 1 : bits == 4 ? 2 : -1;
 }
 
-// Wave-uniform bases of 16 rows (local row lr0) of a page of reduction length K.
+// Wave-uniform bases of the rows from local row lr0 of a page of reduction
+// length K (row tile rt at tiles + rt * tstride).
 template <int B>
 __device__ __forceinline__ PageRows page_rows(const GemmArgs& a, const pw_page_entry& ent, int lr0, int K) {
   const int lane = lane_id();
   PageRows pr;
-  pr.tiles = a.pool + ent.data_off + static_cast<size_t>(lr0 / 16) * (K / 128) * tile_bytes<B>();
+  pr.tstride = static_cast<size_t>(K / 128) * tile_bytes<B>();
+  pr.tiles = a.pool + ent.data_off + static_cast<size_t>(lr0 / 16) * pr.tstride;
   pr.sz = a.pool + ent.sz_off + static_cast<size_t>(lr0) * 4;
   pr.wlo = 16u * static_cast<uint32_t>(lane);
   pr.szlo = 16u * static_cast<uint32_t>(lane >> 4);
@@ -387,36 +411,52 @@ __device__ __forceinline__ PageRows page_rows(const GemmArgs& a, const pw_page_e
   return pr;
 }
 
-// The wave's page in its own format.
-template <int ACT, int SDT, int NT, int GK>
+// The wave's page in format B (16, 8 or 4), or B = 0: in the format its
+// table entry names, chosen here.
+template <int ACT, int SDT, int B, int NT, int GK, int RT>
 __device__ __forceinline__ void page_gemm(const GemmArgs& a, const pw_page_entry& ent, int lr0, int K, uint8_t* lds,
                                           const uint8_t* xbase, const uint32_t (&rowoff)[x_passes<NT>()], int kb0,
-                                          int kb1, bool sums, f32x4 (&acc)[NT]) {
-  const int code = fmt_code(ent.bits);
-  if (code == 0)
-    wave_gemm<ACT, SDT, 16, NT, GK>(lds, xbase, rowoff, K, page_rows<16>(a, ent, lr0, K), kb0, kb1, sums, acc);
-  else if (code == 1)
-    wave_gemm<ACT, SDT, 8, NT, GK>(lds, xbase, rowoff, K, page_rows<8>(a, ent, lr0, K), kb0, kb1, sums, acc);
-  else
-    wave_gemm<ACT, SDT, 4, NT, GK>(lds, xbase, rowoff, K, page_rows<4>(a, ent, lr0, K), kb0, kb1, sums, acc);
+                                          int kb1, bool sums, f32x4 (&acc)[RT][NT]) {
+  if constexpr (B != 0) {
+    wave_gemm<ACT, SDT, B, NT, GK, RT>(lds, xbase, rowoff, K, page_rows<B>(a, ent, lr0, K), kb0, kb1, sums, acc);
+  } else {
+    const int code = fmt_code(ent.bits);
+    if (code == 0)
+      wave_gemm<ACT, SDT, 16, NT, GK, RT>(lds, xbase, rowoff, K, page_rows<16>(a, ent, lr0, K), kb0, kb1, sums, acc);
+    else if (code == 1)
+      wave_gemm<ACT, SDT, 8, NT, GK, RT>(lds, xbase, rowoff, K, page_rows<8>(a, ent, lr0, K), kb0, kb1, sums, acc);
+    else
+      wave_gemm<ACT, SDT, 4, NT, GK, RT>(lds, xbase, rowoff, K, page_rows<4>(a, ent, lr0, K), kb0, kb1, sums, acc);
+  }
 }
 
 // ---------------------------------------------------------------------------
-// gate/up: a workgroup covers 32 rows of gate and the same 32 rows of up for
-// one expert; waves 0-1 stream gate, waves 2-3 stream up (each in its own
-// page format); the SwiGLU output h = silu(g) * u meets through LDS.
+// gate/up: a workgroup covers 32 RT rows of gate and the same rows of up for
+// one expert; waves 0-1 stream gate, waves 2-3 stream up (16 RT rows each,
+// each projection in its own page format); the SwiGLU output h = silu(g) * u
+// meets through LDS.
 // ---------------------------------------------------------------------------
 
-template <int ACT, int SDT, int NT, int GK>
-__device__ void gateup_unit(const GemmArgs& a, uint8_t* lds, int e, int off_e, int n_e, int r32, bool sums) {
+template <int RT> constexpr int gu_rows() { return 32 * RT; }     // gate (and up) rows per workgroup
+template <int RT> constexpr int dn_rows() { return 64 * RT; }     // down rows per workgroup
+
+// [2 waves][RT][NT][64 lanes] f32x4 of the gate waves, in the activation
+// buffers once every wave has finished its K loop.
+template <int NT, int RT>
+constexpr int xch_bytes() { return 2 * RT * NT * 64 * 16; }
+template <int NT, int RT>
+constexpr int gu_lds_bytes() { return lds_x_bytes<NT>() > xch_bytes<NT, RT>() ? lds_x_bytes<NT>() : xch_bytes<NT, RT>(); }
+
+template <int ACT, int SDT, int B, int NT, int GK, int RT>
+__device__ void gateup_unit(const GemmArgs& a, uint8_t* lds, int e, int off_e, int n_e, int unit, bool sums) {
   const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
   const int lane = lane_id(), lc = lane & 15, lg = lane >> 4;
   const int proj = wave >> 1, wsub = wave & 1;
-  const int f0 = r32 * 32 + 16 * wsub;
+  const int f0 = unit * gu_rows<RT>() + 16 * RT * wsub;   // the wave's first row
   const int rb = f0 / a.R, lr0 = f0 - rb * a.R;
   const pw_page_entry ent = a.table[(static_cast<size_t>(e) * 3 + proj) * a.nrb_max + rb];
   const int H = a.H;
-  float* xch = reinterpret_cast<float*>(lds + lds_x_bytes<NT>());   // [2 waves][NT][64 lanes][4]
+  f32x4* xch = reinterpret_cast<f32x4*>(lds);
   for (int mb = 0; mb < n_e; mb += NT * 16) {
     const uint8_t* xbase = reinterpret_cast<const uint8_t*>(a.x);
     uint32_t rowoff[x_passes<NT>()];
@@ -426,12 +466,14 @@ __device__ void gateup_unit(const GemmArgs& a, uint8_t* lds, int e, int off_e, i
       const int slot = clampi(a.sorted_slot[off_e + m], 0, a.S - 1);
       rowoff[j] = static_cast<uint32_t>(slot / a.topk) * static_cast<uint32_t>(H * 2);
     }
-    f32x4 acc[NT];
-    page_gemm<ACT, SDT, NT, GK>(a, ent, lr0, H, lds, xbase, rowoff, 0, H / 128, sums, acc);
+    f32x4 acc[RT][NT];
+    page_gemm<ACT, SDT, B, NT, GK, RT>(a, ent, lr0, H, lds, xbase, rowoff, 0, H / 128, sums, acc);
+    lds_barrier();   // every wave is done with the activation buffers
     if (proj == 0) {
 #pragma unroll
-      for (int t = 0; t < NT; ++t)
-        *reinterpret_cast<f32x4*>(xch + ((wsub * NT + t) * 64 + lane) * 4) = acc[t];
+      for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+        for (int t = 0; t < NT; ++t) xch[((wsub * RT + rt) * NT + t) * 64 + lane] = acc[rt][t];
     }
     lds_barrier();
     if (proj == 1) {
@@ -439,14 +481,17 @@ __device__ void gateup_unit(const GemmArgs& a, uint8_t* lds, int e, int off_e, i
       for (int t = 0; t < NT; ++t) {
         const int m = mb + 16 * t + lc;
         if (m < n_e) {
-          const f32x4 g = *reinterpret_cast<const f32x4*>(xch + ((wsub * NT + t) * 64 + lane) * 4);
-          uint32_t hv[4];
 #pragma unroll
-          for (int r = 0; r < 4; ++r) hv[r] = rne16(g[r] / (1.0f + expf(-g[r])) * acc[t][r], ACT);
-          u32x2 o;
-          o[0] = hv[0] | (hv[1] << 16);
-          o[1] = hv[2] | (hv[3] << 16);
-          *reinterpret_cast<u32x2*>(a.h + static_cast<size_t>(off_e + m) * a.F + f0 + 4 * lg) = o;
+          for (int rt = 0; rt < RT; ++rt) {
+            const f32x4 g = xch[((wsub * RT + rt) * NT + t) * 64 + lane];
+            uint32_t hv[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) hv[r] = rne16(g[r] / (1.0f + expf(-g[r])) * acc[rt][t][r], ACT);
+            u32x2 o;
+            o[0] = hv[0] | (hv[1] << 16);
+            o[1] = hv[2] | (hv[3] << 16);
+            *reinterpret_cast<u32x2*>(a.h + static_cast<size_t>(off_e + m) * a.F + f0 + 16 * rt + 4 * lg) = o;
+          }
         }
       }
     }
@@ -454,41 +499,61 @@ __device__ void gateup_unit(const GemmArgs& a, uint8_t* lds, int e, int off_e, i
   }
 }
 
+// RT = 1: one code body that picks the format inside; RT = 2: each wave runs
+// the whole unit in its own page's format (every format passes the same
+// barriers), which keeps the register allocations of the three apart.
+template <int ACT, int SDT, int NT, int GK, int RT>
+__device__ __forceinline__ void gateup_any(int code, const GemmArgs& a, uint8_t* lds, int e, int off_e, int n_e,
+                                           int unit, bool sums) {
+  if constexpr (RT == 1) {
+    gateup_unit<ACT, SDT, 0, NT, GK, RT>(a, lds, e, off_e, n_e, unit, sums);
+  } else {
+    if (code == 0) gateup_unit<ACT, SDT, 16, NT, GK, RT>(a, lds, e, off_e, n_e, unit, sums);
+    else if (code == 1) gateup_unit<ACT, SDT, 8, NT, GK, RT>(a, lds, e, off_e, n_e, unit, sums);
+    else gateup_unit<ACT, SDT, 4, NT, GK, RT>(a, lds, e, off_e, n_e, unit, sums);
+  }
+}
+
+// NTMAX slot tiles per pass (1, 2 or 4); experts with fewer slots take fewer.
 template <int ACT, int SDT, int NTMAX, int GK>
 __global__ __launch_bounds__(256) void k_gateup(const GemmArgs a) {
-  __shared__ __attribute__((aligned(16))) uint8_t lds[lds_x_bytes<NTMAX>() + 2 * NTMAX * 64 * 16];
-  const int upe = a.F / 32;
-  const int e = blockIdx.x / upe, r32 = blockIdx.x % upe;
+  constexpr int RT = row_tiles<NTMAX>();
+  __shared__ __attribute__((aligned(16))) uint8_t lds[gu_lds_bytes<NTMAX, RT>()];
+  const int upe = a.F / gu_rows<RT>();
+  const int e = blockIdx.x / upe, unit = blockIdx.x % upe;
   const int off_e = clampi(a.offsets[e], 0, a.S);
   const int n_e = clampi(a.offsets[e + 1], off_e, a.S) - off_e;
   if (n_e <= 0) return;
   // every page of the unit must be present; otherwise the whole group returns
-  const int rb = (r32 * 32) / a.R;
+  // (a unit of at most 64 rows lies inside one page: R is a multiple of 64)
+  const int rb = (unit * gu_rows<RT>()) / a.R;
   const int cg = fmt_code(a.table[(static_cast<size_t>(e) * 3 + PW_GATE) * a.nrb_max + rb].bits);
   const int cu = fmt_code(a.table[(static_cast<size_t>(e) * 3 + PW_UP) * a.nrb_max + rb].bits);
   if (cg < 0 || cu < 0) return;
   const bool sums = cg != 0 || cu != 0;
-  if (NTMAX == 1 || n_e <= 16) gateup_unit<ACT, SDT, 1, GK>(a, lds, e, off_e, n_e, r32, sums);
-  else gateup_unit<ACT, SDT, 2, GK>(a, lds, e, off_e, n_e, r32, sums);
+  const int code = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 7) == 0 ? cg : cu;
+  if (NTMAX == 1 || n_e <= 16) gateup_any<ACT, SDT, 1, GK, RT>(code, a, lds, e, off_e, n_e, unit, sums);
+  else if (NTMAX == 2 || n_e <= 32) gateup_any<ACT, SDT, 2, GK, RT>(code, a, lds, e, off_e, n_e, unit, sums);
+  else gateup_any<ACT, SDT, (NTMAX > 2 ? NTMAX : 2), GK, RT>(code, a, lds, e, off_e, n_e, unit, sums);
 }
 
 // ---------------------------------------------------------------------------
-// down: a workgroup covers 64 rows of one down page over one K split of F;
-// fp32 partial sums per split, reduced by the combine.
+// down: a workgroup covers 64 RT rows of the down projection (16 RT per wave;
+// one or two pages) over one K split of F; fp32 partial sums per split,
+// reduced by the combine.
 // ---------------------------------------------------------------------------
 
-template <int ACT, int SDT, int NT, int GK>
-__device__ void down_unit(const GemmArgs& a, uint8_t* lds, int off_e, int n_e, int r64, int split,
-                          const pw_page_entry& ent) {
+template <int ACT, int SDT, int B, int NT, int GK, int RT>
+__device__ void down_unit(const GemmArgs& a, uint8_t* lds, int e, int off_e, int n_e, int unit, int split,
+                          bool sums) {
   const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
   const int lane = lane_id(), lc = lane & 15, lg = lane >> 4;
   const int F = a.F;
-  const int n0 = r64 * 64 + 16 * wave;
+  const int n0 = unit * dn_rows<RT>() + 16 * RT * wave;   // the wave's first row
   const int rb = n0 / a.R, lr0 = n0 - rb * a.R;
+  const pw_page_entry ent = a.table[(static_cast<size_t>(e) * 3 + PW_DOWN) * a.nrb_max + rb];
   const int kb0 = split * a.kb_per_split;
   const int kb1 = min(F / 128, kb0 + a.kb_per_split);
-  if (kb0 >= kb1) return;
-  const bool sums = ent.bits != 16;
   for (int mb = 0; mb < n_e; mb += NT * 16) {
     const uint8_t* xbase = reinterpret_cast<const uint8_t*>(a.h);
     uint32_t rowoff[x_passes<NT>()];
@@ -497,66 +562,95 @@ __device__ void down_unit(const GemmArgs& a, uint8_t* lds, int off_e, int n_e, i
       const int m = clampi(mb + x_row(j), 0, n_e - 1);
       rowoff[j] = static_cast<uint32_t>(off_e + m) * static_cast<uint32_t>(F * 2);
     }
-    f32x4 acc[NT];
-    page_gemm<ACT, SDT, NT, GK>(a, ent, lr0, F, lds, xbase, rowoff, kb0, kb1, sums, acc);
+    f32x4 acc[RT][NT];
+    page_gemm<ACT, SDT, B, NT, GK, RT>(a, ent, lr0, F, lds, xbase, rowoff, kb0, kb1, sums, acc);
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
       const int m = mb + 16 * t + lc;
       if (m < n_e) {
-        float* dst = a.opart + (static_cast<size_t>(split) * a.S + off_e + m) * a.H + r64 * 64 + 16 * wave + 4 * lg;
-        *reinterpret_cast<f32x4*>(dst) = acc[t];
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) {
+          float* dst = a.opart + (static_cast<size_t>(split) * a.S + off_e + m) * a.H + n0 + 16 * rt + 4 * lg;
+          *reinterpret_cast<f32x4*>(dst) = acc[rt][t];
+        }
       }
     }
     lds_barrier();
   }
 }
 
+template <int ACT, int SDT, int NT, int GK, int RT>
+__device__ __forceinline__ void down_any(int code, const GemmArgs& a, uint8_t* lds, int e, int off_e, int n_e,
+                                         int unit, int split, bool sums) {
+  if constexpr (RT == 1) {
+    down_unit<ACT, SDT, 0, NT, GK, RT>(a, lds, e, off_e, n_e, unit, split, sums);
+  } else {
+    if (code == 0) down_unit<ACT, SDT, 16, NT, GK, RT>(a, lds, e, off_e, n_e, unit, split, sums);
+    else if (code == 1) down_unit<ACT, SDT, 8, NT, GK, RT>(a, lds, e, off_e, n_e, unit, split, sums);
+    else down_unit<ACT, SDT, 4, NT, GK, RT>(a, lds, e, off_e, n_e, unit, split, sums);
+  }
+}
+
 template <int ACT, int SDT, int NTMAX, int GK>
 __global__ __launch_bounds__(256) void k_down(const GemmArgs a) {
+  constexpr int RT = row_tiles<NTMAX>();
   __shared__ __attribute__((aligned(16))) uint8_t lds[lds_x_bytes<NTMAX>()];
-  const int upe = a.H / 64;
+  const int upe = a.H / dn_rows<RT>();
   const int split = blockIdx.x % a.nsplit;
   const int rest = blockIdx.x / a.nsplit;
-  const int e = rest / upe, r64 = rest % upe;
+  const int e = rest / upe, unit = rest % upe;
   const int off_e = clampi(a.offsets[e], 0, a.S);
   const int n_e = clampi(a.offsets[e + 1], off_e, a.S) - off_e;
   if (n_e <= 0) return;
-  const int rb = (r64 * 64) / a.R;
-  const pw_page_entry ent = a.table[(static_cast<size_t>(e) * 3 + PW_DOWN) * a.nrb_max + rb];
-  if (fmt_code(ent.bits) < 0) return;
-  if (NTMAX == 1 || n_e <= 16) down_unit<ACT, SDT, 1, GK>(a, lds, off_e, n_e, r64, split, ent);
-  else down_unit<ACT, SDT, 2, GK>(a, lds, off_e, n_e, r64, split, ent);
+  if (split * a.kb_per_split >= a.F / 128) return;
+  // every page of the unit (one, or two when the unit spans pages) must be present
+  bool sums = false;
+  for (int rb = (unit * dn_rows<RT>()) / a.R; rb <= (unit * dn_rows<RT>() + dn_rows<RT>() - 1) / a.R; ++rb) {
+    const int c = fmt_code(a.table[(static_cast<size_t>(e) * 3 + PW_DOWN) * a.nrb_max + rb].bits);
+    if (c < 0) return;
+    sums = sums || c != 0;
+  }
+  const int n0 = unit * dn_rows<RT>() + 16 * RT * __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
+  const int code = fmt_code(a.table[(static_cast<size_t>(e) * 3 + PW_DOWN) * a.nrb_max + n0 / a.R].bits);
+  if (NTMAX == 1 || n_e <= 16) down_any<ACT, SDT, 1, GK, RT>(code, a, lds, e, off_e, n_e, unit, split, sums);
+  else if (NTMAX == 2 || n_e <= 32) down_any<ACT, SDT, 2, GK, RT>(code, a, lds, e, off_e, n_e, unit, split, sums);
+  else down_any<ACT, SDT, (NTMAX > 2 ? NTMAX : 2), GK, RT>(code, a, lds, e, off_e, n_e, unit, split, sums);
+}
+
+template <int ACT, int SDT, int GK, int NTMAX>
+void gemm_launch_nt(const GemmArgs& a, bool gateup, hipStream_t st) {
+  constexpr int RT = row_tiles<NTMAX>();
+  const dim3 block(256);
+  if (gateup)
+    hipLaunchKernelGGL((k_gateup<ACT, SDT, NTMAX, GK>), dim3(a.E * (a.F / gu_rows<RT>())), block, 0, st, a);
+  else
+    hipLaunchKernelGGL((k_down<ACT, SDT, NTMAX, GK>), dim3(a.E * (a.H / dn_rows<RT>()) * a.nsplit), block, 0, st, a);
 }
 
 template <int ACT, int SDT, int GK>
-hipError_t gemm_launch(const GemmArgs& a, bool gateup, hipStream_t st) {
-  const dim3 block(256);
-  if (gateup) {
-    const dim3 grid(a.E * (a.F / 32));
-    if (a.mtb == 1) hipLaunchKernelGGL((k_gateup<ACT, SDT, 1, GK>), grid, block, 0, st, a);
-    else hipLaunchKernelGGL((k_gateup<ACT, SDT, 2, GK>), grid, block, 0, st, a);
-  } else {
-    const dim3 grid(a.E * (a.H / 64) * a.nsplit);
-    if (a.mtb == 1) hipLaunchKernelGGL((k_down<ACT, SDT, 1, GK>), grid, block, 0, st, a);
-    else hipLaunchKernelGGL((k_down<ACT, SDT, 2, GK>), grid, block, 0, st, a);
-  }
-  return hipGetLastError();
+void gemm_launch(const GemmArgs& a, bool gateup, hipStream_t st) {
+  if (a.mtb == 1) gemm_launch_nt<ACT, SDT, GK, 1>(a, gateup, st);
+  else if (a.mtb == 2) gemm_launch_nt<ACT, SDT, GK, 2>(a, gateup, st);
+  else gemm_launch_nt<ACT, SDT, GK, 4>(a, gateup, st);
 }
 
 template <int ACT, int SDT>
-hipError_t gemm_dispatch_g(const GemmArgs& a, bool gateup, hipStream_t st) {
-  if (a.G == 64) return gemm_launch<ACT, SDT, kG64>(a, gateup, st);
-  if (a.G == 128) return gemm_launch<ACT, SDT, kG128>(a, gateup, st);
-  return gemm_launch<ACT, SDT, kGBig>(a, gateup, st);
+void gemm_dispatch_g(const GemmArgs& a, bool gateup, hipStream_t st) {
+  if (a.G == 64) gemm_launch<ACT, SDT, kG64>(a, gateup, st);
+  else if (a.G == 128) gemm_launch<ACT, SDT, kG128>(a, gateup, st);
+  else gemm_launch<ACT, SDT, kGBig>(a, gateup, st);
 }
 
 hipError_t gemm_dispatch(const GemmArgs& a, bool gateup, hipStream_t st) {
-  if (a.mtb != 1 && a.mtb != 2) return hipErrorInvalidValue;
-  if (a.act == PW_BF16)
-    return a.sdt == PW_BF16 ? gemm_dispatch_g<PW_BF16, PW_BF16>(a, gateup, st)
-                            : gemm_dispatch_g<PW_BF16, PW_F16>(a, gateup, st);
-  return a.sdt == PW_BF16 ? gemm_dispatch_g<PW_F16, PW_BF16>(a, gateup, st)
-                          : gemm_dispatch_g<PW_F16, PW_F16>(a, gateup, st);
+  if (a.mtb != 1 && a.mtb != 2 && a.mtb != 4) return hipErrorInvalidValue;
+  if (a.act == PW_BF16) {
+    if (a.sdt == PW_BF16) gemm_dispatch_g<PW_BF16, PW_BF16>(a, gateup, st);
+    else gemm_dispatch_g<PW_BF16, PW_F16>(a, gateup, st);
+  } else {
+    if (a.sdt == PW_BF16) gemm_dispatch_g<PW_F16, PW_BF16>(a, gateup, st);
+    else gemm_dispatch_g<PW_F16, PW_F16>(a, gateup, st);
+  }
+  return hipGetLastError();
 }
 
 }  // namespace

@@ -56,7 +56,7 @@ struct GemmArgs {
   int nsplit, kb_per_split;   // down projection split over K = F (in 128-blocks)
   int out_fp32;
   int act, sdt;
-  int mtb;                    // M tiles (of 16 slots) per pass
+  int mtb;                    // M tiles (of 16 slots) per pass: 1, 2 or 4
 };
 
 hipError_t launch_route_topk(const float* logits, int T, int E, int K, int renorm,

@@ -182,7 +182,7 @@ def test_zero_up_projection_gives_zero():
 
 
 # Large per-expert slot counts (at least 128 expected per expert) take the
-# LDS-tiled GEMM and medium ones (33..127) the streaming GEMM with 64-slot
+# LDS-tiled GEMM and medium ones (49..127) the streaming GEMM with 64-slot
 # tiles; both feed quantized weights to the MFMA as fl32(z + c*s) rounded to
 # the activation dtype, so their fp32 output is compared with the oracle read
 # the same way (w_round).
@@ -217,7 +217,7 @@ def test_tiny_tiled_uniform_and_empty_experts(b):
 
 @pytest.mark.parametrize("T", [300, 211])
 def test_tiny_stream_path_parity(T):
-    """33..127 expected slots per expert: the streaming GEMM (64-slot tiles)."""
+    """49..127 expected slots per expert: the streaming GEMM (64-slot tiles)."""
     cfg, w16, bits, order = case("tiny", T=T)
     say("tiny stream T=%d" % T)
     L = gpu_layer(cfg, w16, bits, order)
@@ -229,9 +229,9 @@ def test_tiny_stream_path_parity(T):
 
 @pytest.mark.parametrize("b", [16, 8, 4])
 def test_tiny_stream_uniform_and_empty_experts(b):
-    """Every page at one bitwidth; 150 tokens all routed to experts 3 and 5
-    (three 64-slot tiles each, the last ragged; six experts with none)."""
-    cfg, w16, _, order = case("tiny", T=150)
+    """Every page at one bitwidth; 200 tokens all routed to experts 3 and 5
+    (four 64-slot tiles each, the last ragged; six experts with none)."""
+    cfg, w16, _, order = case("tiny", T=200)
     bits = [np.full((cfg.E, cfg.nrb(p)), b, np.int32) for p in range(3)]
     lg = synth.logits(cfg).copy()
     lg[:, [3, 5]] += 100.0
@@ -243,15 +243,50 @@ def test_tiny_stream_uniform_and_empty_experts(b):
     L.close()
 
 
+# 21..48 expected slots per expert: the decode kernels with up to four 16-slot
+# tiles per pass, each wave streaming two 16-row weight tiles (exact
+# code-domain arithmetic, so no w_round).
+@pytest.mark.parametrize("T", [100, 190])
+def test_tiny_decode4_path_parity(T):
+    cfg, w16, bits, order = case("tiny", T=T)
+    say("tiny decode, four slot tiles, T=%d" % T)
+    L = gpu_layer(cfg, w16, bits, order)
+    O = oracle_layer(cfg, w16, bits)
+    toks = list(range(0, T, 3)) + [T - 1]
+    e16, e32, _, _ = _forward_parity(cfg, L, O, synth.activations(cfg), synth.logits(cfg), tokens=toks)
+    assert e16 <= TOL16 and e32 <= TOL32, (e16, e32)
+    L.close()
+
+
+@pytest.mark.parametrize("b", [16, 8, 4])
+def test_tiny_decode4_uniform_and_heavy_experts(b):
+    """Every page at one bitwidth; 100 tokens all routed to experts 3 and 5
+    (100 slots each: a 64-slot pass and a ragged 36-slot pass; six experts
+    with none)."""
+    cfg, w16, _, order = case("tiny", T=100)
+    bits = [np.full((cfg.E, cfg.nrb(p)), b, np.int32) for p in range(3)]
+    lg = synth.logits(cfg).copy()
+    lg[:, [3, 5]] += 100.0
+    say("tiny decode4 uniform %d, two experts" % b)
+    L = gpu_layer(cfg, w16, bits, order)
+    O = oracle_layer(cfg, w16, bits)
+    toks = list(range(0, 100, 3)) + [99]
+    e16, e32, _, _ = _forward_parity(cfg, L, O, synth.activations(cfg), lg, tokens=toks)
+    assert e16 <= TOL16 and e32 <= TOL32, (e16, e32)
+    L.close()
+
+
 # Group sizes above 128 (a group spans 2 or 4 128-blocks; on the decode path
 # the down projection's K splits must hold whole groups) and scale/zero dtypes
 # other than the activation dtype, on each of the three GEMM paths: 16 tokens
-# (4 expected slots per expert) decode, 300 the streaming GEMM, 1000 the tiled.
+# (4 expected slots per expert) and 120 tokens (30: four slot tiles, two row
+# tiles per wave) decode, 300 the streaming GEMM, 1000 the tiled.
 @pytest.mark.parametrize("act,sdt,G,H,F,T", [
     (synth.BF16, synth.F16, 256, 256, 512, 16),
     (synth.F16, synth.BF16, 512, 512, 1024, 16),
     (synth.BF16, synth.F16, 128, 256, 512, 16),
     (synth.F16, synth.BF16, 128, 256, 512, 16),
+    (synth.BF16, synth.F16, 256, 256, 512, 120),
     (synth.F16, synth.BF16, 256, 256, 512, 300),
     (synth.BF16, synth.F16, 512, 512, 1024, 1000),
 ])
@@ -262,6 +297,6 @@ def test_tiny_group_sizes_and_scale_dtypes(act, sdt, G, H, F, T):
     O = oracle_layer(cfg, w16, bits)
     toks = None if T <= 16 else list(range(0, T, 9)) + [T - 1]
     e16, e32, _, _ = _forward_parity(cfg, L, O, synth.activations(cfg), synth.logits(cfg), tokens=toks,
-                                     w_round=T > 16)
+                                     w_round=T > 200)
     assert e16 <= TOL16 and e32 <= TOL32, (e16, e32)
     L.close()
