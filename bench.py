@@ -63,13 +63,15 @@ def page_bytes_active(cfg, bits, counts):
     return per
 
 
-def build_layer(cfg):
+def build_layer(cfg, w16=None, bits=None):
     import numpy as np
     from paper_2607_16184_amd import synth
     from paper_2607_16184_amd.layer import PagedLayer
     t0 = time.time()
-    w16 = [synth.expert_weights(cfg, p) for p in range(3)]
-    bits = synth.bitmap(cfg)
+    if w16 is None:
+        w16 = [synth.expert_weights(cfg, p) for p in range(3)]
+    if bits is None:
+        bits = synth.bitmap(cfg)
     L = PagedLayer(cfg, PagedLayer.pool_bytes_for(cfg, bits, slack=0.0))
     L.load_pages(w16, bits, synth.pool_order(cfg))
     log("%s: weights generated and paged in %.1f s" % (cfg.name, time.time() - t0))
@@ -80,61 +82,74 @@ def time_steps(L, cfg, x, logits, steps, warmup):
     """Warm up; time `steps` eager steps with per-kernel HIP-event profiling;
     then capture one step (route + paged GEMMs + combine) in a HIP graph and
     time exactly `steps` replays of it, which is the step time reported. Every
-    replay's output is checked bit-exact against the eager step."""
+    replay's output is checked bit-exact against the eager step. L may be a
+    list of layers holding the same pages in separate pools: step i then runs
+    on layer i mod len(L), so that no step finds another's weights in a cache."""
     import torch
     from paper_2607_16184_amd import pw
     from paper_2607_16184_amd.layer import PagedLayer
+    Ls = L if isinstance(L, (list, tuple)) else [L]
     rbuf = PagedLayer.routing_buffers(cfg.T, cfg.E, cfg.K)
     y = torch.empty((cfg.T, cfg.H), dtype=torch.int16, device="cuda")
 
-    def step():
-        routing = L.route(logits, cfg.K, out=rbuf)
-        L.forward(x, routing, y=y)
+    def step(i):
+        Li = Ls[i % len(Ls)]
+        routing = Li.route(logits, cfg.K, out=rbuf)
+        Li.forward(x, routing, y=y)
 
-    for _ in range(warmup):
-        step()
+    for i in range(max(warmup, len(Ls))):
+        step(i)
     torch.cuda.synchronize()
     y_eager = y.clone()
-    pw.pw_profile_read(L.handle, reset=True)
-    pw.pw_profile_enable(L.handle, True)
+    for Li in Ls:
+        pw.pw_profile_read(Li.handle, reset=True)
+        pw.pw_profile_enable(Li.handle, True)
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     ev0.record()
-    for _ in range(steps):
-        step()
+    for i in range(steps):
+        step(i)
     ev1.record()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    pw.pw_profile_enable(L.handle, False)
-    ms, cnt = pw.pw_profile_read(L.handle, reset=True)
+    ms, cnt = [0.0] * 4, [0] * 4
+    for Li in Ls:
+        pw.pw_profile_enable(Li.handle, False)
+        m, c = pw.pw_profile_read(Li.handle, reset=True)
+        for k in range(4):
+            ms[k] += m[k]
+            cnt[k] += c[k]
     per_kernel = {name: (ms[i] / cnt[i] if cnt[i] else None)
                   for i, name in enumerate(("gateup", "down", "combine", "requant"))}
     counts = (rbuf[2][1:] - rbuf[2][:-1]).cpu().numpy()
     out = {"wall_ms": (t1 - t0) * 1e3 / steps, "eager_ms": ev0.elapsed_time(ev1) / steps,
-           "kernel_ms": per_kernel, "counts": counts, "graph": False}
+           "kernel_ms": per_kernel, "counts": counts, "graph": False, "layers": len(Ls)}
     out["event_ms"] = out["eager_ms"]
     try:
-        g = torch.cuda.CUDAGraph()
+        graphs = []
         side = torch.cuda.Stream()
-        side.wait_stream(torch.cuda.current_stream())
-        with torch.cuda.stream(side):
-            step()                                   # the capture stream's own warm-up
-        torch.cuda.current_stream().wait_stream(side)
-        torch.cuda.synchronize()
-        with torch.cuda.graph(g):
-            step()
-        for _ in range(max(warmup, 2)):
+        for i in range(len(Ls)):
+            g = torch.cuda.CUDAGraph()
+            side.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(side):
+                step(i)                              # the capture stream's own warm-up
+            torch.cuda.current_stream().wait_stream(side)
+            torch.cuda.synchronize()
+            with torch.cuda.graph(g):
+                step(i)
+            graphs.append(g)
+        for i in range(max(warmup, 2) * len(graphs)):
             y.zero_()
-            g.replay()
+            graphs[i % len(graphs)].replay()
             torch.cuda.synchronize()
             if not torch.equal(y, y_eager):
                 raise RuntimeError("graph replay differs from the eager step")
         torch.cuda.synchronize()
         ev0.record()
-        for _ in range(steps):
-            g.replay()
+        for i in range(steps):
+            graphs[i % len(graphs)].replay()
         ev1.record()
         torch.cuda.synchronize()
         if not torch.equal(y, y_eager):
@@ -183,24 +198,31 @@ def cpu_baseline(cfg, w16, bits, logits_np, x16, weight_bytes, budget_s=20.0):
                       "the full step (%.2f s measured, %.1f s per step)" % (done, cfg.T, spent, step_s)}
 
 
-def leg_layer(name, steps, warmup):
-    """Time another workload's full step; GB/s of active pages and MFMA share."""
+def leg_layer(name, steps, warmup, pools=1):
+    """Time another workload's full step; GB/s of active pages and MFMA share.
+    pools > 1: that many copies of the layer in separate pools, stepped in turn
+    (for weight sets that a 256 MB last-level cache could otherwise serve)."""
     import numpy as np
     import torch
     from paper_2607_16184_amd import synth
     cfg = synth.CONFIGS[name]
     L, w16, bits = build_layer(cfg)
+    Ls = [L]
+    for _ in range(pools - 1):
+        Ls.append(build_layer(cfg, w16=w16, bits=bits)[0])
     del w16
     logits = torch.from_numpy(synth.logits(cfg)).cuda()
     x = torch.from_numpy(synth.activations(cfg).view(np.int16)).cuda()
-    r = time_steps(L, cfg, x, logits, steps, warmup)
+    r = time_steps(Ls, cfg, x, logits, steps, warmup)
     per = page_bytes_active(cfg, bits, r["counts"])
     wb = per[0] + per[1] + per[2]
     km = r["kernel_ms"]
     gemm_ms = km["gateup"] + km["down"]
     flops = 6.0 * cfg.T * cfg.K * cfg.H * cfg.F
-    L.close()
+    for Li in Ls:
+        Li.close()
     return {"workload": describe(cfg), "steps": steps, "ms_per_step": round(r["event_ms"], 4),
+            "pools_rotated": pools,
             "eager_ms_per_step": round(r["eager_ms"], 4),
             "step_timing": "hip_graph_replay" if r["graph"] else "eager",
             "weight_GBps_per_step": round(wb / (r["event_ms"] * 1e-3) / 1e9, 1),
@@ -415,7 +437,9 @@ def main():
         if leg == "prefill":
             extras["prefill"] = leg_layer("mixtral_prefill", steps=5, warmup=1)
         elif leg == "finegrained":
-            extras["finegrained"] = leg_layer("finegrained", steps=20, warmup=3)
+            # 0.57 GB of weights: three pools in turn, so no step reads the
+            # previous step's weights from the 256 MB last-level cache
+            extras["finegrained"] = leg_layer("finegrained", steps=21, warmup=3, pools=3)
         elif leg == "downshift":
             extras["downshift"] = leg_downshift()
         log("leg %s done in %.1f s" % (leg, time.time() - t0))
