@@ -300,3 +300,39 @@ def test_tiny_group_sizes_and_scale_dtypes(act, sdt, G, H, F, T):
                                      w_round=T > 200)
     assert e16 <= TOL16 and e32 <= TOL32, (e16, e32)
     L.close()
+
+
+# Edge shapes on the decode path: a single token, every expert selected
+# (K = E), unrenormalised routing weights, a 64-expert top-6 layer with few
+# tokens (most experts empty), and no tokens at all.
+@pytest.mark.parametrize("T,K,E,renorm", [(1, 2, 8, 1), (3, 8, 8, 1), (7, 2, 8, 0), (5, 6, 64, 1)])
+def test_tiny_edge_shapes(T, K, E, renorm):
+    import torch
+    cfg, w16, bits, order = case("tiny", T=T, K=K, E=E)
+    say("tiny edge T=%d K=%d E=%d renorm=%d" % (T, K, E, renorm))
+    L = gpu_layer(cfg, w16, bits, order)
+    O = oracle_layer(cfg, w16, bits)
+    logits, x16 = synth.logits(cfg), synth.activations(cfg)
+    routing = L.route(to_dev(logits), K, renorm=renorm)
+    y32 = L.forward(to_dev16(x16), routing, out_fp32=True)
+    torch.cuda.synchronize()
+    ids, w = oracle.route(logits, K, renorm)
+    assert np.array_equal(routing[0].cpu().numpy(), ids)
+    r2 = O.forward(x16, ids, w, h_round=True)
+    assert rel_err(y32.cpu().numpy(), r2) <= TOL32
+    L.close()
+
+
+def test_zero_tokens():
+    import torch
+    cfg, w16, bits, order = case("tiny")
+    say("tiny, no tokens")
+    L = gpu_layer(cfg, w16, bits, order)
+    logits = torch.zeros((0, cfg.E), dtype=torch.float32, device="cuda")
+    x = torch.zeros((0, cfg.H), dtype=torch.int16, device="cuda")
+    routing = L.route(logits, cfg.K)
+    y = L.forward(x, routing, out_fp32=True)
+    torch.cuda.synchronize()
+    assert tuple(y.shape) == (0, cfg.H)
+    assert not routing[2].cpu().numpy().any()      # every expert offset is 0
+    L.close()
