@@ -67,7 +67,7 @@ typedef enum {
     PW_OK = 0,
     PW_EINVAL = 1,        /* bad argument, shape or size                      */
     PW_ENOMEM = 2,        /* pool or workspace too small                      */
-    PW_EBUSY = 3,         /* the block already has a requantization pending   */
+    PW_EBUSY = 3,         /* a requantization or reload of the block pending  */
     PW_EUNSUPPORTED = 4,  /* e.g. raising a bitwidth (needs a reload)         */
     PW_EHIP = 5,          /* a HIP runtime call failed                        */
     PW_ESTATE = 6         /* layer not ready (a page is missing)              */
@@ -76,8 +76,10 @@ typedef enum {
 typedef enum { PW_F16 = 0, PW_BF16 = 1 } pw_dtype;
 typedef enum { PW_GATE = 0, PW_UP = 1, PW_DOWN = 2 } pw_proj;
 
-/* Page states (Sec. 3.1 page state; only GPU-resident states exist here). */
-enum { PW_PAGE_ABSENT = 0, PW_PAGE_RESIDENT = 1, PW_PAGE_REQUANT_PENDING = 2 };
+/* Page states of the committed GPU page (Sec. 3.1 page state). A block may
+ * also hold a copy in the caller's host pool (pw_offload_block); the table
+ * entry always describes the GPU page the kernels read.                   */
+enum { PW_PAGE_ABSENT = 0, PW_PAGE_RESIDENT = 1, PW_PAGE_REQUANT_PENDING = 2, PW_PAGE_RELOAD_PENDING = 3 };
 
 /* One page-table entry (device array and host mirror). 24 bytes. */
 typedef struct {
@@ -162,7 +164,8 @@ pw_status pw_moe_paged_gemm(const pw_layer* layer, const void* x, int T, int K,
  * b to new_bits < b into a fresh slot on `side_stream`. The committed entry
  * is unchanged until pw_commit. *delta_bytes receives Eq. 3's M^b - M^b'.
  *   new_bits == b: PW_OK, delta 0, no work.
- *   new_bits > b: PW_EUNSUPPORTED.  pending already: PW_EBUSY.
+ *   new_bits > b: PW_EUNSUPPORTED (raising is a reload from a host copy,
+ *   pw_reload_block).  pending already: PW_EBUSY.
  *   no free slot: PW_ENOMEM.                                              */
 pw_status pw_requant_block(pw_layer* layer, int e, int proj, int rb, int new_bits,
                            void* side_stream, size_t* delta_bytes);
@@ -173,14 +176,60 @@ pw_status pw_requant_blocks(pw_layer* layer, int n, const int* e, const int* pro
                             const int* rb, const int* new_bits, void* side_stream,
                             size_t* delta_bytes_total);
 
-/* Publish every pending requantization, ordered on main_stream after its
- * requant finished: the device entries are rewritten by a kernel on
- * main_stream, the host mirror updated, and the old slots retired until
+/* Host copies of pages (Sec. 3.1: a page's higher-precision version moves to
+ * CPU memory before its GPU copy is lowered, and comes back when the
+ * bitwidth is raised again; pages are CPU-resident, GPU-resident or in
+ * transfer).
+ *
+ * pw_layer_set_host_pool: hand the layer a host pool [host_pool, + host_bytes)
+ * (256-byte aligned; page-locked memory, e.g. hipHostMalloc, for the copies
+ * to run asynchronously). The caller owns it and keeps it alive until
+ * pw_layer_destroy. Once per layer (PW_EBUSY after).                       */
+pw_status pw_layer_set_host_pool(pw_layer* layer, void* host_pool, size_t host_bytes);
+
+/* Copy the committed page of each block (codes and scale/zero, Eq. 3's M^b
+ * bytes) into a fresh host slot, device-to-host on `stream`. The GPU page
+ * and the table are unchanged. A host copy at another bitwidth is replaced;
+ * one at the committed bitwidth makes the block a no-op. To lower a block in
+ * the paper's order, offload it and then requantize it on the same stream.
+ *   no host pool, page absent: PW_ESTATE.  requant/reload pending: PW_EBUSY.
+ *   host pool full: PW_ENOMEM (no block of the batch is copied).           */
+pw_status pw_offload_blocks(pw_layer* layer, int n, const int* e, const int* proj, const int* rb,
+                            void* stream);
+pw_status pw_offload_block(pw_layer* layer, int e, int proj, int rb, void* stream);
+
+/* Raise each block back to the bitwidth of its host copy: a fresh device
+ * slot is filled host-to-device on `stream` (after the offload's copy
+ * finished); the block is pending (PW_PAGE_RELOAD_PENDING) until pw_commit
+ * publishes the raised entry, and its old slot is then retired like a
+ * requantized one. *added_bytes_total (may be NULL) receives the sum of
+ * M^b' - M^b. The host copy stays (drop it with pw_drop_host_copy).
+ *   no host copy, page absent: PW_ESTATE.  copy not of a higher bitwidth:
+ *   PW_EUNSUPPORTED.  pending already: PW_EBUSY.  no free slot: PW_ENOMEM.  */
+pw_status pw_reload_blocks(pw_layer* layer, int n, const int* e, const int* proj, const int* rb,
+                           void* stream, size_t* added_bytes_total);
+pw_status pw_reload_block(pw_layer* layer, int e, int proj, int rb, void* stream, size_t* added_bytes);
+
+/* Forget a block's host copy; its host slot is freed by pw_reclaim once the
+ * last transfer that uses it completed. No copy: PW_OK.                    */
+pw_status pw_drop_host_copy(pw_layer* layer, int e, int proj, int rb);
+
+/* Bitwidth of a block's host copy (0: none) and whether its device-to-host
+ * copy completed (*ready = 1).                                             */
+pw_status pw_host_copy_info(pw_layer* layer, int e, int proj, int rb, int* bits, int* ready);
+
+/* Host pool capacity and bytes in host slots. */
+pw_status pw_host_pool_stats(const pw_layer* layer, size_t* capacity, size_t* used);
+
+/* Publish every pending requantization and reload, ordered on main_stream
+ * after its transfer finished: the device entries are rewritten by a kernel
+ * on main_stream, the host mirror updated, and the old slots retired until
  * main_stream passes the commit. *n_committed may be NULL.               */
 pw_status pw_commit(pw_layer* layer, void* main_stream, int* n_committed);
 
-/* Return retired slots whose commit has completed to the pool's free list.
- * *bytes_freed (may be NULL) receives the bytes returned by this call.    */
+/* Return retired slots whose commit has completed to the pool's free list
+ * (and dropped host slots whose last transfer completed to the host pool).
+ * *bytes_freed (may be NULL) receives the device bytes returned.          */
 pw_status pw_reclaim(pw_layer* layer, size_t* bytes_freed);
 
 /* Host-mirror view of one entry. */

@@ -46,6 +46,7 @@ struct pw_layer {
   pw::LayerState st;
   uint8_t* pool;
   pw_page_entry* table;
+  uint8_t* host_pool = nullptr;   // caller's pinned host memory for page copies
   bool prof = false;
   std::vector<ProfRec> recs;
   double tot_ms[PW_NPHASE] = {0, 0, 0, 0};
@@ -408,6 +409,20 @@ pw_status pw_requant_blocks(pw_layer* L, int n, const int* e, const int* proj, c
   }
   if (plan.empty()) return PW_OK;
   hipStream_t st = static_cast<hipStream_t>(side_stream);
+  // a device-to-host copy of a source page still in flight on another stream
+  // must finish before the page can retire (commit waits on this batch)
+  std::set<void*> waits;
+  for (const Planned& p : plan) {
+    void* hev = L->st.host[L->st.index(p.e, p.proj, p.rb)].ev;
+    if (hev && !L->evops.done(hev)) waits.insert(hev);
+  }
+  for (void* w : waits) {
+    hipError_t he = hipStreamWaitEvent(st, static_cast<hipEvent_t>(w), 0);
+    if (he != hipSuccess) {
+      rollback();
+      return hip_fail(he, "hipStreamWaitEvent");
+    }
+  }
   // one launch for the whole plan (jobs of every projection, each with its K)
   std::vector<pw::QJob> jobs;
   for (const Planned& p : plan) {
@@ -448,6 +463,191 @@ pw_status pw_requant_blocks(pw_layer* L, int n, const int* e, const int* proj, c
 pw_status pw_requant_block(pw_layer* L, int e, int proj, int rb, int new_bits, void* side_stream,
                            size_t* delta_bytes) {
   return pw_requant_blocks(L, 1, &e, &proj, &rb, &new_bits, side_stream, delta_bytes);
+}
+
+// ---------------------------------------------------------------------------
+// Host copies of pages: offload (device -> host) and reload (host -> device)
+// ---------------------------------------------------------------------------
+
+pw_status pw_layer_set_host_pool(pw_layer* L, void* host_pool, size_t host_bytes) {
+  if (!L || !host_pool || host_bytes == 0) return fail(PW_EINVAL, "bad argument");
+  if (!mult_of_256(host_pool)) return fail(PW_EINVAL, "host pool must be 256-byte aligned");
+  if (L->st.has_host_pool()) return fail(PW_EBUSY, "the layer already has a host pool");
+  L->host_pool = static_cast<uint8_t*>(host_pool);
+  L->st.set_host_pool(host_bytes);
+  return PW_OK;
+}
+
+namespace {
+
+// Records an event on `st` for a batch of transfers; nullptr (with the error
+// set) on failure.
+void* record_event(pw_layer* L, hipStream_t st, pw_status* s) {
+  void* ev = L->evops.create();
+  if (!ev) {
+    *s = fail(PW_EHIP, "hipEventCreate failed");
+    return nullptr;
+  }
+  hipError_t he = hipEventRecord(static_cast<hipEvent_t>(ev), st);
+  if (he != hipSuccess) {
+    L->evops.destroy(ev);
+    *s = hip_fail(he, "hipEventRecord");
+    return nullptr;
+  }
+  return ev;
+}
+
+bool check_batch(pw_layer* L, int n, const int* e, const int* proj, const int* rb, std::string* err) {
+  std::set<size_t> seen;
+  for (int i = 0; i < n; ++i) {
+    if (!L->st.check_block(e[i], proj[i], rb[i], err)) return false;
+    if (!seen.insert(L->st.index(e[i], proj[i], rb[i])).second) {
+      *err = "a block appears twice in the batch";
+      return false;
+    }
+  }
+  return true;
+}
+
+}  // namespace
+
+pw_status pw_offload_blocks(pw_layer* L, int n, const int* e, const int* proj, const int* rb, void* stream) {
+  if (!L || n < 0 || (n > 0 && (!e || !proj || !rb))) return fail(PW_EINVAL, "bad argument");
+  std::string err;
+  if (!check_batch(L, n, e, proj, rb, &err)) return fail(PW_EINVAL, err);
+  struct Planned {
+    int e, proj, rb;
+    pw_page_entry src;
+    uint64_t host_off;
+  };
+  std::vector<Planned> plan;
+  auto rollback = [&]() {
+    for (const Planned& p : plan) L->st.halloc.release(p.host_off, L->st.page_bytes(p.proj, p.src.bits));
+  };
+  for (int i = 0; i < n; ++i) {
+    Planned p{e[i], proj[i], rb[i], {}, 0};
+    bool same = false;
+    pw_status s = L->st.plan_offload(p.e, p.proj, p.rb, &p.src, &p.host_off, &same, &err);
+    if (s != PW_OK) {
+      rollback();
+      return fail(s, err);
+    }
+    if (!same) plan.push_back(p);
+  }
+  if (plan.empty()) return PW_OK;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  for (const Planned& p : plan) {
+    hipError_t he = hipMemcpyAsync(L->host_pool + p.host_off, L->pool + p.src.data_off,
+                                   L->st.page_bytes(p.proj, p.src.bits), hipMemcpyDeviceToHost, st);
+    if (he != hipSuccess) {
+      rollback();
+      return hip_fail(he, "device-to-host page copy");
+    }
+  }
+  pw_status s = PW_OK;
+  void* ev = record_event(L, st, &s);
+  if (!ev) {
+    rollback();
+    return s;
+  }
+  L->st.ref_event(ev);
+  for (const Planned& p : plan) L->st.finish_offload(p.e, p.proj, p.rb, p.host_off, p.src.bits, ev);
+  L->st.unref_event(ev);
+  return PW_OK;
+}
+
+pw_status pw_offload_block(pw_layer* L, int e, int proj, int rb, void* stream) {
+  return pw_offload_blocks(L, 1, &e, &proj, &rb, stream);
+}
+
+pw_status pw_reload_blocks(pw_layer* L, int n, const int* e, const int* proj, const int* rb, void* stream,
+                           size_t* added_total) {
+  if (!L || n < 0 || (n > 0 && (!e || !proj || !rb))) return fail(PW_EINVAL, "bad argument");
+  if (added_total) *added_total = 0;
+  std::string err;
+  if (!check_batch(L, n, e, proj, rb, &err)) return fail(PW_EINVAL, err);
+  struct Planned {
+    int e, proj, rb;
+    pw_page_entry dst;
+    pw::HostCopy hc;
+  };
+  std::vector<Planned> plan;
+  uint64_t added = 0;
+  auto rollback = [&]() {
+    for (const Planned& p : plan) L->st.abort_slot(p.dst, p.proj);
+  };
+  for (int i = 0; i < n; ++i) {
+    Planned p{e[i], proj[i], rb[i], {}, {}};
+    uint64_t a = 0;
+    pw_status s = L->st.plan_reload(p.e, p.proj, p.rb, &p.dst, &p.hc, &a, &err);
+    if (s != PW_OK) {
+      rollback();
+      return fail(s, err);
+    }
+    added += a;
+    plan.push_back(p);
+  }
+  if (plan.empty()) return PW_OK;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  // each host copy must have arrived before it is read back
+  std::set<void*> waits;
+  for (const Planned& p : plan)
+    if (p.hc.ev && !L->evops.done(p.hc.ev)) waits.insert(p.hc.ev);
+  for (void* w : waits) {
+    hipError_t he = hipStreamWaitEvent(st, static_cast<hipEvent_t>(w), 0);
+    if (he != hipSuccess) {
+      rollback();
+      return hip_fail(he, "hipStreamWaitEvent");
+    }
+  }
+  for (const Planned& p : plan) {
+    hipError_t he = hipMemcpyAsync(L->pool + p.dst.data_off, L->host_pool + p.hc.off,
+                                   L->st.page_bytes(p.proj, p.hc.bits), hipMemcpyHostToDevice, st);
+    if (he != hipSuccess) {
+      rollback();
+      return hip_fail(he, "host-to-device page copy");
+    }
+  }
+  pw_status s = PW_OK;
+  void* ev = record_event(L, st, &s);
+  if (!ev) {
+    rollback();
+    return s;
+  }
+  L->st.ref_event(ev);
+  for (const Planned& p : plan) L->st.add_reload_pending(p.e, p.proj, p.rb, p.dst, ev);
+  L->st.unref_event(ev);
+  if (added_total) *added_total = added;
+  return PW_OK;
+}
+
+pw_status pw_reload_block(pw_layer* L, int e, int proj, int rb, void* stream, size_t* added_bytes) {
+  return pw_reload_blocks(L, 1, &e, &proj, &rb, stream, added_bytes);
+}
+
+pw_status pw_drop_host_copy(pw_layer* L, int e, int proj, int rb) {
+  std::string err;
+  if (!L) return fail(PW_EINVAL, "null layer");
+  if (!L->st.check_block(e, proj, rb, &err)) return fail(PW_EINVAL, err);
+  L->st.drop_host_copy(e, proj, rb);
+  return PW_OK;
+}
+
+pw_status pw_host_copy_info(pw_layer* L, int e, int proj, int rb, int* bits, int* ready) {
+  std::string err;
+  if (!L) return fail(PW_EINVAL, "null layer");
+  if (!L->st.check_block(e, proj, rb, &err)) return fail(PW_EINVAL, err);
+  const pw::HostCopy& h = L->st.host[L->st.index(e, proj, rb)];
+  if (bits) *bits = h.bits;
+  if (ready) *ready = h.bits != 0 && (!h.ev || L->evops.done(h.ev)) ? 1 : 0;
+  return PW_OK;
+}
+
+pw_status pw_host_pool_stats(const pw_layer* L, size_t* capacity, size_t* used) {
+  if (!L) return fail(PW_EINVAL, "null layer");
+  if (capacity) *capacity = L->st.halloc.capacity();
+  if (used) *used = L->st.halloc.used();
+  return PW_OK;
 }
 
 pw_status pw_commit(pw_layer* L, void* main_stream, int* n_committed) {

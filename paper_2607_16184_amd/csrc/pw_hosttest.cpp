@@ -5,6 +5,7 @@
 #include <cstdint>
 #include <set>
 #include <string>
+#include <vector>
 
 #include "pw.h"
 #include "pw_state.hpp"
@@ -112,6 +113,95 @@ void pwt_stats(void* hv, uint64_t* used, uint64_t* free_b, uint64_t* largest, ui
   *free_b = h->st.alloc.free_bytes();
   *largest = h->st.alloc.largest_free();
   *live_events = h->ev.live.size();
+}
+
+void pwt_set_host_pool(void* hv, uint64_t bytes) { static_cast<Handle*>(hv)->st.set_host_pool(bytes); }
+
+// Offload a batch (the library's order: plan all, then register under one
+// event); returns the status and the batch's event id (0: nothing copied).
+int pwt_offload(void* hv, int n, const int* e, const int* proj, const int* rb, uint64_t* event_id) {
+  Handle* h = static_cast<Handle*>(hv);
+  struct P { int e, proj, rb; pw_page_entry src; uint64_t off; };
+  std::vector<P> plan;
+  std::set<size_t> seen;
+  *event_id = 0;
+  for (int i = 0; i < n; ++i) {
+    P p{e[i], proj[i], rb[i], {}, 0};
+    bool same = false;
+    pw_status s = PW_OK;
+    if (!h->st.check_block(p.e, p.proj, p.rb, &g_msg)) s = PW_EINVAL;
+    else if (!seen.insert(h->st.index(p.e, p.proj, p.rb)).second) { g_msg = "duplicate"; s = PW_EINVAL; }
+    else s = h->st.plan_offload(p.e, p.proj, p.rb, &p.src, &p.off, &same, &g_msg);
+    if (s != PW_OK) {
+      for (const P& q : plan) h->st.halloc.release(q.off, h->st.page_bytes(q.proj, q.src.bits));
+      return s;
+    }
+    if (!same) plan.push_back(p);
+  }
+  if (plan.empty()) return PW_OK;
+  void* ev = h->ev.create();
+  h->st.ref_event(ev);
+  for (const P& p : plan) h->st.finish_offload(p.e, p.proj, p.rb, p.off, p.src.bits, ev);
+  h->st.unref_event(ev);
+  *event_id = reinterpret_cast<uintptr_t>(ev);
+  return PW_OK;
+}
+
+int pwt_reload(void* hv, int n, const int* e, const int* proj, const int* rb, uint64_t* added,
+               uint64_t* event_id) {
+  Handle* h = static_cast<Handle*>(hv);
+  struct P { int e, proj, rb; pw_page_entry dst; pw::HostCopy hc; };
+  std::vector<P> plan;
+  std::set<size_t> seen;
+  uint64_t tot = 0;
+  *event_id = 0;
+  *added = 0;
+  for (int i = 0; i < n; ++i) {
+    P p{e[i], proj[i], rb[i], {}, {}};
+    uint64_t a = 0;
+    pw_status s = PW_OK;
+    if (!h->st.check_block(p.e, p.proj, p.rb, &g_msg)) s = PW_EINVAL;
+    else if (!seen.insert(h->st.index(p.e, p.proj, p.rb)).second) { g_msg = "duplicate"; s = PW_EINVAL; }
+    else s = h->st.plan_reload(p.e, p.proj, p.rb, &p.dst, &p.hc, &a, &g_msg);
+    if (s != PW_OK) {
+      for (const P& q : plan) h->st.abort_slot(q.dst, q.proj);
+      return s;
+    }
+    tot += a;
+    plan.push_back(p);
+  }
+  if (plan.empty()) return PW_OK;
+  void* ev = h->ev.create();
+  h->st.ref_event(ev);
+  for (const P& p : plan) h->st.add_reload_pending(p.e, p.proj, p.rb, p.dst, ev);
+  h->st.unref_event(ev);
+  *added = tot;
+  *event_id = reinterpret_cast<uintptr_t>(ev);
+  return PW_OK;
+}
+
+int pwt_drop_host_copy(void* hv, int e, int proj, int rb) {
+  Handle* h = static_cast<Handle*>(hv);
+  if (!h->st.check_block(e, proj, rb, &g_msg)) return PW_EINVAL;
+  h->st.drop_host_copy(e, proj, rb);
+  return PW_OK;
+}
+
+// Host copy of a block: bitwidth (0: none), slot offset and its transfer event.
+int pwt_host_copy(void* hv, int e, int proj, int rb, int* bits, uint64_t* off, uint64_t* event_id) {
+  Handle* h = static_cast<Handle*>(hv);
+  if (!h->st.check_block(e, proj, rb, &g_msg)) return PW_EINVAL;
+  const pw::HostCopy& c = h->st.host[h->st.index(e, proj, rb)];
+  *bits = c.bits;
+  *off = c.off;
+  *event_id = reinterpret_cast<uintptr_t>(c.ev);
+  return PW_OK;
+}
+
+void pwt_host_stats(void* hv, uint64_t* capacity, uint64_t* used) {
+  Handle* h = static_cast<Handle*>(hv);
+  *capacity = h->st.halloc.capacity();
+  *used = h->st.halloc.used();
 }
 
 int pwt_all_present(void* hv) { return static_cast<Handle*>(hv)->st.all_present() ? 1 : 0; }

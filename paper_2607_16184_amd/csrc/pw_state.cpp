@@ -71,6 +71,7 @@ LayerState::LayerState(const pw_layer_desc& d, uint64_t pool_bytes, EventOps* ev
   nrb_max = std::max(d.F, d.H) / d.R;
   n_entries = static_cast<size_t>(d.E) * 3 * nrb_max;
   mirror.assign(n_entries, pw_page_entry{0, 0, 0, PW_PAGE_ABSENT, 0, 0});
+  host.assign(n_entries, HostCopy{});
   n_pages = static_cast<size_t>(d.E) * (2 * (d.F / d.R) + d.H / d.R);
 }
 
@@ -127,9 +128,12 @@ pw_status LayerState::plan_requant(int e, int proj, int rb, int new_bits, pw_pag
   if (new_bits != 16 && new_bits != 8 && new_bits != 4) { *err = "bits must be 16, 8 or 4"; return PW_EINVAL; }
   const pw_page_entry& cur = mirror[index(e, proj, rb)];
   if (cur.bits == 0) { *err = "page not present"; return PW_ESTATE; }
-  if (cur.state == PW_PAGE_REQUANT_PENDING) { *err = "a requantization of this block is pending"; return PW_EBUSY; }
+  if (cur.state != PW_PAGE_RESIDENT) { *err = "a requantization or reload of this block is pending"; return PW_EBUSY; }
   if (new_bits == cur.bits) return PW_OK;
-  if (new_bits > cur.bits) { *err = "raising a bitwidth needs a reload from host memory"; return PW_EUNSUPPORTED; }
+  if (new_bits > cur.bits) {
+    *err = "raising a bitwidth needs a reload from a host copy (pw_reload_block)";
+    return PW_EUNSUPPORTED;
+  }
   uint64_t off = 0;
   if (!alloc.alloc(page_bytes(proj, new_bits), &off)) { *err = "pool exhausted"; return PW_ENOMEM; }
   *src = cur;
@@ -185,7 +189,89 @@ uint64_t LayerState::reclaim() {
     }
   }
   retired_.swap(keep);
+  std::vector<Retired> hkeep;
+  for (const Retired& r : hretired_) {
+    if (!r.ev || evops_->done(r.ev)) {
+      halloc.release(r.off, r.bytes);
+      if (r.ev) unref_event(r.ev);
+    } else {
+      hkeep.push_back(r);
+    }
+  }
+  hretired_.swap(hkeep);
   return freed;
+}
+
+pw_status LayerState::plan_offload(int e, int proj, int rb, pw_page_entry* src, uint64_t* host_off, bool* same,
+                                   std::string* err) {
+  *same = false;
+  if (!check_block(e, proj, rb, err)) return PW_EINVAL;
+  if (!has_host_pool()) { *err = "no host pool (pw_layer_set_host_pool)"; return PW_ESTATE; }
+  const size_t idx = index(e, proj, rb);
+  const pw_page_entry& cur = mirror[idx];
+  if (cur.bits == 0) { *err = "page not present"; return PW_ESTATE; }
+  if (cur.state != PW_PAGE_RESIDENT) { *err = "a requantization or reload of this block is pending"; return PW_EBUSY; }
+  if (host[idx].bits == cur.bits) {
+    *same = true;
+    return PW_OK;
+  }
+  uint64_t off = 0;
+  if (!halloc.alloc(page_bytes(proj, cur.bits), &off)) { *err = "host pool exhausted"; return PW_ENOMEM; }
+  *src = cur;
+  *host_off = off;
+  return PW_OK;
+}
+
+void LayerState::finish_offload(int e, int proj, int rb, uint64_t host_off, int bits, void* ev) {
+  drop_host_copy(e, proj, rb);   // a copy at another bitwidth is replaced
+  HostCopy& h = host[index(e, proj, rb)];
+  h.off = host_off;
+  h.bits = static_cast<uint8_t>(bits);
+  h.ev = ev;
+  ref_event(ev);
+}
+
+pw_status LayerState::plan_reload(int e, int proj, int rb, pw_page_entry* dst, HostCopy* hc, uint64_t* added,
+                                  std::string* err) {
+  *added = 0;
+  if (!check_block(e, proj, rb, err)) return PW_EINVAL;
+  const size_t idx = index(e, proj, rb);
+  const pw_page_entry& cur = mirror[idx];
+  if (cur.bits == 0) { *err = "page not present"; return PW_ESTATE; }
+  if (cur.state != PW_PAGE_RESIDENT) { *err = "a requantization or reload of this block is pending"; return PW_EBUSY; }
+  const HostCopy& h = host[idx];
+  if (h.bits == 0) { *err = "the block has no host copy"; return PW_ESTATE; }
+  if (h.bits <= cur.bits) { *err = "the host copy is not of a higher bitwidth"; return PW_EUNSUPPORTED; }
+  uint64_t off = 0;
+  if (!alloc.alloc(page_bytes(proj, h.bits), &off)) { *err = "pool exhausted"; return PW_ENOMEM; }
+  dst->data_off = off;
+  dst->sz_off = h.bits == 16 ? 0 : off + code_bytes(proj, h.bits);
+  dst->bits = h.bits;
+  dst->state = PW_PAGE_RESIDENT;
+  dst->rsv = 0;
+  dst->gen = cur.gen + 1;
+  *hc = h;
+  *added = page_bytes(proj, h.bits) - page_bytes(proj, cur.bits);
+  return PW_OK;
+}
+
+void LayerState::add_reload_pending(int e, int proj, int rb, const pw_page_entry& dst, void* ev) {
+  const size_t idx = index(e, proj, rb);
+  mirror[idx].state = PW_PAGE_RELOAD_PENDING;
+  pending_.push_back(Pending{idx, proj, dst, ev});
+  ref_event(ev);
+  // the host slot is read by this transfer: it stays allocated until the transfer completed
+  HostCopy& h = host[idx];
+  ref_event(ev);
+  if (h.ev) unref_event(h.ev);
+  h.ev = ev;
+}
+
+void LayerState::drop_host_copy(int e, int proj, int rb) {
+  HostCopy& h = host[index(e, proj, rb)];
+  if (h.bits == 0) return;
+  hretired_.push_back(Retired{h.off, page_bytes(proj, h.bits), h.ev});   // the reference moves along
+  h = HostCopy{};
 }
 
 }  // namespace pw

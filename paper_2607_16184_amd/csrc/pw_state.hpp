@@ -13,6 +13,16 @@
 //   reclaim   -> retired slots whose commit event completed go back to the
 //                free list, so the bytes Delta = M^b - M^b' (Eq. 3) become
 //                available to the caller (e.g. for KV-cache blocks).
+// Host copies (Sec. 3.1 page states, offload order):
+//   offload   -> the committed page is copied to a slot of the caller's
+//                host pool (device-to-host on a stream); the block keeps its
+//                GPU page, and its host copy becomes usable once the copy's
+//                event completed;
+//   reload    -> a host copy of a higher bitwidth goes back into a fresh
+//                device slot (host-to-device on a stream, after the offload
+//                finished); the block is pending like a requant and the
+//                raised entry is published by the next commit;
+//   drop      -> the host slot is freed once its last transfer completed.
 #pragma once
 
 #include <cstdint>
@@ -52,6 +62,13 @@ struct EventOps {
   virtual bool done(void* ev) = 0;     // true once the recorded work completed
 };
 
+// A block's copy in host memory.
+struct HostCopy {
+  uint64_t off = 0;      // byte offset in the host pool
+  uint8_t bits = 0;      // bitwidth of the copy; 0: none
+  void* ev = nullptr;    // the last transfer that touches the slot (reference held)
+};
+
 class LayerState {
  public:
   LayerState(const pw_layer_desc& d, uint64_t pool_bytes, EventOps* ev);
@@ -85,11 +102,30 @@ class LayerState {
                          pw_page_entry* dst, uint64_t* delta, std::string* err);
   void add_pending(int e, int proj, int rb, const pw_page_entry& dst, void* ev);
 
+  // Host pool and host copies.
+  bool has_host_pool() const { return halloc.capacity() > 0; }
+  void set_host_pool(uint64_t bytes) { halloc = SlotAllocator(bytes); }
+  // Offload the committed page of a block: a fresh host slot (*host_off) for
+  // *src's page; *same = true (no work) if a copy at the committed bitwidth
+  // exists already.
+  pw_status plan_offload(int e, int proj, int rb, pw_page_entry* src, uint64_t* host_off, bool* same,
+                         std::string* err);
+  void finish_offload(int e, int proj, int rb, uint64_t host_off, int bits, void* ev);
+  // Reload a block from its host copy into a fresh device slot (*dst), the
+  // copy being of a higher bitwidth than the committed page; *added receives
+  // M^b' - M^b.
+  pw_status plan_reload(int e, int proj, int rb, pw_page_entry* dst, HostCopy* hc, uint64_t* added,
+                        std::string* err);
+  void add_reload_pending(int e, int proj, int rb, const pw_page_entry& dst, void* ev);
+  // Forget a block's host copy; its slot is freed by reclaim once its last
+  // transfer completed.
+  void drop_host_copy(int e, int proj, int rb);
+
   struct Pending {
     size_t idx;
     int proj;
     pw_page_entry next;
-    void* ev;   // requant-done event (shared by a batch; reference counted)
+    void* ev;   // requant / reload done event (shared by a batch; reference counted)
   };
   struct Retired {
     uint64_t off, bytes;
@@ -107,6 +143,8 @@ class LayerState {
 
   std::vector<pw_page_entry> mirror;
   SlotAllocator alloc;
+  std::vector<HostCopy> host;      // per table index
+  SlotAllocator halloc{0};         // host pool (capacity 0: none)
   size_t n_pages = 0;
   size_t n_present = 0;
 
@@ -114,6 +152,7 @@ class LayerState {
   EventOps* evops_;
   std::vector<Pending> pending_;
   std::vector<Retired> retired_;
+  std::vector<Retired> hretired_;  // host slots waiting for their last transfer
   std::map<void*, int> refs_;
 };
 

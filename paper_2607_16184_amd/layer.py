@@ -117,6 +117,35 @@ class PagedLayer:
         return pw.pw_requant_blocks(self.handle, list(es), list(ps), list(rbs),
                                     [new_bits] * len(blocks), _stream(stream))
 
+    # -- host copies (offload / reload) ---------------------------------------
+    def set_host_pool(self, host_bytes: int):
+        """Give the layer a pinned host pool of ``host_bytes`` for page copies."""
+        self._host_t = torch.empty(int(host_bytes) + 256, dtype=torch.uint8, pin_memory=True)
+        p = self._host_t.data_ptr()
+        self.host_ptr = (p + 255) // 256 * 256
+        pw.pw_layer_set_host_pool(self.handle, self.host_ptr, int(host_bytes))
+
+    def offload(self, blocks: Sequence[Tuple[int, int, int]], stream=None):
+        if not blocks:
+            return
+        es, ps, rbs = zip(*blocks)
+        pw.pw_offload_blocks(self.handle, list(es), list(ps), list(rbs), _stream(stream))
+
+    def reload(self, blocks: Sequence[Tuple[int, int, int]], stream=None) -> int:
+        if not blocks:
+            return 0
+        es, ps, rbs = zip(*blocks)
+        return pw.pw_reload_blocks(self.handle, list(es), list(ps), list(rbs), _stream(stream))
+
+    def drop_host_copy(self, e: int, p: int, rb: int):
+        pw.pw_drop_host_copy(self.handle, e, p, rb)
+
+    def host_copy_info(self, e: int, p: int, rb: int):
+        return pw.pw_host_copy_info(self.handle, e, p, rb)
+
+    def host_pool_stats(self):
+        return pw.pw_host_pool_stats(self.handle)
+
     def commit(self, stream=None) -> int:
         return pw.pw_commit(self.handle, _stream(stream))
 

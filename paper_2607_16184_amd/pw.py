@@ -21,7 +21,7 @@ LIB_PATH = os.path.join(_HERE, "libpagedweight.so")
 PW_OK, PW_EINVAL, PW_ENOMEM, PW_EBUSY, PW_EUNSUPPORTED, PW_EHIP, PW_ESTATE = range(7)
 PW_F16, PW_BF16 = 0, 1
 PW_GATE, PW_UP, PW_DOWN = 0, 1, 2
-PW_PAGE_ABSENT, PW_PAGE_RESIDENT, PW_PAGE_REQUANT_PENDING = 0, 1, 2
+PW_PAGE_ABSENT, PW_PAGE_RESIDENT, PW_PAGE_REQUANT_PENDING, PW_PAGE_RELOAD_PENDING = 0, 1, 2, 3
 PW_PH_GATEUP, PW_PH_DOWN, PW_PH_COMBINE, PW_PH_REQUANT, PW_NPHASE = 0, 1, 2, 3, 4
 
 
@@ -59,6 +59,14 @@ def _load():
         "pw_moe_paged_gemm": (i32, [vp, vp, i32, i32, vp, vp, vp, vp, vp, i32, vp, sz, vp]),
         "pw_requant_block": (i32, [vp, i32, i32, i32, i32, vp, P(sz)]),
         "pw_requant_blocks": (i32, [vp, i32, P(i32), P(i32), P(i32), P(i32), vp, P(sz)]),
+        "pw_layer_set_host_pool": (i32, [vp, vp, sz]),
+        "pw_offload_block": (i32, [vp, i32, i32, i32, vp]),
+        "pw_offload_blocks": (i32, [vp, i32, P(i32), P(i32), P(i32), vp]),
+        "pw_reload_block": (i32, [vp, i32, i32, i32, vp, P(sz)]),
+        "pw_reload_blocks": (i32, [vp, i32, P(i32), P(i32), P(i32), vp, P(sz)]),
+        "pw_drop_host_copy": (i32, [vp, i32, i32, i32]),
+        "pw_host_copy_info": (i32, [vp, i32, i32, i32, P(i32), P(i32)]),
+        "pw_host_pool_stats": (i32, [vp, P(sz), P(sz)]),
         "pw_commit": (i32, [vp, vp, P(i32)]),
         "pw_reclaim": (i32, [vp, P(sz)]),
         "pw_page_info": (i32, [vp, i32, i32, i32, P(pw_page_entry)]),
@@ -155,6 +163,50 @@ def pw_requant_blocks(layer: int, es: Sequence[int], projs: Sequence[int], rbs: 
     _check(_lib.pw_requant_blocks(layer, n, arr(*es), arr(*projs), arr(*rbs), arr(*new_bits),
                                   stream, ctypes.byref(d)))
     return d.value
+
+
+def pw_layer_set_host_pool(layer: int, host_ptr: int, host_bytes: int):
+    _check(_lib.pw_layer_set_host_pool(layer, host_ptr, host_bytes))
+
+
+def pw_offload_block(layer: int, e: int, proj: int, rb: int, stream: int):
+    _check(_lib.pw_offload_block(layer, e, proj, rb, stream))
+
+
+def pw_offload_blocks(layer: int, es: Sequence[int], projs: Sequence[int], rbs: Sequence[int], stream: int):
+    n = len(es)
+    arr = ctypes.c_int * max(n, 1)
+    _check(_lib.pw_offload_blocks(layer, n, arr(*es), arr(*projs), arr(*rbs), stream))
+
+
+def pw_reload_block(layer: int, e: int, proj: int, rb: int, stream: int) -> int:
+    d = ctypes.c_size_t()
+    _check(_lib.pw_reload_block(layer, e, proj, rb, stream, ctypes.byref(d)))
+    return d.value
+
+
+def pw_reload_blocks(layer: int, es: Sequence[int], projs: Sequence[int], rbs: Sequence[int], stream: int) -> int:
+    n = len(es)
+    arr = ctypes.c_int * max(n, 1)
+    d = ctypes.c_size_t()
+    _check(_lib.pw_reload_blocks(layer, n, arr(*es), arr(*projs), arr(*rbs), stream, ctypes.byref(d)))
+    return d.value
+
+
+def pw_drop_host_copy(layer: int, e: int, proj: int, rb: int):
+    _check(_lib.pw_drop_host_copy(layer, e, proj, rb))
+
+
+def pw_host_copy_info(layer: int, e: int, proj: int, rb: int) -> Tuple[int, bool]:
+    bits, ready = ctypes.c_int(), ctypes.c_int()
+    _check(_lib.pw_host_copy_info(layer, e, proj, rb, ctypes.byref(bits), ctypes.byref(ready)))
+    return bits.value, bool(ready.value)
+
+
+def pw_host_pool_stats(layer: int) -> Tuple[int, int]:
+    c, u = ctypes.c_size_t(), ctypes.c_size_t()
+    _check(_lib.pw_host_pool_stats(layer, ctypes.byref(c), ctypes.byref(u)))
+    return c.value, u.value
 
 
 def pw_commit(layer: int, stream: int) -> int:

@@ -45,6 +45,12 @@ def L():
     u64p = ctypes.POINTER(ctypes.c_uint64)
     lib.pwt_stats.argtypes = [ctypes.c_void_p, u64p, u64p, u64p, u64p]
     lib.pwt_all_present.argtypes = [ctypes.c_void_p]
+    lib.pwt_set_host_pool.argtypes = [ctypes.c_void_p, ctypes.c_uint64]
+    lib.pwt_offload.argtypes = [ctypes.c_void_p, ctypes.c_int, ip, ip, ip, u64p]
+    lib.pwt_reload.argtypes = [ctypes.c_void_p, ctypes.c_int, ip, ip, ip, u64p, u64p]
+    lib.pwt_drop_host_copy.argtypes = [ctypes.c_void_p] + [ctypes.c_int] * 3
+    lib.pwt_host_copy.argtypes = [ctypes.c_void_p] + [ctypes.c_int] * 3 + [ip, u64p, u64p]
+    lib.pwt_host_stats.argtypes = [ctypes.c_void_p, u64p, u64p]
     lib.pwt_last_error.restype = ctypes.c_char_p
     return lib
 
@@ -84,6 +90,32 @@ class Layer:
         v = [ctypes.c_uint64() for _ in range(4)]
         self.lib.pwt_stats(self.h, *[ctypes.byref(x) for x in v])
         return [x.value for x in v]
+
+    def _batch(self, blocks):
+        n = len(blocks)
+        arr = ctypes.c_int * max(n, 1)
+        es, ps, rbs = (zip(*blocks) if n else ((), (), ()))
+        return n, arr(*es), arr(*ps), arr(*rbs)
+
+    def offload(self, blocks):
+        ev = ctypes.c_uint64()
+        st = self.lib.pwt_offload(self.h, *self._batch(blocks), ctypes.byref(ev))
+        return st, ev.value
+
+    def reload(self, blocks):
+        a, ev = ctypes.c_uint64(), ctypes.c_uint64()
+        st = self.lib.pwt_reload(self.h, *self._batch(blocks), ctypes.byref(a), ctypes.byref(ev))
+        return st, a.value, ev.value
+
+    def host_copy(self, e, p, rb):
+        b, off, ev = ctypes.c_int(), ctypes.c_uint64(), ctypes.c_uint64()
+        assert self.lib.pwt_host_copy(self.h, e, p, rb, ctypes.byref(b), ctypes.byref(off), ctypes.byref(ev)) == 0
+        return b.value, off.value, ev.value
+
+    def host_stats(self):
+        c, u = ctypes.c_uint64(), ctypes.c_uint64()
+        self.lib.pwt_host_stats(self.h, ctypes.byref(c), ctypes.byref(u))
+        return c.value, u.value
 
     def close(self):
         self.lib.pwt_destroy(self.h)
@@ -197,4 +229,102 @@ def test_allocator_coalesces(L):
     used, free, largest, _ = Lx.stats()
     assert used == 3 * ((oracle.page_bytes(R, H, G, 4) + 255) // 256 * 256)
     assert largest >= 2 * one                  # freed neighbours merged
+    Lx.close()
+
+
+def _slot(nbytes):
+    return (nbytes + 255) // 256 * 256
+
+
+def test_offload_lower_reload_cycle(L):
+    """Sec. 3.1: the 16-bit page goes to host memory before the block is
+    lowered; a later reload raises it back. The reload is published by a
+    commit, the lower page retires only after that commit completed, and the
+    host slot stays until its last transfer finished."""
+    need = sum(oracle.page_bytes(R, H if p < 2 else F, G, 16) for (_, p, _) in pages())
+    Lx = Layer(L, 2 * need)
+    _load_all(Lx)
+    L.pwt_set_host_pool(Lx.h, need)
+    p16, p4 = oracle.page_bytes(R, F, G, 16), oracle.page_bytes(R, F, G, 4)
+    st, oev = Lx.offload([(1, 2, 3), (0, 0, 0)])
+    assert st == 0 and oev != 0
+    assert Lx.host_copy(1, 2, 3)[0] == 16 and Lx.host_copy(1, 2, 3)[2] == oev
+    assert Lx.host_stats() == (need, _slot(p16) + _slot(oracle.page_bytes(R, H, G, 16)))
+    assert Lx.offload([(1, 2, 3)]) == (0, 0)            # a copy at this bitwidth exists: no-op
+    old = Lx.entry(1, 2, 3)
+    assert Lx.requant([(1, 2, 3)], 4)[0] == 0
+    n, cev = Lx.commit()
+    L.pwt_complete(Lx.h, cev)
+    assert L.pwt_reclaim(Lx.h) == p16
+    free0 = Lx.stats()[1]
+    low = Lx.entry(1, 2, 3)
+    assert low.bits == 4 and low.gen == old.gen + 1
+    # raise it back
+    st, added, rev = Lx.reload([(1, 2, 3)])
+    assert st == 0 and added == p16 - p4 and rev not in (0, oev)
+    cur = Lx.entry(1, 2, 3)
+    assert (cur.bits, cur.data_off, cur.state) == (4, low.data_off, 3)   # reload pending, 4-bit page served
+    assert Lx.stats()[1] == free0 - _slot(p16)
+    assert Lx.requant([(1, 2, 3)], 8)[0] == 3            # EBUSY while the reload is pending
+    assert Lx.offload([(1, 2, 3)])[0] == 3
+    assert Lx.reload([(1, 2, 3)])[0] == 3
+    assert Lx.host_copy(1, 2, 3)[2] == rev               # the host slot now waits for the reload
+    n, cev2 = Lx.commit()
+    assert n == 1
+    cur = Lx.entry(1, 2, 3)
+    assert (cur.bits, cur.state, cur.gen) == (16, 1, low.gen + 1) and cur.data_off != low.data_off
+    assert L.pwt_reclaim(Lx.h) == 0                      # the 4-bit page retires on the commit
+    L.pwt_complete(Lx.h, cev2)
+    assert L.pwt_reclaim(Lx.h) == p4
+    assert Lx.stats()[1] == free0 - _slot(p16) + _slot(p4)
+    assert Lx.reload([(1, 2, 3)])[0] == 4                # copy not above the committed bitwidth
+    # dropping the copy frees its host slot once the reload's transfer is done
+    used0 = Lx.host_stats()[1]
+    assert L.pwt_drop_host_copy(Lx.h, 1, 2, 3) == 0
+    assert Lx.host_copy(1, 2, 3)[0] == 0
+    L.pwt_reclaim(Lx.h)
+    assert Lx.host_stats()[1] == used0
+    L.pwt_complete(Lx.h, rev)
+    L.pwt_reclaim(Lx.h)
+    assert Lx.host_stats()[1] == used0 - _slot(p16)
+    assert L.pwt_drop_host_copy(Lx.h, 0, 0, 0) == 0
+    L.pwt_complete(Lx.h, oev)
+    L.pwt_reclaim(Lx.h)
+    assert Lx.host_stats()[1] == 0 and Lx.stats()[3] == 0   # every slot and event released
+    Lx.close()
+
+
+def test_offload_reload_errors(L):
+    one16, one8 = oracle.page_bytes(R, H, G, 16), oracle.page_bytes(R, H, G, 8)
+    Lx = Layer(L, 2 * one16 + one8)
+    assert Lx.offload([(0, 0, 0)])[0] == 6               # no host pool: ESTATE
+    L.pwt_set_host_pool(Lx.h, one16 + 256)
+    assert Lx.offload([(0, 0, 0)])[0] == 6               # page absent
+    assert Lx.load(0, 0, 0, 16) == 0 and Lx.load(0, 0, 1, 16) == 0
+    assert Lx.reload([(0, 0, 0)])[0] == 6                # no host copy
+    assert Lx.offload([(0, 0, 0), (0, 0, 0)])[0] == 1    # duplicate in a batch
+    # a batch that does not fit leaves no host slot behind
+    assert Lx.offload([(0, 0, 0), (0, 0, 1)])[0] == 2
+    assert Lx.host_stats()[1] == 0 and Lx.host_copy(0, 0, 0)[0] == 0
+    st, oev = Lx.offload([(0, 0, 0)])
+    assert st == 0
+    # lower to 8 bits; then the pool is too full to take a 16-bit page back
+    assert Lx.requant([(0, 0, 0)], 8)[0] == 0
+    n, cev = Lx.commit()
+    L.pwt_complete(Lx.h, cev)
+    L.pwt_reclaim(Lx.h)
+    assert Lx.load(0, 1, 0, 16) == 0
+    free0 = Lx.stats()[1]
+    before = Lx.entry(0, 0, 0)
+    assert Lx.reload([(0, 0, 0)])[0] == 2                # device pool: ENOMEM, nothing changed
+    after = Lx.entry(0, 0, 0)
+    assert (after.bits, after.state, after.data_off) == (8, 1, before.data_off) and Lx.stats()[1] == free0
+    # offloading the 8-bit page replaces the 16-bit copy (its slot waits for its transfer)
+    assert Lx.offload([(0, 0, 0)])[0] == 2               # the host pool holds the 16-bit copy
+    assert L.pwt_drop_host_copy(Lx.h, 0, 0, 0) == 0
+    L.pwt_complete(Lx.h, oev)
+    L.pwt_reclaim(Lx.h)
+    st, oev2 = Lx.offload([(0, 0, 0)])
+    assert st == 0 and Lx.host_copy(0, 0, 0)[0] == 8
+    assert Lx.reload([(0, 0, 0)])[0] == 4                # the copy is not of a higher bitwidth
     Lx.close()
