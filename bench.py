@@ -341,6 +341,109 @@ def leg_downshift(steps_before=8, steps_after=8):
             "bytes_freed": int(freed), "post_switch_weight_GBps": round(post_bytes / (after * 1e-3) / 1e9, 1)}
 
 
+def leg_offload(steps_before=6, steps_after=6):
+    """Sec. 3.1 offload order on the Mixtral-shaped layer: the 256 16-bit pages
+    of the downshift plan are copied to pinned host memory, lowered to int4,
+    and later reloaded chunk by chunk on a side stream while decode steps run;
+    each chunk is committed at the first step boundary after its transfer
+    completed. Copies cross PCIe: these rates are host-link figures."""
+    import numpy as np
+    import torch
+    from paper_2607_16184_amd import pw, synth
+    from paper_2607_16184_amd.layer import PagedLayer
+    cfg = synth.CONFIGS["downshift"]
+    t0 = time.time()
+    w16 = [synth.expert_weights(cfg, p) for p in range(3)]
+    bits = synth.bitmap(cfg)
+    plan = synth.downshift_plan(cfg, bits)
+    pages = [pg for chunk in plan for pg in chunk]
+    L = PagedLayer(cfg, PagedLayer.pool_bytes_for(cfg, bits, slack=0.1))
+    L.load_pages(w16, bits, synth.pool_order(cfg))
+    del w16
+    b16 = [pw.pw_page_bytes(cfg, p, 16) for (_, p, _) in pages]
+    L.set_host_pool(sum((b + 255) // 256 * 256 for b in b16))
+    side = torch.cuda.Stream()
+    main = torch.cuda.current_stream()
+    # warm-up transfer (first use of the copy engines), then its slot is dropped
+    L.offload([pages[0]], stream=side)
+    torch.cuda.synchronize()
+    L.drop_host_copy(*pages[0])
+    L.reclaim()
+    log("offload layer ready in %.1f s" % (time.time() - t0))
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    side.wait_stream(main)
+    e0.record(side)
+    L.offload(pages, stream=side)
+    e1.record(side)
+    L.requant(pages, 4, stream=side)
+    L.commit()
+    torch.cuda.synchronize()
+    L.reclaim()
+    d2h_ms = e0.elapsed_time(e1)
+    nin = 16
+    ins = []
+    for s in range(nin):
+        lg, x16 = synth.step_inputs(cfg, s)
+        ins.append((torch.from_numpy(lg).cuda(), torch.from_numpy(x16.view(np.int16)).cuda()))
+    rbuf = PagedLayer.routing_buffers(cfg.T, cfg.E, cfg.K)
+    y = torch.empty((cfg.T, cfg.H), dtype=torch.int16, device="cuda")
+    for s in range(2):
+        L.forward(ins[s][1], L.route(ins[s][0], cfg.K, out=rbuf), y=y)
+    torch.cuda.synchronize()
+    ev = []
+    rev = []
+    k, inflight, last = 0, None, None
+    during = []
+    s = 0
+    # bounded: every chunk's reload is issued once the previous one committed
+    while s < 2000 and (last is None or k < len(plan) or inflight is not None or s < last + 1 + steps_after):
+        if s >= steps_before and inflight is None and k < len(plan):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(side)
+            L.reload(plan[k], stream=side)
+            b.record(side)
+            rev.append((a, b))
+            inflight = b
+            k += 1
+        ev.append((torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)))
+        ev[s][0].record()
+        xi = ins[s % nin]
+        L.forward(xi[1], L.route(xi[0], cfg.K, out=rbuf), y=y)
+        ev[s][1].record()
+        if s > 0:
+            ev[s - 1][1].synchronize()   # a serving loop: the host runs one step ahead
+        if inflight is not None:
+            during.append(s)
+            if inflight.query():
+                L.commit()
+                inflight = None
+                last = s
+        L.reclaim()
+        s += 1
+    torch.cuda.synchronize()
+    if inflight is not None:
+        L.commit()
+        torch.cuda.synchronize()
+    L.reclaim()
+    done = all(L.entry(*pg).bits == 16 for pg in pages)
+    step_ms = [a.elapsed_time(b) for a, b in ev]
+    before = float(np.median(step_ms[:steps_before]))
+    dur = float(np.median([step_ms[i] for i in during])) if during else None
+    after = float(np.median(step_ms[last + 1:])) if last is not None and last + 1 < len(step_ms) else None
+    h2d_ms = sum(a.elapsed_time(b) for a, b in rev)
+    L.close()
+    return {"workload": "mixtral_decode layer, 64-token steps; 256 16-bit pages (8 chunks of 32) offloaded "
+                        "to pinned host memory, lowered to int4, then reloaded chunk by chunk during decode",
+            "bytes": int(sum(b16)), "d2h_GBps": round(sum(b16) / (d2h_ms * 1e-3) / 1e9, 1),
+            "h2d_GBps": round(sum(b16) / (h2d_ms * 1e-3) / 1e9, 1),
+            "reload_chunks": len(rev), "reload_all_back_to_16_bits": bool(done),
+            "steps_with_reload_in_flight": len(during),
+            "step_ms_before_plan_pages_int4": round(before, 4),
+            "step_ms_during_reload": round(dur, 4) if dur is not None else None,
+            "step_ms_after_plan_pages_16bit": round(after, 4) if after is not None else None,
+            "decode_slowdown": round(dur / before - 1.0, 4) if dur is not None else None}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -348,7 +451,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="mixtral_decode")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--extras", default="prefill,finegrained,downshift",
+    ap.add_argument("--extras", default="prefill,finegrained,downshift,offload",
                     help="comma list of extra legs on the same JSON line ('' for none)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after the timed steps, run one device copy of this many MiB "
@@ -442,6 +545,8 @@ def main():
             extras["finegrained"] = leg_layer("finegrained", steps=21, warmup=3, pools=3)
         elif leg == "downshift":
             extras["downshift"] = leg_downshift()
+        elif leg == "offload":
+            extras["offload"] = leg_offload()
         log("leg %s done in %.1f s" % (leg, time.time() - t0))
     if extras:
         out["extras"] = extras
