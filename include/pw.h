@@ -247,6 +247,123 @@ enum { PW_PH_GATEUP = 0, PW_PH_DOWN = 1, PW_PH_COMBINE = 2, PW_PH_REQUANT = 3, P
 pw_status pw_profile_enable(pw_layer* layer, int on);
 pw_status pw_profile_read(pw_layer* layer, double* total_ms, int64_t* count, int reset);
 
+/* ------------------------------------------------------------------------
+ * Routing statistics and the runtime planner (Sec. 3.2, Alg. 1).
+ * ---------------------------------------------------------------------- */
+
+/* Per-expert routing statistics of one step, for Eq. 1's routing mass and
+ * the routed-input features of the prompt residual (Sec. 3.2). For each
+ * expert e and each slot routed to it (sorted_slot[offsets[e] ..
+ * offsets[e+1]), in that order), with r the slot's routing weight and |x|
+ * the Euclidean norm of the slot's input row:
+ *   stats[5 e + 0] = sum r        stats[5 e + 1] = number of slots
+ *   stats[5 e + 2] = sum r |x|    stats[5 e + 3] = sum r |x|^2
+ *   stats[5 e + 4] = max |x|
+ * in float64 with a fixed summation order (bit-identical across runs).
+ * rows: [n_rows][dim] 16-bit values of dtype act (16-byte aligned, dim a
+ * multiple of 8). rows_by_position = 0: the row of slot s = t K + k is
+ * token t (the gate/up input x, n_rows = T); 1: the row of the i-th slot
+ * of the expert-major list is row i (the down input h, n_rows = T K).
+ * norm2_ws: device workspace of n_rows doubles. accumulate != 0 adds to
+ * stats (online statistics over steps) instead of overwriting it. All
+ * pointers are device memory; work is enqueued on `stream`.
+ *   bad sizes or pointers: PW_EINVAL.                                     */
+pw_status pw_routing_stats(const void* rows, pw_dtype act, int n_rows, int dim, int rows_by_position,
+                           const float* topk_w, const int32_t* offsets, const int32_t* sorted_slot,
+                           int T, int E, int K, double* norm2_ws, double* stats, int accumulate,
+                           void* stream);
+
+/* The planner (host code; no GPU work). Units are the page-table blocks it
+ * may lower; unit i belongs to expert unit_expert[i] and has linear-block
+ * type unit_type[i] (0: gate_up, for the gate and up projections; 1: down).
+ * unit_bytes[3 i + j] is Eq. 3's M^b of the unit for b = 16, 8, 4 (j = 0,
+ * 1, 2) and unit_sens[3 i + j] the offline sensitivity s^b (Eq. 2).
+ * Bitwidths step down one level at a time (16 -> 8 -> 4).
+ *
+ * Configuration (offline calibration results, Sec. 3.2 and 4.1):
+ *   routing buckets: experts sorted by routing mass (descending, ties to the
+ *     lower index); bucket j takes positions floor(E c_{j-1} + 1/2) ..
+ *     floor(E c_j + 1/2), c_j the running sum of bucket_frac (the last
+ *     bucket takes the rest); mult[j] is its damage multiplier;
+ *   bitwidth-floor stages: floor_bits[s][j] is the lowest bitwidth bucket j
+ *     may reach at stage s (stages relax the floors: the depth caps);
+ *   prompt residual heads [u][t] (t = 0: 16 -> 8, t = 1: 8 -> 4): Eq. 5's
+ *     w and a, Eq. 6's confidence c, strength alpha, clip [rho_min,
+ *     rho_max]; Eq. 8's damage floor eps.                                  */
+#define PW_PLAN_MAX_BUCKETS 8
+#define PW_PLAN_MAX_STAGES 8
+typedef struct {
+    int n_buckets;
+    double bucket_frac[PW_PLAN_MAX_BUCKETS];
+    double mult[PW_PLAN_MAX_BUCKETS];
+    int n_stages;
+    int floor_bits[PW_PLAN_MAX_STAGES][PW_PLAN_MAX_BUCKETS];
+    double alpha, rho_min, rho_max, eps;
+    double head_w[2][2][3];
+    double head_a[2][2];
+    double head_c[2][2];
+} pw_planner_config;
+
+typedef struct pw_planner pw_planner;
+
+/* Result of one planner step. */
+typedef struct {
+    uint64_t target;     /* Eq. 7's D                                          */
+    uint64_t bytes;      /* bytes the selected plan releases (sum of Eq. 3)    */
+    double damage;       /* sum of Eq. 8 over its steps                        */
+    int triggered;       /* D > 0: a plan was selected                         */
+    int stage;           /* stage of the selected plan (-1: none)              */
+    int n_steps;         /* one-level steps in it                              */
+    int n_units;         /* units it lowers                                    */
+} pw_plan_summary;
+
+/* Copies the unit tables; the planner keeps one candidate plan per stage (the
+ * plan queue) between steps.
+ *   bad sizes, types, bitwidth floors or fractions: PW_EINVAL.             */
+pw_status pw_planner_create(int n_experts, int n_units, const int* unit_expert, const int* unit_type,
+                            const uint64_t* unit_bytes, const double* unit_sens,
+                            const pw_planner_config* cfg, pw_planner** out);
+void pw_planner_destroy(pw_planner* p);
+
+/* The batch-level observation (Sec. 3.2, batched serving): each request adds
+ * its routing statistics (host copies of pw_routing_stats for the gate/up
+ * input and, or NULL for zero features, the down input) with its KV-block
+ * weight; masses and features are averaged with those weights.
+ * pw_planner_clear_requests forgets them.                                 */
+pw_status pw_planner_add_request(pw_planner* p, const double* stats_gate_up, const double* stats_down,
+                                 double kv_weight);
+pw_status pw_planner_clear_requests(pw_planner* p);
+
+/* One step of Alg. 1: D from the KV pressure (Eq. 7), a greedy plan per
+ * stage (steps by Eq. 8's damage per released byte, cheapest first, until
+ * D is met), the queue refreshed; when D > 0 the selected plan is the
+ * strictest stage's that meets D, else the one releasing the most bytes.
+ * unit_bits[i] is the unit's committed bitwidth (16, 8 or 4; 0: skip).  */
+pw_status pw_planner_step(pw_planner* p, const int* unit_bits, int free_blocks, int free_threshold,
+                          uint64_t kv_block_bytes, pw_plan_summary* out);
+
+/* The plan of stage `stage` (-1: the selected one) as one entry per unit,
+ * in the order the units were first taken: unit, committed bitwidth,
+ * final bitwidth, bytes released (M^from - M^to). *n receives the count;
+ * at most max_n entries are written. With steps != 0 the one-level steps
+ * are listed instead (from and to one level apart, in the order taken).  */
+pw_status pw_planner_plan(const pw_planner* p, int stage, int steps, int max_n, int* unit, int* from_bits,
+                          int* to_bits, uint64_t* bytes, int* n);
+
+/* Layer helpers: units = every table entry (expert, proj, row block) in
+ * table order (index (e * 3 + proj) * nrb_max + rb; entries past a
+ * projection's row blocks are units with bits 0). sens: [entries][3].
+ * pw_planner_step_layer takes the committed bitwidths from the layer's
+ * host mirror (blocks with a pending requant or reload are skipped);
+ * pw_planner_apply requantizes every unit of the selected plan to its
+ * final bitwidth on side_stream (pw_requant_blocks), *delta_total
+ * receiving the bytes released once committed.                          */
+pw_status pw_planner_create_for_layer(const pw_layer* layer, const double* sens, const pw_planner_config* cfg,
+                                      pw_planner** out);
+pw_status pw_planner_step_layer(pw_planner* p, const pw_layer* layer, int free_blocks, int free_threshold,
+                                uint64_t kv_block_bytes, pw_plan_summary* out);
+pw_status pw_planner_apply(pw_planner* p, pw_layer* layer, void* side_stream, size_t* delta_total);
+
 const char* pw_last_error(void);
 const char* pw_status_str(pw_status s);
 

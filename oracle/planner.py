@@ -13,8 +13,9 @@ Readings where the paper is silent (each also listed in the design notes):
   planner step lowers a unit by one level (16 -> 8 or 8 -> 4), and a unit's
   8 -> 4 step becomes available only after its 16 -> 8 step was taken.
 * Routing buckets: experts sorted by routing mass (descending, ties to the
-  lower index); bucket j holds the experts from position round(E * sum of the
-  fractions before j) up to round(E * sum including j).
+  lower index); bucket j holds the experts from position floor(E * c_{j-1} + 1/2)
+  up to floor(E * c_j + 1/2), c_j being the running sum of the fractions in
+  float64 (the last bucket takes the rest).
 * Bitwidth-floor stages: stage s gives every bucket a floor; a step b -> b' is
   legal at stage s when b' is not below the floor of the unit's bucket. Later
   stages relax the floors (the depth caps).
@@ -135,7 +136,7 @@ def buckets(mass: np.ndarray, frac: Sequence[float]) -> np.ndarray:
     acc, start = 0.0, 0
     for j, f in enumerate(frac):
         acc += f
-        end = E if j == len(frac) - 1 else int(round(E * acc))
+        end = E if j == len(frac) - 1 else int(math.floor(E * acc + 0.5))
         for pos in range(start, min(end, E)):
             b[order[pos]] = j
         start = max(start, end)

@@ -42,6 +42,7 @@ SOURCES = {
     "pw_tgemm.hip": [],
     "pw_api.cpp": [],
     "pw_state.cpp": [],
+    "pw_plan.cpp": [],
 }
 
 

@@ -24,6 +24,14 @@ pw_status hip_fail(hipError_t e, const char* what) {
   return fail(PW_EHIP, std::string(what) + ": " + hipGetErrorString(e));
 }
 
+}  // namespace
+
+namespace pw {
+pw_status set_error(pw_status s, const char* msg) { return fail(s, msg); }
+}  // namespace pw
+
+namespace {
+
 struct HipEvents : pw::EventOps {
   void* create() override {
     hipEvent_t ev = nullptr;
@@ -296,6 +304,25 @@ pw_status pw_route_topk(const float* logits, int T, int E, int K, int renorm, in
   return PW_OK;
 }
 
+pw_status pw_routing_stats(const void* rows, pw_dtype act, int n_rows, int dim, int rows_by_position,
+                           const float* topk_w, const int32_t* offsets, const int32_t* sorted_slot, int T, int E,
+                           int K, double* norm2_ws, double* stats, int accumulate, void* stream) {
+  if (T < 0 || E < 1 || K < 1 || K > E || E > 4096) return fail(PW_EINVAL, "need T >= 0, 1 <= K <= E <= 4096");
+  if (static_cast<int64_t>(T) * K >= (int64_t(1) << 31)) return fail(PW_EINVAL, "T*K too large");
+  if (act != PW_F16 && act != PW_BF16) return fail(PW_EINVAL, "act must be PW_F16 or PW_BF16");
+  const int want = rows_by_position ? T * K : T;
+  if (n_rows != want) return fail(PW_EINVAL, rows_by_position ? "n_rows must be T*K" : "n_rows must be T");
+  if (dim < 8 || dim % 8 != 0) return fail(PW_EINVAL, "dim must be a positive multiple of 8");
+  if (!offsets || !stats || (T > 0 && (!rows || !topk_w || !sorted_slot || !norm2_ws)))
+    return fail(PW_EINVAL, "null argument");
+  if (reinterpret_cast<uintptr_t>(rows) & 15u) return fail(PW_EINVAL, "rows must be 16-byte aligned");
+  hipError_t e = pw::launch_routing_stats(static_cast<const uint16_t*>(rows), act, n_rows, dim, rows_by_position,
+                                          topk_w, offsets, sorted_slot, T * K, E, K, norm2_ws, stats, accumulate,
+                                          static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "routing statistics launch");
+  return PW_OK;
+}
+
 pw_status pw_workspace_bytes(const pw_layer* L, int T, int K, size_t* gemm_ws) {
   if (!L || !gemm_ws || T < 0 || K < 1) return fail(PW_EINVAL, "bad argument");
   *gemm_ws = ws_layout(L->st.desc, T, K).total;
@@ -482,7 +509,7 @@ namespace {
 
 // Records an event on `st` for a batch of transfers; nullptr (with the error
 // set) on failure.
-void* record_event(pw_layer* L, hipStream_t st, pw_status* s) {
+static void* record_event(pw_layer* L, hipStream_t st, pw_status* s) {
   void* ev = L->evops.create();
   if (!ev) {
     *s = fail(PW_EHIP, "hipEventCreate failed");
@@ -497,7 +524,7 @@ void* record_event(pw_layer* L, hipStream_t st, pw_status* s) {
   return ev;
 }
 
-bool check_batch(pw_layer* L, int n, const int* e, const int* proj, const int* rb, std::string* err) {
+static bool check_batch(pw_layer* L, int n, const int* e, const int* proj, const int* rb, std::string* err) {
   std::set<size_t> seen;
   for (int i = 0; i < n; ++i) {
     if (!L->st.check_block(e[i], proj[i], rb[i], err)) return false;
@@ -648,6 +675,77 @@ pw_status pw_host_pool_stats(const pw_layer* L, size_t* capacity, size_t* used) 
   if (capacity) *capacity = L->st.halloc.capacity();
   if (used) *used = L->st.halloc.used();
   return PW_OK;
+}
+
+pw_status pw_planner_create_for_layer(const pw_layer* L, const double* sens, const pw_planner_config* cfg,
+                                      pw_planner** out) {
+  if (!L || !sens || !cfg || !out) return fail(PW_EINVAL, "bad argument");
+  const size_t n = L->st.n_entries;
+  std::vector<int> ex(n), ty(n);
+  std::vector<uint64_t> nb(3 * n);
+  for (int e = 0; e < L->st.desc.E; ++e)
+    for (int p = 0; p < 3; ++p)
+      for (int rb = 0; rb < L->st.nrb_max; ++rb) {
+        const size_t i = L->st.index(e, p, rb);
+        ex[i] = e;
+        ty[i] = p == PW_DOWN ? 1 : 0;
+        nb[3 * i] = L->st.page_bytes(p, 16);
+        nb[3 * i + 1] = L->st.page_bytes(p, 8);
+        nb[3 * i + 2] = L->st.page_bytes(p, 4);
+      }
+  return pw_planner_create(L->st.desc.E, static_cast<int>(n), ex.data(), ty.data(), nb.data(), sens, cfg, out);
+}
+
+namespace {
+
+// Committed bitwidth per table entry; 0 for blocks past a projection's row
+// blocks, absent pages and blocks with a pending requant or reload.
+static std::vector<int> planner_bits(const pw_layer* L) {
+  std::vector<int> q(L->st.n_entries, 0);
+  for (int e = 0; e < L->st.desc.E; ++e)
+    for (int p = 0; p < 3; ++p)
+      for (int rb = 0; rb < L->st.nrb(p); ++rb) {
+        const size_t i = L->st.index(e, p, rb);
+        const pw_page_entry& ent = L->st.mirror[i];
+        if (ent.state == PW_PAGE_RESIDENT) q[i] = ent.bits;
+      }
+  return q;
+}
+
+}  // namespace
+
+pw_status pw_planner_step_layer(pw_planner* P, const pw_layer* L, int free_blocks, int free_threshold,
+                                uint64_t kv_block_bytes, pw_plan_summary* out) {
+  if (!P || !L) return fail(PW_EINVAL, "bad argument");
+  if (pw::planner_units(P) != static_cast<int>(L->st.n_entries))
+    return fail(PW_EINVAL, "planner was not made for this layer's table");
+  const std::vector<int> q = planner_bits(L);
+  return pw_planner_step(P, q.data(), free_blocks, free_threshold, kv_block_bytes, out);
+}
+
+pw_status pw_planner_apply(pw_planner* P, pw_layer* L, void* side_stream, size_t* delta_total) {
+  if (!P || !L) return fail(PW_EINVAL, "bad argument");
+  if (delta_total) *delta_total = 0;
+  if (pw::planner_units(P) != static_cast<int>(L->st.n_entries))
+    return fail(PW_EINVAL, "planner was not made for this layer's table");
+  int n = 0;
+  pw_status s = pw_planner_plan(P, -1, 0, 0, nullptr, nullptr, nullptr, nullptr, &n);
+  if (s != PW_OK || n == 0) return s;
+  std::vector<int> unit(n), from(n), to(n);
+  s = pw_planner_plan(P, -1, 0, n, unit.data(), from.data(), to.data(), nullptr, &n);
+  if (s != PW_OK) return s;
+  const std::vector<int> q = planner_bits(L);
+  std::vector<int> es, ps, rbs, nbits;
+  for (int k = 0; k < n; ++k) {
+    const int i = unit[k];
+    if (q[i] != from[k]) return fail(PW_ESTATE, "the table changed since the planner step");
+    const int rb = i % L->st.nrb_max, ep = i / L->st.nrb_max;
+    es.push_back(ep / 3);
+    ps.push_back(ep % 3);
+    rbs.push_back(rb);
+    nbits.push_back(to[k]);
+  }
+  return pw_requant_blocks(L, n, es.data(), ps.data(), rbs.data(), nbits.data(), side_stream, delta_total);
 }
 
 pw_status pw_commit(pw_layer* L, void* main_stream, int* n_committed) {

@@ -4,6 +4,7 @@
 
 #include <hip/hip_runtime.h>
 #include <cstdint>
+#include <string>
 
 #include "pw.h"
 
@@ -73,5 +74,14 @@ hipError_t launch_combine(const GemmArgs& a, hipStream_t st);
 hipError_t launch_tgemm(const GemmArgs& a, bool gateup, hipStream_t st);
 // small and medium slot counts: register-streamed tiles of 16/32/64 slots
 hipError_t launch_sgemm(const GemmArgs& a, bool gateup, hipStream_t st);
+// Per-expert routing statistics (row norms, then a fixed-order reduction).
+hipError_t launch_routing_stats(const uint16_t* rows, int act, int n_rows, int dim, int by_position,
+                                const float* topk_w, const int32_t* offsets, const int32_t* sorted_slot, int S,
+                                int E, int K, double* norm2, double* stats, int accumulate, hipStream_t st);
+
+// Error reporting of the C ABI (thread-local message, returned status).
+pw_status set_error(pw_status s, const char* msg);
+inline pw_status set_error(pw_status s, const std::string& msg) { return set_error(s, msg.c_str()); }
+int planner_units(const pw_planner* p);
 
 }  // namespace pw

@@ -501,6 +501,80 @@ __global__ __launch_bounds__(256) void k_combine(const GemmArgs a) {
 
 }  // namespace
 
+namespace {
+
+// ---------------------------------------------------------------------------
+// Routing statistics for the planner (Eq. 1's numerator and the routed-input
+// features of Sec. 3.2), in float64 with a fixed summation order.
+// ---------------------------------------------------------------------------
+
+// One wave per row: squared Euclidean norm of a 16-bit row. Lane l sums the
+// values l * 8 .. + 8 of every 512-value span in order, then a butterfly.
+template <int ACT>
+__global__ __launch_bounds__(256) void k_row_norm2(const uint16_t* rows, int n_rows, int dim, double* out) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (row >= n_rows) return;
+  const uint16_t* r = rows + static_cast<size_t>(row) * dim;
+  double acc = 0.0;
+  for (int k = lane * 8; k < dim; k += 512) {
+    const u32x4 v = *reinterpret_cast<const u32x4*>(r + k);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const double a = val16(v[q] & 0xFFFFu, ACT), b = val16(v[q] >> 16, ACT);
+      acc += a * a;   // exact products of 16-bit values
+      acc += b * b;
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o);
+  if (lane == 0) out[row] = acc;
+}
+
+// One workgroup per expert: thread j takes the expert's slots j, j + 256, ...
+// in order, then a fixed tree over the 256 partial sums.
+__global__ __launch_bounds__(256) void k_expert_stats(const double* norm2, int by_position, const float* topk_w,
+                                                      const int32_t* offsets, const int32_t* sorted_slot, int S,
+                                                      int K, int n_rows, double* stats, int accumulate) {
+  __shared__ double red[5][256];
+  const int e = blockIdx.x, tid = threadIdx.x;
+  const int o = clampi(offsets[e], 0, S);
+  const int n = clampi(offsets[e + 1], o, S) - o;
+  double a0 = 0.0, a1 = 0.0, a2 = 0.0, a3 = 0.0, a4 = 0.0;
+  for (int i = tid; i < n; i += 256) {
+    const int slot = clampi(sorted_slot[o + i], 0, S - 1);
+    const int row = clampi(by_position ? o + i : slot / K, 0, n_rows - 1);
+    const double r = topk_w[slot];
+    const double n2 = norm2[row];
+    const double nn = sqrt(n2);
+    a0 += r;
+    a1 += 1.0;
+    a2 += r * nn;
+    a3 += r * n2;
+    a4 = fmax(a4, nn);
+  }
+  red[0][tid] = a0;
+  red[1][tid] = a1;
+  red[2][tid] = a2;
+  red[3][tid] = a3;
+  red[4][tid] = a4;
+  __syncthreads();
+  for (int s = 128; s > 0; s >>= 1) {
+    if (tid < s) {
+#pragma unroll
+      for (int c = 0; c < 4; ++c) red[c][tid] += red[c][tid + s];
+      red[4][tid] = fmax(red[4][tid], red[4][tid + s]);
+    }
+    __syncthreads();
+  }
+  if (tid < 5) {
+    const double v = red[tid][0];
+    double* d = stats + 5 * static_cast<size_t>(e) + tid;
+    *d = !accumulate ? v : tid == 4 ? fmax(*d, v) : *d + v;
+  }
+}
+
+}  // namespace
+
 // ---------------------------------------------------------------------------
 // launchers
 // ---------------------------------------------------------------------------
@@ -556,6 +630,21 @@ hipError_t launch_combine(const GemmArgs& a, hipStream_t st) {
   if (a.T <= 0) return hipSuccess;
   const dim3 grid(a.T, (a.H / 4 + 255) / 256), block(256);
   hipLaunchKernelGGL(k_combine, grid, block, 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_routing_stats(const uint16_t* rows, int act, int n_rows, int dim, int by_position,
+                                const float* topk_w, const int32_t* offsets, const int32_t* sorted_slot, int S,
+                                int E, int K, double* norm2, double* stats, int accumulate, hipStream_t st) {
+  if (n_rows > 0) {
+    const dim3 grid((n_rows + 3) / 4);
+    if (act == PW_BF16)
+      hipLaunchKernelGGL(k_row_norm2<PW_BF16>, grid, dim3(256), 0, st, rows, n_rows, dim, norm2);
+    else
+      hipLaunchKernelGGL(k_row_norm2<PW_F16>, grid, dim3(256), 0, st, rows, n_rows, dim, norm2);
+  }
+  hipLaunchKernelGGL(k_expert_stats, dim3(E), dim3(256), 0, st, norm2, by_position, topk_w, offsets, sorted_slot, S,
+                     K, n_rows, stats, accumulate);
   return hipGetLastError();
 }
 

@@ -109,6 +109,34 @@ class PagedLayer:
                              ws_ptr, ws_bytes, _stream(stream))
         return y
 
+    # -- planner observations (Sec. 3.2) ------------------------------------
+    def routing_stats(self, rows: torch.Tensor, routing, rows_by_position: bool = False,
+                      out: torch.Tensor = None, accumulate: bool = False, stream=None) -> torch.Tensor:
+        """[E, 5] float64 routing statistics of one step (pw_routing_stats):
+        rows = x [T, H] (gate/up input, one row per token) or the SwiGLU rows
+        [T K, F] in expert-major slot order (down input, rows_by_position)."""
+        ids, w, offsets, ss, _ = routing
+        T, K = ids.shape
+        if out is None:
+            out = torch.zeros((self.cfg.E, 5), dtype=torch.float64, device=rows.device)
+        norm2 = torch.empty(max(rows.shape[0], 1), dtype=torch.float64, device=rows.device)
+        pw.pw_routing_stats(rows.data_ptr(), self.cfg.act, rows.shape[0], rows.shape[1], int(rows_by_position),
+                            w.data_ptr(), offsets.data_ptr(), ss.data_ptr(), T, self.cfg.E, K, norm2.data_ptr(),
+                            out.data_ptr(), int(accumulate), _stream(stream))
+        return out
+
+    def hidden_rows(self, T: int, K: int) -> torch.Tensor:
+        """The SwiGLU output of the last forward, [T K, F] 16-bit, expert-major
+        slot order (a view of the workspace)."""
+        self.workspace(T, K)
+        off = self._ws_ptr - self._ws.data_ptr()
+        n = T * K * self.cfg.F
+        return self._ws[off:off + 2 * n].view(torch.int16).view(T * K, self.cfg.F)
+
+    def planner(self, sens: np.ndarray, cfg) -> "Planner":
+        """A runtime planner over this layer's table entries (sens: [entries, 3])."""
+        return Planner(pw.pw_planner_create_for_layer(self.handle, sens, cfg))
+
     # -- runtime downshift -------------------------------------------------
     def requant(self, blocks: Sequence[Tuple[int, int, int]], new_bits: int, stream=None) -> int:
         if not blocks:
@@ -174,6 +202,41 @@ class PagedLayer:
         if self.handle:
             torch.cuda.synchronize(self.device)
             pw.pw_layer_destroy(self.handle)
+            self.handle = 0
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class Planner:
+    """Host-side runtime planner (Alg. 1); see pw_planner_* in include/pw.h."""
+
+    def __init__(self, handle: int):
+        self.handle = handle
+
+    def add_request(self, stats_gate_up, stats_down=None, kv_weight: float = 1.0):
+        g = stats_gate_up.cpu().numpy() if isinstance(stats_gate_up, torch.Tensor) else stats_gate_up
+        d = stats_down.cpu().numpy() if isinstance(stats_down, torch.Tensor) else stats_down
+        pw.pw_planner_add_request(self.handle, g, d, kv_weight)
+
+    def clear_requests(self):
+        pw.pw_planner_clear_requests(self.handle)
+
+    def step(self, layer: PagedLayer, free_blocks: int, free_threshold: int, kv_block_bytes: int):
+        return pw.pw_planner_step_layer(self.handle, layer.handle, free_blocks, free_threshold, kv_block_bytes)
+
+    def plan(self, stage: int = -1, steps: bool = False):
+        return pw.pw_planner_plan(self.handle, stage, steps)
+
+    def apply(self, layer: PagedLayer, stream=None) -> int:
+        return pw.pw_planner_apply(self.handle, layer.handle, _stream(stream))
+
+    def close(self):
+        if self.handle:
+            pw.pw_planner_destroy(self.handle)
             self.handle = 0
 
     def __del__(self):

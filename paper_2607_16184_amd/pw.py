@@ -15,6 +15,8 @@ import ctypes
 import os
 from typing import Sequence, Tuple
 
+import numpy as np
+
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libpagedweight.so")
 
@@ -35,6 +37,29 @@ class pw_layer_desc(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int) for n in ("E", "H", "F", "R", "G", "act", "sdt")]
 
 
+PW_PLAN_MAX_BUCKETS = 8
+PW_PLAN_MAX_STAGES = 8
+
+
+class pw_planner_config(ctypes.Structure):
+    _fields_ = [("n_buckets", ctypes.c_int),
+                ("bucket_frac", ctypes.c_double * PW_PLAN_MAX_BUCKETS),
+                ("mult", ctypes.c_double * PW_PLAN_MAX_BUCKETS),
+                ("n_stages", ctypes.c_int),
+                ("floor_bits", (ctypes.c_int * PW_PLAN_MAX_BUCKETS) * PW_PLAN_MAX_STAGES),
+                ("alpha", ctypes.c_double), ("rho_min", ctypes.c_double), ("rho_max", ctypes.c_double),
+                ("eps", ctypes.c_double),
+                ("head_w", ((ctypes.c_double * 3) * 2) * 2),
+                ("head_a", (ctypes.c_double * 2) * 2),
+                ("head_c", (ctypes.c_double * 2) * 2)]
+
+
+class pw_plan_summary(ctypes.Structure):
+    _fields_ = [("target", ctypes.c_uint64), ("bytes", ctypes.c_uint64), ("damage", ctypes.c_double),
+                ("triggered", ctypes.c_int), ("stage", ctypes.c_int), ("n_steps", ctypes.c_int),
+                ("n_units", ctypes.c_int)]
+
+
 class PWError(RuntimeError):
     def __init__(self, status: int, msg: str):
         super().__init__("%s: %s" % (_status_name(status), msg))
@@ -42,6 +67,13 @@ class PWError(RuntimeError):
 
 
 def _load():
+    # The library binds to whatever HIP runtime the process has loaded. PyTorch
+    # ships its own copy: load it first, so the library and PyTorch share one
+    # runtime (two runtimes in one process do not both reach the device).
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     if not os.path.exists(LIB_PATH):
         from . import build as _build
         _build.build_all()
@@ -73,6 +105,17 @@ def _load():
         "pw_pool_stats": (i32, [vp, P(sz), P(sz), P(sz)]),
         "pw_profile_enable": (i32, [vp, i32]),
         "pw_profile_read": (i32, [vp, P(ctypes.c_double), P(ctypes.c_int64), i32]),
+        "pw_routing_stats": (i32, [vp, i32, i32, i32, i32, vp, vp, vp, i32, i32, i32, vp, vp, i32, vp]),
+        "pw_planner_create": (i32, [i32, i32, P(i32), P(i32), P(ctypes.c_uint64), P(ctypes.c_double),
+                                    P(pw_planner_config), P(vp)]),
+        "pw_planner_destroy": (None, [vp]),
+        "pw_planner_add_request": (i32, [vp, P(ctypes.c_double), P(ctypes.c_double), ctypes.c_double]),
+        "pw_planner_clear_requests": (i32, [vp]),
+        "pw_planner_step": (i32, [vp, P(i32), i32, i32, ctypes.c_uint64, P(pw_plan_summary)]),
+        "pw_planner_plan": (i32, [vp, i32, i32, i32, P(i32), P(i32), P(i32), P(ctypes.c_uint64), P(i32)]),
+        "pw_planner_create_for_layer": (i32, [vp, P(ctypes.c_double), P(pw_planner_config), P(vp)]),
+        "pw_planner_step_layer": (i32, [vp, vp, i32, i32, ctypes.c_uint64, P(pw_plan_summary)]),
+        "pw_planner_apply": (i32, [vp, vp, vp, P(sz)]),
         "pw_last_error": (ctypes.c_char_p, []),
         "pw_status_str": (ctypes.c_char_p, [i32]),
     }
@@ -246,3 +289,108 @@ def pw_profile_read(layer: int, reset: bool = True):
 
 def pw_last_error() -> str:
     return _lib.pw_last_error().decode()
+
+
+# --------------------------------------------------------------------------
+# routing statistics and the runtime planner (Sec. 3.2, Alg. 1)
+# --------------------------------------------------------------------------
+
+def pw_routing_stats(rows_ptr: int, act: int, n_rows: int, dim: int, rows_by_position: int, w_ptr: int,
+                     offsets_ptr: int, sorted_slot_ptr: int, T: int, E: int, K: int, norm2_ptr: int,
+                     stats_ptr: int, accumulate: int, stream: int):
+    _check(_lib.pw_routing_stats(rows_ptr, act, n_rows, dim, rows_by_position, w_ptr, offsets_ptr,
+                                 sorted_slot_ptr, T, E, K, norm2_ptr, stats_ptr, accumulate, stream))
+
+
+def planner_config(bucket_frac, mult, floors, alpha=1.0, rho_min=-1.0, rho_max=1.0, eps=1e-9,
+                   head_w=None, head_a=None, head_c=None) -> pw_planner_config:
+    """Fills a pw_planner_config; floors is [stage][bucket]; head_* indexed [u][step]."""
+    c = pw_planner_config()
+    c.n_buckets = len(bucket_frac)
+    c.n_stages = len(floors)
+    for j, (f, m) in enumerate(zip(bucket_frac, mult)):
+        c.bucket_frac[j] = float(f)
+        c.mult[j] = float(m)
+    for s_, row in enumerate(floors):
+        for j, b in enumerate(row):
+            c.floor_bits[s_][j] = int(b)
+    c.alpha, c.rho_min, c.rho_max, c.eps = float(alpha), float(rho_min), float(rho_max), float(eps)
+    for u in range(2):
+        for t in range(2):
+            for k in range(3):
+                c.head_w[u][t][k] = 0.0 if head_w is None else float(head_w[u][t][k])
+            c.head_a[u][t] = 0.0 if head_a is None else float(head_a[u][t])
+            c.head_c[u][t] = 1.0 if head_c is None else float(head_c[u][t])
+    return c
+
+
+def _dp(a):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+
+
+def pw_planner_create(n_experts: int, unit_expert, unit_type, unit_bytes, unit_sens, cfg) -> int:
+    ue = np.ascontiguousarray(unit_expert, np.int32)
+    ut = np.ascontiguousarray(unit_type, np.int32)
+    ub = np.ascontiguousarray(unit_bytes, np.uint64).reshape(-1)
+    us = np.ascontiguousarray(unit_sens, np.float64).reshape(-1)
+    h = ctypes.c_void_p()
+    _check(_lib.pw_planner_create(n_experts, len(ue), ue.ctypes.data_as(ctypes.POINTER(ctypes.c_int)),
+                                  ut.ctypes.data_as(ctypes.POINTER(ctypes.c_int)),
+                                  ub.ctypes.data_as(ctypes.POINTER(ctypes.c_uint64)), _dp(us),
+                                  ctypes.byref(cfg), ctypes.byref(h)))
+    return h.value
+
+
+def pw_planner_destroy(p: int):
+    _lib.pw_planner_destroy(p)
+
+
+def pw_planner_add_request(p: int, stats_gate_up, stats_down, kv_weight: float):
+    sg = np.ascontiguousarray(stats_gate_up, np.float64)
+    sd = None if stats_down is None else np.ascontiguousarray(stats_down, np.float64)
+    _check(_lib.pw_planner_add_request(p, _dp(sg), None if sd is None else _dp(sd), float(kv_weight)))
+
+
+def pw_planner_clear_requests(p: int):
+    _check(_lib.pw_planner_clear_requests(p))
+
+
+def pw_planner_step(p: int, unit_bits, free_blocks: int, free_threshold: int, kv_block_bytes: int) -> pw_plan_summary:
+    q = np.ascontiguousarray(unit_bits, np.int32)
+    out = pw_plan_summary()
+    _check(_lib.pw_planner_step(p, q.ctypes.data_as(ctypes.POINTER(ctypes.c_int)), free_blocks, free_threshold,
+                                kv_block_bytes, ctypes.byref(out)))
+    return out
+
+
+def pw_planner_plan(p: int, stage: int = -1, steps: bool = False):
+    """[(unit, from_bits, to_bits, bytes)] of a stage's plan (-1: the selected one)."""
+    n = ctypes.c_int()
+    _check(_lib.pw_planner_plan(p, stage, int(steps), 0, None, None, None, None, ctypes.byref(n)))
+    m = n.value
+    u, f, t = (np.zeros(max(m, 1), np.int32) for _ in range(3))
+    b = np.zeros(max(m, 1), np.uint64)
+    ip = lambda a: a.ctypes.data_as(ctypes.POINTER(ctypes.c_int))
+    _check(_lib.pw_planner_plan(p, stage, int(steps), m, ip(u), ip(f), ip(t),
+                                b.ctypes.data_as(ctypes.POINTER(ctypes.c_uint64)), ctypes.byref(n)))
+    return [(int(u[k]), int(f[k]), int(t[k]), int(b[k])) for k in range(m)]
+
+
+def pw_planner_create_for_layer(layer: int, sens, cfg) -> int:
+    s_ = np.ascontiguousarray(sens, np.float64).reshape(-1)
+    h = ctypes.c_void_p()
+    _check(_lib.pw_planner_create_for_layer(layer, _dp(s_), ctypes.byref(cfg), ctypes.byref(h)))
+    return h.value
+
+
+def pw_planner_step_layer(p: int, layer: int, free_blocks: int, free_threshold: int,
+                          kv_block_bytes: int) -> pw_plan_summary:
+    out = pw_plan_summary()
+    _check(_lib.pw_planner_step_layer(p, layer, free_blocks, free_threshold, kv_block_bytes, ctypes.byref(out)))
+    return out
+
+
+def pw_planner_apply(p: int, layer: int, stream: int) -> int:
+    d = ctypes.c_size_t()
+    _check(_lib.pw_planner_apply(p, layer, stream, ctypes.byref(d)))
+    return d.value
