@@ -444,6 +444,95 @@ def leg_offload(steps_before=6, steps_after=6):
             "decode_slowdown": round(dur / before - 1.0, 4) if dur is not None else None}
 
 
+def leg_planner():
+    """Alg. 1 on the Mixtral-shaped decode layer: per-expert routing statistics
+    on the GPU each step, one planner step over the whole table under a
+    128 MiB KV-pressure target (synthetic sensitivities and heads: the
+    calibration tables need trained weights), and the plan requantized on a
+    side stream and committed."""
+    import numpy as np
+    import torch
+    from paper_2607_16184_amd import pw, synth
+    from paper_2607_16184_amd.layer import PagedLayer
+    cfg = synth.CONFIGS["mixtral_decode"]
+    w16 = [synth.expert_weights(cfg, p) for p in range(3)]
+    bits = synth.bitmap(cfg)
+    L = PagedLayer(cfg, PagedLayer.pool_bytes_for(cfg, bits, slack=0.1))
+    L.load_pages(w16, bits, synth.pool_order(cfg))
+    del w16
+    rng = np.random.default_rng(2000 + 9)
+    sens = np.sort(rng.gamma(1.0, 1.0, (L.n_entries, 3)), 1)
+    pcfg = pw.planner_config(bucket_frac=[0.25, 0.25, 0.5], mult=[8.0, 2.0, 1.0],
+                             floors=[[16, 8, 8], [8, 8, 4], [8, 4, 4], [4, 4, 4]], alpha=0.5,
+                             rho_min=-0.5, rho_max=0.5, eps=1e-9, head_w=rng.normal(0, 0.01, (2, 2, 3)),
+                             head_a=rng.normal(0, 0.2, (2, 2)), head_c=rng.uniform(0.3, 1.0, (2, 2)))
+    planner = L.planner(sens, pcfg)
+    lg, x16 = synth.step_inputs(cfg, 0)
+    logits = torch.from_numpy(lg).cuda()
+    x = torch.from_numpy(x16.view(np.int16)).cuda()
+    rbuf = PagedLayer.routing_buffers(cfg.T, cfg.E, cfg.K)
+    y = torch.empty((cfg.T, cfg.H), dtype=torch.int16, device="cuda")
+    routing = L.route(logits, cfg.K, out=rbuf)
+    stats = torch.zeros((cfg.E, 5), dtype=torch.float64, device="cuda")
+    stats_dn = torch.zeros((cfg.E, 5), dtype=torch.float64, device="cuda")
+    for _ in range(3):
+        L.forward(x, routing, y=y)
+        L.routing_stats(x, routing, out=stats)
+        L.routing_stats(L.hidden_rows(cfg.T, cfg.K), routing, rows_by_position=True, out=stats_dn)
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    n = 20
+    ev[0].record()
+    for _ in range(n):
+        L.routing_stats(x, routing, out=stats)
+    ev[1].record()
+    for _ in range(n):
+        L.routing_stats(L.hidden_rows(cfg.T, cfg.K), routing, rows_by_position=True, out=stats_dn)
+    ev[2].record()
+    for _ in range(n):
+        L.forward(x, routing, y=y)
+    ev[3].record()
+    torch.cuda.synchronize()
+    st_x_ms = ev[0].elapsed_time(ev[1]) / n
+    st_h_ms = ev[1].elapsed_time(ev[2]) / n
+    before = ev[2].elapsed_time(ev[3]) / n
+    planner.add_request(stats, stats_dn, 1.0)
+    kvb, thr = 2 << 20, 63
+    t0 = time.perf_counter()
+    reps = 5
+    for _ in range(reps):
+        r = planner.step(L, free_blocks=0, free_threshold=thr, kv_block_bytes=kvb)
+    host_ms = (time.perf_counter() - t0) * 1e3 / reps
+    plan = planner.plan()
+    free0 = L.stats()[1]
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    pw.pw_profile_read(L.handle, reset=True)
+    pw.pw_profile_enable(L.handle, True)
+    delta = planner.apply(L, stream=side)
+    L.commit()
+    torch.cuda.synchronize()
+    pw.pw_profile_enable(L.handle, False)
+    rq_ms = pw.pw_profile_read(L.handle, reset=True)[0][pw.PW_PH_REQUANT]
+    L.reclaim()
+    freed = L.stats()[1] - free0
+    ev[0].record()
+    for _ in range(n):
+        L.forward(x, routing, y=y)
+    ev[1].record()
+    torch.cuda.synchronize()
+    after = ev[0].elapsed_time(ev[1]) / n
+    planner.close()
+    L.close()
+    return {"workload": "mixtral_decode layer (2688 table entries, 2048 pages); 64-token step statistics; "
+                        "one planner step, 4 bitwidth-floor stages, KV target 64 blocks of 2 MiB",
+            "stats_gate_up_input_ms": round(st_x_ms, 4), "stats_down_input_ms": round(st_h_ms, 4),
+            "plan_step_host_ms": round(host_ms, 3), "target_bytes": int(r.target), "plan_bytes": int(r.bytes),
+            "plan_stage": int(r.stage), "plan_units": len(plan), "bytes_freed": int(freed),
+            "requant_ms": round(rq_ms, 4), "eager_step_ms_before": round(before, 4),
+            "eager_step_ms_after": round(after, 4)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -451,7 +540,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="mixtral_decode")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--extras", default="prefill,finegrained,downshift,offload",
+    ap.add_argument("--extras", default="prefill,finegrained,downshift,offload,planner",
                     help="comma list of extra legs on the same JSON line ('' for none)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after the timed steps, run one device copy of this many MiB "
@@ -547,6 +636,8 @@ def main():
             extras["downshift"] = leg_downshift()
         elif leg == "offload":
             extras["offload"] = leg_offload()
+        elif leg == "planner":
+            extras["planner"] = leg_planner()
         log("leg %s done in %.1f s" % (leg, time.time() - t0))
     if extras:
         out["extras"] = extras
