@@ -1,0 +1,189 @@
+"""Oracle of the nested bit-plane page format (test infrastructure only).
+
+Sec. 2-3 of the paper build on any-precision weights: a linear-block holds
+non-uniform codes whose top b bits form its b-bit code, stored as bit-planes,
+with one lookup table (LUT) of reconstruction values per row and precision;
+lowering a block's bitwidth drops its lowest bit-planes (no requantization),
+and only the LUT of the committed precision is read. The paper leaves the
+quantizer to the cited any-precision method; the deterministic reading used
+here (also in the design notes):
+
+* codes have 8 bits; supported precisions are 8 and 4 (planes 0-3 give the
+  4-bit code, planes 0-7 the 8-bit code; plane 0 is the most significant);
+* 4-bit seed, per row: 16 centroids initialised at lo + (hi - lo)(2j+1)/32
+  (lo, hi the row's minimum and maximum), then 8 Lloyd iterations (assign
+  each value to the nearest centroid, ties to the lower index; replace each
+  centroid with the mean of its members, summed in order of k; an empty
+  cluster keeps its centroid), then a final assignment;
+* upscaling one bit at a time (levels 5..8): every parent cluster p with
+  members (its values under the current assignment) gets two children
+  initialised at (lo_p + m_p)/2 and (m_p + hi_p)/2 (m_p the members' mean),
+  4 Lloyd iterations among the members, then a final assignment; code
+  2p + child. A parent without members passes its centroid to both children;
+* LUT_b[r][c] = the level-b centroid rounded to the activation dtype (nearest
+  even); a weight at precision b reconstructs as LUT_b[r][code >> (8 - b)].
+
+All arithmetic is float64 with sums in order of k (numpy's cumulative sum is
+sequential), so any implementation that keeps that order reproduces it bit
+for bit. Only the test suite, the smoke check and the benchmark's CPU leg may
+import this module; it shares no code with the library.
+
+Page layout of an R x K block (R a multiple of 16, K of 128), byte offsets:
+  planes 0-3 at 0 (plane j at j RK/8), LUT_4 at RK/2 (R x 16 entries,
+  row-major), planes 4-7 after it, LUT_8 after them (R x 256 entries).
+Inside a plane, the 16-row x 128-value tile t = rt (K/128) + kb occupies
+256 bytes at 256 t: lane l (0..63) owns the 32-bit word at 4 l, whose bit
+8 i + q holds code bit (7 - j) of row 16 rt + l mod 16, column
+128 kb + 32 i + 8 (l div 16) + q (i < 4, q < 8) -- the order in which a
+64-lane wave feeds 16 x 32 matrix-core fragments.
+"""
+from __future__ import annotations
+
+from typing import Tuple
+
+import numpy as np
+
+SEED_BITS = 4
+MAX_BITS = 8
+SEED_ITERS = 8
+SPLIT_ITERS = 4
+
+
+def _seq_sum(x: np.ndarray) -> np.ndarray:
+    """Sums along the last axis in order (sequential float64 accumulation)."""
+    if x.shape[-1] == 0:
+        return np.zeros(x.shape[:-1])
+    return np.cumsum(x, axis=-1)[..., -1]
+
+
+def _assign(v: np.ndarray, c: np.ndarray) -> np.ndarray:
+    """Nearest centroid per value (ties to the lower index); v [R,K], c [R,J]."""
+    d = np.abs(v[:, :, None] - c[:, None, :])
+    return np.argmin(d, axis=2)
+
+
+def _means(v: np.ndarray, a: np.ndarray, J: int, c_old: np.ndarray) -> np.ndarray:
+    c = c_old.copy()
+    for j in range(J):
+        m = a == j
+        n = m.sum(axis=1)
+        s = _seq_sum(np.where(m, v, 0.0))
+        nz = n > 0
+        c[nz, j] = s[nz] / n[nz]
+    return c
+
+
+def quantize_rows(v: np.ndarray) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """(8-bit codes [R,K] uint8, level-4 centroids [R,16], level-8 centroids
+    [R,256]) of rows v (float64, the 16-bit weights' values)."""
+    v = np.asarray(v, np.float64)
+    R, K = v.shape
+    lo, hi = v.min(axis=1), v.max(axis=1)
+    c = lo[:, None] + (hi - lo)[:, None] * ((2.0 * np.arange(16) + 1.0) / 32.0)[None, :]
+    for _ in range(SEED_ITERS):
+        a = _assign(v, c)
+        c = _means(v, a, 16, c)
+    a = _assign(v, c)
+    c4 = c.copy()
+    for level in range(SEED_BITS + 1, MAX_BITS + 1):
+        P = 1 << (level - 1)
+        child = np.zeros((R, 2 * P))
+        a_next = np.zeros_like(a)
+        for p in range(P):
+            m = a == p
+            n = m.sum(axis=1)
+            has = n > 0
+            mean = np.where(has, _seq_sum(np.where(m, v, 0.0)) / np.maximum(n, 1), c[:, p])
+            lo_p = np.where(has, np.where(m, v, np.inf).min(axis=1), c[:, p])
+            hi_p = np.where(has, np.where(m, v, -np.inf).max(axis=1), c[:, p])
+            ch = np.stack([np.where(has, (lo_p + mean) / 2.0, c[:, p]),
+                           np.where(has, (mean + hi_p) / 2.0, c[:, p])], axis=1)
+            for _ in range(SPLIT_ITERS):
+                pick = (np.abs(v - ch[:, 1:2]) < np.abs(v - ch[:, 0:1])).astype(np.int64)
+                for k in range(2):
+                    mk = m & (pick == k)
+                    nk = mk.sum(axis=1)
+                    sk = _seq_sum(np.where(mk, v, 0.0))
+                    ok = nk > 0
+                    ch[ok, k] = sk[ok] / nk[ok]
+            child[:, 2 * p] = ch[:, 0]
+            child[:, 2 * p + 1] = ch[:, 1]
+            pick = (np.abs(v - ch[:, 1:2]) < np.abs(v - ch[:, 0:1])).astype(np.int64)
+            a_next = np.where(m, 2 * p + pick, a_next)
+        a = a_next
+        c = child
+    return a.astype(np.uint8), c4, c
+
+
+def lut16(c: np.ndarray, fmt: int) -> np.ndarray:
+    """Centroids rounded to the 16-bit activation dtype (nearest even), as bit patterns."""
+    from oracle import round_nearest16
+    flat = np.asarray(c, np.float64).reshape(-1)
+    return np.array([round_nearest16(float(x), fmt) for x in flat], np.uint16).reshape(np.shape(c))
+
+
+def page_bytes(R: int, K: int, bits: int) -> int:
+    """Eq. 3's M^b of a nested bit-plane block: b planes and the LUTs up to b."""
+    rk8 = R * K // 8
+    if bits == 4:
+        return 4 * rk8 + 32 * R
+    if bits == 8:
+        return 8 * rk8 + 32 * R + 512 * R
+    raise ValueError("bits must be 8 or 4")
+
+
+def lut4_offset(R: int, K: int) -> int:
+    return 4 * (R * K // 8)
+
+
+def encode_page(codes: np.ndarray, lut4: np.ndarray, lut8: np.ndarray) -> np.ndarray:
+    """The 8-bit page bytes (layout in the module docstring)."""
+    R, K = codes.shape
+    rk8 = R * K // 8
+    out = np.zeros(page_bytes(R, K, 8), np.uint8)
+    nkb = K // 128
+    for j in range(8):
+        base = j * rk8 if j < 4 else 4 * rk8 + 32 * R + (j - 4) * rk8
+        bit = ((codes >> (7 - j)) & 1).astype(np.uint32)
+        words = np.zeros((R // 16, nkb, 64), np.uint32)
+        for l in range(64):
+            r = np.arange(R // 16) * 16 + (l % 16)
+            for i in range(4):
+                for q in range(8):
+                    k = np.arange(nkb) * 128 + 32 * i + 8 * (l // 16) + q
+                    words[:, :, l] |= bit[r][:, k] << np.uint32(8 * i + q)
+        out[base:base + rk8] = words.reshape(-1).view(np.uint8)
+    off4 = 4 * rk8
+    out[off4:off4 + 32 * R] = np.ascontiguousarray(lut4, np.uint16).reshape(-1).view(np.uint8)
+    off8 = 8 * rk8 + 32 * R
+    out[off8:off8 + 512 * R] = np.ascontiguousarray(lut8, np.uint16).reshape(-1).view(np.uint8)
+    return out
+
+
+def decode_page(buf: np.ndarray, R: int, K: int, bits: int) -> Tuple[np.ndarray, np.ndarray]:
+    """(codes at the given precision [R,K], that precision's LUT [R, 2^bits]) from page bytes."""
+    rk8 = R * K // 8
+    nkb = K // 128
+    codes = np.zeros((R, K), np.uint32)
+    for j in range(bits):
+        base = j * rk8 if j < 4 else 4 * rk8 + 32 * R + (j - 4) * rk8
+        words = np.frombuffer(buf[base:base + rk8].tobytes(), np.uint32).reshape(R // 16, nkb, 64)
+        for l in range(64):
+            r = np.arange(R // 16) * 16 + (l % 16)
+            for i in range(4):
+                for q in range(8):
+                    k = np.arange(nkb) * 128 + 32 * i + 8 * (l // 16) + q
+                    b = (words[:, :, l] >> np.uint32(8 * i + q)) & 1
+                    codes[np.ix_(r, k)] |= b << np.uint32(bits - 1 - j)
+    if bits == 4:
+        lut = np.frombuffer(buf[4 * rk8:4 * rk8 + 32 * R].tobytes(), np.uint16).reshape(R, 16)
+    else:
+        off8 = 8 * rk8 + 32 * R
+        lut = np.frombuffer(buf[off8:off8 + 512 * R].tobytes(), np.uint16).reshape(R, 256)
+    return codes.astype(np.uint8), lut
+
+
+def dequant(codes8: np.ndarray, lut: np.ndarray, bits: int) -> np.ndarray:
+    """16-bit reconstruction (bit patterns) at precision bits: LUT_b[r][code >> (8 - b)]."""
+    idx = (codes8.astype(np.int64) >> (8 - bits))
+    return np.take_along_axis(np.asarray(lut), idx, axis=1).astype(np.uint16)
