@@ -81,13 +81,19 @@ typedef enum { PW_GATE = 0, PW_UP = 1, PW_DOWN = 2 } pw_proj;
  * entry always describes the GPU page the kernels read.                   */
 enum { PW_PAGE_ABSENT = 0, PW_PAGE_RESIDENT = 1, PW_PAGE_REQUANT_PENDING = 2, PW_PAGE_RELOAD_PENDING = 3 };
 
+/* Page formats (pw_page_entry.rsv): group-wise RTN codes with scale/zero
+ * (16-bit pages are plain values), or nested bit-planes with per-row LUTs
+ * (pw_layer_load_pages_apl).                                              */
+enum { PW_FMT_RTN = 0, PW_FMT_APL = 1 };
+
 /* One page-table entry (device array and host mirror). 24 bytes. */
 typedef struct {
-    uint64_t data_off;  /* byte offset of the page (values or code block) in the pool */
-    uint64_t sz_off;    /* byte offset of the scale/zero block; 0 for 16-bit pages    */
+    uint64_t data_off;  /* byte offset of the page (values, code block or bit-planes) */
+    uint64_t sz_off;    /* byte offset of the scale/zero block (RTN; 0 for 16-bit
+                           pages) or of the 4-bit LUT (nested bit-planes)             */
     uint8_t bits;       /* committed bitwidth q_i: 16, 8, 4; 0 = absent               */
     uint8_t state;      /* PW_PAGE_*                                                  */
-    uint16_t rsv;
+    uint16_t rsv;       /* page format, PW_FMT_*                                      */
     uint32_t gen;       /* bumped at every commit                                     */
 } pw_page_entry;
 
@@ -246,6 +252,41 @@ pw_status pw_pool_stats(const pw_layer* layer, size_t* used, size_t* free_bytes,
 enum { PW_PH_GATEUP = 0, PW_PH_DOWN = 1, PW_PH_COMBINE = 2, PW_PH_REQUANT = 3, PW_NPHASE = 4 };
 pw_status pw_profile_enable(pw_layer* layer, int on);
 pw_status pw_profile_read(pw_layer* layer, double* total_ms, int64_t* count, int reset);
+
+/* ------------------------------------------------------------------------
+ * Nested bit-plane pages (any-precision weights, Sec. 2.2 and 3.1: a block's
+ * b-bit code is the top b bits of its 8-bit code; bit-planes and one LUT per
+ * row and precision; lowering drops bit-planes).
+ * ---------------------------------------------------------------------- */
+
+/* Quantize n blocks into nested bit-plane pages at 8 or 4 bits. rows16[i]
+ * (a host array of device pointers) holds block i's R x K 16-bit weights
+ * (act dtype, row-major). Per row, in float64 with sums in order of k: a
+ * 4-bit seed of 16 centroids at lo + (hi - lo)(2j+1)/32 refined by 8 Lloyd
+ * iterations (nearest centroid, ties to the lower index; empty clusters keep
+ * their centroid), then four one-bit splits to 8 bits (each cluster's two
+ * children start at (lo + mean)/2 and (mean + hi)/2 of its members and take
+ * 4 Lloyd iterations among them); LUT_b = the level-b centroids rounded to
+ * act (nearest even). Page layout of an R x K block at 8 bits (4 bits: the
+ * first two parts): planes 0-3 (plane 0 = most significant code bit,
+ * RK/8 bytes each) | LUT_4 (R x 16 act values) | planes 4-7 | LUT_8
+ * (R x 256). Inside a plane, 16-row x 128-column tile t = rt (K/128) + kb
+ * takes 256 bytes at 256 t: lane l's 32-bit word at 4 l holds, at bit
+ * 8 i + q, the plane's bit of row 16 rt + l mod 16, column
+ * 128 kb + 32 i + 8 (l div 16) + q. The entry's sz_off points at LUT_4;
+ * rsv = PW_FMT_APL. Eq. 3: M^8 = RK + 32 R + 512 R, M^4 = RK/2 + 32 R.
+ * ws: device workspace of pw_apl_workspace_bytes(n) bytes. Work is
+ * enqueued on `stream`; the table entries are written there too.
+ *   bits not 8 or 4, R not a multiple of 16: PW_EINVAL.  present: PW_EBUSY.
+ *   pool full: PW_ENOMEM (no page of the batch is placed).
+ * A layer holding such pages runs the streaming GEMM kernel for every batch
+ * size; pw_requant_block takes them from 8 to 4 bits without a kernel (the
+ * tail of the slot, planes 4-7 and LUT_8, is freed by pw_reclaim after the
+ * commit); host copies of them are not supported (PW_EUNSUPPORTED).      */
+pw_status pw_apl_workspace_bytes(const pw_layer* layer, int n, size_t* bytes);
+pw_status pw_layer_load_pages_apl(pw_layer* layer, int n, const int* e, const int* proj, const int* rb,
+                                  const int* bits, const void* const* rows16, void* ws, size_t ws_bytes,
+                                  void* stream);
 
 /* ------------------------------------------------------------------------
  * Routing statistics and the runtime planner (Sec. 3.2, Alg. 1).

@@ -51,9 +51,8 @@ SPLIT_ITERS = 4
 
 def _seq_sum(x: np.ndarray) -> np.ndarray:
     """Sums along the last axis in order (sequential float64 accumulation)."""
-    if x.shape[-1] == 0:
-        return np.zeros(x.shape[:-1])
-    return np.cumsum(x, axis=-1)[..., -1]
+    z = np.zeros(x.shape[:-1] + (1,))
+    return np.cumsum(np.concatenate([z, x], axis=-1), axis=-1)[..., -1]   # from +0.0, in order
 
 
 def _assign(v: np.ndarray, c: np.ndarray) -> np.ndarray:

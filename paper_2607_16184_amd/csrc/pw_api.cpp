@@ -102,21 +102,23 @@ struct WsLayout {
 // kernel. The last two need 32/64-row staging inside one page, 128-row down
 // blocks and 32-bit activation row offsets (and the tiled kernel 256-row down
 // blocks).
-GemmPath pick_path(const pw_layer_desc& d, size_t S) {
+GemmPath pick_path(const pw_layer_desc& d, size_t S, bool apl) {
   const size_t expect = (S + d.E - 1) / d.E;
   const bool fits = S * d.F * 2 < (size_t(1) << 32) && S * d.H * 2 < (size_t(1) << 32);
   const bool tiles = fits && d.G >= 64 && d.R % 64 == 0 && d.F % 128 == 0;
+  // nested bit-plane pages are read by the streaming kernel only
+  if (apl) return GemmPath::kStream;
   if (expect >= 128 && tiles && d.H % 256 == 0) return GemmPath::kTiled;
   if (expect > 48 && tiles && d.H % 128 == 0) return GemmPath::kStream;
   return GemmPath::kDecode;
 }
 
-WsLayout ws_layout(const pw_layer_desc& d, int T, int K) {
+WsLayout ws_layout(const pw_layer_desc& d, int T, int K, bool apl) {
   WsLayout w{};
   const size_t S = static_cast<size_t>(T) * K;
   const int nkbF = d.F / 128;
   const int expect = static_cast<int>((S + d.E - 1) / d.E);
-  w.path = pick_path(d, S);
+  w.path = pick_path(d, S, apl);
   // The decode kernels split the down projection's K = F when too few
   // (expert, row-block) units exist to fill the chip; deterministic in
   // (desc, T, K).
@@ -288,6 +290,88 @@ pw_status pw_layer_load_page(pw_layer* L, int e, int proj, int rb, int bits, con
   return PW_OK;
 }
 
+static size_t apl_job_bytes(const pw_layer* L) {
+  const pw_layer_desc& d = L->st.desc;
+  const size_t R = static_cast<size_t>(d.R), Kmax = static_cast<size_t>(std::max(d.H, d.F));
+  return (R * Kmax + R * pw::kAplScratchRow + 255) / 256 * 256;
+}
+
+pw_status pw_apl_workspace_bytes(const pw_layer* L, int n, size_t* bytes) {
+  if (!L || !bytes || n < 0) return fail(PW_EINVAL, "bad argument");
+  *bytes = static_cast<size_t>(std::min(n, pw::kMaxAplJobs)) * apl_job_bytes(L);
+  return PW_OK;
+}
+
+pw_status pw_layer_load_pages_apl(pw_layer* L, int n, const int* e, const int* proj, const int* rb,
+                                  const int* bits, const void* const* rows16, void* ws, size_t ws_bytes,
+                                  void* stream) {
+  if (!L || n < 0 || (n > 0 && (!e || !proj || !rb || !bits || !rows16 || !ws))) return fail(PW_EINVAL, "bad argument");
+  if (n == 0) return PW_OK;
+  const size_t jb = apl_job_bytes(L);
+  if (ws_bytes < static_cast<size_t>(std::min(n, pw::kMaxAplJobs)) * jb)
+    return fail(PW_ENOMEM, "workspace smaller than pw_apl_workspace_bytes");
+  if (!mult_of_256(ws)) return fail(PW_EINVAL, "workspace must be 256-byte aligned");
+  std::string err;
+  std::set<size_t> seen;
+  std::vector<pw_page_entry> ents(n);
+  auto rollback = [&](int upto) {
+    for (int i = 0; i < upto; ++i) L->st.abort_slot(ents[i], proj[i]);
+  };
+  for (int i = 0; i < n; ++i) {
+    if (!rows16[i] || (reinterpret_cast<uintptr_t>(rows16[i]) & 1u)) {
+      rollback(i);
+      return fail(PW_EINVAL, "null or misaligned source rows");
+    }
+    pw_status s = L->st.plan_load_apl(e[i], proj[i], rb[i], bits[i], &ents[i], &err);
+    if (s == PW_OK && !seen.insert(L->st.index(e[i], proj[i], rb[i])).second) {
+      L->st.abort_slot(ents[i], proj[i]);
+      s = PW_EINVAL;
+      err = "a block appears twice in the batch";
+    }
+    if (s != PW_OK) {
+      rollback(i);
+      return fail(s, err);
+    }
+  }
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  uint8_t* wsb = static_cast<uint8_t*>(ws);
+  for (int base = 0; base < n; base += pw::kMaxAplJobs) {
+    pw::AplBatch b{};
+    b.n_jobs = std::min(pw::kMaxAplJobs, n - base);
+    b.R = L->st.desc.R;
+    b.act = L->st.desc.act;
+    uint32_t rows = 0;
+    for (int j = 0; j < b.n_jobs; ++j) {
+      const int i = base + j;
+      pw::AplJob& J = b.job[j];
+      J.src = static_cast<const uint16_t*>(rows16[i]);
+      J.page = L->pool + ents[i].data_off;
+      J.codes = wsb + static_cast<size_t>(j) * jb;
+      J.scratch = J.codes + static_cast<size_t>(b.R) * std::max(L->st.desc.H, L->st.desc.F);
+      J.row_base = rows;
+      J.K = L->st.kdim(proj[i]);
+      J.bits = bits[i];
+      rows += static_cast<uint32_t>(b.R);
+    }
+    b.total_rows = rows;
+    hipError_t he = pw::launch_apl_quant(b, st);
+    if (he == hipSuccess) he = pw::launch_apl_pack(b, st);
+    if (he != hipSuccess) {
+      rollback(n);
+      return hip_fail(he, "bit-plane quantization launch");
+    }
+  }
+  std::vector<std::pair<size_t, pw_page_entry>> w;
+  for (int i = 0; i < n; ++i) w.push_back({L->st.index(e[i], proj[i], rb[i]), ents[i]});
+  pw_status s = write_entries(L, w, st);
+  if (s != PW_OK) {
+    rollback(n);
+    return s;
+  }
+  for (int i = 0; i < n; ++i) L->st.finish_load(e[i], proj[i], rb[i], ents[i]);
+  return PW_OK;
+}
+
 pw_status pw_route_topk(const float* logits, int T, int E, int K, int renorm, int32_t* ids,
                         float* w, int32_t* offsets, int32_t* sorted_slot, int32_t* slot_pos,
                         void* stream) {
@@ -325,7 +409,7 @@ pw_status pw_routing_stats(const void* rows, pw_dtype act, int n_rows, int dim, 
 
 pw_status pw_workspace_bytes(const pw_layer* L, int T, int K, size_t* gemm_ws) {
   if (!L || !gemm_ws || T < 0 || K < 1) return fail(PW_EINVAL, "bad argument");
-  *gemm_ws = ws_layout(L->st.desc, T, K).total;
+  *gemm_ws = ws_layout(L->st.desc, T, K, L->st.n_apl > 0).total;
   return PW_OK;
 }
 
@@ -341,7 +425,14 @@ pw_status pw_moe_paged_gemm(const pw_layer* Lc, const void* x, int T, int K, con
     return fail(PW_EINVAL, "null argument");
   if (!L->st.all_present()) return fail(PW_ESTATE, "every page of the layer must be loaded");
   if (static_cast<int64_t>(T) * K >= (int64_t(1) << 31)) return fail(PW_EINVAL, "T*K too large");
-  const WsLayout wl = ws_layout(L->st.desc, T, K);
+  const WsLayout wl = ws_layout(L->st.desc, T, K, L->st.n_apl > 0);
+  if (L->st.n_apl > 0) {
+    const pw_layer_desc& dd = L->st.desc;
+    const size_t S = static_cast<size_t>(T) * K;
+    if (!(S * dd.F * 2 < (size_t(1) << 32) && S * dd.H * 2 < (size_t(1) << 32)) || dd.R % 64 || dd.G < 64 ||
+        dd.H % 128)
+      return fail(PW_EUNSUPPORTED, "nested bit-plane pages need the streaming kernel's shapes");
+  }
   if (ws_bytes < wl.total) return fail(PW_ENOMEM, "workspace smaller than pw_workspace_bytes");
   if (!mult_of_256(ws)) return fail(PW_EINVAL, "workspace must be 256-byte aligned");
   if ((reinterpret_cast<uintptr_t>(x) & 15u) || (reinterpret_cast<uintptr_t>(y) & 15u))
@@ -373,6 +464,7 @@ pw_status pw_moe_paged_gemm(const pw_layer* Lc, const void* x, int T, int K, con
   a.act = d.act;
   a.sdt = d.sdt;
   a.mtb = wl.mtb;
+  a.apl = L->st.n_apl > 0 ? 1 : 0;
   hipStream_t st = static_cast<hipStream_t>(stream);
   hipError_t e;
   {
@@ -453,6 +545,7 @@ pw_status pw_requant_blocks(pw_layer* L, int n, const int* e, const int* proj, c
   // one launch for the whole plan (jobs of every projection, each with its K)
   std::vector<pw::QJob> jobs;
   for (const Planned& p : plan) {
+    if (p.dst.rsv & pw::LayerState::kInPlace) continue;   // a bit-plane drop needs no kernel
     pw::QJob j{};
     j.src = L->pool + p.src.data_off;
     j.src_sz = p.src.bits == 16 ? nullptr : L->pool + p.src.sz_off;
@@ -761,7 +854,7 @@ pw_status pw_commit(pw_layer* L, void* main_stream, int* n_committed) {
     if (he != hipSuccess) return hip_fail(he, "hipStreamWaitEvent");
   }
   std::vector<std::pair<size_t, pw_page_entry>> w;
-  for (const auto& p : pend) w.push_back({p.idx, p.next});
+  for (const auto& p : pend) w.push_back({p.idx, pw::LayerState::published(p.next)});
   pw_status s = write_entries(L, w, st);
   if (s != PW_OK) return s;
   void* cev = L->evops.create();

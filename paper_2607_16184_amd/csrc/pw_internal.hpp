@@ -33,6 +33,28 @@ struct QJobBatch {
   uint32_t total_items;
 };
 
+// Nested bit-plane quantization of whole blocks (one thread per row).
+constexpr int kMaxAplJobs = 32;
+// per-row float64 scratch: centroids of levels 4..8 (16 + 32 + 64 + 128 + 256),
+// cluster counts (256 int32), sums (256), parent minima and maxima (128 each)
+constexpr size_t kAplScratchRow = 496 * 8 + 256 * 4 + 256 * 8 + 128 * 8 * 2;
+struct AplJob {
+  const uint16_t* src;     // R x K 16-bit weights, row-major
+  uint8_t* page;           // the page slot (planes and LUTs)
+  uint8_t* codes;          // R x K bytes of workspace: 8-bit codes
+  uint8_t* scratch;        // R x kAplScratchRow bytes of workspace
+  uint32_t row_base;       // first global row of this job
+  int K;
+  int bits;                // 8 or 4
+};
+struct AplBatch {
+  AplJob job[kMaxAplJobs];
+  int n_jobs;
+  int R;
+  int act;
+  uint32_t total_rows;
+};
+
 // Page-table writes performed by a kernel on the caller's stream.
 constexpr int kMaxEntryWrites = 64;
 struct EntryWrites {
@@ -58,6 +80,7 @@ struct GemmArgs {
   int out_fp32;
   int act, sdt;
   int mtb;                    // M tiles (of 16 slots) per pass: 1, 2 or 4
+  int apl;                    // the layer holds nested bit-plane pages
 };
 
 hipError_t launch_route_topk(const float* logits, int T, int E, int K, int renorm,
@@ -74,6 +97,8 @@ hipError_t launch_combine(const GemmArgs& a, hipStream_t st);
 hipError_t launch_tgemm(const GemmArgs& a, bool gateup, hipStream_t st);
 // small and medium slot counts: register-streamed tiles of 16/32/64 slots
 hipError_t launch_sgemm(const GemmArgs& a, bool gateup, hipStream_t st);
+hipError_t launch_apl_quant(const AplBatch& b, hipStream_t st);
+hipError_t launch_apl_pack(const AplBatch& b, hipStream_t st);
 // Per-expert routing statistics (row norms, then a fixed-order reduction).
 hipError_t launch_routing_stats(const uint16_t* rows, int act, int n_rows, int dim, int by_position,
                                 const float* topk_w, const int32_t* offsets, const int32_t* sorted_slot, int S,

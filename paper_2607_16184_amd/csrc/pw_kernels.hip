@@ -504,6 +504,201 @@ __global__ __launch_bounds__(256) void k_combine(const GemmArgs a) {
 namespace {
 
 // ---------------------------------------------------------------------------
+// Nested bit-plane pages: quantization of a block (one thread per row, every
+// sum in order of k in float64, so the result is reproducible bit for bit)
+// and the packing of its 8-bit codes into bit-planes in lane order.
+// ---------------------------------------------------------------------------
+
+// Nearest-even rounding of a double straight to the 16-bit format (one
+// rounding): r = rint(x / q) q with q the format's spacing at x is exact.
+__device__ __forceinline__ uint32_t rne16_d(double x, int fmt) {
+  if (x == 0.0) return __builtin_signbit(x) ? 0x8000u : 0u;
+  const int emin = fmt == PW_BF16 ? -126 : -14;
+  const int frac = fmt == PW_BF16 ? 7 : 10;
+  int e = 0;
+  (void)frexp(x, &e);
+  const int ex = e - 1 > emin ? e - 1 : emin;
+  const double q = ldexp(1.0, ex - frac);
+  const float r = static_cast<float>(rint(x / q) * q);
+  return fmt == PW_BF16 ? (__float_as_uint(r) >> 16) : f16_rne(r);
+}
+
+__device__ __forceinline__ int apl_nearest16(const double (&c)[16], double x) {
+  int jb = 0;
+  double best = fabs(x - c[0]);
+#pragma unroll
+  for (int j = 1; j < 16; ++j) {
+    const double d = fabs(x - c[j]);
+    if (d < best) {
+      best = d;
+      jb = j;
+    }
+  }
+  return jb;
+}
+
+template <int ACT>
+__global__ __launch_bounds__(64) void k_apl_quant(const AplBatch b) {
+#pragma clang fp contract(off)
+  const uint32_t g = blockIdx.x * 64u + threadIdx.x;
+  if (g >= b.total_rows) return;
+  int jb = 0;
+  while (jb + 1 < b.n_jobs && b.job[jb + 1].row_base <= g) ++jb;
+  const AplJob& J = b.job[jb];
+  const int r = static_cast<int>(g - J.row_base), K = J.K, R = b.R;
+  const uint16_t* v = J.src + static_cast<size_t>(r) * K;
+  uint8_t* code = J.codes + static_cast<size_t>(r) * K;
+  double* cent = reinterpret_cast<double*>(J.scratch + static_cast<size_t>(r) * kAplScratchRow);
+  int* an = reinterpret_cast<int*>(cent + 496);
+  double* as = reinterpret_cast<double*>(an + 256);
+  double* pmin = as + 256;
+  double* pmax = pmin + 128;
+  const size_t rk8 = static_cast<size_t>(R) * K / 8;
+  // 4-bit seed
+  double lo = val16(v[0], ACT), hi = lo;
+  for (int k = 1; k < K; ++k) {
+    const double x = val16(v[k], ACT);
+    lo = x < lo ? x : lo;
+    hi = x > hi ? x : hi;
+  }
+  double c[16];
+#pragma unroll
+  for (int j = 0; j < 16; ++j) c[j] = lo + (hi - lo) * ((2.0 * j + 1.0) / 32.0);
+  for (int it = 0; it < 8; ++it) {
+    double S[16];
+    int N[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      S[j] = 0.0;
+      N[j] = 0;
+    }
+    for (int k = 0; k < K; ++k) {
+      const double x = val16(v[k], ACT);
+      const int a = apl_nearest16(c, x);
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {   // S never holds -0.0, so adding +0.0 leaves it unchanged
+        S[j] += j == a ? x : 0.0;
+        N[j] += j == a ? 1 : 0;
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < 16; ++j)
+      if (N[j] > 0) c[j] = S[j] / N[j];
+  }
+  for (int k = 0; k < K; ++k) code[k] = static_cast<uint8_t>(apl_nearest16(c, val16(v[k], ACT)));
+  uint16_t* lut4 = reinterpret_cast<uint16_t*>(J.page + 4 * rk8) + static_cast<size_t>(r) * 16;
+#pragma unroll
+  for (int j = 0; j < 16; ++j) {
+    cent[j] = c[j];
+    lut4[j] = static_cast<uint16_t>(rne16_d(c[j], ACT));
+  }
+  if (J.bits != 8) {
+    for (int k = 0; k < K; ++k) code[k] = static_cast<uint8_t>(code[k] << 4);
+    return;
+  }
+  // one-bit splits to 8 bits
+  double* cp = cent;          // parents (P of them)
+  double* cc = cent + 16;     // children (2 P)
+  for (int P = 16; P <= 128; P *= 2) {
+    for (int p = 0; p < P; ++p) {
+      an[p] = 0;
+      as[p] = 0.0;
+      pmin[p] = 0.0;
+      pmax[p] = 0.0;
+    }
+    for (int k = 0; k < K; ++k) {
+      const double x = val16(v[k], ACT);
+      const int p = code[k];
+      if (an[p] == 0) {
+        pmin[p] = x;
+        pmax[p] = x;
+      } else {
+        pmin[p] = x < pmin[p] ? x : pmin[p];
+        pmax[p] = x > pmax[p] ? x : pmax[p];
+      }
+      an[p] += 1;
+      as[p] += x;
+    }
+    for (int p = 0; p < P; ++p) {
+      if (an[p] > 0) {
+        const double m = as[p] / an[p];
+        cc[2 * p] = (pmin[p] + m) / 2.0;
+        cc[2 * p + 1] = (m + pmax[p]) / 2.0;
+      } else {
+        cc[2 * p] = cp[p];
+        cc[2 * p + 1] = cp[p];
+      }
+    }
+    for (int it = 0; it < 4; ++it) {
+      for (int q = 0; q < 2 * P; ++q) {
+        an[q] = 0;
+        as[q] = 0.0;
+      }
+      for (int k = 0; k < K; ++k) {
+        const double x = val16(v[k], ACT);
+        const int p = code[k];
+        const int ch = fabs(x - cc[2 * p + 1]) < fabs(x - cc[2 * p]) ? 1 : 0;
+        an[2 * p + ch] += 1;
+        as[2 * p + ch] += x;
+      }
+      for (int q = 0; q < 2 * P; ++q)
+        if (an[q] > 0) cc[q] = as[q] / an[q];
+    }
+    for (int k = 0; k < K; ++k) {
+      const double x = val16(v[k], ACT);
+      const int p = code[k];
+      code[k] = static_cast<uint8_t>(2 * p + (fabs(x - cc[2 * p + 1]) < fabs(x - cc[2 * p]) ? 1 : 0));
+    }
+    cp = cc;
+    cc += 2 * P;
+  }
+  uint16_t* lut8 = reinterpret_cast<uint16_t*>(J.page + 8 * rk8 + 32 * static_cast<size_t>(R)) +
+                   static_cast<size_t>(r) * 256;
+  for (int j = 0; j < 256; ++j) lut8[j] = static_cast<uint16_t>(rne16_d(cp[j], ACT));
+}
+
+// One thread per (job, plane, tile, lane) word: bit 8 i + q of lane l's word
+// is plane j's bit of row 16 rt + l mod 16, column 128 kb + 32 i + 8 (l / 16) + q.
+__global__ __launch_bounds__(256) void k_apl_pack(const AplBatch b) {
+  const uint32_t g = blockIdx.x * 256u + threadIdx.x;
+  // job of this word: the batch's words are laid out job after job
+  uint32_t base = 0;
+  int jb = -1;
+  uint32_t words = 0;
+  for (int j = 0; j < b.n_jobs; ++j) {
+    words = static_cast<uint32_t>(b.job[j].bits) * (b.R / 16) * (b.job[j].K / 128) * 64;
+    if (g < base + words) {
+      jb = j;
+      break;
+    }
+    base += words;
+  }
+  if (jb < 0) return;
+  const AplJob& J = b.job[jb];
+  const uint32_t w = g - base;
+  const int nkb = J.K / 128;
+  const uint32_t per_plane = static_cast<uint32_t>(b.R / 16) * nkb * 64;
+  const int plane = static_cast<int>(w / per_plane);
+  const uint32_t rest = w % per_plane;
+  const int t = static_cast<int>(rest / 64), lane = static_cast<int>(rest % 64);
+  const int rt = t / nkb, kb = t % nkb;
+  const int row = 16 * rt + (lane & 15);
+  const uint8_t* cr = J.codes + static_cast<size_t>(row) * J.K + 128 * kb + 8 * (lane >> 4);
+  uint32_t word = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int q = 0; q < 8; ++q) word |= static_cast<uint32_t>((cr[32 * i + q] >> (7 - plane)) & 1u) << (8 * i + q);
+  const size_t rk8 = static_cast<size_t>(b.R) * J.K / 8;
+  const size_t pbase = plane < 4 ? plane * rk8 : 4 * rk8 + 32 * static_cast<size_t>(b.R) + (plane - 4) * rk8;
+  reinterpret_cast<uint32_t*>(J.page + pbase)[static_cast<size_t>(t) * 64 + lane] = word;
+}
+
+}  // namespace
+
+namespace {
+
+// ---------------------------------------------------------------------------
 // Routing statistics for the planner (Eq. 1's numerator and the routed-input
 // features of Sec. 3.2), in float64 with a fixed summation order.
 // ---------------------------------------------------------------------------
@@ -630,6 +825,24 @@ hipError_t launch_combine(const GemmArgs& a, hipStream_t st) {
   if (a.T <= 0) return hipSuccess;
   const dim3 grid(a.T, (a.H / 4 + 255) / 256), block(256);
   hipLaunchKernelGGL(k_combine, grid, block, 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_apl_quant(const AplBatch& b, hipStream_t st) {
+  const dim3 grid((b.total_rows + 63) / 64);
+  if (b.act == PW_BF16)
+    hipLaunchKernelGGL(k_apl_quant<PW_BF16>, grid, dim3(64), 0, st, b);
+  else
+    hipLaunchKernelGGL(k_apl_quant<PW_F16>, grid, dim3(64), 0, st, b);
+  return hipGetLastError();
+}
+
+hipError_t launch_apl_pack(const AplBatch& b, hipStream_t st) {
+  uint64_t words = 0;
+  for (int j = 0; j < b.n_jobs; ++j)
+    words += static_cast<uint64_t>(b.job[j].bits) * (b.R / 16) * (b.job[j].K / 128) * 64;
+  if (words == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_apl_pack, dim3(static_cast<unsigned>((words + 255) / 256)), dim3(256), 0, st, b);
   return hipGetLastError();
 }
 

@@ -89,6 +89,12 @@ uint64_t LayerState::page_bytes(int proj, int bits) const {
   return code_bytes(proj, bits) + sz;
 }
 
+uint64_t LayerState::apl_bytes(int proj, int bits) const {
+  const uint64_t rk8 = static_cast<uint64_t>(desc.R) * kdim(proj) / 8;
+  const uint64_t lut4 = 32ull * desc.R, lut8 = 512ull * desc.R;
+  return bits == 8 ? 8 * rk8 + lut4 + lut8 : 4 * rk8 + lut4;
+}
+
 bool LayerState::check_block(int e, int proj, int rb, std::string* err) const {
   if (e < 0 || e >= desc.E) { *err = "expert index out of range"; return false; }
   if (proj < 0 || proj > 2) { *err = "projection must be PW_GATE, PW_UP or PW_DOWN"; return false; }
@@ -112,13 +118,31 @@ pw_status LayerState::plan_load(int e, int proj, int rb, int bits, pw_page_entry
   return PW_OK;
 }
 
+pw_status LayerState::plan_load_apl(int e, int proj, int rb, int bits, pw_page_entry* ent, std::string* err) {
+  if (!check_block(e, proj, rb, err)) return PW_EINVAL;
+  if (bits != 8 && bits != 4) { *err = "nested bit-plane pages hold 8 or 4 bits"; return PW_EINVAL; }
+  if (desc.R % 16 || kdim(proj) % 128) { *err = "R must be a multiple of 16 and K of 128"; return PW_EINVAL; }
+  if (mirror[index(e, proj, rb)].bits != 0) { *err = "page already present"; return PW_EBUSY; }
+  uint64_t off = 0;
+  if (!alloc.alloc(apl_bytes(proj, bits), &off)) { *err = "pool exhausted"; return PW_ENOMEM; }
+  ent->data_off = off;
+  ent->sz_off = off + 4 * (static_cast<uint64_t>(desc.R) * kdim(proj) / 8);   // LUT_4
+  ent->bits = static_cast<uint8_t>(bits);
+  ent->state = PW_PAGE_RESIDENT;
+  ent->rsv = PW_FMT_APL;
+  ent->gen = 1;
+  return PW_OK;
+}
+
 void LayerState::finish_load(int e, int proj, int rb, const pw_page_entry& ent) {
   mirror[index(e, proj, rb)] = ent;
   ++n_present;
+  if ((ent.rsv & 0xFF) == PW_FMT_APL) ++n_apl;
 }
 
 void LayerState::abort_slot(const pw_page_entry& ent, int proj) {
-  alloc.release(ent.data_off, page_bytes(proj, ent.bits));
+  if (ent.rsv & kInPlace) return;   // a plane drop allocated nothing
+  alloc.release(ent.data_off, entry_bytes(proj, ent));
 }
 
 pw_status LayerState::plan_requant(int e, int proj, int rb, int new_bits, pw_page_entry* src,
@@ -133,6 +157,18 @@ pw_status LayerState::plan_requant(int e, int proj, int rb, int new_bits, pw_pag
   if (new_bits > cur.bits) {
     *err = "raising a bitwidth needs a reload from a host copy (pw_reload_block)";
     return PW_EUNSUPPORTED;
+  }
+  if ((cur.rsv & 0xFF) == PW_FMT_APL) {
+    // nested bit-planes: 8 -> 4 keeps planes 0-3 and LUT_4 where they are;
+    // the page tail (planes 4-7, LUT_8) is freed after the commit
+    if (cur.bits != 8 || new_bits != 4) { *err = "nested bit-plane pages go from 8 to 4 bits only"; return PW_EUNSUPPORTED; }
+    *src = cur;
+    *dst = cur;
+    dst->bits = 4;
+    dst->rsv = static_cast<uint16_t>(PW_FMT_APL | kInPlace);
+    dst->gen = cur.gen + 1;
+    *delta = apl_bytes(proj, 8) - apl_bytes(proj, 4);
+    return PW_OK;
   }
   uint64_t off = 0;
   if (!alloc.alloc(page_bytes(proj, new_bits), &off)) { *err = "pool exhausted"; return PW_ENOMEM; }
@@ -168,9 +204,14 @@ void LayerState::add_pending(int e, int proj, int rb, const pw_page_entry& dst, 
 void LayerState::committed(void* commit_ev) {
   for (const Pending& p : pending_) {
     pw_page_entry& cur = mirror[p.idx];
-    retired_.push_back(Retired{cur.data_off, page_bytes(p.proj, cur.bits), commit_ev});
+    if (p.next.rsv & kInPlace) {
+      const uint64_t keep = apl_bytes(p.proj, p.next.bits);
+      retired_.push_back(Retired{cur.data_off + keep, apl_bytes(p.proj, cur.bits) - keep, commit_ev});
+    } else {
+      retired_.push_back(Retired{cur.data_off, entry_bytes(p.proj, cur), commit_ev});
+    }
     ref_event(commit_ev);
-    cur = p.next;
+    cur = published(p.next);
     unref_event(p.ev);
   }
   pending_.clear();
@@ -211,6 +252,7 @@ pw_status LayerState::plan_offload(int e, int proj, int rb, pw_page_entry* src, 
   const pw_page_entry& cur = mirror[idx];
   if (cur.bits == 0) { *err = "page not present"; return PW_ESTATE; }
   if (cur.state != PW_PAGE_RESIDENT) { *err = "a requantization or reload of this block is pending"; return PW_EBUSY; }
+  if ((cur.rsv & 0xFF) == PW_FMT_APL) { *err = "host copies of nested bit-plane pages are not supported"; return PW_EUNSUPPORTED; }
   if (host[idx].bits == cur.bits) {
     *same = true;
     return PW_OK;

@@ -88,12 +88,26 @@ class LayerState {
   int nrb(int proj) const { return rows(proj) / desc.R; }
   uint64_t code_bytes(int proj, int bits) const;   // bytes of values / codes
   uint64_t page_bytes(int proj, int bits) const;   // Eq. 3's M^b
+  // Nested bit-plane pages: b planes of R K / 8 bytes and the LUTs up to b.
+  uint64_t apl_bytes(int proj, int bits) const;
+  uint64_t entry_bytes(int proj, const pw_page_entry& e) const {
+    return (e.rsv & 0xFF) == PW_FMT_APL ? apl_bytes(proj, e.bits) : page_bytes(proj, e.bits);
+  }
+  // A pending entry that reuses its block's slot (a bit-plane drop) carries
+  // this flag until it is published.
+  static constexpr uint16_t kInPlace = 0x100;
+  static pw_page_entry published(pw_page_entry e) {
+    e.rsv = static_cast<uint16_t>(e.rsv & ~kInPlace);
+    return e;
+  }
+  size_t n_apl = 0;                // present nested bit-plane pages
 
   bool check_block(int e, int proj, int rb, std::string* err) const;
   bool all_present() const { return n_present == n_pages; }
 
   // Loading an absent page: reserve a slot and describe the new entry.
   pw_status plan_load(int e, int proj, int rb, int bits, pw_page_entry* ent, std::string* err);
+  pw_status plan_load_apl(int e, int proj, int rb, int bits, pw_page_entry* ent, std::string* err);
   void finish_load(int e, int proj, int rb, const pw_page_entry& ent);
   void abort_slot(const pw_page_entry& ent, int proj);
 

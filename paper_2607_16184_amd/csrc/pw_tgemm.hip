@@ -40,16 +40,40 @@ template <> struct WStage<16> { u32x4 v[4]; };                 // fragment f at 
 template <> struct WStage<8> { u32x4 v[2]; uint32_t sz[2]; };  // tile t: both steps
 template <> struct WStage<4> { u32x2 v[2]; uint32_t sz[2]; };  // tile t: one word per step
 
+// Nested bit-plane pages (format codes 108 and 104: 8 and 4 planes). Per row
+// tile and 128-value block, lane l holds one 32-bit word per plane covering
+// its four k-steps; `lut` points at the wave's 32 LUT rows staged in LDS.
+constexpr int kApl8 = 108, kApl4 = 104;
+template <int B> constexpr int apl_planes() { return B == kApl8 ? 8 : 4; }
+template <> struct WStage<kApl8> { uint32_t p[2][8]; int hh; const uint16_t* lut; };
+template <> struct WStage<kApl4> { uint32_t p[2][4]; int hh; const uint16_t* lut; };
+
 // A wave's activation share: slot tiles 2 * wave + j / 2, k-step j mod 2.
 struct XStage {
   u32x4 v[4];
 };
 
 // Weights are re-read by the other slot tiles of the expert: plain (cached) loads.
+// For nested bit-plane pages tile0 is the page base plus the wave's row-tile
+// offset inside a plane, and szrow carries the wave's LUT rows in LDS.
 template <int B>
 __device__ __forceinline__ void w_fetch(WStage<B>& w, const uint8_t* tile0, const uint8_t* szrow, int kb, int hh,
                                         int g, int nkb, int R) {
   const int lane = lane_id();
+  if constexpr (B == kApl8 || B == kApl4) {
+    const size_t rk8 = static_cast<size_t>(R) * nkb * 16;
+#pragma unroll
+    for (int j = 0; j < apl_planes<B>(); ++j) {
+      const size_t pb = j < 4 ? j * rk8 : 4 * rk8 + 32 * static_cast<size_t>(R) + (j - 4) * rk8;
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+        w.p[t][j] = *reinterpret_cast<const uint32_t*>(tile0 + pb + (static_cast<size_t>(t) * nkb + kb) * 256 +
+                                                       4 * lane);
+    }
+    w.hh = hh;
+    w.lut = reinterpret_cast<const uint16_t*>(szrow);
+    (void)g;
+  } else {
 #pragma unroll
   for (int t = 0; t < 2; ++t) {
     const uint8_t* tp = tile0 + (static_cast<size_t>(t) * nkb + kb) * tile_bytes<B>() + 16 * lane;
@@ -66,6 +90,7 @@ __device__ __forceinline__ void w_fetch(WStage<B>& w, const uint8_t* tile0, cons
 #pragma unroll
     for (int t = 0; t < 2; ++t)
       w.sz[t] = *reinterpret_cast<const uint32_t*>(szrow + (static_cast<size_t>(g) * R + 16 * t) * 4);
+  }
   }
 }
 
@@ -91,7 +116,33 @@ __device__ __forceinline__ u32x4 pack8(const float (&v)[8]) {
 // become fl32(z + c s) (c s is exact in fp32, so one fma rounds once).
 template <int ACT, int SDT, int B>
 __device__ __forceinline__ u32x4 w_piece(const WStage<B>& w, int f) {
-  if constexpr (B == 16) {
+  if constexpr (B == kApl8 || B == kApl4) {
+    // plane j's eight bits of this k-step go to byte 7 - j; an 8 x 8 bit
+    // transpose leaves element q's code in byte q (plane 0 in the top bit)
+    const int t = f >> 1, sh = 8 * (2 * w.hh + (f & 1));
+    uint64_t x = 0;
+#pragma unroll
+    for (int j = 0; j < apl_planes<B>(); ++j) x |= static_cast<uint64_t>((w.p[t][j] >> sh) & 0xFFu) << (8 * (7 - j));
+    uint64_t y = (x ^ (x >> 7)) & 0x00AA00AA00AA00AAull;
+    x = x ^ y ^ (y << 7);
+    y = (x ^ (x >> 14)) & 0x0000CCCC0000CCCCull;
+    x = x ^ y ^ (y << 14);
+    y = (x ^ (x >> 28)) & 0x00000000F0F0F0F0ull;
+    x = x ^ y ^ (y << 28);
+    constexpr int nl = B == kApl8 ? 256 : 16;
+    const uint16_t* lut = w.lut + (16 * t + (lane_id() & 15)) * nl;
+    u32x4 o;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      uint32_t i0 = static_cast<uint32_t>(x >> (16 * q)) & 0xFFu, i1 = static_cast<uint32_t>(x >> (16 * q + 8)) & 0xFFu;
+      if constexpr (B == kApl4) {
+        i0 >>= 4;
+        i1 >>= 4;
+      }
+      o[q] = static_cast<uint32_t>(lut[i0]) | (static_cast<uint32_t>(lut[i1]) << 16);
+    }
+    return o;
+  } else if constexpr (B == 16) {
     return w.v[f];
   } else {
     const int t = f >> 1, i = f & 1;
@@ -324,7 +375,7 @@ __global__ __launch_bounds__(kThreads) void k_tgemm(const GemmArgs a, int nblk, 
 // dtype, as in the large-tile kernel.
 // ---------------------------------------------------------------------------
 
-template <int B> constexpr int sg_depth() { return B == 16 ? 2 : B == 8 ? 4 : 8; }
+template <int B> constexpr int sg_depth() { return B == 16 ? 2 : B == 8 || B == kApl8 ? 4 : 8; }
 constexpr int kSgStagePad = 8;   // stage counts are padded to a multiple of every depth
 
 template <int MT> constexpr int sg_xbuf() { return MT * kTK * 2; }            // one activation buffer
@@ -402,9 +453,12 @@ __device__ __forceinline__ void sg_loop(uint8_t* lds, const uint8_t* tile0, cons
   }
 }
 
-template <int ACT, int SDT, bool GATEUP, int MT>
+// LUT rows of the four waves (32 rows x 256 values each) for nested bit-plane pages
+constexpr int kSgLutWave = 32 * 256 * 2;
+
+template <int ACT, int SDT, bool GATEUP, int MT, bool APL>
 __global__ __launch_bounds__(256) void k_sgemm(const GemmArgs a, int nblk, int mtmax) {
-  __shared__ __attribute__((aligned(16))) uint8_t lds[sg_lds<MT>()];
+  __shared__ __attribute__((aligned(16))) uint8_t lds[sg_lds<MT>() + (APL ? 4 * kSgLutWave : 0)];
   const int per_xcd = gridDim.x / 8;
   const int logical = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
   const int band = logical / (kGN * mtmax), inb = logical % (kGN * mtmax);
@@ -444,9 +498,21 @@ __global__ __launch_bounds__(256) void k_sgemm(const GemmArgs a, int nblk, int m
   const int rb = grow / R, lr0 = grow - rb * R;
   const pw_page_entry ent = a.table[(static_cast<size_t>(e) * 3 + proj) * a.nrb_max + rb];
   const int bits = ent.bits;
-  const size_t tbytes = bits == 16 ? 4096 : bits == 8 ? 2048 : 1024;
+  const bool apl_page = APL && (ent.rsv & 0xFF) == PW_FMT_APL;
+  const size_t tbytes = apl_page ? 256 : bits == 16 ? 4096 : bits == 8 ? 2048 : 1024;
   const uint8_t* tile0 = a.pool + ent.data_off + static_cast<size_t>(lr0 / 16) * (K / 128) * tbytes;
   const uint8_t* szrow = a.pool + ent.sz_off + static_cast<size_t>(lr0 + lc) * 4;
+  if (APL && apl_page) {
+    // the wave's 32 LUT rows of the committed precision go to its LDS area
+    const int nl = bits == 8 ? 256 : 16;
+    const size_t rk8 = static_cast<size_t>(R) * K / 8;
+    const uint8_t* src = a.pool + ent.sz_off + (bits == 8 ? 32 * static_cast<size_t>(R) + 4 * rk8 : 0) +
+                         static_cast<size_t>(lr0) * nl * 2;
+    uint8_t* dst = lds + sg_lds<MT>() + wave * kSgLutWave;
+    for (int o = 16 * lane; o < 32 * nl * 2; o += 16 * 64)
+      *reinterpret_cast<u32x4*>(dst + o) = *reinterpret_cast<const u32x4*>(src + o);
+    szrow = dst;
+  }
   // this wave's activation fragments start at xf = wave * XF (slot tile xf / 2)
   constexpr int XF = MT >= 32 ? MT / 32 : 1;
   const int xf = wave * XF;
@@ -463,9 +529,22 @@ __global__ __launch_bounds__(256) void k_sgemm(const GemmArgs a, int nblk, int m
   f32x4 acc[2][MT / 16];
   const int nkb = K / 128;
   const int gshift = 31 - __builtin_clz(a.G);     // G is a power of two, at least 64
-  if (bits == 16) sg_loop<ACT, SDT, 16, MT>(lds, tile0, szrow, xrow, xf, nkb, R, gshift, wave, acc);
-  else if (bits == 8) sg_loop<ACT, SDT, 8, MT>(lds, tile0, szrow, xrow, xf, nkb, R, gshift, wave, acc);
-  else sg_loop<ACT, SDT, 4, MT>(lds, tile0, szrow, xrow, xf, nkb, R, gshift, wave, acc);
+  if constexpr (APL) {
+    if (apl_page) {
+      if (bits == 8) sg_loop<ACT, SDT, kApl8, MT>(lds, tile0, szrow, xrow, xf, nkb, R, gshift, wave, acc);
+      else sg_loop<ACT, SDT, kApl4, MT>(lds, tile0, szrow, xrow, xf, nkb, R, gshift, wave, acc);
+    } else if (bits == 16) {
+      sg_loop<ACT, SDT, 16, MT>(lds, tile0, szrow, xrow, xf, nkb, R, gshift, wave, acc);
+    } else if (bits == 8) {
+      sg_loop<ACT, SDT, 8, MT>(lds, tile0, szrow, xrow, xf, nkb, R, gshift, wave, acc);
+    } else {
+      sg_loop<ACT, SDT, 4, MT>(lds, tile0, szrow, xrow, xf, nkb, R, gshift, wave, acc);
+    }
+  } else {
+    if (bits == 16) sg_loop<ACT, SDT, 16, MT>(lds, tile0, szrow, xrow, xf, nkb, R, gshift, wave, acc);
+    else if (bits == 8) sg_loop<ACT, SDT, 8, MT>(lds, tile0, szrow, xrow, xf, nkb, R, gshift, wave, acc);
+    else sg_loop<ACT, SDT, 4, MT>(lds, tile0, szrow, xrow, xf, nkb, R, gshift, wave, acc);
+  }
 
   const int wr = wave & 1;
   if (GATEUP) {
@@ -517,10 +596,16 @@ void sgemm_go(const GemmArgs& a, bool gateup, hipStream_t st) {
   const int nblk = gateup ? a.F / 64 : a.H / 128;
   const int mtmax = (a.S + MT - 1) / MT + a.E;
   const int n = ((nblk + kGN - 1) / kGN * kGN * mtmax + 7) / 8 * 8;
-  if (gateup)
-    hipLaunchKernelGGL((k_sgemm<ACT, SDT, true, MT>), dim3(n), dim3(256), 0, st, a, nblk, mtmax);
-  else
-    hipLaunchKernelGGL((k_sgemm<ACT, SDT, false, MT>), dim3(n), dim3(256), 0, st, a, nblk, mtmax);
+  if (a.apl) {
+    if (gateup)
+      hipLaunchKernelGGL((k_sgemm<ACT, SDT, true, MT, true>), dim3(n), dim3(256), 0, st, a, nblk, mtmax);
+    else
+      hipLaunchKernelGGL((k_sgemm<ACT, SDT, false, MT, true>), dim3(n), dim3(256), 0, st, a, nblk, mtmax);
+  } else if (gateup) {
+    hipLaunchKernelGGL((k_sgemm<ACT, SDT, true, MT, false>), dim3(n), dim3(256), 0, st, a, nblk, mtmax);
+  } else {
+    hipLaunchKernelGGL((k_sgemm<ACT, SDT, false, MT, false>), dim3(n), dim3(256), 0, st, a, nblk, mtmax);
+  }
 }
 
 template <int ACT, int SDT>

@@ -72,6 +72,31 @@ class PagedLayer:
         torch.cuda.current_stream().synchronize() if stream is None else stream.synchronize()
         del dev
 
+    def load_pages_apl(self, w16: Sequence[np.ndarray], pages: Iterable[Tuple[int, int, int, int]],
+                       stream=None):
+        """Quantize blocks into nested bit-plane pages: pages = [(e, p, rb, bits)]
+        with bits 8 or 4, placed in that order (pw_layer_load_pages_apl)."""
+        st = _stream(stream)
+        cfg = self.cfg
+        pages = list(pages)
+        if not pages:
+            return
+        dev = [torch.from_numpy(np.ascontiguousarray(w16[p]).view(np.int16)).to(self.device) for p in (GATE, UP, DOWN)]
+        chunk = 32
+        ws_bytes = pw.pw_apl_workspace_bytes(self.handle, min(chunk, len(pages)))
+        ws_t, ws_ptr = _aligned_empty(ws_bytes, self.device)
+        for i in range(0, len(pages), chunk):
+            part = pages[i:i + chunk]
+            ptrs = []
+            for (e, p, rb, b) in part:
+                rows, cols = w16[p].shape[1:]
+                ptrs.append(dev[p].data_ptr() + ((e * rows + rb * cfg.R) * cols) * 2)
+            es, ps, rbs, bs = zip(*part)
+            pw.pw_layer_load_pages_apl(self.handle, list(es), list(ps), list(rbs), list(bs), ptrs, ws_ptr,
+                                       ws_bytes, st)
+        torch.cuda.current_stream().synchronize() if stream is None else stream.synchronize()
+        del dev, ws_t
+
     # -- hot path ------------------------------------------------------------
     @staticmethod
     def routing_buffers(T: int, E: int, K: int, device="cuda"):
@@ -187,7 +212,11 @@ class PagedLayer:
     def page_image(self, e: int, p: int, rb: int) -> np.ndarray:
         """The page's bytes as stored in the pool (host copy)."""
         ent = self.entry(e, p, rb)
-        n = pw.pw_page_bytes(self.desc, p, int(ent.bits))
+        if ent.rsv & 0xFF == pw.PW_FMT_APL:
+            R, K = self.cfg.R, (self.cfg.F if p == DOWN else self.cfg.H)
+            n = R * K * int(ent.bits) // 8 + 32 * R + (512 * R if ent.bits == 8 else 0)
+        else:
+            n = pw.pw_page_bytes(self.desc, p, int(ent.bits))
         base = self.pool_ptr - self._pool_t.data_ptr() + ent.data_off
         return self._pool_t[base:base + n].cpu().numpy()
 

@@ -37,6 +37,7 @@ class pw_layer_desc(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int) for n in ("E", "H", "F", "R", "G", "act", "sdt")]
 
 
+PW_FMT_RTN, PW_FMT_APL = 0, 1
 PW_PLAN_MAX_BUCKETS = 8
 PW_PLAN_MAX_STAGES = 8
 
@@ -105,6 +106,8 @@ def _load():
         "pw_pool_stats": (i32, [vp, P(sz), P(sz), P(sz)]),
         "pw_profile_enable": (i32, [vp, i32]),
         "pw_profile_read": (i32, [vp, P(ctypes.c_double), P(ctypes.c_int64), i32]),
+        "pw_apl_workspace_bytes": (i32, [vp, i32, P(sz)]),
+        "pw_layer_load_pages_apl": (i32, [vp, i32, P(i32), P(i32), P(i32), P(i32), P(vp), vp, sz, vp]),
         "pw_routing_stats": (i32, [vp, i32, i32, i32, i32, vp, vp, vp, i32, i32, i32, vp, vp, i32, vp]),
         "pw_planner_create": (i32, [i32, i32, P(i32), P(i32), P(ctypes.c_uint64), P(ctypes.c_double),
                                     P(pw_planner_config), P(vp)]),
@@ -394,3 +397,21 @@ def pw_planner_apply(p: int, layer: int, stream: int) -> int:
     d = ctypes.c_size_t()
     _check(_lib.pw_planner_apply(p, layer, stream, ctypes.byref(d)))
     return d.value
+
+
+# --------------------------------------------------------------------------
+# nested bit-plane pages
+# --------------------------------------------------------------------------
+
+def pw_apl_workspace_bytes(layer: int, n: int) -> int:
+    out = ctypes.c_size_t()
+    _check(_lib.pw_apl_workspace_bytes(layer, n, ctypes.byref(out)))
+    return out.value
+
+
+def pw_layer_load_pages_apl(layer: int, es, projs, rbs, bits, row_ptrs, ws_ptr: int, ws_bytes: int, stream: int):
+    n = len(es)
+    arr = ctypes.c_int * max(n, 1)
+    ptrs = (ctypes.c_void_p * max(n, 1))(*row_ptrs)
+    _check(_lib.pw_layer_load_pages_apl(layer, n, arr(*es), arr(*projs), arr(*rbs), arr(*bits), ptrs, ws_ptr,
+                                        ws_bytes, stream))

@@ -1,0 +1,162 @@
+"""Nested bit-plane pages on the GPU (any-precision weights: Sec. 2.2 and 3.1).
+
+Checked: every quantized page is byte-identical to the oracle's (codes,
+bit-planes and both LUTs); the forward through the streaming kernel matches
+the oracle's dense MoE of the reconstructed 16-bit weights; lowering 8 -> 4
+bits runs no kernel, keeps the page prefix, frees exactly the page tail
+(Eq. 3), and the forward then follows the 4-bit LUTs; unsupported moves are
+refused.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from oracle import apl
+from helpers import case, oracle_layer, rel_err, say, to_dev, to_dev16, y16_values
+from paper_2607_16184_amd import pw, synth
+
+pytestmark = pytest.mark.gpu
+
+TOL16, TOL32 = 2e-2, 1e-3
+
+
+def _oracle_pages(cfg, w16, bits):
+    """{(e, p, rb): (8-bit page bytes, codes8, lut4, lut8)} for every quantized block."""
+    out = {}
+    for p in range(3):
+        for e in range(cfg.E):
+            for rb in range(cfg.nrb(p)):
+                if bits[p][e, rb] == 16:
+                    continue
+                rows = w16[p][e, rb * cfg.R:(rb + 1) * cfg.R]
+                v = oracle.decode16(rows, cfg.act).astype(np.float64)
+                codes, c4, c8 = apl.quantize_rows(v)
+                l4, l8 = apl.lut16(c4, cfg.act), apl.lut16(c8, cfg.act)
+                out[(e, p, rb)] = (apl.encode_page(codes, l4, l8), codes, l4, l8)
+    return out
+
+
+def _effective_w16(cfg, w16, bits, pages):
+    """16-bit weights the kernels must reproduce: LUT values of each quantized block."""
+    eff = [np.array(w, copy=True) for w in w16]
+    for (e, p, rb), (_, codes, l4, l8) in pages.items():
+        b = int(bits[p][e, rb])
+        eff[p][e, rb * cfg.R:(rb + 1) * cfg.R] = apl.dequant(codes, l8 if b == 8 else l4, b)
+    return eff
+
+
+def _layer(cfg, w16, bits, slack=0.25):
+    from paper_2607_16184_amd.layer import PagedLayer
+    R = cfg.R
+    need = 0
+    for p in range(3):
+        K = cfg.F if p == 2 else cfg.H
+        for b in np.asarray(bits[p]).ravel():
+            need += pw.pw_page_bytes(cfg, p, 16) if b == 16 else apl.page_bytes(R, K, int(b))
+    L = PagedLayer(cfg, int(need * (1 + slack)) + 4096)
+    order = synth.pool_order(cfg)
+    L.load_pages(w16, bits, [pg for pg in order if bits[pg[1]][pg[0], pg[2]] == 16])
+    L.load_pages_apl(w16, [(e, p, rb, int(bits[p][e, rb])) for (e, p, rb) in order if bits[p][e, rb] != 16])
+    return L
+
+
+def _forward_check(L, cfg, eff, T=None):
+    import torch
+    logits = synth.logits(cfg, T=T)
+    x16 = synth.activations(cfg, T=T)
+    O = oracle_layer(cfg, eff, [np.full_like(b, 16) for b in (synth.bitmap(cfg))])
+    routing = L.route(to_dev(logits), cfg.K)
+    x = to_dev16(x16)
+    y16 = L.forward(x, routing)
+    y32 = L.forward(x, routing, out_fp32=True)
+    torch.cuda.synchronize()
+    ids, w = oracle.route(logits, cfg.K)
+    r1 = O.forward(x16, ids, w, h_round=False)
+    r2 = O.forward(x16, ids, w, h_round=True)
+    return rel_err(y16_values(y16, cfg.act), r1), rel_err(y32.cpu().numpy(), r2)
+
+
+def test_apl_pages_bit_exact_and_forward():
+    cfg, w16, bits, _ = case("tiny")
+    say("bit-plane pages: tiny layer, quantize %d blocks" % sum(int((b != 16).sum()) for b in bits))
+    L = _layer(cfg, w16, bits)
+    pages = _oracle_pages(cfg, w16, bits)
+    for (e, p, rb), (buf, _, _, _) in pages.items():
+        got = L.page_image(e, p, rb)
+        want = buf[:got.size]
+        K = cfg.F if p == 2 else cfg.H
+        assert got.size == apl.page_bytes(cfg.R, K, int(bits[p][e, rb]))
+        if not np.array_equal(got, want):
+            b = int(bits[p][e, rb])
+            gc, gl = apl.decode_page(got, cfg.R, K, b)
+            wc, wl = apl.decode_page(want, cfg.R, K, b)
+            raise AssertionError("page %s: %d code and %d LUT mismatches" % ((e, p, rb), (gc != wc).sum(),
+                                                                          (gl != wl).sum()))
+        assert L.entry(e, p, rb).rsv == pw.PW_FMT_APL
+    eff = _effective_w16(cfg, w16, bits, pages)
+    for T in (None, 200):
+        say("bit-plane forward T=%s" % T)
+        e16, e32 = _forward_check(L, cfg, eff, T)
+        assert e16 <= TOL16 and e32 <= TOL32, (T, e16, e32)
+    L.close()
+
+
+def test_apl_downshift_drops_planes():
+    import torch
+    cfg, w16, bits, _ = case("tiny")
+    say("bit-plane downshift 8 -> 4")
+    L = _layer(cfg, w16, bits)
+    pages = _oracle_pages(cfg, w16, bits)
+    eight = [k for k in pages if bits[k[1]][k[0], k[2]] == 8]
+    free0 = L.stats()[1]
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    pw.pw_profile_read(L.handle, reset=True)
+    pw.pw_profile_enable(L.handle, True)
+    delta = L.requant(eight, 4, stream=side)
+    want = sum(apl.page_bytes(cfg.R, cfg.F if p == 2 else cfg.H, 8) - apl.page_bytes(cfg.R, cfg.F if p == 2 else cfg.H, 4)
+               for (e, p, rb) in eight)
+    assert delta == want
+    assert L.commit() == len(eight)
+    torch.cuda.synchronize()
+    pw.pw_profile_enable(L.handle, False)
+    assert pw.pw_profile_read(L.handle, reset=True)[1][pw.PW_PH_REQUANT] == 0   # no requant kernel ran
+    L.reclaim()
+    assert L.stats()[1] - free0 == want
+    bits4 = [b.copy() for b in bits]
+    for (e, p, rb) in eight:
+        bits4[p][e, rb] = 4
+        ent = L.entry(e, p, rb)
+        assert ent.bits == 4 and ent.rsv == pw.PW_FMT_APL
+        got = L.page_image(e, p, rb)
+        assert np.array_equal(got, pages[(e, p, rb)][0][:got.size])
+    e16, e32 = _forward_check(L, cfg, _effective_w16(cfg, w16, bits4, pages))
+    assert e16 <= TOL16 and e32 <= TOL32, (e16, e32)
+    # refused moves: below 4 bits, a plane page to 16 bits, host copies
+    blk = eight[0]
+    with pytest.raises(pw.PWError) as ei:
+        L.requant([blk], 16)
+    assert ei.value.status == 4
+    assert L.requant([blk], 4) == 0                                    # same bitwidth: no-op
+    L.set_host_pool(1 << 20)
+    with pytest.raises(pw.PWError) as ei:
+        L.offload([blk])
+    assert ei.value.status == 4
+    L.close()
+
+
+def test_apl_load_errors():
+    import torch
+    cfg, w16, bits, _ = case("tiny")
+    say("bit-plane load errors")
+    from paper_2607_16184_amd.layer import PagedLayer
+    L = PagedLayer(cfg, 4 << 20)
+    with pytest.raises(pw.PWError) as ei:
+        L.load_pages_apl(w16, [(0, 0, 0, 16)])
+    assert ei.value.status == 1
+    L.load_pages_apl(w16, [(0, 0, 0, 8)])
+    with pytest.raises(pw.PWError) as ei:
+        L.load_pages_apl(w16, [(0, 0, 0, 4)])
+    assert ei.value.status == 3
+    torch.cuda.synchronize()
+    L.close()
