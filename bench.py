@@ -533,6 +533,87 @@ def leg_planner():
             "eager_step_ms_after": round(after, 4)}
 
 
+def leg_apl(steps=20):
+    """Nested bit-plane pages on the Mixtral-shaped decode layer: the quantized
+    pages of the 50/25/25 % mix (8-bit and 4-bit) are bit-plane pages with
+    per-row LUTs (16-bit pages stay plain). Reports the quantization time, the
+    decode step (streaming kernel, every page at its committed bitwidth) and
+    the 8 -> 4 downshift of all 8-bit pages, which runs no kernel: the commit
+    republishes the entries and reclaim frees the page tails."""
+    import numpy as np
+    import torch
+    from paper_2607_16184_amd import pw, synth
+    from paper_2607_16184_amd.layer import PagedLayer
+    cfg = synth.CONFIGS["mixtral_decode"]
+    w16 = [synth.expert_weights(cfg, p) for p in range(3)]
+    bits = synth.bitmap(cfg)
+    R = cfg.R
+    sizes = {p: {16: pw.pw_page_bytes(cfg, p, 16),
+                 8: R * (cfg.F if p == 2 else cfg.H) + 544 * R,
+                 4: R * (cfg.F if p == 2 else cfg.H) // 2 + 32 * R} for p in range(3)}
+    need = sum(sizes[p][int(b)] for p in range(3) for b in np.asarray(bits[p]).ravel())
+    L = PagedLayer(cfg, int(need * 1.05) + (1 << 20))
+    order = synth.pool_order(cfg)
+    L.load_pages(w16, bits, [pg for pg in order if bits[pg[1]][pg[0], pg[2]] == 16])
+    qp = [(e, p, rb, int(bits[p][e, rb])) for (e, p, rb) in order if bits[p][e, rb] != 16]
+    torch.cuda.synchronize()
+    t0 = time.time()
+    L.load_pages_apl(w16, qp)
+    quant_s = time.time() - t0
+    del w16
+    lg, x16 = synth.step_inputs(cfg, 0)
+    logits = torch.from_numpy(lg).cuda()
+    x = torch.from_numpy(x16.view(np.int16)).cuda()
+    rbuf = PagedLayer.routing_buffers(cfg.T, cfg.E, cfg.K)
+    y = torch.empty((cfg.T, cfg.H), dtype=torch.int16, device="cuda")
+
+    def timed():
+        for _ in range(3):
+            L.forward(x, L.route(logits, cfg.K, out=rbuf), y=y)
+        torch.cuda.synchronize()
+        pw.pw_profile_read(L.handle, reset=True)
+        pw.pw_profile_enable(L.handle, True)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(steps):
+            L.forward(x, L.route(logits, cfg.K, out=rbuf), y=y)
+        b.record()
+        torch.cuda.synchronize()
+        pw.pw_profile_enable(L.handle, False)
+        ms, cnt = pw.pw_profile_read(L.handle, reset=True)
+        return a.elapsed_time(b) / steps, ms[pw.PW_PH_GATEUP] / max(cnt[pw.PW_PH_GATEUP], 1), \
+            ms[pw.PW_PH_DOWN] / max(cnt[pw.PW_PH_DOWN], 1)
+
+    cur = [b.copy() for b in bits]
+    wbytes = sum(sizes[p][int(b)] for p in range(3) for b in np.asarray(cur[p]).ravel())
+    step0, gu0, dn0 = timed()
+    eight = [(e, p, rb) for (e, p, rb, b) in qp if b == 8]
+    free0 = L.stats()[1]
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    t0 = time.perf_counter()
+    delta = L.requant(eight, 4, stream=side)
+    L.commit()
+    torch.cuda.synchronize()
+    L.reclaim()
+    drop_ms = (time.perf_counter() - t0) * 1e3
+    freed = L.stats()[1] - free0
+    for (e, p, rb) in eight:
+        cur[p][e, rb] = 4
+    wbytes1 = sum(sizes[p][int(b)] for p in range(3) for b in np.asarray(cur[p]).ravel())
+    step1, gu1, dn1 = timed()
+    L.close()
+    return {"workload": "mixtral_decode layer, 64-token steps; 8-bit and 4-bit pages as nested bit-planes "
+                        "with per-row LUTs (streaming kernel); then every 8-bit page dropped to 4 bits",
+            "quantize_s": round(quant_s, 2), "pages_bitplane": len(qp),
+            "eager_step_ms": round(step0, 4), "gateup_ms": round(gu0, 4), "down_ms": round(dn0, 4),
+            "weight_GBps": round(wbytes / (step0 * 1e-3) / 1e9, 1),
+            "downshift_pages": len(eight), "downshift_bytes_freed": int(freed), "downshift_delta": int(delta),
+            "downshift_host_ms": round(drop_ms, 3),
+            "eager_step_ms_after": round(step1, 4), "gateup_ms_after": round(gu1, 4), "down_ms_after": round(dn1, 4),
+            "weight_GBps_after": round(wbytes1 / (step1 * 1e-3) / 1e9, 1)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -540,7 +621,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="mixtral_decode")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--extras", default="prefill,finegrained,downshift,offload,planner",
+    ap.add_argument("--extras", default="prefill,finegrained,downshift,offload,planner,apl",
                     help="comma list of extra legs on the same JSON line ('' for none)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after the timed steps, run one device copy of this many MiB "
@@ -638,6 +719,8 @@ def main():
             extras["offload"] = leg_offload()
         elif leg == "planner":
             extras["planner"] = leg_planner()
+        elif leg == "apl":
+            extras["apl"] = leg_apl()
         log("leg %s done in %.1f s" % (leg, time.time() - t0))
     if extras:
         out["extras"] = extras
