@@ -23,9 +23,8 @@ here (also in the design notes):
 * LUT_b[r][c] = the level-b centroid rounded to the activation dtype (nearest
   even); a weight at precision b reconstructs as LUT_b[r][code >> (8 - b)].
 
-All arithmetic is float64 with sums in order of k (numpy's cumulative sum is
-sequential), so any implementation that keeps that order reproduces it bit
-for bit. Only the test suite, the smoke check and the benchmark's CPU leg may
+All arithmetic is float64 with sums accumulated from +0.0 in order of k, so
+any implementation that keeps that order reproduces it bit for bit. Only the test suite, the smoke check and the benchmark's CPU leg may
 import this module; it shares no code with the library.
 
 Page layout of an R x K block (R a multiple of 16, K of 128), byte offsets:
@@ -49,26 +48,30 @@ SEED_ITERS = 8
 SPLIT_ITERS = 4
 
 
-def _seq_sum(x: np.ndarray) -> np.ndarray:
-    """Sums along the last axis in order (sequential float64 accumulation)."""
-    z = np.zeros(x.shape[:-1] + (1,))
-    return np.cumsum(np.concatenate([z, x], axis=-1), axis=-1)[..., -1]   # from +0.0, in order
-
-
 def _assign(v: np.ndarray, c: np.ndarray) -> np.ndarray:
     """Nearest centroid per value (ties to the lower index); v [R,K], c [R,J]."""
     d = np.abs(v[:, :, None] - c[:, None, :])
     return np.argmin(d, axis=2)
 
 
-def _means(v: np.ndarray, a: np.ndarray, J: int, c_old: np.ndarray) -> np.ndarray:
-    c = c_old.copy()
-    for j in range(J):
-        m = a == j
-        n = m.sum(axis=1)
-        s = _seq_sum(np.where(m, v, 0.0))
-        nz = n > 0
-        c[nz, j] = s[nz] / n[nz]
+def _cluster_sums(v: np.ndarray, a: np.ndarray, J: int) -> Tuple[np.ndarray, np.ndarray]:
+    """Per row and cluster: member count and the members' sum, accumulated from
+    +0.0 one value at a time in order of k (np.add.at is unbuffered and adds
+    in index order)."""
+    R, K = v.shape
+    rows = np.repeat(np.arange(R), K)
+    s = np.zeros((R, J))
+    np.add.at(s, (rows, a.reshape(-1)), v.reshape(-1))
+    n = np.zeros((R, J), np.int64)
+    np.add.at(n, (rows, a.reshape(-1)), 1)
+    return n, s
+
+
+def _update(c: np.ndarray, n: np.ndarray, s: np.ndarray) -> np.ndarray:
+    """Lloyd update: each non-empty cluster's centroid becomes its mean."""
+    c = c.copy()
+    nz = n > 0
+    c[nz] = s[nz] / n[nz]
     return c
 
 
@@ -77,40 +80,34 @@ def quantize_rows(v: np.ndarray) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
     [R,256]) of rows v (float64, the 16-bit weights' values)."""
     v = np.asarray(v, np.float64)
     R, K = v.shape
+    r = np.arange(R)[:, None]
     lo, hi = v.min(axis=1), v.max(axis=1)
     c = lo[:, None] + (hi - lo)[:, None] * ((2.0 * np.arange(16) + 1.0) / 32.0)[None, :]
     for _ in range(SEED_ITERS):
         a = _assign(v, c)
-        c = _means(v, a, 16, c)
+        c = _update(c, *_cluster_sums(v, a, 16))
     a = _assign(v, c)
     c4 = c.copy()
     for level in range(SEED_BITS + 1, MAX_BITS + 1):
         P = 1 << (level - 1)
-        child = np.zeros((R, 2 * P))
-        a_next = np.zeros_like(a)
-        for p in range(P):
-            m = a == p
-            n = m.sum(axis=1)
-            has = n > 0
-            mean = np.where(has, _seq_sum(np.where(m, v, 0.0)) / np.maximum(n, 1), c[:, p])
-            lo_p = np.where(has, np.where(m, v, np.inf).min(axis=1), c[:, p])
-            hi_p = np.where(has, np.where(m, v, -np.inf).max(axis=1), c[:, p])
-            ch = np.stack([np.where(has, (lo_p + mean) / 2.0, c[:, p]),
-                           np.where(has, (mean + hi_p) / 2.0, c[:, p])], axis=1)
-            for _ in range(SPLIT_ITERS):
-                pick = (np.abs(v - ch[:, 1:2]) < np.abs(v - ch[:, 0:1])).astype(np.int64)
-                for k in range(2):
-                    mk = m & (pick == k)
-                    nk = mk.sum(axis=1)
-                    sk = _seq_sum(np.where(mk, v, 0.0))
-                    ok = nk > 0
-                    ch[ok, k] = sk[ok] / nk[ok]
-            child[:, 2 * p] = ch[:, 0]
-            child[:, 2 * p + 1] = ch[:, 1]
-            pick = (np.abs(v - ch[:, 1:2]) < np.abs(v - ch[:, 0:1])).astype(np.int64)
-            a_next = np.where(m, 2 * p + pick, a_next)
-        a = a_next
-        c = child
+        # parent statistics: members' count, sum (in order of k), minimum, maximum
+        n, s = _cluster_sums(v, a, P)
+        pmin = np.full((R, P), np.inf)
+        pmax = np.full((R, P), -np.inf)
+        rows = np.repeat(np.arange(R), K)
+        np.minimum.at(pmin, (rows, a.reshape(-1)), v.reshape(-1))
+        np.maximum.at(pmax, (rows, a.reshape(-1)), v.reshape(-1))
+        has = n > 0
+        mean = np.where(has, s / np.maximum(n, 1), c)
+        ch = np.empty((R, 2 * P))
+        ch[:, 0::2] = np.where(has, (pmin + mean) / 2.0, c)
+        ch[:, 1::2] = np.where(has, (mean + pmax) / 2.0, c)
+        for _ in range(SPLIT_ITERS):
+            pick = (np.abs(v - ch[r, 2 * a + 1]) < np.abs(v - ch[r, 2 * a])).astype(np.int64)
+            ch = _update(ch, *_cluster_sums(v, 2 * a + pick, 2 * P))
+        pick = (np.abs(v - ch[r, 2 * a + 1]) < np.abs(v - ch[r, 2 * a])).astype(np.int64)
+        a = 2 * a + pick
+        c = ch
     return a.astype(np.uint8), c4, c
 
 

@@ -64,7 +64,7 @@ def _forward_check(L, cfg, eff, T=None):
     import torch
     logits = synth.logits(cfg, T=T)
     x16 = synth.activations(cfg, T=T)
-    O = oracle_layer(cfg, eff, [np.full_like(b, 16) for b in (synth.bitmap(cfg))])
+    O = oracle_layer(cfg, eff, [np.full_like(b, 16) for b in synth.bitmap(cfg)])
     routing = L.route(to_dev(logits), cfg.K)
     x = to_dev16(x16)
     y16 = L.forward(x, routing)
@@ -76,9 +76,10 @@ def _forward_check(L, cfg, eff, T=None):
     return rel_err(y16_values(y16, cfg.act), r1), rel_err(y32.cpu().numpy(), r2)
 
 
-def test_apl_pages_bit_exact_and_forward():
-    cfg, w16, bits, _ = case("tiny")
-    say("bit-plane pages: tiny layer, quantize %d blocks" % sum(int((b != 16).sum()) for b in bits))
+@pytest.mark.parametrize("act", [oracle.F16, oracle.BF16])
+def test_apl_pages_bit_exact_and_forward(act):
+    cfg, w16, bits, _ = case("tiny", act=act, sdt=act)
+    say("bit-plane pages: tiny layer act %d, quantize %d blocks" % (act, sum(int((b != 16).sum()) for b in bits)))
     L = _layer(cfg, w16, bits)
     pages = _oracle_pages(cfg, w16, bits)
     for (e, p, rb), (buf, _, _, _) in pages.items():
@@ -159,4 +160,38 @@ def test_apl_load_errors():
         L.load_pages_apl(w16, [(0, 0, 0, 4)])
     assert ei.value.status == 3
     torch.cuda.synchronize()
+    L.close()
+
+
+def test_apl_mixtral_sampled_pages():
+    """The Mixtral-shaped decode layer with its quantized pages as bit-plane
+    pages (the configuration the benchmark times): sampled pages of every
+    projection and both precisions are byte-identical to the oracle's
+    (rows of 4096 and 14336 values, bf16 LUTs)."""
+    import torch
+    cfg = synth.CONFIGS["mixtral_decode"]
+    w16 = [synth.expert_weights(cfg, p) for p in range(3)]
+    bits = synth.bitmap(cfg)
+    say("bit-plane pages: Mixtral decode layer")
+    L = _layer(cfg, w16, bits, slack=0.05)
+    rng = np.random.default_rng(7)
+    picks = []
+    for p, b in ((0, 8), (1, 4), (2, 8), (2, 4)):
+        cand = [(e, p, rb) for e in range(cfg.E) for rb in range(cfg.nrb(p)) if bits[p][e, rb] == b]
+        picks.append(cand[int(rng.integers(len(cand)))])
+    for (e, p, rb) in picks:
+        say("oracle page %s" % ((e, p, rb),))
+        rows = w16[p][e, rb * cfg.R:(rb + 1) * cfg.R]
+        codes, c4, c8 = apl.quantize_rows(oracle.decode16(rows, cfg.act).astype(np.float64))
+        want = apl.encode_page(codes, apl.lut16(c4, cfg.act), apl.lut16(c8, cfg.act))
+        got = L.page_image(e, p, rb)
+        assert np.array_equal(got, want[:got.size]), (e, p, rb)
+    # the step runs (streaming kernel) and is deterministic
+    logits, x16 = synth.logits(cfg), synth.activations(cfg)
+    routing = L.route(to_dev(logits), cfg.K)
+    x = to_dev16(x16)
+    y1 = L.forward(x, routing, out_fp32=True)
+    y2 = L.forward(x, routing, out_fp32=True)
+    torch.cuda.synchronize()
+    assert torch.equal(y1, y2) and bool(torch.isfinite(y1).all())
     L.close()
