@@ -4,15 +4,22 @@
 // D = W X^T for one expert: gate/up tiles are 128 rows of gate plus the same
 // 128 rows of up (SwiGLU applied in the epilogue), down tiles are 256 rows of
 // the down projection. Wave (wn, wm), wn = wave / 4, wm = wave mod 4, owns
-// rows 128 wn .. + 128 and slots 64 wm .. + 64: 8 x 4 MFMA 16x16x32 tiles,
+// rows 128 wn .. + 128 and slots 64 wm .. + 64: 4 x 2 MFMA 32x32x16 tiles,
 // 128 fp32 accumulators. K advances in stages of 64 through a double-buffered
-// LDS stage of 64 KiB in MFMA fragment order (1 KiB per 16-row x 32-k
+// LDS stage of 64 KiB in 32x32x16 fragment order (1 KiB per 32-row x 16-k
 // fragment, lane order), so every operand read and staging write is a
 // conflict-free 16-byte LDS access. Each wave stages 32 weight rows (one page,
-// dequantized once to the activation dtype) and 32 slots. Two waves per SIMD
-// let one wave's staging (global loads, dequantization, LDS writes) overlap
-// the other's MFMAs. The quantized weight enters the MFMA as fl32(z + c s)
-// rounded to the activation dtype.
+// dequantized once to the activation dtype) and 32 slots.
+//
+// Schedule (ping-pong): the two waves of a SIMD belong to different halves
+// (wn = 0 and wn = 1), and the wn = 1 half runs one barrier interval behind.
+// Between two workgroup barriers one half issues 16 MFMAs from operands
+// already in registers while the other half does memory work: LDS writes of
+// the next stage, global loads two stages ahead, and the LDS reads of its next
+// MFMA operands. So the matrix core of every SIMD is fed by one wave while the
+// other waits on memory, and a global load has about four intervals to land.
+// The quantized weight enters the MFMA as fl32(z + c s) rounded to the
+// activation dtype.
 #include "pw_device.hpp"
 #include "pw_internal.hpp"
 
@@ -28,10 +35,13 @@ constexpr int kWB = kTN * kTK * 2;          // 32 KiB of weights per stage
 constexpr int kXB = kTM * kTK * 2;          // 32 KiB of activations per stage
 constexpr int kSB = kWB + kXB;              // one stage buffer
 constexpr int kGN = 4;                      // weight blocks per raster band
+// s_getreg operand for HW_REG_HW_ID (register 4) bits 5:4, the wave's SIMD.
+constexpr int kHwRegSimdId = 4 | (4 << 6) | ((2 - 1) << 11);
 
-// Fragment (tile, k-step) offset inside a stage buffer part: 16-row tiles of
-// two 1 KiB k-step blocks, each in lane order (lane l: row l mod 16, k-run l / 16).
-__device__ __forceinline__ int frag_off(int tile, int i) { return (tile * 2 + i) * 1024; }
+// Fragment (tile, k-step) offset inside a stage buffer part: 32-row tiles of
+// four 1 KiB 16-k blocks, each in 32x32x16 operand lane order (lane l: row
+// l mod 32, k-run l / 32 of eight values).
+__device__ __forceinline__ int frag32(int tile, int ks) { return (tile * 4 + ks) * 1024; }
 
 // A wave's weight share of a stage: 32 rows (two 16-row tiles) of one page as
 // four fragments f = 2 * tile + step.
@@ -175,76 +185,131 @@ __device__ __forceinline__ void x_fetch(XStage& x, const uint8_t* const (&xrow)[
     x.v[j] = *reinterpret_cast<const u32x4*>(xrow[j >> 1] + static_cast<size_t>(k0 + 32 * (j & 1) + 8 * lg) * 2);
 }
 
-// Writes the wave's staged fragments (4 weight, 4 activation) to a buffer.
+// Writes the wave's staged pieces (32 weight rows and 32 slots over the
+// stage's 64 k) to a buffer in 32x32x16 fragment order. A loaded piece holds
+// row 16 t + l mod 16 (t: 16-row half), k = 32 i + 8 (l / 16) .. + 7 (i: k-step
+// of 32); it goes to 16-k block 2 i + (l / 16) / 2 at lane 16 t + l mod 16 +
+// 32 ((l / 16) mod 2). Each group of 16 lanes writes 256 contiguous bytes.
 template <int ACT, int SDT, int B>
 __device__ __forceinline__ void stage_store(const WStage<B>& w, const XStage& x, uint8_t* buf, int wave) {
-  uint8_t* d = buf + 4096 * wave + 16 * lane_id();   // fragments 4 wave + f of each part
+  const int lane = lane_id(), lc = lane & 15, lg = lane >> 4;
+  uint8_t* d = buf + frag32(wave, lg >> 1) + 16 * (lc + 32 * (lg & 1));
 #pragma unroll
-  for (int f = 0; f < 4; ++f) {
-    *reinterpret_cast<u32x4*>(d + 1024 * f) = w_piece<ACT, SDT, B>(w, f);
-    *reinterpret_cast<u32x4*>(d + kWB + 1024 * f) = x.v[f];
-  }
-}
-
-// The 64 MFMAs of one stage for the wave's 128 x 64 sub-tile. The next weight
-// fragment is read from LDS while the current one feeds its 4 MFMAs.
-template <int ACT>
-__device__ __forceinline__ void stage_mma(const uint8_t* buf, int wn, int wm, f32x4 (&acc)[8][4]) {
-  const int lane = lane_id();
-  const uint8_t* wbuf = buf + 16 * lane;
-  const uint8_t* xbuf = buf + kWB + 16 * lane;
+  for (int t = 0; t < 2; ++t)
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    u32x4 b[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) b[u] = ld16(xbuf + frag_off(wm * 4 + u, i));
-    u32x4 at = ld16(wbuf + frag_off(wn * 8, i));
-#pragma unroll
-    for (int t = 0; t < 8; ++t) {
-      u32x4 an = at;
-      if (t < 7) an = ld16(wbuf + frag_off(wn * 8 + t + 1, i));
-#pragma unroll
-      for (int u = 0; u < 4; ++u) acc[t][u] = mma<ACT>(at, b[u], acc[t][u]);
-      at = an;
-      __builtin_amdgcn_sched_barrier(0);
+    for (int i = 0; i < 2; ++i) {
+      *reinterpret_cast<u32x4*>(d + 2048 * i + 256 * t) = w_piece<ACT, SDT, B>(w, 2 * t + i);
+      *reinterpret_cast<u32x4*>(d + kWB + 2048 * i + 256 * t) = x.v[2 * t + i];
     }
+}
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+template <int ACT>
+__device__ __forceinline__ f32x16 mma32(u32x4 a, u32x4 b, f32x16 c) {
+  if constexpr (ACT == PW_BF16)
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c,
+                                                   0, 0, 0);
+  else
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c,
+                                                  0, 0, 0);
+}
+
+// MFMA operands of one half stage (two 16-k blocks) for the wave's 128 x 64
+// sub-tile: four 32-row weight fragments and two 32-slot fragments per block.
+struct Ops {
+  u32x4 a[2][4];
+  u32x4 b[2][2];
+};
+
+__device__ __forceinline__ void ops_read(Ops& o, const uint8_t* buf, int wn, int wm, int half) {
+  const uint8_t* wb = buf + 16 * lane_id();
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) o.a[q][r] = ld16(wb + frag32(4 * wn + r, 2 * half + q));
+#pragma unroll
+    for (int c = 0; c < 2; ++c) o.b[q][c] = ld16(wb + kWB + frag32(2 * wm + c, 2 * half + q));
   }
 }
 
-// The K loop of one wave (its weight share is one page of format B): the
-// registers for stage s + 1 are fetched before stage s is computed and written
-// to the other buffer after it; one barrier per stage.
+template <int ACT>
+__device__ __forceinline__ void ops_mma(const Ops& o, f32x16 (&acc)[4][2]) {
+#pragma unroll
+  for (int q = 0; q < 2; ++q)
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int c = 0; c < 2; ++c) acc[r][c] = mma32<ACT>(o.a[q][r], o.b[q][c], acc[r][c]);
+}
+
+// Wait for this wave's LDS operations, then a workgroup barrier. There is no
+// memory fence: the global loads of later stages stay in flight across it.
+__device__ __forceinline__ void lds_sync() {
+  __builtin_amdgcn_sched_barrier(0);
+  __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+// The K loop of one wave (its weight share is one page of format B). Per
+// stage s, in barrier intervals:
+//   MMA(s, first half) | stage s+1 -> LDS, loads of stage s+2 issued,
+//   operands of (s, second half) read | MMA(s, second half) | operands of
+//   (s+1, first half) read.
+// The wn = 1 half passes one extra barrier before its loop and the wn = 0 half
+// one after, so the two halves alternate and every wave passes the same
+// number of barriers. Stage s+1 is written into the buffer of stage s-1 two
+// intervals after that buffer's last read, and first read two intervals
+// after its last write.
 template <int ACT, int SDT, int B>
 __device__ __forceinline__ void tile_loop(uint8_t* lds, const uint8_t* tile0, const uint8_t* szrow,
                                           const uint8_t* const (&xrow)[2], int nkb, int R, int G, int wave,
-                                          f32x4 (&acc)[8][4]) {
-  const int wn = wave >> 2, wm = wave & 3;
+                                          int wn, int wm, f32x16 (&acc)[4][2]) {
 #pragma unroll
-  for (int t = 0; t < 8; ++t)
+  for (int r = 0; r < 4; ++r)
 #pragma unroll
-    for (int u = 0; u < 4; ++u) acc[t][u] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[r][c][e] = 0.0f;
   const int nstage = nkb * 128 / kTK;
   auto group_of = [&](int st) { return G == 64 ? st : (st * kTK) / G; };
   WStage<B> ws;
   XStage xs;
+  Ops op;
   w_fetch<B>(ws, tile0, szrow, 0, 0, group_of(0), nkb, R);
   x_fetch(xs, xrow, 0);
   stage_store<ACT, SDT, B>(ws, xs, lds, wave);
-  __syncthreads();
-  for (int st = 0; st < nstage; ++st) {
-    uint8_t* cur = lds + (st & 1) * kSB;
-    uint8_t* nxt = lds + ((st + 1) & 1) * kSB;
-    const bool more = st + 1 < nstage;
-    if (more) {
-      const int s1 = st + 1;
-      w_fetch<B>(ws, tile0, szrow, s1 >> 1, s1 & 1, group_of(s1), nkb, R);
-      x_fetch(xs, xrow, s1 * kTK);
-    }
-    stage_mma<ACT>(cur, wn, wm, acc);
-    if (more) stage_store<ACT, SDT, B>(ws, xs, nxt, wave);
-    __syncthreads();
+  if (nstage > 1) {
+    w_fetch<B>(ws, tile0, szrow, 0, 1, group_of(1), nkb, R);
+    x_fetch(xs, xrow, kTK);
   }
+  lds_sync();
+  ops_read(op, lds, wn, wm, 0);
+  if (wn == 1) lds_sync();
+  for (int st = 0; st < nstage; ++st) {
+    const uint8_t* cur = lds + (st & 1) * kSB;
+    uint8_t* nxt = lds + ((st + 1) & 1) * kSB;
+    ops_mma<ACT>(op, acc);
+    lds_sync();
+    if (st + 1 < nstage) {
+      stage_store<ACT, SDT, B>(ws, xs, nxt, wave);
+      if (st + 2 < nstage) {
+        const int s2 = st + 2;
+        w_fetch<B>(ws, tile0, szrow, s2 >> 1, s2 & 1, group_of(s2), nkb, R);
+        x_fetch(xs, xrow, s2 * kTK);
+      }
+    }
+    ops_read(op, cur, wn, wm, 1);
+    lds_sync();
+    ops_mma<ACT>(op, acc);
+    lds_sync();
+    if (st + 1 < nstage) ops_read(op, nxt, wn, wm, 0);
+    lds_sync();
+  }
+  if (wn == 0) lds_sync();
 }
+
 
 // Maps a tile index to (expert, first slot) from the routing offsets.
 __device__ __forceinline__ bool tile_expert(const GemmArgs& a, int mt, int* e_out, int* off_e, int* n_e, int* m0) {
@@ -267,6 +332,7 @@ __device__ __forceinline__ bool tile_expert(const GemmArgs& a, int mt, int* e_ou
 template <int ACT, int SDT, bool GATEUP>
 __global__ __launch_bounds__(kThreads) void k_tgemm(const GemmArgs a, int nblk, int mtmax) {
   __shared__ __attribute__((aligned(16))) uint8_t lds[2 * kSB];
+  __shared__ int simd_of[kWaves];
   // XCD-aware order: each XCD takes a contiguous range of tiles; inside it,
   // bands of kGN weight blocks step the weight block first, so the workgroups
   // resident on an XCD share both weight and slot tiles in its L2.
@@ -278,8 +344,29 @@ __global__ __launch_bounds__(kThreads) void k_tgemm(const GemmArgs a, int nblk, 
   int e, off_e, n_e, m0;
   if (!tile_expert(a, mt, &e, &off_e, &n_e, &m0)) return;
 
-  const int wave = threadIdx.x >> 6, lane = lane_id(), lc = lane & 15, lg = lane >> 4;
-  const int wn = wave >> 2, wm = wave & 3;
+  const int wave = threadIdx.x >> 6, lane = lane_id(), lc = lane & 15;
+  // Compute roles: the two waves of a SIMD take wn = 0 and wn = 1 (their rank
+  // on the SIMD) and wm = the SIMD, so each SIMD holds one wave of each
+  // ping-pong half whatever the wave placement. If a SIMD does not hold
+  // exactly two waves, roles follow the wave index. Either way each role is
+  // taken once; staging duties follow the wave index.
+  if (lane == 0) simd_of[wave] = static_cast<int>(__builtin_amdgcn_s_getreg(kHwRegSimdId));
+  __syncthreads();
+  int wn = wave >> 2, wm = wave & 3;
+  {
+    const int mine = simd_of[wave];
+    int cnt[4] = {0, 0, 0, 0}, rank = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      const int sw = simd_of[w] & 3;
+      cnt[sw] += 1;
+      rank += (w < wave && sw == mine) ? 1 : 0;
+    }
+    if (cnt[0] == 2 && cnt[1] == 2 && cnt[2] == 2 && cnt[3] == 2) {
+      wn = rank;
+      wm = mine & 3;
+    }
+  }
   const int K = GATEUP ? a.H : a.F;
   const int R = a.R;
   // this wave's 32 weight rows for the staging loader
@@ -312,51 +399,70 @@ __global__ __launch_bounds__(kThreads) void k_tgemm(const GemmArgs a, int nblk, 
 
   // The host checks that every page is present, so bits is 16, 8 or 4 here; a
   // wave never leaves early (the loop's barriers need all eight).
-  f32x4 acc[8][4];
+  f32x16 acc[4][2];
+  // The down kernel keeps its accumulators in AGPRs (the MFMA's C/D operands
+  // then leave the VGPR file to the staging wave of the same SIMD): naming an
+  // AGPR in an empty asm statement makes the compiler pick that MFMA form.
+  // It fits two waves per SIMD there (about 100 VGPRs + 128 AGPRs); the
+  // gate/up kernel would not, and keeps the VGPR form.
+  if constexpr (!GATEUP) asm volatile("" ::: "a0");
   const int nkb = K / 128;
-  if (bits == 16) tile_loop<ACT, SDT, 16>(lds, tile0, szrow, xrow, nkb, R, a.G, wave, acc);
-  else if (bits == 8) tile_loop<ACT, SDT, 8>(lds, tile0, szrow, xrow, nkb, R, a.G, wave, acc);
-  else tile_loop<ACT, SDT, 4>(lds, tile0, szrow, xrow, nkb, R, a.G, wave, acc);
+  if (bits == 16) tile_loop<ACT, SDT, 16>(lds, tile0, szrow, xrow, nkb, R, a.G, wave, wn, wm, acc);
+  else if (bits == 8) tile_loop<ACT, SDT, 8>(lds, tile0, szrow, xrow, nkb, R, a.G, wave, wn, wm, acc);
+  else tile_loop<ACT, SDT, 4>(lds, tile0, szrow, xrow, nkb, R, a.G, wave, wn, wm, acc);
 
+  // Accumulator element 4 q + r of tile (rt, ct) is row 32 rt + 8 q + 4 (lane / 32)
+  // + r of the wave's 128 rows, slot 32 ct + lane mod 32 of its 64 slots.
+  const int rsub = 4 * (lane >> 5), msub = lane & 31;
   if (GATEUP) {
     // gate waves (wn = 0) hand their 128 x 64 accumulators to the up wave of
-    // the same slots through LDS (free after the loop's last barrier)
-    float* xch = reinterpret_cast<float*>(lds) + wm * (8 * 4 * 64 * 4);
+    // the same slots through LDS (free once every wave has left the loop)
+    f32x4* xch = reinterpret_cast<f32x4*>(lds) + wm * (4 * 2 * 4 * 64);
     if (wn == 0) {
 #pragma unroll
-      for (int t = 0; t < 8; ++t)
+      for (int rt = 0; rt < 4; ++rt)
 #pragma unroll
-        for (int u = 0; u < 4; ++u) *reinterpret_cast<f32x4*>(xch + ((t * 4 + u) * 64 + lane) * 4) = acc[t][u];
+        for (int ct = 0; ct < 2; ++ct)
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            xch[((rt * 2 + ct) * 4 + q) * 64 + lane] =
+                f32x4{acc[rt][ct][4 * q], acc[rt][ct][4 * q + 1], acc[rt][ct][4 * q + 2], acc[rt][ct][4 * q + 3]};
     }
     __syncthreads();
     if (wn == 1) {
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int m = m0 + wm * 64 + u * 16 + lc;
+      for (int ct = 0; ct < 2; ++ct) {
+        const int m = m0 + wm * 64 + ct * 32 + msub;
         if (m < n_e) {
 #pragma unroll
-          for (int t = 0; t < 8; ++t) {
-            const f32x4 g = *reinterpret_cast<const f32x4*>(xch + ((t * 4 + u) * 64 + lane) * 4);
-            uint32_t hv[4];
+          for (int rt = 0; rt < 4; ++rt)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) hv[r] = rne16(g[r] / (1.0f + expf(-g[r])) * acc[t][u][r], ACT);
-            u32x2 o;
-            o[0] = hv[0] | (hv[1] << 16);
-            o[1] = hv[2] | (hv[3] << 16);
-            *reinterpret_cast<u32x2*>(a.h + static_cast<size_t>(off_e + m) * a.F + nb * 128 + t * 16 + 4 * lg) = o;
-          }
+            for (int q = 0; q < 4; ++q) {
+              const f32x4 g = xch[((rt * 2 + ct) * 4 + q) * 64 + lane];
+              uint32_t hv[4];
+#pragma unroll
+              for (int r = 0; r < 4; ++r) hv[r] = rne16(g[r] / (1.0f + expf(-g[r])) * acc[rt][ct][4 * q + r], ACT);
+              u32x2 o;
+              o[0] = hv[0] | (hv[1] << 16);
+              o[1] = hv[2] | (hv[3] << 16);
+              *reinterpret_cast<u32x2*>(a.h + static_cast<size_t>(off_e + m) * a.F + nb * 128 + rt * 32 + q * 8 +
+                                        rsub) = o;
+            }
         }
       }
     }
   } else {
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int m = m0 + wm * 64 + u * 16 + lc;
+    for (int ct = 0; ct < 2; ++ct) {
+      const int m = m0 + wm * 64 + ct * 32 + msub;
       if (m < n_e) {
 #pragma unroll
-        for (int t = 0; t < 8; ++t)
-          *reinterpret_cast<f32x4*>(a.opart + static_cast<size_t>(off_e + m) * a.H + nb * 256 + wn * 128 + t * 16 +
-                                    4 * lg) = acc[t][u];
+        for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            *reinterpret_cast<f32x4*>(a.opart + static_cast<size_t>(off_e + m) * a.H + nb * 256 + wn * 128 +
+                                      rt * 32 + q * 8 + rsub) =
+                f32x4{acc[rt][ct][4 * q], acc[rt][ct][4 * q + 1], acc[rt][ct][4 * q + 2], acc[rt][ct][4 * q + 3]};
       }
     }
   }
