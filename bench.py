@@ -85,6 +85,7 @@ def time_steps(L, cfg, x, logits, steps, warmup):
     replay's output is checked bit-exact against the eager step. L may be a
     list of layers holding the same pages in separate pools: step i then runs
     on layer i mod len(L), so that no step finds another's weights in a cache."""
+    import numpy as np
     import torch
     from paper_2607_16184_amd import pw
     from paper_2607_16184_amd.layer import PagedLayer
@@ -147,14 +148,17 @@ def time_steps(L, cfg, x, logits, steps, warmup):
             if not torch.equal(y, y_eager):
                 raise RuntimeError("graph replay differs from the eager step")
         torch.cuda.synchronize()
-        ev0.record()
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+        evs[0].record()
         for i in range(steps):
             graphs[i % len(graphs)].replay()
-        ev1.record()
+            evs[i + 1].record()
         torch.cuda.synchronize()
         if not torch.equal(y, y_eager):
             raise RuntimeError("graph replay differs from the eager step")
-        out["event_ms"] = ev0.elapsed_time(ev1) / steps
+        out["event_ms"] = evs[0].elapsed_time(evs[-1]) / steps
+        per = sorted(evs[i].elapsed_time(evs[i + 1]) for i in range(steps))
+        out["step_ms_p10_p50_p90"] = [round(float(np.percentile(per, q)), 4) for q in (10, 50, 90)]
         out["graph"] = True
     except Exception as exc:                          # report eager timing instead
         log("graph timing unavailable (%s); reporting eager steps" % exc)
@@ -225,6 +229,7 @@ def leg_layer(name, steps, warmup, pools=1):
             "pools_rotated": pools,
             "eager_ms_per_step": round(r["eager_ms"], 4),
             "step_timing": "hip_graph_replay" if r["graph"] else "eager",
+            "step_ms_p10_p50_p90": r.get("step_ms_p10_p50_p90"),
             "weight_GBps_per_step": round(wb / (r["event_ms"] * 1e-3) / 1e9, 1),
             "gateup_ms": round(km["gateup"], 4), "down_ms": round(km["down"], 4),
             "combine_ms": round(km["combine"], 4),
@@ -698,6 +703,7 @@ def main():
             "wall_ms_per_step_eager": round(r["wall_ms"], 4),
             "eager_ms_per_step": round(r["eager_ms"], 4),
             "step_timing": "hip_graph_replay" if r["graph"] else "eager",
+            "step_ms_p10_p50_p90": r.get("step_ms_p10_p50_p90"),
         },
     }
     if not args.no_cpu_baseline:
@@ -708,11 +714,11 @@ def main():
     for leg in [e for e in args.extras.split(",") if e]:
         t0 = time.time()
         if leg == "prefill":
-            extras["prefill"] = leg_layer("mixtral_prefill", steps=5, warmup=1)
+            extras["prefill"] = leg_layer("mixtral_prefill", steps=20, warmup=2)
         elif leg == "finegrained":
             # 0.57 GB of weights: three pools in turn, so no step reads the
             # previous step's weights from the 256 MB last-level cache
-            extras["finegrained"] = leg_layer("finegrained", steps=21, warmup=3, pools=3)
+            extras["finegrained"] = leg_layer("finegrained", steps=51, warmup=3, pools=3)
         elif leg == "downshift":
             extras["downshift"] = leg_downshift()
         elif leg == "offload":
