@@ -198,22 +198,26 @@ __device__ __forceinline__ void load_slot(Slot<B, GK, RT>& sl, const PageRows& p
 // values): thread tid stages the 16-byte pieces q = tid + 256 j, i.e. row
 // q / kPieces, piece q % kPieces. rowoff[j] are byte offsets of its rows.
 constexpr int kPieces = kCK * 128 / 8;            // 16-byte pieces per row
-constexpr int kRowsPerPass = 256 / kPieces;
-template <int NT> constexpr int x_passes() { return NT * 16 / kRowsPerPass; }
-__device__ __forceinline__ int x_row(int j) { return static_cast<int>(threadIdx.x) / kPieces + kRowsPerPass * j; }
+// NW waves per workgroup stage a chunk together: rows per pass and passes.
+template <int NW> constexpr int rows_per_pass() { return 64 * NW / kPieces; }
+template <int NT, int NW> constexpr int x_passes() { return NT * 16 / rows_per_pass<NW>(); }
+template <int NW>
+__device__ __forceinline__ int x_row(int j) {
+  return static_cast<int>(threadIdx.x) / kPieces + rows_per_pass<NW>() * j;
+}
 
-template <int NT>
+template <int NT, int NW>
 struct XStage {
-  u32x4 v[x_passes<NT>()];
+  u32x4 v[x_passes<NT, NW>()];
 };
 
-template <int NT>
-__device__ __forceinline__ void x_fetch(XStage<NT>& s, const uint8_t* base, const uint32_t (&rowoff)[x_passes<NT>()],
-                                        int kel, int K) {
+template <int NT, int NW>
+__device__ __forceinline__ void x_fetch(XStage<NT, NW>& s, const uint8_t* base,
+                                        const uint32_t (&rowoff)[x_passes<NT, NW>()], int kel, int K) {
   const int col = (threadIdx.x % kPieces) * 8;
   const int k = min(kel + col, K - 8);
 #pragma unroll
-  for (int j = 0; j < x_passes<NT>(); ++j) s.v[j] = ld16(base + rowoff[j] + static_cast<size_t>(k) * 2);
+  for (int j = 0; j < x_passes<NT, NW>(); ++j) s.v[j] = ld16(base + rowoff[j] + static_cast<size_t>(k) * 2);
 }
 
 // Sum of the eight 16-bit values of a piece: four dot products with (1, 1).
@@ -254,18 +258,18 @@ __device__ __forceinline__ float sum8(float v) {
 // Writes the staged rows and, when a quantized page reads them, per row the
 // sums of each 64-value half block (8 consecutive pieces held by 8
 // consecutive lanes).
-template <int ACT, int NT>
-__device__ __forceinline__ void x_store(const XStage<NT>& s, uint8_t* buf, bool sums) {
+template <int ACT, int NT, int NW>
+__device__ __forceinline__ void x_store(const XStage<NT, NW>& s, uint8_t* buf, bool sums) {
   const int col = threadIdx.x % kPieces;
 #pragma unroll
-  for (int j = 0; j < x_passes<NT>(); ++j)
-    *reinterpret_cast<u32x4*>(buf + x_row(j) * kXRow + col * 16) = s.v[j];
+  for (int j = 0; j < x_passes<NT, NW>(); ++j)
+    *reinterpret_cast<u32x4*>(buf + x_row<NW>(j) * kXRow + col * 16) = s.v[j];
   if (sums) {
     float* hs = reinterpret_cast<float*>(buf + NT * 16 * kXRow);
 #pragma unroll
-    for (int j = 0; j < x_passes<NT>(); ++j) {
+    for (int j = 0; j < x_passes<NT, NW>(); ++j) {
       const float acc = sum8(piece_sum<ACT>(s.v[j]));
-      if ((col & 7) == 0) hs[x_row(j) * (2 * kCK) + (col >> 3)] = acc;
+      if ((col & 7) == 0) hs[x_row<NW>(j) * (2 * kCK) + (col >> 3)] = acc;
     }
   }
 }
@@ -344,8 +348,8 @@ __device__ __forceinline__ void compute_block(const Slot<B, GK, RT>& sl, const u
 // | barrier. Every load is unconditional (addresses clamped to the range), so
 // all wait counts are static; the workgroup passes nchunk - 1 barriers here.
 // `sums`: some wave of the workgroup reads a quantized page (workgroup-uniform).
-template <int ACT, int SDT, int B, int NT, int GK, int RT>
-__device__ void wave_gemm(uint8_t* lds, const uint8_t* xbase, const uint32_t (&rowoff)[x_passes<NT>()], int K,
+template <int ACT, int SDT, int B, int NT, int GK, int RT, int NW>
+__device__ void wave_gemm(uint8_t* lds, const uint8_t* xbase, const uint32_t (&rowoff)[x_passes<NT, NW>()], int K,
                           const PageRows& pr, int kb0, int kb1, bool sums, f32x4 (&acc)[RT][NT]) {
   constexpr int W = window<B, RT>();
   static_assert(W % kCK == 0, "window must cover whole chunks");
@@ -364,11 +368,11 @@ __device__ void wave_gemm(uint8_t* lds, const uint8_t* xbase, const uint32_t (&r
     xs[t] = 0.0f;
   }
   Slot<B, GK, RT> win[W];
-  XStage<NT> xr;
-  x_fetch<NT>(xr, xbase, rowoff, kb0 * 128, K);
+  XStage<NT, NW> xr;
+  x_fetch<NT, NW>(xr, xbase, rowoff, kb0 * 128, K);
 #pragma unroll
   for (int j = 0; j < W; ++j) load_slot<B, GK, RT>(win[j], pr, min(kb0 + j, kmax));
-  x_store<ACT, NT>(xr, lds, sums);
+  x_store<ACT, NT, NW>(xr, lds, sums);
   lds_barrier();
   for (int base = 0; base < nkb; base += W) {
 #pragma unroll
@@ -376,14 +380,14 @@ __device__ void wave_gemm(uint8_t* lds, const uint8_t* xbase, const uint32_t (&r
       const int b = base + j;                       // block index within the range
       const int c = b / kCK;                        // chunk
       uint8_t* buf = lds + (c & 1) * xbuf_bytes<NT>();
-      if (j % kCK == 0) x_fetch<NT>(xr, xbase, rowoff, (kb0 + (c + 1) * kCK) * 128, K);
+      if (j % kCK == 0) x_fetch<NT, NW>(xr, xbase, rowoff, (kb0 + (c + 1) * kCK) * 128, K);
       if (b < nkb)
         compute_block<ACT, SDT, B, NT, GK, RT>(win[j], buf + (b % kCK) * 256,
                                            reinterpret_cast<const float*>(buf + NT * 16 * kXRow), 2 * (b % kCK),
                                            ((kb0 + b + 1) & gmask) == 0, magic, acc, p, xs);
       load_slot<B, GK, RT>(win[j], pr, min(kb0 + b + W, kmax));
       if (j % kCK == kCK - 1 && c + 1 < nchunk) {
-        x_store<ACT, NT>(xr, lds + ((c + 1) & 1) * xbuf_bytes<NT>(), sums);
+        x_store<ACT, NT, NW>(xr, lds + ((c + 1) & 1) * xbuf_bytes<NT>(), sums);
         lds_barrier();
       }
       __builtin_amdgcn_sched_barrier(0);
@@ -413,61 +417,67 @@ __device__ __forceinline__ PageRows page_rows(const GemmArgs& a, const pw_page_e
 
 // The wave's page in format B (16, 8 or 4), or B = 0: in the format its
 // table entry names, chosen here.
-template <int ACT, int SDT, int B, int NT, int GK, int RT>
+template <int ACT, int SDT, int B, int NT, int GK, int RT, int NW>
 __device__ __forceinline__ void page_gemm(const GemmArgs& a, const pw_page_entry& ent, int lr0, int K, uint8_t* lds,
-                                          const uint8_t* xbase, const uint32_t (&rowoff)[x_passes<NT>()], int kb0,
+                                          const uint8_t* xbase, const uint32_t (&rowoff)[x_passes<NT, NW>()], int kb0,
                                           int kb1, bool sums, f32x4 (&acc)[RT][NT]) {
   if constexpr (B != 0) {
-    wave_gemm<ACT, SDT, B, NT, GK, RT>(lds, xbase, rowoff, K, page_rows<B>(a, ent, lr0, K), kb0, kb1, sums, acc);
+    wave_gemm<ACT, SDT, B, NT, GK, RT, NW>(lds, xbase, rowoff, K, page_rows<B>(a, ent, lr0, K), kb0, kb1, sums, acc);
   } else {
     const int code = fmt_code(ent.bits);
     if (code == 0)
-      wave_gemm<ACT, SDT, 16, NT, GK, RT>(lds, xbase, rowoff, K, page_rows<16>(a, ent, lr0, K), kb0, kb1, sums, acc);
+      wave_gemm<ACT, SDT, 16, NT, GK, RT, NW>(lds, xbase, rowoff, K, page_rows<16>(a, ent, lr0, K), kb0, kb1, sums,
+                                              acc);
     else if (code == 1)
-      wave_gemm<ACT, SDT, 8, NT, GK, RT>(lds, xbase, rowoff, K, page_rows<8>(a, ent, lr0, K), kb0, kb1, sums, acc);
+      wave_gemm<ACT, SDT, 8, NT, GK, RT, NW>(lds, xbase, rowoff, K, page_rows<8>(a, ent, lr0, K), kb0, kb1, sums,
+                                             acc);
     else
-      wave_gemm<ACT, SDT, 4, NT, GK, RT>(lds, xbase, rowoff, K, page_rows<4>(a, ent, lr0, K), kb0, kb1, sums, acc);
+      wave_gemm<ACT, SDT, 4, NT, GK, RT, NW>(lds, xbase, rowoff, K, page_rows<4>(a, ent, lr0, K), kb0, kb1, sums,
+                                             acc);
   }
 }
 
 // ---------------------------------------------------------------------------
-// gate/up: a workgroup covers 32 RT rows of gate and the same rows of up for
-// one expert; waves 0-1 stream gate, waves 2-3 stream up (16 RT rows each,
-// each projection in its own page format); the SwiGLU output h = silu(g) * u
-// meets through LDS.
+// gate/up: a workgroup of NW waves covers 8 RT NW rows of gate and the same
+// rows of up for one expert; the first NW / 2 waves stream gate, the others
+// up (16 RT rows each, each wave in its own page's format); the SwiGLU output
+// h = silu(g) * u meets through LDS. NW = 8 at four slot tiles (each staged
+// activation chunk then serves twice the weight rows), else 4.
 // ---------------------------------------------------------------------------
 
-template <int RT> constexpr int gu_rows() { return 32 * RT; }     // gate (and up) rows per workgroup
-template <int RT> constexpr int dn_rows() { return 64 * RT; }     // down rows per workgroup
+template <int RT, int NW> constexpr int gu_rows() { return 8 * RT * NW; }    // gate (and up) rows per workgroup
+template <int RT, int NW> constexpr int dn_rows() { return 16 * RT * NW; }   // down rows per workgroup
 
-// [2 waves][RT][NT][64 lanes] f32x4 of the gate waves, in the activation
+// [NW / 2 waves][RT][NT][64 lanes] f32x4 of the gate waves, in the activation
 // buffers once every wave has finished its K loop.
-template <int NT, int RT>
-constexpr int xch_bytes() { return 2 * RT * NT * 64 * 16; }
-template <int NT, int RT>
-constexpr int gu_lds_bytes() { return lds_x_bytes<NT>() > xch_bytes<NT, RT>() ? lds_x_bytes<NT>() : xch_bytes<NT, RT>(); }
+template <int NT, int RT, int NW>
+constexpr int xch_bytes() { return NW / 2 * RT * NT * 64 * 16; }
+template <int NT, int RT, int NW>
+constexpr int gu_lds_bytes() {
+  return lds_x_bytes<NT>() > xch_bytes<NT, RT, NW>() ? lds_x_bytes<NT>() : xch_bytes<NT, RT, NW>();
+}
 
-template <int ACT, int SDT, int B, int NT, int GK, int RT>
+template <int ACT, int SDT, int B, int NT, int GK, int RT, int NW>
 __device__ void gateup_unit(const GemmArgs& a, uint8_t* lds, int e, int off_e, int n_e, int unit, bool sums) {
   const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
   const int lane = lane_id(), lc = lane & 15, lg = lane >> 4;
-  const int proj = wave >> 1, wsub = wave & 1;
-  const int f0 = unit * gu_rows<RT>() + 16 * RT * wsub;   // the wave's first row
+  const int proj = wave / (NW / 2), wsub = wave % (NW / 2);
+  const int f0 = unit * gu_rows<RT, NW>() + 16 * RT * wsub;   // the wave's first row
   const int rb = f0 / a.R, lr0 = f0 - rb * a.R;
   const pw_page_entry ent = a.table[(static_cast<size_t>(e) * 3 + proj) * a.nrb_max + rb];
   const int H = a.H;
   f32x4* xch = reinterpret_cast<f32x4*>(lds);
   for (int mb = 0; mb < n_e; mb += NT * 16) {
     const uint8_t* xbase = reinterpret_cast<const uint8_t*>(a.x);
-    uint32_t rowoff[x_passes<NT>()];
+    uint32_t rowoff[x_passes<NT, NW>()];
 #pragma unroll
-    for (int j = 0; j < x_passes<NT>(); ++j) {
-      const int m = clampi(mb + x_row(j), 0, n_e - 1);
+    for (int j = 0; j < x_passes<NT, NW>(); ++j) {
+      const int m = clampi(mb + x_row<NW>(j), 0, n_e - 1);
       const int slot = clampi(a.sorted_slot[off_e + m], 0, a.S - 1);
       rowoff[j] = static_cast<uint32_t>(slot / a.topk) * static_cast<uint32_t>(H * 2);
     }
     f32x4 acc[RT][NT];
-    page_gemm<ACT, SDT, B, NT, GK, RT>(a, ent, lr0, H, lds, xbase, rowoff, 0, H / 128, sums, acc);
+    page_gemm<ACT, SDT, B, NT, GK, RT, NW>(a, ent, lr0, H, lds, xbase, rowoff, 0, H / 128, sums, acc);
     lds_barrier();   // every wave is done with the activation buffers
     if (proj == 0) {
 #pragma unroll
@@ -502,68 +512,74 @@ __device__ void gateup_unit(const GemmArgs& a, uint8_t* lds, int e, int off_e, i
 // RT = 1: one code body that picks the format inside; RT = 2: each wave runs
 // the whole unit in its own page's format (every format passes the same
 // barriers), which keeps the register allocations of the three apart.
-template <int ACT, int SDT, int NT, int GK, int RT>
+template <int ACT, int SDT, int NT, int GK, int RT, int NW>
 __device__ __forceinline__ void gateup_any(int code, const GemmArgs& a, uint8_t* lds, int e, int off_e, int n_e,
                                            int unit, bool sums) {
   if constexpr (RT == 1) {
-    gateup_unit<ACT, SDT, 0, NT, GK, RT>(a, lds, e, off_e, n_e, unit, sums);
+    gateup_unit<ACT, SDT, 0, NT, GK, RT, NW>(a, lds, e, off_e, n_e, unit, sums);
   } else {
-    if (code == 0) gateup_unit<ACT, SDT, 16, NT, GK, RT>(a, lds, e, off_e, n_e, unit, sums);
-    else if (code == 1) gateup_unit<ACT, SDT, 8, NT, GK, RT>(a, lds, e, off_e, n_e, unit, sums);
-    else gateup_unit<ACT, SDT, 4, NT, GK, RT>(a, lds, e, off_e, n_e, unit, sums);
+    if (code == 0) gateup_unit<ACT, SDT, 16, NT, GK, RT, NW>(a, lds, e, off_e, n_e, unit, sums);
+    else if (code == 1) gateup_unit<ACT, SDT, 8, NT, GK, RT, NW>(a, lds, e, off_e, n_e, unit, sums);
+    else gateup_unit<ACT, SDT, 4, NT, GK, RT, NW>(a, lds, e, off_e, n_e, unit, sums);
   }
 }
 
 // NTMAX slot tiles per pass (1, 2 or 4); experts with fewer slots take fewer.
-template <int ACT, int SDT, int NTMAX, int GK>
-__global__ __launch_bounds__(256) void k_gateup(const GemmArgs a) {
+template <int ACT, int SDT, int NTMAX, int GK, int NW>
+__global__ __launch_bounds__(64 * NW) void k_gateup(const GemmArgs a) {
   constexpr int RT = row_tiles<NTMAX>();
-  __shared__ __attribute__((aligned(16))) uint8_t lds[gu_lds_bytes<NTMAX, RT>()];
-  const int upe = a.F / gu_rows<RT>();
+  constexpr int GU = gu_rows<RT, NW>();
+  __shared__ __attribute__((aligned(16))) uint8_t lds[gu_lds_bytes<NTMAX, RT, NW>()];
+  const int upe = a.F / GU;
   const int e = blockIdx.x / upe, unit = blockIdx.x % upe;
   const int off_e = clampi(a.offsets[e], 0, a.S);
   const int n_e = clampi(a.offsets[e + 1], off_e, a.S) - off_e;
   if (n_e <= 0) return;
-  // every page of the unit must be present; otherwise the whole group returns
-  // (a unit of at most 64 rows lies inside one page: R is a multiple of 64)
-  const int rb = (unit * gu_rows<RT>()) / a.R;
-  const int cg = fmt_code(a.table[(static_cast<size_t>(e) * 3 + PW_GATE) * a.nrb_max + rb].bits);
-  const int cu = fmt_code(a.table[(static_cast<size_t>(e) * 3 + PW_UP) * a.nrb_max + rb].bits);
-  if (cg < 0 || cu < 0) return;
-  const bool sums = cg != 0 || cu != 0;
-  const int code = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 7) == 0 ? cg : cu;
-  if (NTMAX == 1 || n_e <= 16) gateup_any<ACT, SDT, 1, GK, RT>(code, a, lds, e, off_e, n_e, unit, sums);
-  else if (NTMAX == 2 || n_e <= 32) gateup_any<ACT, SDT, 2, GK, RT>(code, a, lds, e, off_e, n_e, unit, sums);
-  else gateup_any<ACT, SDT, (NTMAX > 2 ? NTMAX : 2), GK, RT>(code, a, lds, e, off_e, n_e, unit, sums);
+  // every page of the unit (one, or several when it spans pages) must be
+  // present; otherwise the whole group returns
+  bool sums = false;
+  for (int rb = (unit * GU) / a.R; rb <= (unit * GU + GU - 1) / a.R; ++rb) {
+    const int cg = fmt_code(a.table[(static_cast<size_t>(e) * 3 + PW_GATE) * a.nrb_max + rb].bits);
+    const int cu = fmt_code(a.table[(static_cast<size_t>(e) * 3 + PW_UP) * a.nrb_max + rb].bits);
+    if (cg < 0 || cu < 0) return;
+    sums = sums || cg != 0 || cu != 0;
+  }
+  // the format of this wave's own page (its 16 RT rows lie inside one page)
+  const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
+  const int proj = wave / (NW / 2), f0 = unit * GU + 16 * RT * (wave % (NW / 2));
+  const int code = fmt_code(a.table[(static_cast<size_t>(e) * 3 + proj) * a.nrb_max + f0 / a.R].bits);
+  if (NTMAX == 1 || n_e <= 16) gateup_any<ACT, SDT, 1, GK, RT, NW>(code, a, lds, e, off_e, n_e, unit, sums);
+  else if (NTMAX == 2 || n_e <= 32) gateup_any<ACT, SDT, 2, GK, RT, NW>(code, a, lds, e, off_e, n_e, unit, sums);
+  else gateup_any<ACT, SDT, (NTMAX > 2 ? NTMAX : 2), GK, RT, NW>(code, a, lds, e, off_e, n_e, unit, sums);
 }
 
 // ---------------------------------------------------------------------------
-// down: a workgroup covers 64 RT rows of the down projection (16 RT per wave;
-// one or two pages) over one K split of F; fp32 partial sums per split,
-// reduced by the combine.
+// down: a workgroup of NW waves covers 16 RT NW rows of the down projection
+// (16 RT per wave; one or more pages) over one K split of F; fp32 partial
+// sums per split, reduced by the combine.
 // ---------------------------------------------------------------------------
 
-template <int ACT, int SDT, int B, int NT, int GK, int RT>
+template <int ACT, int SDT, int B, int NT, int GK, int RT, int NW>
 __device__ void down_unit(const GemmArgs& a, uint8_t* lds, int e, int off_e, int n_e, int unit, int split,
                           bool sums) {
   const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
   const int lane = lane_id(), lc = lane & 15, lg = lane >> 4;
   const int F = a.F;
-  const int n0 = unit * dn_rows<RT>() + 16 * RT * wave;   // the wave's first row
+  const int n0 = unit * dn_rows<RT, NW>() + 16 * RT * wave;   // the wave's first row
   const int rb = n0 / a.R, lr0 = n0 - rb * a.R;
   const pw_page_entry ent = a.table[(static_cast<size_t>(e) * 3 + PW_DOWN) * a.nrb_max + rb];
   const int kb0 = split * a.kb_per_split;
   const int kb1 = min(F / 128, kb0 + a.kb_per_split);
   for (int mb = 0; mb < n_e; mb += NT * 16) {
     const uint8_t* xbase = reinterpret_cast<const uint8_t*>(a.h);
-    uint32_t rowoff[x_passes<NT>()];
+    uint32_t rowoff[x_passes<NT, NW>()];
 #pragma unroll
-    for (int j = 0; j < x_passes<NT>(); ++j) {
-      const int m = clampi(mb + x_row(j), 0, n_e - 1);
+    for (int j = 0; j < x_passes<NT, NW>(); ++j) {
+      const int m = clampi(mb + x_row<NW>(j), 0, n_e - 1);
       rowoff[j] = static_cast<uint32_t>(off_e + m) * static_cast<uint32_t>(F * 2);
     }
     f32x4 acc[RT][NT];
-    page_gemm<ACT, SDT, B, NT, GK, RT>(a, ent, lr0, F, lds, xbase, rowoff, kb0, kb1, sums, acc);
+    page_gemm<ACT, SDT, B, NT, GK, RT, NW>(a, ent, lr0, F, lds, xbase, rowoff, kb0, kb1, sums, acc);
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
       const int m = mb + 16 * t + lc;
@@ -579,23 +595,24 @@ __device__ void down_unit(const GemmArgs& a, uint8_t* lds, int e, int off_e, int
   }
 }
 
-template <int ACT, int SDT, int NT, int GK, int RT>
+template <int ACT, int SDT, int NT, int GK, int RT, int NW>
 __device__ __forceinline__ void down_any(int code, const GemmArgs& a, uint8_t* lds, int e, int off_e, int n_e,
                                          int unit, int split, bool sums) {
   if constexpr (RT == 1) {
-    down_unit<ACT, SDT, 0, NT, GK, RT>(a, lds, e, off_e, n_e, unit, split, sums);
+    down_unit<ACT, SDT, 0, NT, GK, RT, NW>(a, lds, e, off_e, n_e, unit, split, sums);
   } else {
-    if (code == 0) down_unit<ACT, SDT, 16, NT, GK, RT>(a, lds, e, off_e, n_e, unit, split, sums);
-    else if (code == 1) down_unit<ACT, SDT, 8, NT, GK, RT>(a, lds, e, off_e, n_e, unit, split, sums);
-    else down_unit<ACT, SDT, 4, NT, GK, RT>(a, lds, e, off_e, n_e, unit, split, sums);
+    if (code == 0) down_unit<ACT, SDT, 16, NT, GK, RT, NW>(a, lds, e, off_e, n_e, unit, split, sums);
+    else if (code == 1) down_unit<ACT, SDT, 8, NT, GK, RT, NW>(a, lds, e, off_e, n_e, unit, split, sums);
+    else down_unit<ACT, SDT, 4, NT, GK, RT, NW>(a, lds, e, off_e, n_e, unit, split, sums);
   }
 }
 
-template <int ACT, int SDT, int NTMAX, int GK>
-__global__ __launch_bounds__(256) void k_down(const GemmArgs a) {
+template <int ACT, int SDT, int NTMAX, int GK, int NW>
+__global__ __launch_bounds__(64 * NW) void k_down(const GemmArgs a) {
   constexpr int RT = row_tiles<NTMAX>();
+  constexpr int DN = dn_rows<RT, NW>();
   __shared__ __attribute__((aligned(16))) uint8_t lds[lds_x_bytes<NTMAX>()];
-  const int upe = a.H / dn_rows<RT>();
+  const int upe = a.H / DN;
   const int split = blockIdx.x % a.nsplit;
   const int rest = blockIdx.x / a.nsplit;
   const int e = rest / upe, unit = rest % upe;
@@ -605,26 +622,42 @@ __global__ __launch_bounds__(256) void k_down(const GemmArgs a) {
   if (split * a.kb_per_split >= a.F / 128) return;
   // every page of the unit (one, or two when the unit spans pages) must be present
   bool sums = false;
-  for (int rb = (unit * dn_rows<RT>()) / a.R; rb <= (unit * dn_rows<RT>() + dn_rows<RT>() - 1) / a.R; ++rb) {
+  for (int rb = (unit * DN) / a.R; rb <= (unit * DN + DN - 1) / a.R; ++rb) {
     const int c = fmt_code(a.table[(static_cast<size_t>(e) * 3 + PW_DOWN) * a.nrb_max + rb].bits);
     if (c < 0) return;
     sums = sums || c != 0;
   }
-  const int n0 = unit * dn_rows<RT>() + 16 * RT * __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
+  const int n0 = unit * DN + 16 * RT * __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
   const int code = fmt_code(a.table[(static_cast<size_t>(e) * 3 + PW_DOWN) * a.nrb_max + n0 / a.R].bits);
-  if (NTMAX == 1 || n_e <= 16) down_any<ACT, SDT, 1, GK, RT>(code, a, lds, e, off_e, n_e, unit, split, sums);
-  else if (NTMAX == 2 || n_e <= 32) down_any<ACT, SDT, 2, GK, RT>(code, a, lds, e, off_e, n_e, unit, split, sums);
-  else down_any<ACT, SDT, (NTMAX > 2 ? NTMAX : 2), GK, RT>(code, a, lds, e, off_e, n_e, unit, split, sums);
+  if (NTMAX == 1 || n_e <= 16) down_any<ACT, SDT, 1, GK, RT, NW>(code, a, lds, e, off_e, n_e, unit, split, sums);
+  else if (NTMAX == 2 || n_e <= 32)
+    down_any<ACT, SDT, 2, GK, RT, NW>(code, a, lds, e, off_e, n_e, unit, split, sums);
+  else down_any<ACT, SDT, (NTMAX > 2 ? NTMAX : 2), GK, RT, NW>(code, a, lds, e, off_e, n_e, unit, split, sums);
+}
+
+// Waves per workgroup: 8 at four slot tiles when the shapes divide into the
+// larger units, else 4.
+template <int NTMAX> constexpr int waves_for() { return NTMAX == 4 ? 8 : 4; }
+
+template <int ACT, int SDT, int GK, int NTMAX, int NW>
+void gemm_launch_nw(const GemmArgs& a, bool gateup, hipStream_t st) {
+  constexpr int RT = row_tiles<NTMAX>();
+  const dim3 block(64 * NW);
+  if (gateup)
+    hipLaunchKernelGGL((k_gateup<ACT, SDT, NTMAX, GK, NW>), dim3(a.E * (a.F / gu_rows<RT, NW>())), block, 0, st, a);
+  else
+    hipLaunchKernelGGL((k_down<ACT, SDT, NTMAX, GK, NW>), dim3(a.E * (a.H / dn_rows<RT, NW>()) * a.nsplit), block, 0,
+                       st, a);
 }
 
 template <int ACT, int SDT, int GK, int NTMAX>
 void gemm_launch_nt(const GemmArgs& a, bool gateup, hipStream_t st) {
   constexpr int RT = row_tiles<NTMAX>();
-  const dim3 block(256);
-  if (gateup)
-    hipLaunchKernelGGL((k_gateup<ACT, SDT, NTMAX, GK>), dim3(a.E * (a.F / gu_rows<RT>())), block, 0, st, a);
+  constexpr int NW = waves_for<NTMAX>();
+  if (NW != 4 && a.F % gu_rows<RT, NW>() == 0 && a.H % dn_rows<RT, NW>() == 0)
+    gemm_launch_nw<ACT, SDT, GK, NTMAX, NW>(a, gateup, st);
   else
-    hipLaunchKernelGGL((k_down<ACT, SDT, NTMAX, GK>), dim3(a.E * (a.H / dn_rows<RT>()) * a.nsplit), block, 0, st, a);
+    gemm_launch_nw<ACT, SDT, GK, NTMAX, 4>(a, gateup, st);
 }
 
 template <int ACT, int SDT, int GK>
