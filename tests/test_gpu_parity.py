@@ -280,13 +280,16 @@ def test_tiny_decode4_uniform_and_heavy_experts(b):
 # the down projection's K splits must hold whole groups) and scale/zero dtypes
 # other than the activation dtype, on each of the three GEMM paths: 16 tokens
 # (4 expected slots per expert) and 120 tokens (30: four slot tiles, two row
-# tiles per wave) decode, 300 the streaming GEMM, 1000 the tiled.
+# tiles per wave; 8-wave workgroups, or 4-wave ones when H = 384 does not
+# divide into 256-row down units) decode, 300 the streaming GEMM, 1000 the
+# tiled.
 @pytest.mark.parametrize("act,sdt,G,H,F,T", [
     (synth.BF16, synth.F16, 256, 256, 512, 16),
     (synth.F16, synth.BF16, 512, 512, 1024, 16),
     (synth.BF16, synth.F16, 128, 256, 512, 16),
     (synth.F16, synth.BF16, 128, 256, 512, 16),
     (synth.BF16, synth.F16, 256, 256, 512, 120),
+    (synth.BF16, synth.BF16, 128, 384, 512, 120),
     (synth.F16, synth.BF16, 256, 256, 512, 300),
     (synth.BF16, synth.F16, 512, 512, 1024, 1000),
 ])
