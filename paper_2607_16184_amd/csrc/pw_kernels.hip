@@ -384,6 +384,91 @@ __device__ __forceinline__ void q_rowreduce(float& lo0, float& hi0, float& lo1, 
   }
 }
 
+// Register-lean form of the one-block path (G <= 128): the block stays in
+// its loaded words and each value is widened again where it is used (the
+// group extremes, then the codes, each packed as soon as it is computed), so
+// no 32-value fp32 array is live and more waves fit on a SIMD. The values are
+// the same: a 16-bit value exactly, or fl32(z + c s).
+template <int ACT, int SDT, int SRC>
+__device__ __forceinline__ float q_elem(const QRaw& raw, int e) {
+  const int i = e >> 3, q = e & 7;
+  if constexpr (SRC == 16) {
+    const uint32_t w = raw.w[i][q >> 1];
+    return val16((q & 1) ? (w >> 16) : w, ACT);
+  } else {
+    uint32_t c;
+    if constexpr (SRC == 8) c = (raw.w[e >> 4][(e >> 2) & 3] >> (8 * (e & 3))) & 0xFFu;
+    else c = (raw.w[0][i] >> ((q & 1) ? 16 + 4 * (q >> 1) : 4 * (q >> 1))) & 15u;
+    const float s = val16(raw.sz[i], SDT), z = val16(raw.sz[i] >> 16, SDT);
+    return z + static_cast<float>(c) * s;   // c*s exact
+  }
+}
+
+template <int ACT, int SDT, int GK, int SRC>
+__device__ __forceinline__ void q_block(const QJob& job, const QJobBatch& b, const QRaw& raw, int tau, int blk, int lg,
+                                        int r, int Q) {
+  const int lane = lane_id();
+  const size_t tile = static_cast<size_t>(tau) * (job.K / 128) + blk;
+  if (job.dst_bits == 16) {          // layout transform of a 16-bit page
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      u32x4 o;
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        o[q] = rne16(q_elem<ACT, SDT, SRC>(raw, 8 * i + 2 * q), ACT) |
+               (rne16(q_elem<ACT, SDT, SRC>(raw, 8 * i + 2 * q + 1), ACT) << 16);
+      *reinterpret_cast<u32x4*>(job.dst + tile * 4096 + 1024 * i + 16 * lane) = o;
+    }
+    return;
+  }
+  float lo0 = __builtin_inff(), hi0 = -__builtin_inff(), lo1 = lo0, hi1 = hi0;
+#pragma unroll
+  for (int e = 0; e < 32; ++e) {
+    const float v = q_elem<ACT, SDT, SRC>(raw, e);
+    if (GK == kQG64 && e >= 16) {
+      lo1 = fminf(lo1, v);
+      hi1 = fmaxf(hi1, v);
+    } else {
+      lo0 = fminf(lo0, v);
+      hi0 = fmaxf(hi0, v);
+    }
+  }
+  q_rowreduce(lo0, hi0, lo1, hi1);
+  uint32_t sb0, zb0, sb1 = 0u, zb1 = 0u;
+  q_params<SDT>(lo0, hi0, Q, &sb0, &zb0);
+  if (GK == kQG64) q_params<SDT>(lo1, hi1, Q, &sb1, &zb1);
+  const QGroup g0 = q_group<SDT>(sb0, zb0), g1 = q_group<SDT>(sb1, zb1);
+  auto code = [&](int e) { return q_code(q_elem<ACT, SDT, SRC>(raw, e), (GK == kQG64 && e >= 16) ? g1 : g0, Q); };
+  if (job.dst_bits == 8) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      u32x4 o;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const int e = 16 * u + 4 * w;
+        o[w] = code(e) | (code(e + 1) << 8) | (code(e + 2) << 16) | (code(e + 3) << 24);
+      }
+      *reinterpret_cast<u32x4*>(job.dst + tile * 2048 + 1024 * u + 16 * lane) = o;
+    }
+  } else {
+    u32x4 o;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      uint32_t w = 0u;
+#pragma unroll
+      for (int t = 0; t < 4; ++t) w |= (code(8 * i + 2 * t) << (4 * t)) | (code(8 * i + 2 * t + 1) << (16 + 4 * t));
+      o[i] = w;
+    }
+    *reinterpret_cast<u32x4*>(job.dst + tile * 1024 + 16 * lane) = o;
+  }
+  if (lg == 0) {
+    const int gi = GK == kQG64 ? 2 * blk : blk;
+    *reinterpret_cast<uint32_t*>(job.dst_sz + (static_cast<size_t>(gi) * b.R + r) * 4) = sb0 | (zb0 << 16);
+    if (GK == kQG64)
+      *reinterpret_cast<uint32_t*>(job.dst_sz + (static_cast<size_t>(gi + 1) * b.R + r) * 4) = sb1 | (zb1 << 16);
+  }
+}
+
 // Work item -> (job j, 16-row tile tau, span sp of max(G, 128) values); job
 // j's items start at job[j].item_base.
 struct QItem {
@@ -405,7 +490,7 @@ __device__ __forceinline__ QItem q_item(const QJobBatch& b, uint32_t item, int s
 // inside one block): one block, quantized from registers in one pass. G > 128:
 // G / 128 blocks, two passes (the group's extremes, then the codes).
 template <int ACT, int SDT, int GK>
-__global__ __launch_bounds__(256) void k_qjobs(const QJobBatch b) {
+__device__ __forceinline__ void qjobs_item(const QJobBatch& b) {
   const uint32_t item = blockIdx.x * 4u + (threadIdx.x >> 6);
   if (item >= b.total_items) return;
   const int lane = lane_id(), lc = lane & 15, lg = lane >> 4;
@@ -416,28 +501,15 @@ __global__ __launch_bounds__(256) void k_qjobs(const QJobBatch b) {
   const int tau = it.tau, sp = it.sp;
   const int r = tau * 16 + lc;
   const int Q = (1 << job.dst_bits) - 1;
-  float v[32];
   if constexpr (GK != kQGBig) {
-    const int blk = sp;
-    q_read<ACT, SDT, GK>(job, b, tau, blk, v);
-    if (job.dst_bits == 16) {      // layout transform of a 16-bit page
-      q_store16<ACT>(job, tau, blk, v);
-      return;
-    }
-    float lo0 = __builtin_inff(), hi0 = -__builtin_inff(), lo1 = lo0, hi1 = hi0;
-    q_extremes<GK>(v, lo0, hi0, lo1, hi1);
-    q_rowreduce(lo0, hi0, lo1, hi1);
-    uint32_t sb0, zb0, sb1 = 0u, zb1 = 0u;
-    q_params<SDT>(lo0, hi0, Q, &sb0, &zb0);
-    if (GK == kQG64) q_params<SDT>(lo1, hi1, Q, &sb1, &zb1);
-    q_store_codes<SDT, GK>(job, tau, blk, v, sb0, zb0, sb1, zb1, Q);
-    if (lg == 0) {
-      const int g0 = GK == kQG64 ? 2 * blk : blk;
-      *reinterpret_cast<uint32_t*>(job.dst_sz + (static_cast<size_t>(g0) * R + r) * 4) = sb0 | (zb0 << 16);
-      if (GK == kQG64)
-        *reinterpret_cast<uint32_t*>(job.dst_sz + (static_cast<size_t>(g0 + 1) * R + r) * 4) = sb1 | (zb1 << 16);
-    }
+    QRaw raw;
+    q_load<GK>(job, b, tau, sp, raw);
+    if (job.src_bits == 16) q_block<ACT, SDT, GK, 16>(job, b, raw, tau, sp, lg, r, Q);
+    else if (job.src_bits == 8) q_block<ACT, SDT, GK, 8>(job, b, raw, tau, sp, lg, r, Q);
+    else q_block<ACT, SDT, GK, 4>(job, b, raw, tau, sp, lg, r, Q);
+    (void)R;
   } else {
+    float v[32];
     if (job.dst_bits == 16) {
       for (int blk = sp * span; blk < (sp + 1) * span; ++blk) {
         q_read<ACT, SDT, GK>(job, b, tau, blk, v);
@@ -459,6 +531,20 @@ __global__ __launch_bounds__(256) void k_qjobs(const QJobBatch b) {
     }
     if (lg == 0) *reinterpret_cast<uint32_t*>(job.dst_sz + (static_cast<size_t>(sp) * R + r) * 4) = sb0 | (zb0 << 16);
   }
+}
+
+template <int ACT, int SDT, int GK>
+__global__ __launch_bounds__(256) void k_qjobs(const QJobBatch b) {
+  qjobs_item<ACT, SDT, GK>(b);
+}
+
+// G = 128 (one group per block): the one-block path fits in 64 VGPRs, so
+// eight waves per SIMD and 32 blocks per CU are in flight. A requant wave is
+// latency-bound (it loads one 4 KiB block, then computes and stores), so the
+// bytes in flight set the rate.
+template <int ACT, int SDT>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void k_qjobs_g128(const QJobBatch b) {
+  qjobs_item<ACT, SDT, kQG128>(b);
 }
 
 __global__ void k_entry_writes(pw_page_entry* table, const EntryWrites w) {
@@ -792,7 +878,7 @@ template <int ACT, int SDT>
 static void qjobs_go(const QJobBatch& b, hipStream_t st) {
   const dim3 grid((b.total_items + 3) / 4), block(256);
   if (b.G == 64) hipLaunchKernelGGL((k_qjobs<ACT, SDT, kQG64>), grid, block, 0, st, b);
-  else if (b.G == 128) hipLaunchKernelGGL((k_qjobs<ACT, SDT, kQG128>), grid, block, 0, st, b);
+  else if (b.G == 128) hipLaunchKernelGGL((k_qjobs_g128<ACT, SDT>), grid, block, 0, st, b);
   else hipLaunchKernelGGL((k_qjobs<ACT, SDT, kQGBig>), grid, block, 0, st, b);
 }
 
