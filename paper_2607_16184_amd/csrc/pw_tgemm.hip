@@ -714,9 +714,15 @@ void sgemm_go(const GemmArgs& a, bool gateup, hipStream_t st) {
   }
 }
 
+// Layers with nested bit-plane pages run this kernel at every batch size;
+// at decode sizes (up to 24 expected slots per expert) 32-slot tiles halve
+// the activation staging, and with the LUT rows the workgroup's LDS then fits
+// twice per CU.
 template <int ACT, int SDT>
 void sgemm_mt(const GemmArgs& a, bool gateup, hipStream_t st) {
-  sgemm_go<ACT, SDT, 64>(a, gateup, st);
+  const int expect = (a.S + a.E - 1) / a.E;
+  if (a.apl && expect <= 24) sgemm_go<ACT, SDT, 32>(a, gateup, st);
+  else sgemm_go<ACT, SDT, 64>(a, gateup, st);
 }
 
 template <int ACT, int SDT>
