@@ -128,6 +128,13 @@ WsLayout ws_layout(const pw_layer_desc& d, int T, int K, bool apl) {
     const size_t units = active * (d.H / 64);
     nsplit = static_cast<int>(std::max<size_t>(1, std::min<size_t>(8, 2048 / std::max<size_t>(units, 1))));
   }
+  // likewise the streaming kernel with 32-slot tiles (bit-plane layers at
+  // decode sizes): 128-row down workgroups, two per CU
+  if (w.path == GemmPath::kStream && apl && expect <= 24 && S <= 4096) {
+    const size_t active = std::min<size_t>(d.E, S);
+    const size_t units = active * (d.H / 128);
+    nsplit = static_cast<int>(std::max<size_t>(1, std::min<size_t>(8, 1024 / std::max<size_t>(units, 1))));
+  }
   nsplit = std::min(nsplit, nkbF);
   // a split holds whole quantization groups (G = 256, 512 span 2, 4 blocks)
   const int bpg = d.G > 128 ? d.G / 128 : 1;

@@ -490,10 +490,11 @@ template <int MT> constexpr int sg_lds() { return 2 * sg_xbuf<MT>() + 4 * 1024; 
 // The loop body has no branches (every load and store is unconditional, with
 // clamped indices), so the compiler's wait counts stay static and the ring's
 // D stages really are in flight.
+// The wave's rows over 128-blocks [kb0, kb1) of the nkb blocks of a row.
 template <int ACT, int SDT, int B, int MT>
 __device__ __forceinline__ void sg_loop(uint8_t* lds, const uint8_t* tile0, const uint8_t* szrow,
-                                        const uint8_t* xrow, int xf, int nkb, int R, int gshift, int wave,
-                                        f32x4 (&acc)[2][MT / 16]) {
+                                        const uint8_t* xrow, int xf, int nkb, int kb0, int kb1, int R, int gshift,
+                                        int wave, f32x4 (&acc)[2][MT / 16]) {
   constexpr int D = sg_depth<B>();
   constexpr int XF = MT >= 32 ? MT / 32 : 1;       // activation fragments per wave
   constexpr int XB = sg_xbuf<MT>();
@@ -502,18 +503,19 @@ __device__ __forceinline__ void sg_loop(uint8_t* lds, const uint8_t* tile0, cons
   for (int t = 0; t < 2; ++t)
 #pragma unroll
     for (int u = 0; u < MT / 16; ++u) acc[t][u] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const int nstage = nkb * 128 / kTK;
+  const int nstage = (kb1 - kb0) * 128 / kTK;
+  const int st0 = kb0 * 128 / kTK;                 // first stage of the range within the row
   const int npad = (nstage + kSgStagePad - 1) / kSgStagePad * kSgStagePad;
   auto group_of = [&](int st) { return (st * kTK) >> gshift; };
   // waves past the tile's activation fragments write a discard area instead
   const int xoff = xf < MT / 8 ? 1024 * xf : 2 * XB + 1024 * wave - 1024 * xf;
   auto fetch_w = [&](WStage<B>& w, int st) {
-    const int s = min(st, nstage - 1);
+    const int s = st0 + min(st, nstage - 1);
     w_fetch<B>(w, tile0, szrow, s >> 1, s & 1, group_of(s), nkb, R);
   };
   // activation fragment q of this wave: xf + q (slot tile (xf + q) / 2, k-step (xf + q) mod 2)
   auto fetch_x = [&](u32x4 (&xv)[XF], int st) {
-    const int s = min(st, nstage - 1);
+    const int s = st0 + min(st, nstage - 1);
 #pragma unroll
     for (int q = 0; q < XF; ++q)
       xv[q] = ld16(xrow + static_cast<size_t>(s * kTK + 32 * ((xf + q) & 1) + 8 * lg) * 2);
@@ -565,8 +567,13 @@ constexpr int kSgLutWave = 32 * 256 * 2;
 template <int ACT, int SDT, bool GATEUP, int MT, bool APL>
 __global__ __launch_bounds__(256) void k_sgemm(const GemmArgs a, int nblk, int mtmax) {
   __shared__ __attribute__((aligned(16))) uint8_t lds[sg_lds<MT>() + (APL ? 4 * kSgLutWave : 0)];
-  const int per_xcd = gridDim.x / 8;
-  const int logical = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+  // the down projection may split K = F into a.nsplit ranges (fp32 partials,
+  // summed by the combine); split-major block order
+  const int nsplit = GATEUP ? 1 : a.nsplit;
+  const int per_split = gridDim.x / nsplit;
+  const int split = blockIdx.x / per_split, bid = blockIdx.x % per_split;
+  const int per_xcd = per_split / 8;
+  const int logical = (bid % 8) * per_xcd + bid / 8;
   const int band = logical / (kGN * mtmax), inb = logical % (kGN * mtmax);
   const int nb = band * kGN + inb % kGN, mt = inb / kGN;
   if (nb >= nblk) return;
@@ -634,22 +641,25 @@ __global__ __launch_bounds__(256) void k_sgemm(const GemmArgs a, int nblk, int m
   // wave never leaves early (the loop's barriers need all four).
   f32x4 acc[2][MT / 16];
   const int nkb = K / 128;
+  const int kb0 = GATEUP ? 0 : split * a.kb_per_split;
+  const int kb1 = GATEUP ? nkb : min(nkb, kb0 + a.kb_per_split);
+  if (kb0 >= kb1) return;                         // (whole workgroup: no barrier passed yet)
   const int gshift = 31 - __builtin_clz(a.G);     // G is a power of two, at least 64
   if constexpr (APL) {
     if (apl_page) {
-      if (bits == 8) sg_loop<ACT, SDT, kApl8, MT>(lds, tile0, szrow, xrow, xf, nkb, R, gshift, wave, acc);
-      else sg_loop<ACT, SDT, kApl4, MT>(lds, tile0, szrow, xrow, xf, nkb, R, gshift, wave, acc);
+      if (bits == 8) sg_loop<ACT, SDT, kApl8, MT>(lds, tile0, szrow, xrow, xf, nkb, kb0, kb1, R, gshift, wave, acc);
+      else sg_loop<ACT, SDT, kApl4, MT>(lds, tile0, szrow, xrow, xf, nkb, kb0, kb1, R, gshift, wave, acc);
     } else if (bits == 16) {
-      sg_loop<ACT, SDT, 16, MT>(lds, tile0, szrow, xrow, xf, nkb, R, gshift, wave, acc);
+      sg_loop<ACT, SDT, 16, MT>(lds, tile0, szrow, xrow, xf, nkb, kb0, kb1, R, gshift, wave, acc);
     } else if (bits == 8) {
-      sg_loop<ACT, SDT, 8, MT>(lds, tile0, szrow, xrow, xf, nkb, R, gshift, wave, acc);
+      sg_loop<ACT, SDT, 8, MT>(lds, tile0, szrow, xrow, xf, nkb, kb0, kb1, R, gshift, wave, acc);
     } else {
-      sg_loop<ACT, SDT, 4, MT>(lds, tile0, szrow, xrow, xf, nkb, R, gshift, wave, acc);
+      sg_loop<ACT, SDT, 4, MT>(lds, tile0, szrow, xrow, xf, nkb, kb0, kb1, R, gshift, wave, acc);
     }
   } else {
-    if (bits == 16) sg_loop<ACT, SDT, 16, MT>(lds, tile0, szrow, xrow, xf, nkb, R, gshift, wave, acc);
-    else if (bits == 8) sg_loop<ACT, SDT, 8, MT>(lds, tile0, szrow, xrow, xf, nkb, R, gshift, wave, acc);
-    else sg_loop<ACT, SDT, 4, MT>(lds, tile0, szrow, xrow, xf, nkb, R, gshift, wave, acc);
+    if (bits == 16) sg_loop<ACT, SDT, 16, MT>(lds, tile0, szrow, xrow, xf, nkb, kb0, kb1, R, gshift, wave, acc);
+    else if (bits == 8) sg_loop<ACT, SDT, 8, MT>(lds, tile0, szrow, xrow, xf, nkb, kb0, kb1, R, gshift, wave, acc);
+    else sg_loop<ACT, SDT, 4, MT>(lds, tile0, szrow, xrow, xf, nkb, kb0, kb1, R, gshift, wave, acc);
   }
 
   const int wr = wave & 1;
@@ -690,7 +700,8 @@ __global__ __launch_bounds__(256) void k_sgemm(const GemmArgs a, int nblk, int m
       if (mm < n_e) {
 #pragma unroll
         for (int t = 0; t < 2; ++t)
-          *reinterpret_cast<f32x4*>(a.opart + static_cast<size_t>(off_e + mm) * a.H + grow + t * 16 + 4 * lg) =
+          *reinterpret_cast<f32x4*>(a.opart + (static_cast<size_t>(split) * a.S + off_e + mm) * a.H + grow + t * 16 +
+                                    4 * lg) =
               acc[t][u];
       }
     }
@@ -701,7 +712,7 @@ template <int ACT, int SDT, int MT>
 void sgemm_go(const GemmArgs& a, bool gateup, hipStream_t st) {
   const int nblk = gateup ? a.F / 64 : a.H / 128;
   const int mtmax = (a.S + MT - 1) / MT + a.E;
-  const int n = ((nblk + kGN - 1) / kGN * kGN * mtmax + 7) / 8 * 8;
+  const int n = ((nblk + kGN - 1) / kGN * kGN * mtmax + 7) / 8 * 8 * (gateup ? 1 : a.nsplit);
   if (a.apl) {
     if (gateup)
       hipLaunchKernelGGL((k_sgemm<ACT, SDT, true, MT, true>), dim3(n), dim3(256), 0, st, a, nblk, mtmax);
