@@ -524,7 +524,8 @@ __device__ __forceinline__ void gateup_any(int code, const GemmArgs& a, uint8_t*
   }
 }
 
-// NTMAX slot tiles per pass (1, 2 or 4); experts with fewer slots take fewer.
+// NTMAX slot tiles per pass (1, 2 or 4); experts with fewer slots take fewer
+// (at NTMAX = 4 also three).
 template <int ACT, int SDT, int NTMAX, int GK, int NW>
 __global__ __launch_bounds__(64 * NW) void k_gateup(const GemmArgs a) {
   constexpr int RT = row_tiles<NTMAX>();
@@ -550,6 +551,7 @@ __global__ __launch_bounds__(64 * NW) void k_gateup(const GemmArgs a) {
   const int code = fmt_code(a.table[(static_cast<size_t>(e) * 3 + proj) * a.nrb_max + f0 / a.R].bits);
   if (NTMAX == 1 || n_e <= 16) gateup_any<ACT, SDT, 1, GK, RT, NW>(code, a, lds, e, off_e, n_e, unit, sums);
   else if (NTMAX == 2 || n_e <= 32) gateup_any<ACT, SDT, 2, GK, RT, NW>(code, a, lds, e, off_e, n_e, unit, sums);
+  else if (n_e <= 48) gateup_any<ACT, SDT, 3, GK, RT, NW>(code, a, lds, e, off_e, n_e, unit, sums);
   else gateup_any<ACT, SDT, (NTMAX > 2 ? NTMAX : 2), GK, RT, NW>(code, a, lds, e, off_e, n_e, unit, sums);
 }
 
@@ -632,6 +634,7 @@ __global__ __launch_bounds__(64 * NW) void k_down(const GemmArgs a) {
   if (NTMAX == 1 || n_e <= 16) down_any<ACT, SDT, 1, GK, RT, NW>(code, a, lds, e, off_e, n_e, unit, split, sums);
   else if (NTMAX == 2 || n_e <= 32)
     down_any<ACT, SDT, 2, GK, RT, NW>(code, a, lds, e, off_e, n_e, unit, split, sums);
+  else if (n_e <= 48) down_any<ACT, SDT, 3, GK, RT, NW>(code, a, lds, e, off_e, n_e, unit, split, sums);
   else down_any<ACT, SDT, (NTMAX > 2 ? NTMAX : 2), GK, RT, NW>(code, a, lds, e, off_e, n_e, unit, split, sums);
 }
 
