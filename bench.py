@@ -619,6 +619,46 @@ def leg_apl(steps=20):
             "weight_GBps_after": round(wbytes1 / (step1 * 1e-3) / 1e9, 1)}
 
 
+def leg_ceilings(reps=5):
+    """What the device delivers: a plain streaming read of 4 GiB (16-byte
+    nontemporal loads, 8 workgroups per CU) and back-to-back independent
+    32x32x16 bf16 MFMAs from two waves per SIMD, each timed with HIP events
+    on the stream it runs on (median of `reps` launches)."""
+    import numpy as np
+    import torch
+    from paper_2607_16184_amd import pw
+    st = torch.cuda.current_stream()
+    nbytes, nblk_r = 4 << 30, 2048
+    buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    buf.fill_(1)
+    out = torch.zeros(2 * nblk_r, dtype=torch.int32, device="cuda")
+    iters, nblk_m = 4096, 1024
+    outm = torch.zeros(nblk_m, dtype=torch.float32, device="cuda")
+
+    def timed(fn):
+        fn()
+        ms = []
+        for _ in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(st)
+            fn()
+            b.record(st)
+            torch.cuda.synchronize()
+            ms.append(a.elapsed_time(b))
+        return float(np.median(ms))
+
+    ms_r = timed(lambda: pw.pw_probe_read(buf.data_ptr(), nbytes, nblk_r, out.data_ptr(), st.cuda_stream))
+    if int(out[nblk_r:].sum().item()) != nblk_r:
+        raise RuntimeError("read probe: not every workgroup completed")
+    ms_m = timed(lambda: pw.pw_probe_mfma(iters, nblk_m, outm.data_ptr(), st.cuda_stream))
+    flops = float(nblk_m) * 8 * iters * 4 * 32768
+    del buf
+    return {"stream_read_GBps": round(nbytes / (ms_r * 1e-3) / 1e9, 1), "stream_read_bytes": nbytes,
+            "mfma_bf16_TFLOPs": round(flops / (ms_m * 1e-3) / 1e12, 1),
+            "of_published_peaks": {"hbm": round(nbytes / (ms_r * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                                   "mfma_bf16": round(flops / (ms_m * 1e-3) / MFMA_PEAK_BF16, 4)}}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -626,7 +666,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="mixtral_decode")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--extras", default="prefill,finegrained,downshift,offload,planner,apl",
+    ap.add_argument("--extras", default="ceilings,prefill,finegrained,downshift,offload,planner,apl",
                     help="comma list of extra legs on the same JSON line ('' for none)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after the timed steps, run one device copy of this many MiB "
@@ -713,7 +753,9 @@ def main():
     extras = {}
     for leg in [e for e in args.extras.split(",") if e]:
         t0 = time.time()
-        if leg == "prefill":
+        if leg == "ceilings":
+            extras["ceilings"] = leg_ceilings()
+        elif leg == "prefill":
             extras["prefill"] = leg_layer("mixtral_prefill", steps=20, warmup=2)
         elif leg == "finegrained":
             # 0.57 GB of weights: three pools in turn, so no step reads the

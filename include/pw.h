@@ -405,6 +405,27 @@ pw_status pw_planner_step_layer(pw_planner* p, const pw_layer* layer, int free_b
                                 uint64_t kv_block_bytes, pw_plan_summary* out);
 pw_status pw_planner_apply(pw_planner* p, pw_layer* layer, void* side_stream, size_t* delta_total);
 
+/* ---- Ceiling probes (diagnostics beside the hot path) ---------------------
+ * What the device delivers, for reading the kernels' roofline fractions
+ * against the achievable as well as the published peaks.
+ *
+ * pw_probe_read: nblocks workgroups of 256 threads each stream one
+ * contiguous span of bytes / nblocks bytes of buf (device memory, caller-
+ * owned, at least `bytes` long, 16-byte aligned) with 16-byte nontemporal
+ * loads. bytes must be a positive multiple of nblocks * 32768. out: device,
+ * 2 * nblocks uint32 (a completion flag per workgroup in out[nblocks..]).
+ * Bytes read per launch = bytes. Time it with events on `stream`.
+ *
+ * pw_probe_mfma: nblocks workgroups of 8 waves (one per CU, by a 96 KiB
+ * LDS request) issue independent v_mfma_f32_32x32x16_bf16 back to back:
+ * each wave runs iters rounds of 4. out: device, nblocks floats. Flops per
+ * launch = nblocks * 8 * iters * 4 * 32768.
+ *
+ * Errors: PW_EINVAL for the argument conditions above; PW_EHIP if the
+ * launch fails.                                                           */
+pw_status pw_probe_read(const void* buf, size_t bytes, int nblocks, uint32_t* out, void* stream);
+pw_status pw_probe_mfma(int iters, int nblocks, float* out, void* stream);
+
 const char* pw_last_error(void);
 const char* pw_status_str(pw_status s);
 

@@ -40,6 +40,7 @@ SOURCES = {
     "pw_kernels.hip": [],
     "pw_decode.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
     "pw_tgemm.hip": [],
+    "pw_probe.hip": [],
     "pw_api.cpp": [],
     "pw_state.cpp": [],
     "pw_plan.cpp": [],

@@ -395,6 +395,22 @@ pw_status pw_route_topk(const float* logits, int T, int E, int K, int renorm, in
   return PW_OK;
 }
 
+pw_status pw_probe_read(const void* buf, size_t bytes, int nblocks, uint32_t* out, void* stream) {
+  constexpr size_t kUnit = 8 * 4096;   // one round of the probe's loads per workgroup
+  if (!buf || !out || nblocks < 1 || nblocks > (1 << 20)) return fail(PW_EINVAL, "need buf, out and 1 <= nblocks <= 2^20");
+  if (bytes == 0 || bytes % (kUnit * static_cast<size_t>(nblocks)) != 0)
+    return fail(PW_EINVAL, "bytes must be a positive multiple of nblocks * 32768");
+  hipError_t e = pw::launch_probe_read(buf, bytes, nblocks, out, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? PW_OK : hip_fail(e, "read probe launch");
+}
+
+pw_status pw_probe_mfma(int iters, int nblocks, float* out, void* stream) {
+  if (!out || iters < 1 || nblocks < 1 || nblocks > (1 << 20))
+    return fail(PW_EINVAL, "need out, iters >= 1 and 1 <= nblocks <= 2^20");
+  hipError_t e = pw::launch_probe_mfma(iters, nblocks, out, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? PW_OK : hip_fail(e, "MFMA probe launch");
+}
+
 pw_status pw_routing_stats(const void* rows, pw_dtype act, int n_rows, int dim, int rows_by_position,
                            const float* topk_w, const int32_t* offsets, const int32_t* sorted_slot, int T, int E,
                            int K, double* norm2_ws, double* stats, int accumulate, void* stream) {

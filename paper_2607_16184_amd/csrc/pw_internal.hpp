@@ -98,6 +98,9 @@ hipError_t launch_tgemm(const GemmArgs& a, bool gateup, hipStream_t st);
 // small and medium slot counts: register-streamed tiles of 16/32/64 slots
 hipError_t launch_sgemm(const GemmArgs& a, bool gateup, hipStream_t st);
 hipError_t launch_apl_quant(const AplBatch& b, hipStream_t st);
+// ceiling probes: a plain streaming read and back-to-back bf16 MFMAs
+hipError_t launch_probe_read(const void* buf, size_t bytes, int nblocks, uint32_t* out, hipStream_t st);
+hipError_t launch_probe_mfma(int iters, int nblocks, float* out, hipStream_t st);
 hipError_t launch_apl_pack(const AplBatch& b, hipStream_t st);
 // Per-expert routing statistics (row norms, then a fixed-order reduction).
 hipError_t launch_routing_stats(const uint16_t* rows, int act, int n_rows, int dim, int by_position,

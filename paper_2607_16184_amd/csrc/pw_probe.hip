@@ -1,0 +1,64 @@
+// Ceiling probes for gfx950: the achievable HBM read rate of a plain stream
+// and the achievable dense bf16 MFMA rate, measured on the same device as the
+// paged GEMMs so that their roofline fractions can be read against what the
+// chip delivers as well as against its published peaks.
+#include "pw_device.hpp"
+#include "pw_internal.hpp"
+
+namespace pw {
+namespace {
+
+// Each workgroup reads one contiguous span with 16-byte nontemporal loads,
+// eight in flight per lane, and folds them into one word it writes out (so
+// the loads are not removed). Spans are whole multiples of 8 x 256 x 16 B.
+__global__ __launch_bounds__(256) void k_probe_read(const uint8_t* buf, size_t span, uint32_t* out) {
+  const uint8_t* p = buf + static_cast<size_t>(blockIdx.x) * span + 16 * threadIdx.x;
+  u32x4 acc = {0u, 0u, 0u, 0u};
+  for (size_t o = 0; o < span; o += 8 * 4096) {
+    u32x4 v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = ld16_nt(p + o + 4096 * j);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc ^= v[j];
+  }
+  const uint32_t r = acc[0] ^ acc[1] ^ acc[2] ^ acc[3];
+  if (r == 0x9E3779B9u) out[blockIdx.x] = r;   // practically never; keeps the loads
+  if (threadIdx.x == 0) out[gridDim.x + blockIdx.x] = 1u;
+}
+
+// Back-to-back independent v_mfma_f32_32x32x16_bf16 from two waves per SIMD
+// (eight waves per workgroup, one workgroup per CU by its LDS request): each
+// wave keeps four accumulators in flight over `iters` rounds of 4 MFMAs.
+__global__ __launch_bounds__(512) void k_probe_mfma(int iters, float* out) {
+  extern __shared__ uint8_t occupy[];   // requested at launch: one workgroup per CU
+  typedef float f32x16 __attribute__((ext_vector_type(16)));
+  const uint32_t seed = 0x3F803F80u ^ (threadIdx.x & 7u);
+  const bf16x8 a = __builtin_bit_cast(bf16x8, u32x4{seed, seed, seed, seed});
+  const bf16x8 b = __builtin_bit_cast(bf16x8, u32x4{0x3C003C00u, 0x3C003C00u, 0x3C003C00u, 0x3C003C00u});
+  f32x16 c0 = {}, c1 = {}, c2 = {}, c3 = {};
+  for (int i = 0; i < iters; ++i) {
+    c0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c0, 0, 0, 0);
+    c1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c1, 0, 0, 0);
+    c2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c2, 0, 0, 0);
+    c3 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c3, 0, 0, 0);
+  }
+  float s = 0.0f;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) s += c0[e] + c1[e] + c2[e] + c3[e];
+  if (threadIdx.x == 0) out[blockIdx.x] = s + static_cast<float>(occupy[0] & 0);
+}
+
+}  // namespace
+
+hipError_t launch_probe_read(const void* buf, size_t bytes, int nblocks, uint32_t* out, hipStream_t st) {
+  const size_t span = bytes / static_cast<size_t>(nblocks);
+  hipLaunchKernelGGL(k_probe_read, dim3(nblocks), dim3(256), 0, st, static_cast<const uint8_t*>(buf), span, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_probe_mfma(int iters, int nblocks, float* out, hipStream_t st) {
+  hipLaunchKernelGGL(k_probe_mfma, dim3(nblocks), dim3(512), 96 * 1024, st, iters, out);
+  return hipGetLastError();
+}
+
+}  // namespace pw

@@ -88,6 +88,8 @@ def _load():
         "pw_layer_destroy": (i32, [vp]),
         "pw_layer_load_page": (i32, [vp, i32, i32, i32, i32, vp, vp]),
         "pw_route_topk": (i32, [vp, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp]),
+        "pw_probe_read": (i32, [vp, sz, i32, vp, vp]),
+        "pw_probe_mfma": (i32, [i32, i32, vp, vp]),
         "pw_workspace_bytes": (i32, [vp, i32, i32, P(sz)]),
         "pw_moe_paged_gemm": (i32, [vp, vp, i32, i32, vp, vp, vp, vp, vp, i32, vp, sz, vp]),
         "pw_requant_block": (i32, [vp, i32, i32, i32, i32, vp, P(sz)]),
@@ -180,6 +182,14 @@ def pw_route_topk(logits_ptr: int, T: int, E: int, K: int, renorm: int, ids_ptr:
                   offsets_ptr: int, sorted_slot_ptr: int, slot_pos_ptr: int, stream: int):
     _check(_lib.pw_route_topk(logits_ptr, T, E, K, renorm, ids_ptr, w_ptr, offsets_ptr,
                               sorted_slot_ptr, slot_pos_ptr, stream))
+
+
+def pw_probe_read(buf_ptr: int, nbytes: int, nblocks: int, out_ptr: int, stream: int):
+    _check(_lib.pw_probe_read(buf_ptr, nbytes, nblocks, out_ptr, stream))
+
+
+def pw_probe_mfma(iters: int, nblocks: int, out_ptr: int, stream: int):
+    _check(_lib.pw_probe_mfma(iters, nblocks, out_ptr, stream))
 
 
 def pw_workspace_bytes(layer: int, T: int, K: int) -> int:
