@@ -27,10 +27,10 @@ __global__ __launch_bounds__(256) void k_probe_read(const uint8_t* buf, size_t s
 }
 
 // Back-to-back independent v_mfma_f32_32x32x16_bf16 from two waves per SIMD
-// (eight waves per workgroup, one workgroup per CU by its LDS request): each
-// wave keeps four accumulators in flight over `iters` rounds of 4 MFMAs.
+// (eight waves per workgroup; the launch requests 96 KiB of LDS, which keeps
+// one workgroup per CU): each wave keeps four accumulators in flight over
+// `iters` rounds of 4 MFMAs.
 __global__ __launch_bounds__(512) void k_probe_mfma(int iters, float* out) {
-  extern __shared__ uint8_t occupy[];   // requested at launch: one workgroup per CU
   typedef float f32x16 __attribute__((ext_vector_type(16)));
   const uint32_t seed = 0x3F803F80u ^ (threadIdx.x & 7u);
   const bf16x8 a = __builtin_bit_cast(bf16x8, u32x4{seed, seed, seed, seed});
@@ -45,7 +45,7 @@ __global__ __launch_bounds__(512) void k_probe_mfma(int iters, float* out) {
   float s = 0.0f;
 #pragma unroll
   for (int e = 0; e < 16; ++e) s += c0[e] + c1[e] + c2[e] + c3[e];
-  if (threadIdx.x == 0) out[blockIdx.x] = s + static_cast<float>(occupy[0] & 0);
+  if (threadIdx.x == 0) out[blockIdx.x] = s;
 }
 
 }  // namespace
