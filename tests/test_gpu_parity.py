@@ -87,12 +87,18 @@ def test_tiny_quantized_pages_bit_exact():
     L.close()
 
 
-@pytest.mark.parametrize("src,dst", [(16, 8), (16, 4), (8, 4)])
-def test_tiny_requant_bit_exact(src, dst):
+# G = 64 (fp16) runs the generic requant kernel, G = 128 the one-group-per-
+# block kernel, here also with bf16 activations and scales.
+@pytest.mark.parametrize("src,dst,G,act,sdt", [
+    (16, 8, 64, synth.F16, synth.F16), (16, 4, 64, synth.F16, synth.F16), (8, 4, 64, synth.F16, synth.F16),
+    (16, 8, 128, synth.BF16, synth.BF16), (16, 4, 128, synth.BF16, synth.BF16), (8, 4, 128, synth.BF16, synth.BF16),
+    (8, 4, 128, synth.F16, synth.BF16),
+])
+def test_tiny_requant_bit_exact(src, dst, G, act, sdt):
     import torch
-    cfg, w16, _, order = case("tiny")
+    cfg, w16, _, order = case("tiny", G=G, act=act, sdt=sdt)
     bits = [np.full((cfg.E, cfg.nrb(p)), src, np.int32) for p in range(3)]
-    say("tiny requant %d->%d" % (src, dst))
+    say("tiny requant %d->%d G=%d act=%d sdt=%d" % (src, dst, G, act, sdt))
     L = gpu_layer(cfg, w16, bits, order, slack=1.0)
     O = oracle_layer(cfg, w16, bits)
     blocks = [pg for i, pg in enumerate(order) if i % 3 == 0]
