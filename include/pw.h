@@ -194,10 +194,12 @@ pw_status pw_requant_blocks(pw_layer* layer, int n, const int* e, const int* pro
 pw_status pw_layer_set_host_pool(pw_layer* layer, void* host_pool, size_t host_bytes);
 
 /* Copy the committed page of each block (codes and scale/zero, Eq. 3's M^b
- * bytes) into a fresh host slot, device-to-host on `stream`. The GPU page
+ * bytes; for a nested bit-plane page its planes and LUTs of the committed
+ * precision) into a fresh host slot, device-to-host on `stream`. The GPU page
  * and the table are unchanged. A host copy at another bitwidth is replaced;
  * one at the committed bitwidth makes the block a no-op. To lower a block in
- * the paper's order, offload it and then requantize it on the same stream.
+ * the paper's order, offload it and then requantize it on the same stream
+ * (a bit-plane page: drop its planes 8 -> 4).
  *   no host pool, page absent: PW_ESTATE.  requant/reload pending: PW_EBUSY.
  *   host pool full: PW_ENOMEM (no block of the batch is copied).           */
 pw_status pw_offload_blocks(pw_layer* layer, int n, const int* e, const int* proj, const int* rb,
@@ -208,10 +210,13 @@ pw_status pw_offload_block(pw_layer* layer, int e, int proj, int rb, void* strea
  * slot is filled host-to-device on `stream` (after the offload's copy
  * finished); the block is pending (PW_PAGE_RELOAD_PENDING) until pw_commit
  * publishes the raised entry, and its old slot is then retired like a
- * requantized one. *added_bytes_total (may be NULL) receives the sum of
- * M^b' - M^b. The host copy stays (drop it with pw_drop_host_copy).
- *   no host copy, page absent: PW_ESTATE.  copy not of a higher bitwidth:
- *   PW_EUNSUPPORTED.  pending already: PW_EBUSY.  no free slot: PW_ENOMEM.  */
+ * requantized one. A bit-plane page comes back whole (planes 0-7 and both
+ * LUTs from its 8-bit copy) as a bit-plane entry. *added_bytes_total (may be
+ * NULL) receives the sum of M^b' - M^b. The host copy stays (drop it with
+ * pw_drop_host_copy).
+ *   no host copy, page absent: PW_ESTATE.  copy not of a higher bitwidth, or
+ *   of another format than the committed page: PW_EUNSUPPORTED.  pending
+ *   already: PW_EBUSY.  no free slot: PW_ENOMEM.                           */
 pw_status pw_reload_blocks(pw_layer* layer, int n, const int* e, const int* proj, const int* rb,
                            void* stream, size_t* added_bytes_total);
 pw_status pw_reload_block(pw_layer* layer, int e, int proj, int rb, void* stream, size_t* added_bytes);

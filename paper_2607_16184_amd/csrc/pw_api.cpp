@@ -665,7 +665,7 @@ pw_status pw_offload_blocks(pw_layer* L, int n, const int* e, const int* proj, c
   };
   std::vector<Planned> plan;
   auto rollback = [&]() {
-    for (const Planned& p : plan) L->st.halloc.release(p.host_off, L->st.page_bytes(p.proj, p.src.bits));
+    for (const Planned& p : plan) L->st.halloc.release(p.host_off, L->st.entry_bytes(p.proj, p.src));
   };
   for (int i = 0; i < n; ++i) {
     Planned p{e[i], proj[i], rb[i], {}, 0};
@@ -681,7 +681,7 @@ pw_status pw_offload_blocks(pw_layer* L, int n, const int* e, const int* proj, c
   hipStream_t st = static_cast<hipStream_t>(stream);
   for (const Planned& p : plan) {
     hipError_t he = hipMemcpyAsync(L->host_pool + p.host_off, L->pool + p.src.data_off,
-                                   L->st.page_bytes(p.proj, p.src.bits), hipMemcpyDeviceToHost, st);
+                                   L->st.entry_bytes(p.proj, p.src), hipMemcpyDeviceToHost, st);
     if (he != hipSuccess) {
       rollback();
       return hip_fail(he, "device-to-host page copy");
@@ -694,7 +694,8 @@ pw_status pw_offload_blocks(pw_layer* L, int n, const int* e, const int* proj, c
     return s;
   }
   L->st.ref_event(ev);
-  for (const Planned& p : plan) L->st.finish_offload(p.e, p.proj, p.rb, p.host_off, p.src.bits, ev);
+  for (const Planned& p : plan)
+    L->st.finish_offload(p.e, p.proj, p.rb, p.host_off, p.src.bits, (p.src.rsv & 0xFF) == PW_FMT_APL, ev);
   L->st.unref_event(ev);
   return PW_OK;
 }
@@ -745,7 +746,7 @@ pw_status pw_reload_blocks(pw_layer* L, int n, const int* e, const int* proj, co
   }
   for (const Planned& p : plan) {
     hipError_t he = hipMemcpyAsync(L->pool + p.dst.data_off, L->host_pool + p.hc.off,
-                                   L->st.page_bytes(p.proj, p.hc.bits), hipMemcpyHostToDevice, st);
+                                   L->st.host_bytes(p.proj, p.hc), hipMemcpyHostToDevice, st);
     if (he != hipSuccess) {
       rollback();
       return hip_fail(he, "host-to-device page copy");

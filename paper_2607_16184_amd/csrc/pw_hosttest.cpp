@@ -133,7 +133,7 @@ int pwt_offload(void* hv, int n, const int* e, const int* proj, const int* rb, u
     else if (!seen.insert(h->st.index(p.e, p.proj, p.rb)).second) { g_msg = "duplicate"; s = PW_EINVAL; }
     else s = h->st.plan_offload(p.e, p.proj, p.rb, &p.src, &p.off, &same, &g_msg);
     if (s != PW_OK) {
-      for (const P& q : plan) h->st.halloc.release(q.off, h->st.page_bytes(q.proj, q.src.bits));
+      for (const P& q : plan) h->st.halloc.release(q.off, h->st.entry_bytes(q.proj, q.src));
       return s;
     }
     if (!same) plan.push_back(p);
@@ -141,7 +141,8 @@ int pwt_offload(void* hv, int n, const int* e, const int* proj, const int* rb, u
   if (plan.empty()) return PW_OK;
   void* ev = h->ev.create();
   h->st.ref_event(ev);
-  for (const P& p : plan) h->st.finish_offload(p.e, p.proj, p.rb, p.off, p.src.bits, ev);
+  for (const P& p : plan)
+    h->st.finish_offload(p.e, p.proj, p.rb, p.off, p.src.bits, (p.src.rsv & 0xFF) == PW_FMT_APL, ev);
   h->st.unref_event(ev);
   *event_id = reinterpret_cast<uintptr_t>(ev);
   return PW_OK;

@@ -252,23 +252,26 @@ pw_status LayerState::plan_offload(int e, int proj, int rb, pw_page_entry* src, 
   const pw_page_entry& cur = mirror[idx];
   if (cur.bits == 0) { *err = "page not present"; return PW_ESTATE; }
   if (cur.state != PW_PAGE_RESIDENT) { *err = "a requantization or reload of this block is pending"; return PW_EBUSY; }
-  if ((cur.rsv & 0xFF) == PW_FMT_APL) { *err = "host copies of nested bit-plane pages are not supported"; return PW_EUNSUPPORTED; }
-  if (host[idx].bits == cur.bits) {
+  const bool apl = (cur.rsv & 0xFF) == PW_FMT_APL;
+  if (host[idx].bits == cur.bits && (host[idx].apl != 0) == apl) {
     *same = true;
     return PW_OK;
   }
+  // the copy is the committed page: a bit-plane page's planes and LUTs of its
+  // committed precision (the 8-bit page, or the 4-bit prefix)
   uint64_t off = 0;
-  if (!halloc.alloc(page_bytes(proj, cur.bits), &off)) { *err = "host pool exhausted"; return PW_ENOMEM; }
+  if (!halloc.alloc(entry_bytes(proj, cur), &off)) { *err = "host pool exhausted"; return PW_ENOMEM; }
   *src = cur;
   *host_off = off;
   return PW_OK;
 }
 
-void LayerState::finish_offload(int e, int proj, int rb, uint64_t host_off, int bits, void* ev) {
+void LayerState::finish_offload(int e, int proj, int rb, uint64_t host_off, int bits, bool apl, void* ev) {
   drop_host_copy(e, proj, rb);   // a copy at another bitwidth is replaced
   HostCopy& h = host[index(e, proj, rb)];
   h.off = host_off;
   h.bits = static_cast<uint8_t>(bits);
+  h.apl = apl ? 1 : 0;
   h.ev = ev;
   ref_event(ev);
 }
@@ -284,16 +287,26 @@ pw_status LayerState::plan_reload(int e, int proj, int rb, pw_page_entry* dst, H
   const HostCopy& h = host[idx];
   if (h.bits == 0) { *err = "the block has no host copy"; return PW_ESTATE; }
   if (h.bits <= cur.bits) { *err = "the host copy is not of a higher bitwidth"; return PW_EUNSUPPORTED; }
+  if ((h.apl != 0) != ((cur.rsv & 0xFF) == PW_FMT_APL)) {
+    *err = "the host copy and the committed page are of different formats";
+    return PW_EUNSUPPORTED;
+  }
   uint64_t off = 0;
-  if (!alloc.alloc(page_bytes(proj, h.bits), &off)) { *err = "pool exhausted"; return PW_ENOMEM; }
+  if (!alloc.alloc(host_bytes(proj, h), &off)) { *err = "pool exhausted"; return PW_ENOMEM; }
   dst->data_off = off;
-  dst->sz_off = h.bits == 16 ? 0 : off + code_bytes(proj, h.bits);
+  if (h.apl) {
+    // the full page comes back; LUT_4 follows planes 0-3 as in a loaded page
+    dst->sz_off = off + 4 * (static_cast<uint64_t>(desc.R) * kdim(proj) / 8);
+    dst->rsv = PW_FMT_APL;
+  } else {
+    dst->sz_off = h.bits == 16 ? 0 : off + code_bytes(proj, h.bits);
+    dst->rsv = 0;
+  }
   dst->bits = h.bits;
   dst->state = PW_PAGE_RESIDENT;
-  dst->rsv = 0;
   dst->gen = cur.gen + 1;
   *hc = h;
-  *added = page_bytes(proj, h.bits) - page_bytes(proj, cur.bits);
+  *added = host_bytes(proj, h) - entry_bytes(proj, cur);
   return PW_OK;
 }
 
@@ -312,7 +325,7 @@ void LayerState::add_reload_pending(int e, int proj, int rb, const pw_page_entry
 void LayerState::drop_host_copy(int e, int proj, int rb) {
   HostCopy& h = host[index(e, proj, rb)];
   if (h.bits == 0) return;
-  hretired_.push_back(Retired{h.off, page_bytes(proj, h.bits), h.ev});   // the reference moves along
+  hretired_.push_back(Retired{h.off, host_bytes(proj, h), h.ev});   // the reference moves along
   h = HostCopy{};
 }
 

@@ -66,6 +66,7 @@ struct EventOps {
 struct HostCopy {
   uint64_t off = 0;      // byte offset in the host pool
   uint8_t bits = 0;      // bitwidth of the copy; 0: none
+  uint8_t apl = 0;       // 1: a nested bit-plane page (planes and LUTs)
   void* ev = nullptr;    // the last transfer that touches the slot (reference held)
 };
 
@@ -92,6 +93,9 @@ class LayerState {
   uint64_t apl_bytes(int proj, int bits) const;
   uint64_t entry_bytes(int proj, const pw_page_entry& e) const {
     return (e.rsv & 0xFF) == PW_FMT_APL ? apl_bytes(proj, e.bits) : page_bytes(proj, e.bits);
+  }
+  uint64_t host_bytes(int proj, const HostCopy& h) const {
+    return h.apl ? apl_bytes(proj, h.bits) : page_bytes(proj, h.bits);
   }
   // A pending entry that reuses its block's slot (a bit-plane drop) carries
   // this flag until it is published.
@@ -124,7 +128,7 @@ class LayerState {
   // exists already.
   pw_status plan_offload(int e, int proj, int rb, pw_page_entry* src, uint64_t* host_off, bool* same,
                          std::string* err);
-  void finish_offload(int e, int proj, int rb, uint64_t host_off, int bits, void* ev);
+  void finish_offload(int e, int proj, int rb, uint64_t host_off, int bits, bool apl, void* ev);
   // Reload a block from its host copy into a fresh device slot (*dst), the
   // copy being of a higher bitwidth than the committed page; *added receives
   // M^b' - M^b.

@@ -133,16 +133,73 @@ def test_apl_downshift_drops_planes():
         assert np.array_equal(got, pages[(e, p, rb)][0][:got.size])
     e16, e32 = _forward_check(L, cfg, _effective_w16(cfg, w16, bits4, pages))
     assert e16 <= TOL16 and e32 <= TOL32, (e16, e32)
-    # refused moves: below 4 bits, a plane page to 16 bits, host copies
+    # refused moves: a plane page to 16 bits; the same bitwidth is a no-op
     blk = eight[0]
     with pytest.raises(pw.PWError) as ei:
         L.requant([blk], 16)
     assert ei.value.status == 4
-    assert L.requant([blk], 4) == 0                                    # same bitwidth: no-op
-    L.set_host_pool(1 << 20)
+    assert L.requant([blk], 4) == 0
+    L.close()
+
+
+def _slot(n):
+    return (n + 255) // 256 * 256
+
+
+def test_apl_offload_drop_reload():
+    """Sec. 3.1's page states with bit-plane pages: the 8-bit pages are copied
+    to host memory, lowered in place to 4 bits (tail freed), and raised back
+    from their host copies; each state's pages are byte-identical to the
+    oracle's and the forward follows the committed precision."""
+    import torch
+    cfg, w16, bits, _ = case("tiny")
+    say("bit-plane offload, 8 -> 4 drop, reload")
+    # a reload takes a fresh 8-bit slot while the 4-bit prefix is still held
+    # (the freed tails are smaller than a page): room for every raised page
+    L = _layer(cfg, w16, bits, slack=1.0)
+    pages = _oracle_pages(cfg, w16, bits)
+    eight = [k for k in pages if bits[k[1]][k[0], k[2]] == 8]
+    kdim = lambda p: cfg.F if p == 2 else cfg.H
+    host_need = sum(_slot(apl.page_bytes(cfg.R, kdim(p), 8)) for (_, p, _) in eight)
+    L.set_host_pool(host_need)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    L.offload(eight, stream=side)
+    assert L.host_pool_stats() == (host_need, host_need)
+    L.offload(eight, stream=side)                                      # same bitwidth: no-op
+    delta = L.requant(eight, 4, stream=side)
+    assert delta == sum(apl.page_bytes(cfg.R, kdim(p), 8) - apl.page_bytes(cfg.R, kdim(p), 4) for (_, p, _) in eight)
+    assert L.commit() == len(eight)
+    torch.cuda.synchronize()
+    L.reclaim()
+    bits4 = [b.copy() for b in bits]
+    for (e, p, rb) in eight:
+        bits4[p][e, rb] = 4
+        assert L.host_copy_info(e, p, rb) == (8, True)
+    e16, e32 = _forward_check(L, cfg, _effective_w16(cfg, w16, bits4, pages))
+    assert e16 <= TOL16 and e32 <= TOL32, (e16, e32)
+
+    say("bit-plane reload 4 -> 8")
+    added = L.reload(eight, stream=side)
+    assert added == delta
+    for (e, p, rb) in eight:
+        assert L.entry(e, p, rb).state == pw.PW_PAGE_RELOAD_PENDING
+    assert L.commit() == len(eight)
+    torch.cuda.synchronize()
+    L.reclaim()
+    for (e, p, rb) in eight:
+        ent = L.entry(e, p, rb)
+        assert ent.bits == 8 and ent.rsv == pw.PW_FMT_APL and ent.state == pw.PW_PAGE_RESIDENT
+        got = L.page_image(e, p, rb)
+        assert got.size == apl.page_bytes(cfg.R, kdim(p), 8)
+        assert np.array_equal(got, pages[(e, p, rb)][0]), (e, p, rb)
+    e16, e32 = _forward_check(L, cfg, _effective_w16(cfg, w16, bits, pages))
+    assert e16 <= TOL16 and e32 <= TOL32, (e16, e32)
+    # raising again from a copy of the committed bitwidth is refused
     with pytest.raises(pw.PWError) as ei:
-        L.offload([blk])
+        L.reload([eight[0]], stream=side)
     assert ei.value.status == 4
+    torch.cuda.synchronize()
     L.close()
 
 
