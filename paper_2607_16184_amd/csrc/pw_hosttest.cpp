@@ -52,6 +52,14 @@ int pwt_load(void* hv, int e, int proj, int rb, int bits) {
   return s;
 }
 
+int pwt_load_apl(void* hv, int e, int proj, int rb, int bits) {
+  Handle* h = static_cast<Handle*>(hv);
+  pw_page_entry ent{};
+  pw_status s = h->st.plan_load_apl(e, proj, rb, bits, &ent, &g_msg);
+  if (s == PW_OK) h->st.finish_load(e, proj, rb, ent);
+  return s;
+}
+
 // Requantize a batch; on success returns the batch's (simulated) event id.
 int pwt_requant(void* hv, int n, const int* e, const int* proj, const int* rb, const int* nb,
                 uint64_t* delta_total, uint64_t* event_id) {

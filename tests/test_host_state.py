@@ -9,6 +9,7 @@ import os
 import pytest
 
 import oracle
+from oracle import apl
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIBP = os.path.join(os.path.dirname(HERE), "paper_2607_16184_amd", "libpw_hosttest.so")
@@ -33,6 +34,7 @@ def L():
     lib.pwt_create.argtypes = [ctypes.POINTER(Desc), ctypes.c_uint64]
     lib.pwt_destroy.argtypes = [ctypes.c_void_p]
     lib.pwt_load.argtypes = [ctypes.c_void_p] + [ctypes.c_int] * 4
+    lib.pwt_load_apl.argtypes = [ctypes.c_void_p] + [ctypes.c_int] * 4
     ip = ctypes.POINTER(ctypes.c_int)
     lib.pwt_requant.argtypes = [ctypes.c_void_p, ctypes.c_int, ip, ip, ip, ip,
                                 ctypes.POINTER(ctypes.c_uint64), ctypes.POINTER(ctypes.c_uint64)]
@@ -56,6 +58,7 @@ def L():
 
 
 R, G, E, H, F = 64, 64, 2, 256, 512
+PW_FMT_APL = 1
 
 
 class Layer:
@@ -66,6 +69,9 @@ class Layer:
 
     def load(self, e, p, rb, b):
         return self.lib.pwt_load(self.h, e, p, rb, b)
+
+    def load_apl(self, e, p, rb, b):
+        return self.lib.pwt_load_apl(self.h, e, p, rb, b)
 
     def requant(self, blocks, nb):
         n = len(blocks)
@@ -291,6 +297,70 @@ def test_offload_lower_reload_cycle(L):
     L.pwt_complete(Lx.h, oev)
     L.pwt_reclaim(Lx.h)
     assert Lx.host_stats()[1] == 0 and Lx.stats()[3] == 0   # every slot and event released
+    Lx.close()
+
+
+def test_bitplane_offload_lower_reload_cycle(L):
+    """Sec. 3.1 with nested bit-plane pages (Sec. 3.2, Eq. 3): the host copy
+    is the whole committed page (planes and LUTs), the 8 -> 4 drop frees the
+    page tail in place, and the reload brings the whole 8-bit page back into
+    a fresh slot, with LUT_4 right after planes 0-3 as in a loaded page."""
+    K = H                                              # gate rows read H inputs
+    a8, a4 = apl.page_bytes(R, K, 8), apl.page_bytes(R, K, 4)
+    assert a8 == R * K + 544 * R and a4 == R * K // 2 + 32 * R
+    Lx = Layer(L, 3 * _slot(a8) + _slot(oracle.page_bytes(R, K, G, 16)))
+    assert Lx.load_apl(0, 0, 0, 8) == 0 and Lx.load_apl(0, 0, 1, 4) == 0
+    assert Lx.load_apl(0, 0, 0, 8) == 3                # already present
+    assert Lx.load_apl(0, 0, 2, 16) == 1               # bit-plane pages hold 8 or 4 bits
+    assert Lx.load(1, 0, 0, 16) == 0
+    ld = Lx.entry(0, 0, 0)
+    assert (ld.bits, ld.rsv, ld.sz_off) == (8, PW_FMT_APL, ld.data_off + R * K // 2)
+    L.pwt_set_host_pool(Lx.h, 4 * _slot(a8))
+    st, oev = Lx.offload([(0, 0, 0), (0, 0, 1)])
+    assert st == 0 and oev != 0
+    assert Lx.host_stats()[1] == _slot(a8) + _slot(a4)  # each copy is its committed page
+    assert Lx.host_copy(0, 0, 0)[0] == 8 and Lx.host_copy(0, 0, 1)[0] == 4
+    assert Lx.offload([(0, 0, 0)]) == (0, 0)            # same bitwidth and format: no-op
+    # 8 -> 4 in place: the slot keeps planes 0-3 and LUT_4, the tail retires after the commit
+    st, d, _ = Lx.requant([(0, 0, 0)], 4)
+    assert st == 0 and d == a8 - a4
+    n, cev = Lx.commit()
+    assert n == 1 and L.pwt_reclaim(Lx.h) == 0
+    L.pwt_complete(Lx.h, cev)
+    assert L.pwt_reclaim(Lx.h) == a8 - a4
+    low = Lx.entry(0, 0, 0)
+    assert (low.bits, low.rsv, low.data_off, low.sz_off, low.gen) == (4, PW_FMT_APL, ld.data_off, ld.sz_off, 2)
+    assert Lx.requant([(0, 0, 0)], 8)[0] == 4           # raising needs the host copy
+    free0 = Lx.stats()[1]
+    st, added, rev = Lx.reload([(0, 0, 0)])
+    assert st == 0 and added == a8 - a4 and rev not in (0, oev)
+    assert Lx.entry(0, 0, 0).state == 3 and Lx.stats()[1] == free0 - _slot(a8)
+    n, cev2 = Lx.commit()
+    cur = Lx.entry(0, 0, 0)
+    assert (cur.bits, cur.rsv, cur.state, cur.gen) == (8, PW_FMT_APL, 1, 3)
+    assert cur.data_off != low.data_off and cur.sz_off == cur.data_off + R * K // 2
+    L.pwt_complete(Lx.h, cev2)
+    assert L.pwt_reclaim(Lx.h) == a4                    # the 4-bit prefix retires
+    assert Lx.stats()[1] == free0 - _slot(a8) + _slot(a4)
+    # a 4-bit page has no higher copy to reload; offloading it again at 4 bits replaces nothing
+    assert Lx.reload([(0, 0, 1)])[0] == 4
+    # the reloaded page can be lowered again, and a copy of the lower page replaces the 8-bit one
+    assert Lx.requant([(0, 0, 0)], 4)[0] == 0
+    n, cev3 = Lx.commit()
+    L.pwt_complete(Lx.h, cev3)
+    L.pwt_complete(Lx.h, rev)
+    L.pwt_reclaim(Lx.h)
+    st, oev2 = Lx.offload([(0, 0, 0)])
+    assert st == 0 and Lx.host_copy(0, 0, 0)[0] == 4
+    L.pwt_complete(Lx.h, oev)
+    L.pwt_complete(Lx.h, oev2)
+    L.pwt_reclaim(Lx.h)
+    assert Lx.host_stats()[1] == 2 * _slot(a4)
+    assert Lx.reload([(0, 0, 0)])[0] == 4               # copy not above the committed bitwidth
+    for blk in ((0, 0, 0), (0, 0, 1)):
+        assert L.pwt_drop_host_copy(Lx.h, *blk) == 0
+    L.pwt_reclaim(Lx.h)
+    assert Lx.host_stats()[1] == 0 and Lx.stats()[3] == 0
     Lx.close()
 
 
