@@ -619,6 +619,33 @@ def leg_apl(steps=20):
             "weight_GBps_after": round(wbytes1 / (step1 * 1e-3) / 1e9, 1)}
 
 
+def leg_bitwidths(steps=30, warmup=5):
+    """The decode layer with every page at one bitwidth (16, 8, 4) beside the
+    50/25/25 % mix: per-format rates of the paged GEMMs, counted over the pages
+    of the experts the step routes to."""
+    import numpy as np
+    import torch
+    from paper_2607_16184_amd import synth
+    cfg = synth.CONFIGS["mixtral_decode"]
+    w16 = [synth.expert_weights(cfg, p) for p in range(3)]
+    mixed = synth.bitmap(cfg)
+    logits = torch.from_numpy(synth.logits(cfg)).cuda()
+    x = torch.from_numpy(synth.activations(cfg).view(np.int16)).cuda()
+    res = {"workload": "mixtral_decode layer, 64-token steps, every page at one bitwidth vs the mix"}
+    for name, b in (("mix", None), ("all16", 16), ("all8", 8), ("all4", 4)):
+        bits = mixed if b is None else [np.full_like(bp, b) for bp in mixed]
+        L = build_layer(cfg, w16=w16, bits=bits)[0]
+        r = time_steps(L, cfg, x, logits, steps, warmup)
+        L.close()
+        per = page_bytes_active(cfg, bits, r["counts"])
+        km = r["kernel_ms"]
+        res[name] = {"step_ms": round(r["event_ms"], 4), "gateup_ms": round(km["gateup"], 4),
+                     "gateup_page_GBps": round((per[0] + per[1]) / (km["gateup"] * 1e-3) / 1e9, 1),
+                     "down_ms": round(km["down"], 4),
+                     "down_page_GBps": round(per[2] / (km["down"] * 1e-3) / 1e9, 1)}
+    return res
+
+
 def leg_ceilings(reps=5):
     """What the device delivers: a plain streaming read of 4 GiB (16-byte
     nontemporal loads, 8 workgroups per CU) and back-to-back independent
@@ -666,7 +693,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="mixtral_decode")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--extras", default="ceilings,prefill,finegrained,downshift,offload,planner,apl",
+    ap.add_argument("--extras", default="ceilings,bitwidths,prefill,finegrained,downshift,offload,planner,apl",
                     help="comma list of extra legs on the same JSON line ('' for none)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after the timed steps, run one device copy of this many MiB "
@@ -755,6 +782,8 @@ def main():
         t0 = time.time()
         if leg == "ceilings":
             extras["ceilings"] = leg_ceilings()
+        elif leg == "bitwidths":
+            extras["bitwidths"] = leg_bitwidths()
         elif leg == "prefill":
             extras["prefill"] = leg_layer("mixtral_prefill", steps=20, warmup=2)
         elif leg == "finegrained":
