@@ -99,8 +99,8 @@ typedef struct {
 
 /* Layer shape. act is the activation dtype (and the dtype of 16-bit pages);
  * sdt the dtype of scales and zeros. Constraints: R a multiple of 64;
- * F and H multiples of R and of 128; G a multiple of 32 dividing 128 or a
- * multiple of 128, and dividing F and H.                                   */
+ * F and H multiples of R and of 128; G one of 64, 128, 256, 512 dividing F
+ * and H (PW_EINVAL otherwise).                                             */
 typedef struct {
     int E, H, F, R, G;
     int act;
@@ -116,19 +116,28 @@ size_t pw_table_entries(const pw_layer_desc* desc);
 /* Bytes of one page of projection `proj` at `bits` (Eq. 3's M_i^b). */
 pw_status pw_page_bytes(const pw_layer_desc* desc, int proj, int bits, size_t* bytes);
 
-/* Create a layer over a caller-owned pool [pool_dev, pool_dev + pool_bytes)
- * (256-byte aligned) and device table table_dev (pw_table_entries entries).
- * The table is cleared to absent entries on the null stream.              */
+/* Sec. 3.1 (weight page table: one row per block with its committed
+ * bitwidth and memory size). Create a layer over a caller-owned pool
+ * [pool_dev, pool_dev + pool_bytes) (256-byte aligned) and device table
+ * table_dev (pw_table_entries entries, 8-byte aligned). The table is cleared
+ * to absent entries on the null stream, which is synchronized.
+ *   bad shape (see pw_layer_desc), null or misaligned pointers: PW_EINVAL.
+ *   clearing the table failed: PW_EHIP (no handle is returned).            */
 pw_status pw_layer_create(const pw_layer_desc* desc, void* pool_dev, size_t pool_bytes,
                           pw_page_entry* table_dev, pw_layer** out);
 
 /* Destroy the handle (waits for the library's events). */
 pw_status pw_layer_destroy(pw_layer* layer);
 
-/* Place page (e, proj, rb) into a fresh pool slot at `bits`: rows16_dev holds
- * the page's R x K 16-bit values (act dtype, row-major, device memory, read
- * on `stream`). 16 -> copied; 8/4 -> quantized on the GPU. The table entry is
- * written on `stream` after the data. The page must be absent.             */
+/* Sec. 3.1 (a block's page at its bitwidth q_i, placed in the pool and
+ * described by its table row). Place page (e, proj, rb) into a fresh pool
+ * slot at `bits`: rows16_dev holds the page's R x K 16-bit values (act dtype,
+ * row-major, device memory, read on `stream`). 16 -> copied; 8/4 ->
+ * quantized on the GPU. The table entry is written on `stream` after the
+ * data; later work on another stream must be ordered after `stream`.
+ *   bad block or bits: PW_EINVAL.  page present: PW_EBUSY.
+ *   no free slot: PW_ENOMEM.  launch failed: PW_EHIP (the slot is released
+ *   after `stream` drained).                                               */
 pw_status pw_layer_load_page(pw_layer* layer, int e, int proj, int rb, int bits,
                              const void* rows16_dev, void* stream);
 
@@ -142,7 +151,8 @@ pw_status pw_layer_load_page(pw_layer* layer, int e, int proj, int rb, int bits,
  *   sorted_slot [T*K] int32 out: slots s = t*K + k grouped by expert, in
  *            increasing s within an expert
  *   slot_pos [T*K] int32 out: inverse permutation of sorted_slot
- * Constraints: 1 <= K <= E <= 1024, K <= 16, T*K < 2^31.                   */
+ * Constraints: 1 <= K <= E <= 256, K <= 16, T*K < 2^31 (PW_EINVAL
+ * otherwise). T = 0 writes offsets only.                                    */
 pw_status pw_route_topk(const float* logits, int T, int E, int K, int renorm,
                         int32_t* topk_ids, float* topk_w, int32_t* offsets,
                         int32_t* sorted_slot, int32_t* slot_pos, void* stream);
@@ -159,6 +169,8 @@ pw_status pw_workspace_bytes(const pw_layer* layer, int T, int K, size_t* gemm_w
  *   topk_w, offsets, sorted_slot, slot_pos: as produced by pw_route_topk.
  *   ws: device workspace of at least pw_workspace_bytes bytes.
  * Requires every page of the layer to be present (PW_ESTATE otherwise).
+ * Sizes: T*K < 2^31, and T*K*max(F, H)*2 < 2^32 (32-bit row offsets in the
+ * kernels; PW_EUNSUPPORTED otherwise: split the batch).
  * Deterministic: no floating-point atomics; a fixed summation order.      */
 pw_status pw_moe_paged_gemm(const pw_layer* layer, const void* x, int T, int K,
                             const float* topk_w, const int32_t* offsets,
@@ -176,8 +188,11 @@ pw_status pw_moe_paged_gemm(const pw_layer* layer, const void* x, int T, int K,
 pw_status pw_requant_block(pw_layer* layer, int e, int proj, int rb, int new_bits,
                            void* side_stream, size_t* delta_bytes);
 
-/* Batched form of pw_requant_block over n blocks (one kernel launch per 64
- * blocks). On error no block of the batch is left pending.               */
+/* Batched form of pw_requant_block over n blocks (one kernel launch per 32
+ * blocks). On error no block of the batch is left pending.
+ * Ordering: the kernels read the source pages on side_stream; the caller
+ * orders side_stream after the stream that loaded or last wrote them (the
+ * library itself waits only for host-copy transfers of those pages).     */
 pw_status pw_requant_blocks(pw_layer* layer, int n, const int* e, const int* proj,
                             const int* rb, const int* new_bits, void* side_stream,
                             size_t* delta_bytes_total);
@@ -232,15 +247,24 @@ pw_status pw_host_copy_info(pw_layer* layer, int e, int proj, int rb, int* bits,
 /* Host pool capacity and bytes in host slots. */
 pw_status pw_host_pool_stats(const pw_layer* layer, size_t* capacity, size_t* used);
 
-/* Publish every pending requantization and reload, ordered on main_stream
- * after its transfer finished: the device entries are rewritten by a kernel
- * on main_stream, the host mirror updated, and the old slots retired until
- * main_stream passes the commit. *n_committed may be NULL.               */
+/* Sec. 3.3 (page movement becomes visible only at a safe boundary between
+ * kernel steps) and Sec. 3.1 (offload order: the lower bitwidth is committed
+ * before the old pages are freed). Publish every pending requantization and
+ * reload, ordered on main_stream after its transfer finished: the device
+ * entries are rewritten by a kernel on main_stream, the host mirror updated,
+ * and the old slots retired until main_stream passes the commit. A GEMM
+ * enqueued on main_stream before the commit reads the old entries, one after
+ * it the new ones. *n_committed may be NULL.
+ *   a launch or event failed: PW_EHIP; the device entries are put back to
+ *   the committed ones and the blocks stay pending.                        */
 pw_status pw_commit(pw_layer* layer, void* main_stream, int* n_committed);
 
-/* Return retired slots whose commit has completed to the pool's free list
- * (and dropped host slots whose last transfer completed to the host pool).
- * *bytes_freed (may be NULL) receives the device bytes returned.          */
+/* Sec. 3.1 (freed weight pages go back to the memory the KV cache draws
+ * from; Eq. 3's Delta = M^b - M^b' per lowered block). Return retired slots
+ * whose commit has completed to the pool's free list (and dropped host slots
+ * whose last transfer completed to the host pool). Never blocks.
+ * *bytes_freed (may be NULL) receives the device bytes returned (whole
+ * 256-byte granules; every page size of a valid layer is such a multiple). */
 pw_status pw_reclaim(pw_layer* layer, size_t* bytes_freed);
 
 /* Host-mirror view of one entry. */

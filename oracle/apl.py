@@ -75,12 +75,41 @@ def _update(c: np.ndarray, n: np.ndarray, s: np.ndarray) -> np.ndarray:
     return c
 
 
+def split_level(v: np.ndarray, a: np.ndarray, c: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
+    """One bit of upscaling. v [R,K] values, a [R,K] their parent cluster
+    (0 .. P-1), c [R,P] the parent centroids. Every parent p with members gets
+    two children initialised at (lo_p + m_p)/2 and (m_p + hi_p)/2 (lo_p, hi_p,
+    m_p the members' minimum, maximum and mean); SPLIT_ITERS Lloyd iterations
+    move each member between its parent's two children (child 1 only when it
+    is strictly nearer); a final assignment gives the code 2p + child. A
+    parent without members passes its centroid to both children. Returns
+    (codes [R,K], child centroids [R,2P])."""
+    R, K = v.shape
+    P = c.shape[1]
+    r = np.arange(R)[:, None]
+    # parent statistics: members' count, sum (in order of k), minimum, maximum
+    n, s = _cluster_sums(v, a, P)
+    pmin = np.full((R, P), np.inf)
+    pmax = np.full((R, P), -np.inf)
+    rows = np.repeat(np.arange(R), K)
+    np.minimum.at(pmin, (rows, a.reshape(-1)), v.reshape(-1))
+    np.maximum.at(pmax, (rows, a.reshape(-1)), v.reshape(-1))
+    has = n > 0
+    mean = np.where(has, s / np.maximum(n, 1), c)
+    ch = np.empty((R, 2 * P))
+    ch[:, 0::2] = np.where(has, (pmin + mean) / 2.0, c)
+    ch[:, 1::2] = np.where(has, (mean + pmax) / 2.0, c)
+    for _ in range(SPLIT_ITERS):
+        pick = (np.abs(v - ch[r, 2 * a + 1]) < np.abs(v - ch[r, 2 * a])).astype(np.int64)
+        ch = _update(ch, *_cluster_sums(v, 2 * a + pick, 2 * P))
+    pick = (np.abs(v - ch[r, 2 * a + 1]) < np.abs(v - ch[r, 2 * a])).astype(np.int64)
+    return 2 * a + pick, ch
+
+
 def quantize_rows(v: np.ndarray) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
     """(8-bit codes [R,K] uint8, level-4 centroids [R,16], level-8 centroids
     [R,256]) of rows v (float64, the 16-bit weights' values)."""
     v = np.asarray(v, np.float64)
-    R, K = v.shape
-    r = np.arange(R)[:, None]
     lo, hi = v.min(axis=1), v.max(axis=1)
     c = lo[:, None] + (hi - lo)[:, None] * ((2.0 * np.arange(16) + 1.0) / 32.0)[None, :]
     for _ in range(SEED_ITERS):
@@ -88,26 +117,8 @@ def quantize_rows(v: np.ndarray) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
         c = _update(c, *_cluster_sums(v, a, 16))
     a = _assign(v, c)
     c4 = c.copy()
-    for level in range(SEED_BITS + 1, MAX_BITS + 1):
-        P = 1 << (level - 1)
-        # parent statistics: members' count, sum (in order of k), minimum, maximum
-        n, s = _cluster_sums(v, a, P)
-        pmin = np.full((R, P), np.inf)
-        pmax = np.full((R, P), -np.inf)
-        rows = np.repeat(np.arange(R), K)
-        np.minimum.at(pmin, (rows, a.reshape(-1)), v.reshape(-1))
-        np.maximum.at(pmax, (rows, a.reshape(-1)), v.reshape(-1))
-        has = n > 0
-        mean = np.where(has, s / np.maximum(n, 1), c)
-        ch = np.empty((R, 2 * P))
-        ch[:, 0::2] = np.where(has, (pmin + mean) / 2.0, c)
-        ch[:, 1::2] = np.where(has, (mean + pmax) / 2.0, c)
-        for _ in range(SPLIT_ITERS):
-            pick = (np.abs(v - ch[r, 2 * a + 1]) < np.abs(v - ch[r, 2 * a])).astype(np.int64)
-            ch = _update(ch, *_cluster_sums(v, 2 * a + pick, 2 * P))
-        pick = (np.abs(v - ch[r, 2 * a + 1]) < np.abs(v - ch[r, 2 * a])).astype(np.int64)
-        a = 2 * a + pick
-        c = ch
+    for _level in range(SEED_BITS + 1, MAX_BITS + 1):
+        a, c = split_level(v, a, c)
     return a.astype(np.uint8), c4, c
 
 

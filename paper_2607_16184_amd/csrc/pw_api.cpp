@@ -152,6 +152,11 @@ WsLayout ws_layout(const pw_layer_desc& d, int T, int K, bool apl) {
   return w;
 }
 
+// Waits until the work already enqueued on `st` has finished, so that slots
+// its kernels or copies write can be released after a later step of the same
+// call failed (a failing call must not hand out memory still being written).
+void drain(hipStream_t st) { (void)hipStreamSynchronize(st); }
+
 pw_status check_hip_last(const char* what) {
   hipError_t e = hipGetLastError();
   return e == hipSuccess ? PW_OK : hip_fail(e, what);
@@ -240,7 +245,6 @@ pw_status pw_layer_create(const pw_layer_desc* d, void* pool_dev, size_t pool_by
   if (!d || !out || !pool_dev || !table_dev) return fail(PW_EINVAL, "null argument");
   *out = nullptr;
   if (!pw::LayerState::valid_desc(*d, &err)) return fail(PW_EINVAL, err);
-  if (d->G > 512 || (d->G % 64)) return fail(PW_EUNSUPPORTED, "G must be 64, 128, 256 or 512");
   if (!mult_of_256(pool_dev)) return fail(PW_EINVAL, "pool must be 256-byte aligned");
   if (reinterpret_cast<uintptr_t>(table_dev) & 7u) return fail(PW_EINVAL, "table must be 8-byte aligned");
   pw_layer* L = new pw_layer(*d, pool_dev, pool_bytes, table_dev);
@@ -284,12 +288,9 @@ pw_status pw_layer_load_page(pw_layer* L, int e, int proj, int rb, int bits, con
   j.dst_bits = static_cast<uint8_t>(bits);
   j.src_plain = 1;
   s = run_qjobs(L, {j}, st);
+  if (s == PW_OK) s = write_entries(L, {{L->st.index(e, proj, rb), ent}}, st);
   if (s != PW_OK) {
-    L->st.abort_slot(ent, proj);
-    return s;
-  }
-  s = write_entries(L, {{L->st.index(e, proj, rb), ent}}, st);
-  if (s != PW_OK) {
+    drain(st);
     L->st.abort_slot(ent, proj);
     return s;
   }
@@ -364,6 +365,7 @@ pw_status pw_layer_load_pages_apl(pw_layer* L, int n, const int* e, const int* p
     hipError_t he = pw::launch_apl_quant(b, st);
     if (he == hipSuccess) he = pw::launch_apl_pack(b, st);
     if (he != hipSuccess) {
+      drain(st);
       rollback(n);
       return hip_fail(he, "bit-plane quantization launch");
     }
@@ -372,6 +374,7 @@ pw_status pw_layer_load_pages_apl(pw_layer* L, int n, const int* e, const int* p
   for (int i = 0; i < n; ++i) w.push_back({L->st.index(e[i], proj[i], rb[i]), ents[i]});
   pw_status s = write_entries(L, w, st);
   if (s != PW_OK) {
+    drain(st);
     rollback(n);
     return s;
   }
@@ -448,6 +451,12 @@ pw_status pw_moe_paged_gemm(const pw_layer* Lc, const void* x, int T, int K, con
     return fail(PW_EINVAL, "null argument");
   if (!L->st.all_present()) return fail(PW_ESTATE, "every page of the layer must be loaded");
   if (static_cast<int64_t>(T) * K >= (int64_t(1) << 31)) return fail(PW_EINVAL, "T*K too large");
+  {
+    // the GEMM kernels address activation and SwiGLU rows with 32-bit byte offsets
+    const uint64_t S = static_cast<uint64_t>(T) * K, lim = uint64_t(1) << 32;
+    if (S * L->st.desc.F * 2 >= lim || S * L->st.desc.H * 2 >= lim)
+      return fail(PW_EUNSUPPORTED, "T*K*max(F,H)*2 must stay below 2^32 (split the batch)");
+  }
   const WsLayout wl = ws_layout(L->st.desc, T, K, L->st.n_apl > 0);
   if (L->st.n_apl > 0) {
     const pw_layer_desc& dd = L->st.desc;
@@ -582,17 +591,20 @@ pw_status pw_requant_blocks(pw_layer* L, int n, const int* e, const int* proj, c
   }
   pw_status rs = run_qjobs(L, jobs, st);
   if (rs != PW_OK) {
+    drain(st);
     rollback();
     return rs;
   }
   void* ev = L->evops.create();
   if (!ev) {
+    drain(st);
     rollback();
     return fail(PW_EHIP, "hipEventCreate failed");
   }
   hipError_t he = hipEventRecord(static_cast<hipEvent_t>(ev), st);
   if (he != hipSuccess) {
     L->evops.destroy(ev);
+    drain(st);
     rollback();
     return hip_fail(he, "hipEventRecord");
   }
@@ -683,6 +695,7 @@ pw_status pw_offload_blocks(pw_layer* L, int n, const int* e, const int* proj, c
     hipError_t he = hipMemcpyAsync(L->host_pool + p.host_off, L->pool + p.src.data_off,
                                    L->st.entry_bytes(p.proj, p.src), hipMemcpyDeviceToHost, st);
     if (he != hipSuccess) {
+      drain(st);
       rollback();
       return hip_fail(he, "device-to-host page copy");
     }
@@ -690,6 +703,7 @@ pw_status pw_offload_blocks(pw_layer* L, int n, const int* e, const int* proj, c
   pw_status s = PW_OK;
   void* ev = record_event(L, st, &s);
   if (!ev) {
+    drain(st);
     rollback();
     return s;
   }
@@ -748,6 +762,7 @@ pw_status pw_reload_blocks(pw_layer* L, int n, const int* e, const int* proj, co
     hipError_t he = hipMemcpyAsync(L->pool + p.dst.data_off, L->host_pool + p.hc.off,
                                    L->st.host_bytes(p.proj, p.hc), hipMemcpyHostToDevice, st);
     if (he != hipSuccess) {
+      drain(st);
       rollback();
       return hip_fail(he, "host-to-device page copy");
     }
@@ -755,6 +770,7 @@ pw_status pw_reload_blocks(pw_layer* L, int n, const int* e, const int* proj, co
   pw_status s = PW_OK;
   void* ev = record_event(L, st, &s);
   if (!ev) {
+    drain(st);
     rollback();
     return s;
   }
@@ -879,14 +895,37 @@ pw_status pw_commit(pw_layer* L, void* main_stream, int* n_committed) {
   }
   std::vector<std::pair<size_t, pw_page_entry>> w;
   for (const auto& p : pend) w.push_back({p.idx, pw::LayerState::published(p.next)});
+  // On a failure after part of the table was rewritten, the device entries
+  // are put back to the committed ones of the host mirror (which the failed
+  // call leaves unchanged) before the error is returned.
+  auto restore = [&]() {
+    std::vector<std::pair<size_t, pw_page_entry>> old;
+    for (const auto& p : pend) {
+      pw_page_entry cur = L->st.mirror[p.idx];
+      cur.state = PW_PAGE_RESIDENT;
+      old.push_back({p.idx, cur});
+    }
+    const std::string keep = g_err;
+    (void)write_entries(L, old, st);
+    drain(st);
+    g_err = keep;
+  };
   pw_status s = write_entries(L, w, st);
-  if (s != PW_OK) return s;
+  if (s != PW_OK) {
+    restore();
+    return s;
+  }
   void* cev = L->evops.create();
-  if (!cev) return fail(PW_EHIP, "hipEventCreate failed");
+  if (!cev) {
+    restore();
+    return fail(PW_EHIP, "hipEventCreate failed");
+  }
   hipError_t he = hipEventRecord(static_cast<hipEvent_t>(cev), st);
   if (he != hipSuccess) {
     L->evops.destroy(cev);
-    return hip_fail(he, "hipEventRecord");
+    s = hip_fail(he, "hipEventRecord");
+    restore();
+    return s;
   }
   const int n = static_cast<int>(pend.size());
   L->st.committed(cev);

@@ -59,8 +59,8 @@ bool LayerState::valid_desc(const pw_layer_desc& d, std::string* err) {
   if (d.R % 64) return bad("R must be a multiple of 64");
   if (d.F % d.R || d.H % d.R) return bad("F and H must be multiples of R");
   if (d.F % 128 || d.H % 128) return bad("F and H must be multiples of 128");
-  if (d.G % 32) return bad("G must be a multiple of 32");
-  if (128 % d.G && d.G % 128) return bad("G must divide 128 or be a multiple of 128");
+  // the kernels index groups by shifts and masks: G is a power of two
+  if (d.G != 64 && d.G != 128 && d.G != 256 && d.G != 512) return bad("G must be 64, 128, 256 or 512");
   if (d.F % d.G || d.H % d.G) return bad("G must divide F and H");
   if (static_cast<int64_t>(d.F) * d.H >= (int64_t(1) << 31)) return bad("F*H too large");
   return true;

@@ -60,3 +60,22 @@ def say(msg):
     """Name the case before a GPU step, flushed (survives a lost box)."""
     sys.stdout.write("[case] %s\n" % msg)
     sys.stdout.flush()
+
+
+def assert_all_pages_equal(L, O, cfg, blocks=None):
+    """Every page (or the listed (e, p, rb) blocks) of GPU layer L byte-identical
+    to the oracle layer O's page image. The pool is copied to the host once."""
+    pool = L._pool_t.cpu().numpy()
+    base = L.pool_ptr - L._pool_t.data_ptr()
+    if blocks is None:
+        blocks = [(e, p, rb) for p in range(3) for e in range(cfg.E) for rb in range(cfg.nrb(p))]
+    bad = []
+    for (e, p, rb) in blocks:
+        ent = L.entry(e, p, rb)
+        want = O.page_image(p, e, rb)
+        assert int(ent.bits) == int(O.bits[p][e, rb]), (e, p, rb)
+        got = pool[base + ent.data_off:base + ent.data_off + want.size]
+        if not np.array_equal(got, want):
+            bad.append((e, p, rb))
+    assert not bad, "%d of %d pages differ, first %s" % (len(bad), len(blocks), bad[:4])
+    return len(blocks)

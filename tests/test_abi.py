@@ -56,3 +56,22 @@ def test_host_validation_without_gpu():
         pw.pw_layer_create(pw.pw_layer_desc(8, 256, 512, 64, 64, 0, 0), 0, 0, 0)
     assert ei.value.status == pw.PW_EINVAL
     assert "null" in pw.pw_last_error()
+
+
+@pytest.mark.parametrize("G", [32, 96, 192, 384, 1024])
+def test_group_size_outside_the_kernels_set_is_refused(G):
+    """The kernels index groups with shifts and masks: only G = 64, 128, 256,
+    512 are accepted; any other value is refused before a layer exists."""
+    from paper_2607_16184_amd import pw
+    d = pw.pw_layer_desc(8, 3072, 6144, 128, G, pw.PW_BF16, pw.PW_BF16)
+    with pytest.raises(pw.PWError) as ei:
+        pw.pw_page_bytes(d, pw.PW_GATE, 8)
+    assert ei.value.status == pw.PW_EINVAL
+    assert "G must be" in pw.pw_last_error()
+
+
+@pytest.mark.parametrize("G", [64, 128, 256, 512])
+def test_power_of_two_group_sizes_are_accepted(G):
+    from paper_2607_16184_amd import pw
+    d = pw.pw_layer_desc(8, 3072, 6144, 128, G, pw.PW_BF16, pw.PW_BF16)
+    assert pw.pw_page_bytes(d, pw.PW_GATE, 4) == oracle.page_bytes(128, 3072, G, 4)

@@ -252,3 +252,36 @@ def test_apl_mixtral_sampled_pages():
     torch.cuda.synchronize()
     assert torch.equal(y1, y2) and bool(torch.isfinite(y1).all())
     L.close()
+
+
+def test_apl_mixtral_forward_full():
+    """The Mixtral-shaped decode layer (4096/14336, 64 tokens) with two
+    bit-plane pages per projection and precision and every other page 16-bit:
+    the layer then runs the streaming kernel for both GEMMs with 32-slot tiles
+    and the down projection split over K, as the benchmark's bit-plane leg
+    does. Every token of the output is compared with the oracle's dense MoE of
+    the reconstructed weights."""
+    import torch
+    cfg = synth.CONFIGS["mixtral_decode"]
+    w16 = [synth.expert_weights(cfg, p) for p in range(3)]
+    bits = [np.full_like(b, 16) for b in synth.bitmap(cfg)]
+    rng = np.random.default_rng(11)
+    for p in range(3):
+        cand = [(e, rb) for e in range(cfg.E) for rb in range(cfg.nrb(p))]
+        pick = rng.permutation(len(cand))[:4]
+        for j, i in enumerate(pick):
+            e, rb = cand[i]
+            bits[p][e, rb] = 8 if j < 2 else 4
+    say("bit-plane Mixtral forward: 12 bit-plane pages, rest 16-bit")
+    L = _layer(cfg, w16, bits, slack=0.05)
+    pages = _oracle_pages(cfg, w16, bits)
+    assert len(pages) == 12
+    for (e, p, rb), (buf, _, _, _) in pages.items():
+        got = L.page_image(e, p, rb)
+        assert np.array_equal(got, buf[:got.size]), (e, p, rb)
+    eff = _effective_w16(cfg, w16, bits, pages)
+    say("bit-plane Mixtral forward: oracle on all 64 tokens")
+    e16, e32 = _forward_check(L, cfg, eff)
+    assert e16 <= TOL16 and e32 <= TOL32, (e16, e32)
+    torch.cuda.synchronize()
+    L.close()

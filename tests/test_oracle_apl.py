@@ -2,6 +2,8 @@
 representable 16-level row), the nesting of codes and LUTs, the squared-error
 order of the two precisions, a bit-by-bit placement check of the page
 layout, and the page sizes of Eq. 3."""
+import os
+
 import numpy as np
 
 import oracle
@@ -93,3 +95,46 @@ def test_dequant_uses_the_committed_precision():
         np.testing.assert_array_equal(lt, lut)
         w = apl.dequant(codes, lt, bits)
         np.testing.assert_array_equal(w, np.take_along_axis(lut, (codes >> (8 - bits)).astype(np.int64), 1))
+
+
+def _golden(name):
+    out = {}
+    for line in open(os.path.join(os.path.dirname(__file__), "golden", name)):
+        line = line.split("#", 1)[0].strip()
+        if "=" in line:
+            k, v = line.split("=", 1)
+            out[k.strip()] = v.split()
+    return out
+
+
+def test_split_level_matches_hand_worked_example():
+    """The one-bit split (child initialisation, exactly 4 Lloyd iterations,
+    strict nearness for child 1, empty parent) reproduces the hand-worked
+    example in tests/golden/apl_split_example.txt bit for bit."""
+    from fractions import Fraction
+    g = _golden("apl_split_example.txt")
+    v = np.array([[float(x) for x in g["values"]]])
+    a = np.array([[int(x) for x in g["parents"]]])
+    c = np.array([[float(x) for x in g["centroids"]]])
+    codes, ch = apl.split_level(v, a, c)
+    assert codes.tolist() == [[int(x) for x in g["codes"]]]
+    want = [float(Fraction(x)) for x in g["child_centroids"]]
+    assert ch.tolist() == [want]
+
+
+def test_split_iteration_count_is_visible():
+    """The example discriminates the iteration count: 3 or 5 Lloyd
+    iterations give other codes than the 4 the reading fixes."""
+    g = _golden("apl_split_example.txt")
+    v = np.array([[float(x) for x in g["values"]]])
+    a = np.array([[int(x) for x in g["parents"]]])
+    c = np.array([[float(x) for x in g["centroids"]]])
+    want = [int(x) for x in g["codes"]]
+    saved = apl.SPLIT_ITERS
+    try:
+        for n in (3, 5):
+            apl.SPLIT_ITERS = n
+            codes, _ = apl.split_level(v, a, c)
+            assert codes.tolist() != [want], n
+    finally:
+        apl.SPLIT_ITERS = saved
