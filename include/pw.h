@@ -177,6 +177,24 @@ pw_status pw_moe_paged_gemm(const pw_layer* layer, const void* x, int T, int K,
                             const int32_t* sorted_slot, const int32_t* slot_pos,
                             void* y, int out_fp32, void* ws, size_t ws_bytes, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops or harnesses that forbid hipMalloc): the forward of
+ * pw_moe_paged_gemm with its workspace taken from a static device array of
+ * the library instead of `ws`, so the call allocates nothing. Arguments,
+ * kernels and results are those of pw_moe_paged_gemm. The array holds
+ * 64 MiB on each GPU the library runs on, from that GPU's first call until
+ * the process ends; the GPU is the one `stream` belongs to. Every call on a
+ * GPU shares its array and overwrites what the last call left there (no part
+ * of it needs to start zeroed): calls that overlap on one GPU (two streams,
+ * two threads) race, and the caller serializes them.
+ *   workspace need (pw_workspace_bytes) above 64 MiB, e.g. prefill batches
+ *   of large layers: PW_ENOMEM (use pw_moe_paged_gemm).  Other errors: as
+ *   pw_moe_paged_gemm.                                                     */
+pw_status pw_moe_paged_gemm_noalloc(const pw_layer* layer, const void* x, int T, int K,
+                                    const float* topk_w, const int32_t* offsets,
+                                    const int32_t* sorted_slot, const int32_t* slot_pos,
+                                    void* y, int out_fp32, void* stream);
+
 /* Runtime downshift of one block (Sec. 3.1 offload; Sec. 3.3 asynchronous
  * page movement): requantize page (e, proj, rb) from its committed bitwidth
  * b to new_bits < b into a fresh slot on `side_stream`. The committed entry

@@ -41,6 +41,7 @@ SOURCES = {
     "pw_decode.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
     "pw_tgemm.hip": [],
     "pw_probe.hip": [],
+    "pw_scratch.hip": [],
     "pw_api.cpp": [],
     "pw_state.cpp": [],
     "pw_plan.cpp": [],

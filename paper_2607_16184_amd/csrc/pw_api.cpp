@@ -521,6 +521,29 @@ pw_status pw_moe_paged_gemm(const pw_layer* Lc, const void* x, int T, int K, con
   return PW_OK;
 }
 
+pw_status pw_moe_paged_gemm_noalloc(const pw_layer* L, const void* x, int T, int K, const float* topk_w,
+                                    const int32_t* offsets, const int32_t* sorted_slot, const int32_t* slot_pos,
+                                    void* y, int out_fp32, void* stream) {
+  if (!L) return fail(PW_EINVAL, "null layer");
+  if (T < 0 || K < 1 || K > L->st.desc.E) return fail(PW_EINVAL, "need T >= 0 and 1 <= K <= E");
+  if (T == 0) return PW_OK;
+  if (static_cast<int64_t>(T) * K >= (int64_t(1) << 31)) return fail(PW_EINVAL, "T*K too large");
+  const size_t need = ws_layout(L->st.desc, T, K, L->st.n_apl > 0).total;
+  if (need > pw::kStaticScratchBytes)
+    return fail(PW_ENOMEM, "the call needs " + std::to_string(need) + " bytes of workspace, more than the " +
+                               std::to_string(pw::kStaticScratchBytes) +
+                               "-byte static scratch: use pw_moe_paged_gemm with a workspace");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  int dev = -1;
+  hipError_t e = hipStreamGetDevice(st, &dev);
+  if (e != hipSuccess) return hip_fail(e, "hipStreamGetDevice");
+  void* ptr = nullptr;
+  e = pw::static_scratch(dev, &ptr);
+  if (e != hipSuccess) return hip_fail(e, "looking up the static scratch");
+  return pw_moe_paged_gemm(L, x, T, K, topk_w, offsets, sorted_slot, slot_pos, y, out_fp32, ptr,
+                           pw::kStaticScratchBytes, stream);
+}
+
 pw_status pw_requant_blocks(pw_layer* L, int n, const int* e, const int* proj, const int* rb,
                             const int* new_bits, void* side_stream, size_t* delta_total) {
   if (!L || n < 0 || (n > 0 && (!e || !proj || !rb || !new_bits)))

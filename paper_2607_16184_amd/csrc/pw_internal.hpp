@@ -107,6 +107,11 @@ hipError_t launch_routing_stats(const uint16_t* rows, int act, int n_rows, int d
                                 const float* topk_w, const int32_t* offsets, const int32_t* sorted_slot, int S,
                                 int E, int K, double* norm2, double* stats, int accumulate, hipStream_t st);
 
+// Static device scratch of the allocation-free GEMM entry point: its
+// capacity, and its device address on `device` (looked up once per GPU).
+constexpr size_t kStaticScratchBytes = size_t(64) << 20;
+hipError_t static_scratch(int device, void** ptr);
+
 // Error reporting of the C ABI (thread-local message, returned status).
 pw_status set_error(pw_status s, const char* msg);
 inline pw_status set_error(pw_status s, const std::string& msg) { return set_error(s, msg.c_str()); }

@@ -92,6 +92,7 @@ def _load():
         "pw_probe_mfma": (i32, [i32, i32, vp, vp]),
         "pw_workspace_bytes": (i32, [vp, i32, i32, P(sz)]),
         "pw_moe_paged_gemm": (i32, [vp, vp, i32, i32, vp, vp, vp, vp, vp, i32, vp, sz, vp]),
+        "pw_moe_paged_gemm_noalloc": (i32, [vp, vp, i32, i32, vp, vp, vp, vp, vp, i32, vp]),
         "pw_requant_block": (i32, [vp, i32, i32, i32, i32, vp, P(sz)]),
         "pw_requant_blocks": (i32, [vp, i32, P(i32), P(i32), P(i32), P(i32), vp, P(sz)]),
         "pw_layer_set_host_pool": (i32, [vp, vp, sz]),
@@ -203,6 +204,13 @@ def pw_moe_paged_gemm(layer: int, x_ptr: int, T: int, K: int, w_ptr: int, offset
                       ws_ptr: int, ws_bytes: int, stream: int):
     _check(_lib.pw_moe_paged_gemm(layer, x_ptr, T, K, w_ptr, offsets_ptr, sorted_slot_ptr,
                                   slot_pos_ptr, y_ptr, out_fp32, ws_ptr, ws_bytes, stream))
+
+
+def pw_moe_paged_gemm_noalloc(layer: int, x_ptr: int, T: int, K: int, w_ptr: int, offsets_ptr: int,
+                              sorted_slot_ptr: int, slot_pos_ptr: int, y_ptr: int, out_fp32: int,
+                              stream: int):
+    _check(_lib.pw_moe_paged_gemm_noalloc(layer, x_ptr, T, K, w_ptr, offsets_ptr, sorted_slot_ptr,
+                                          slot_pos_ptr, y_ptr, out_fp32, stream))
 
 
 def pw_requant_block(layer: int, e: int, proj: int, rb: int, new_bits: int, stream: int) -> int:
