@@ -242,6 +242,28 @@ def route(logits: np.ndarray, K: int, renorm: int = 1) -> Tuple[np.ndarray, np.n
     return ids, w
 
 
+def route_shared(logits: np.ndarray, K: int, n_shared: int, gate: Optional[np.ndarray] = None,
+                 renorm: int = 1) -> Tuple[np.ndarray, np.ndarray]:
+    """Routing of a layer whose last n_shared experts are shared experts
+    (Table 1 of the paper: MoE layers with experts every token uses beside
+    the routed ones). logits [T, E] covers the routed experts only; each
+    token gets its routed top-K (as route()) followed by the shared experts
+    E .. E + n_shared - 1 with weight gate[t, j] (1 without a gate). The
+    layer output is then the plain weighted sum over all K + n_shared
+    columns: the routed mixture plus each shared expert's FFN times its gate
+    (the reading taken here; the paper does not spell the combination out).
+    Returns ids [T, K + n_shared] int32 and weights float64."""
+    ids, w = route(logits, K, renorm)
+    T, E = np.shape(logits)
+    sid = np.tile(np.arange(E, E + n_shared, dtype=np.int32), (T, 1))
+    if gate is None:
+        sw = np.ones((T, n_shared), np.float64)
+    else:
+        sw = np.asarray(gate, np.float32).astype(np.float64).reshape(T, n_shared)
+    return (np.ascontiguousarray(np.concatenate([ids, sid], axis=1), np.int32),
+            np.ascontiguousarray(np.concatenate([w, sw], axis=1)))
+
+
 def permute(ids: np.ndarray, E: int):
     """(counts[E], offsets[E+1], sorted_slot[S], slot_pos[S]) for slot s = t*K + k."""
     ids = np.ascontiguousarray(ids, np.int32)
