@@ -157,6 +157,34 @@ pw_status pw_route_topk(const float* logits, int T, int E, int K, int renorm,
                         int32_t* topk_ids, float* topk_w, int32_t* offsets,
                         int32_t* sorted_slot, int32_t* slot_pos, void* stream);
 
+/* Shared experts (Table 1 lists MoE layers with experts every token uses
+ * beside the routed ones: 60 routed + 4 shared, 128 routed + 1 shared; the
+ * paper does not give their combination, read here as the routed sum plus
+ * each shared expert's output times a per-token gate, 1 unless the caller
+ * supplies one). A layer of E experts declares its last n_shared experts as
+ * shared (0 <= n_shared < E; 0 by default; PW_EINVAL otherwise); its pages
+ * are paged, quantized, requantized and committed like any other expert's.
+ * Routing for such a layer comes from pw_route_topk_shared, and
+ * pw_moe_paged_gemm is then called with K = routed top-K + n_shared: each
+ * token's last n_shared columns must be the shared experts (in order), its
+ * first columns routed experts only. The GEMM runs the routed and the shared
+ * experts as separate launches, each with the kernels suited to its slots
+ * per expert (a shared expert has T). No GPU work; takes effect for the
+ * next GEMM call.                                                          */
+pw_status pw_layer_set_shared_experts(pw_layer* layer, int n_shared);
+
+/* Router with shared experts: the top-K of pw_route_topk over the E routed
+ * experts' logits ([T,E] fp32), and for every token n_shared more columns,
+ * expert E + j with weight shared_gate[t * n_shared + j] (fp32 device
+ * [T, n_shared]; NULL: weight 1). topk_ids and topk_w are [T, K + n_shared];
+ * the permutation covers E + n_shared experts (offsets [E + n_shared + 1],
+ * sorted_slot and slot_pos [T (K + n_shared)]).
+ * Constraints: 1 <= K <= E, K <= 16, n_shared >= 0, E + n_shared <= 256,
+ * T (K + n_shared) < 2^31 (PW_EINVAL otherwise).                           */
+pw_status pw_route_topk_shared(const float* logits, int T, int E, int K, int renorm, int n_shared,
+                               const float* shared_gate, int32_t* topk_ids, float* topk_w,
+                               int32_t* offsets, int32_t* sorted_slot, int32_t* slot_pos, void* stream);
+
 /* Workspace bytes pw_moe_paged_gemm needs for T tokens with top-K. */
 pw_status pw_workspace_bytes(const pw_layer* layer, int T, int K, size_t* gemm_ws);
 

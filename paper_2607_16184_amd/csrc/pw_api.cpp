@@ -55,6 +55,7 @@ struct pw_layer {
   uint8_t* pool;
   pw_page_entry* table;
   uint8_t* host_pool = nullptr;   // caller's pinned host memory for page copies
+  int n_shared = 0;               // the last n_shared experts are shared experts
   bool prof = false;
   std::vector<ProfRec> recs;
   double tot_ms[PW_NPHASE] = {0, 0, 0, 0};
@@ -89,22 +90,32 @@ bool mult_of_256(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 255u)
 // Device workspace layout of pw_moe_paged_gemm.
 enum class GemmPath { kDecode, kStream, kTiled };
 
-struct WsLayout {
-  size_t h_off, h_bytes, op_off, op_bytes, total;
-  int nsplit, kb_per_split, mtb;
+// One expert range of a call, run by its own GEMM launches: the routed
+// experts [0, E - n_shared), and the shared experts (the last n_shared, each
+// used by every token). Its kernel path, the decode kernels' slot tiles per
+// pass and the down projection's K splits follow the range's own slots.
+struct RangePlan {
+  int e0, ne;          // experts [e0, e0 + ne)
+  size_t S;            // slots routed to them
   GemmPath path;
+  int nsplit, kb_per_split, mtb;
 };
 
-// Which GEMM kernels serve a call, from the expected slots per expert
-// S / E: up to 48, the decode kernels (weights streamed in registers, exact
+struct WsLayout {
+  size_t h_off, h_bytes, op_off, op_bytes, total;
+  RangePlan r[2];      // routed, shared (ne = 0 without shared experts)
+};
+
+// Which GEMM kernels serve a range, from its expected slots per expert
+// S / ne: up to 48, the decode kernels (weights streamed in registers, exact
 // code-domain arithmetic, up to four 16-slot tiles per pass); up to 127, the
 // streaming kernel with 64-slot tiles; from 128, the LDS-tiled 256 x 256
 // kernel. The last two need 32/64-row staging inside one page, 128-row down
 // blocks and 32-bit activation row offsets (and the tiled kernel 256-row down
 // blocks).
-GemmPath pick_path(const pw_layer_desc& d, size_t S, bool apl) {
-  const size_t expect = (S + d.E - 1) / d.E;
-  const bool fits = S * d.F * 2 < (size_t(1) << 32) && S * d.H * 2 < (size_t(1) << 32);
+GemmPath pick_path(const pw_layer_desc& d, size_t S, size_t S_all, int ne, bool apl) {
+  const size_t expect = (S + ne - 1) / ne;
+  const bool fits = S_all * d.F * 2 < (size_t(1) << 32) && S_all * d.H * 2 < (size_t(1) << 32);
   const bool tiles = fits && d.G >= 64 && d.R % 64 == 0 && d.F % 128 == 0;
   // nested bit-plane pages are read by the streaming kernel only
   if (apl) return GemmPath::kStream;
@@ -113,41 +124,58 @@ GemmPath pick_path(const pw_layer_desc& d, size_t S, bool apl) {
   return GemmPath::kDecode;
 }
 
-WsLayout ws_layout(const pw_layer_desc& d, int T, int K, bool apl) {
-  WsLayout w{};
-  const size_t S = static_cast<size_t>(T) * K;
+RangePlan plan_range(const pw_layer_desc& d, int e0, int ne, size_t S, size_t S_all, bool apl) {
+  RangePlan r{};
+  r.e0 = e0;
+  r.ne = ne;
+  r.S = S;
+  if (ne <= 0) {
+    r.nsplit = 1;
+    r.kb_per_split = d.F / 128;
+    r.mtb = 1;
+    return r;
+  }
   const int nkbF = d.F / 128;
-  const int expect = static_cast<int>((S + d.E - 1) / d.E);
-  w.path = pick_path(d, S, apl);
+  const int expect = static_cast<int>((S + ne - 1) / ne);
+  r.path = pick_path(d, S, S_all, ne, apl);
   // The decode kernels split the down projection's K = F when too few
   // (expert, row-block) units exist to fill the chip; deterministic in
   // (desc, T, K).
   int nsplit = 1;
-  if (w.path == GemmPath::kDecode && S <= 4096) {
-    const size_t active = std::min<size_t>(d.E, S);
+  if (r.path == GemmPath::kDecode && S <= 4096) {
+    const size_t active = std::min<size_t>(ne, S);
     const size_t units = active * (d.H / 64);
     nsplit = static_cast<int>(std::max<size_t>(1, std::min<size_t>(8, 2048 / std::max<size_t>(units, 1))));
   }
   // likewise the streaming kernel with 32-slot tiles (bit-plane layers at
   // decode sizes): 128-row down workgroups, two per CU
-  if (w.path == GemmPath::kStream && apl && expect <= 24 && S <= 4096) {
-    const size_t active = std::min<size_t>(d.E, S);
+  if (r.path == GemmPath::kStream && apl && expect <= 24 && S <= 4096) {
+    const size_t active = std::min<size_t>(ne, S);
     const size_t units = active * (d.H / 128);
     nsplit = static_cast<int>(std::max<size_t>(1, std::min<size_t>(8, 1024 / std::max<size_t>(units, 1))));
   }
   nsplit = std::min(nsplit, nkbF);
   // a split holds whole quantization groups (G = 256, 512 span 2, 4 blocks)
   const int bpg = d.G > 128 ? d.G / 128 : 1;
-  w.kb_per_split = ((nkbF + nsplit - 1) / nsplit + bpg - 1) / bpg * bpg;
-  w.nsplit = (nkbF + w.kb_per_split - 1) / w.kb_per_split;
+  r.kb_per_split = ((nkbF + nsplit - 1) / nsplit + bpg - 1) / bpg * bpg;
+  r.nsplit = (nkbF + r.kb_per_split - 1) / r.kb_per_split;
   // slot tiles per pass of the decode kernels: 1, 2 or 4 (with 4, a wave
   // streams two 16-row weight tiles)
-  w.mtb = expect <= 12 ? 1 : expect <= 20 ? 2 : 4;
+  r.mtb = expect <= 12 ? 1 : expect <= 20 ? 2 : 4;
+  return r;
+}
+
+WsLayout ws_layout(const pw_layer_desc& d, int T, int K, bool apl, int n_shared) {
+  WsLayout w{};
+  const size_t S = static_cast<size_t>(T) * K;
+  const size_t S_sh = static_cast<size_t>(T) * n_shared;
+  w.r[0] = plan_range(d, 0, d.E - n_shared, S - S_sh, S, apl);
+  w.r[1] = plan_range(d, d.E - n_shared, n_shared, S_sh, S, apl);
   auto al = [](size_t b) { return (b + 255) / 256 * 256; };
   w.h_off = 0;
   w.h_bytes = al(S * d.F * 2);
   w.op_off = w.h_bytes;
-  w.op_bytes = al(static_cast<size_t>(w.nsplit) * S * d.H * 4);
+  w.op_bytes = al(static_cast<size_t>(std::max(w.r[0].nsplit, w.r[1].nsplit)) * S * d.H * 4);
   w.total = w.h_bytes + w.op_bytes;
   return w;
 }
@@ -382,19 +410,35 @@ pw_status pw_layer_load_pages_apl(pw_layer* L, int n, const int* e, const int* p
   return PW_OK;
 }
 
-pw_status pw_route_topk(const float* logits, int T, int E, int K, int renorm, int32_t* ids,
-                        float* w, int32_t* offsets, int32_t* sorted_slot, int32_t* slot_pos,
-                        void* stream) {
-  if (T < 0 || E < 1 || K < 1 || K > E || K > 16 || E > 256)
-    return fail(PW_EINVAL, "need 1 <= K <= E <= 256, K <= 16, T >= 0");
-  if (static_cast<int64_t>(T) * K >= (int64_t(1) << 31)) return fail(PW_EINVAL, "T*K too large");
+pw_status pw_route_topk_shared(const float* logits, int T, int E, int K, int renorm, int n_shared,
+                               const float* shared_gate, int32_t* ids, float* w, int32_t* offsets,
+                               int32_t* sorted_slot, int32_t* slot_pos, void* stream) {
+  if (T < 0 || E < 1 || K < 1 || K > E || K > 16 || n_shared < 0 || E + n_shared > 256)
+    return fail(PW_EINVAL, "need 1 <= K <= E, K <= 16, n_shared >= 0, E + n_shared <= 256, T >= 0");
+  const int Kt = K + n_shared;
+  if (static_cast<int64_t>(T) * Kt >= (int64_t(1) << 31)) return fail(PW_EINVAL, "T*K too large");
   if (!offsets || (T > 0 && (!logits || !ids || !w || !sorted_slot || !slot_pos)))
     return fail(PW_EINVAL, "null argument");
   hipStream_t st = static_cast<hipStream_t>(stream);
-  hipError_t e = pw::launch_route_topk(logits, T, E, K, renorm, ids, w, st);
+  hipError_t e = pw::launch_route_topk(logits, T, E, K, renorm, n_shared, shared_gate, ids, w, st);
   if (e != hipSuccess) return hip_fail(e, "router launch");
-  e = pw::launch_permute(ids, T, K, E, offsets, sorted_slot, slot_pos, st);
+  e = pw::launch_permute(ids, T, Kt, E + n_shared, offsets, sorted_slot, slot_pos, st);
   if (e != hipSuccess) return hip_fail(e, "permute launch");
+  return PW_OK;
+}
+
+pw_status pw_route_topk(const float* logits, int T, int E, int K, int renorm, int32_t* ids,
+                        float* w, int32_t* offsets, int32_t* sorted_slot, int32_t* slot_pos,
+                        void* stream) {
+  return pw_route_topk_shared(logits, T, E, K, renorm, 0, nullptr, ids, w, offsets, sorted_slot, slot_pos,
+                              stream);
+}
+
+pw_status pw_layer_set_shared_experts(pw_layer* L, int n_shared) {
+  if (!L) return fail(PW_EINVAL, "null layer");
+  if (n_shared < 0 || n_shared >= L->st.desc.E)
+    return fail(PW_EINVAL, "need 0 <= n_shared < E (at least one routed expert)");
+  L->n_shared = n_shared;
   return PW_OK;
 }
 
@@ -435,7 +479,8 @@ pw_status pw_routing_stats(const void* rows, pw_dtype act, int n_rows, int dim, 
 
 pw_status pw_workspace_bytes(const pw_layer* L, int T, int K, size_t* gemm_ws) {
   if (!L || !gemm_ws || T < 0 || K < 1) return fail(PW_EINVAL, "bad argument");
-  *gemm_ws = ws_layout(L->st.desc, T, K, L->st.n_apl > 0).total;
+  if (L->n_shared > 0 && K <= L->n_shared) return fail(PW_EINVAL, "K must exceed the shared experts");
+  *gemm_ws = ws_layout(L->st.desc, T, K, L->st.n_apl > 0, L->n_shared).total;
   return PW_OK;
 }
 
@@ -446,6 +491,8 @@ pw_status pw_moe_paged_gemm(const pw_layer* Lc, const void* x, int T, int K, con
   pw_layer* L = const_cast<pw_layer*>(Lc);
   if (!L) return fail(PW_EINVAL, "null layer");
   if (T < 0 || K < 1 || K > L->st.desc.E) return fail(PW_EINVAL, "need T >= 0 and 1 <= K <= E");
+  if (L->n_shared > 0 && K <= L->n_shared)
+    return fail(PW_EINVAL, "K counts the routed and the shared columns: it must exceed the shared experts");
   if (T == 0) return PW_OK;
   if (!x || !topk_w || !offsets || !sorted_slot || !slot_pos || !y || !ws)
     return fail(PW_EINVAL, "null argument");
@@ -457,7 +504,7 @@ pw_status pw_moe_paged_gemm(const pw_layer* Lc, const void* x, int T, int K, con
     if (S * L->st.desc.F * 2 >= lim || S * L->st.desc.H * 2 >= lim)
       return fail(PW_EUNSUPPORTED, "T*K*max(F,H)*2 must stay below 2^32 (split the batch)");
   }
-  const WsLayout wl = ws_layout(L->st.desc, T, K, L->st.n_apl > 0);
+  const WsLayout wl = ws_layout(L->st.desc, T, K, L->st.n_apl > 0, L->n_shared);
   if (L->st.n_apl > 0) {
     const pw_layer_desc& dd = L->st.desc;
     const size_t S = static_cast<size_t>(T) * K;
@@ -490,29 +537,38 @@ pw_status pw_moe_paged_gemm(const pw_layer* Lc, const void* x, int T, int K, con
   a.topk = K;
   a.T = T;
   a.S = T * K;
-  a.nsplit = wl.nsplit;
-  a.kb_per_split = wl.kb_per_split;
   a.out_fp32 = out_fp32 ? 1 : 0;
   a.act = d.act;
   a.sdt = d.sdt;
-  a.mtb = wl.mtb;
   a.apl = L->st.n_apl > 0 ? 1 : 0;
+  a.n_shared = L->n_shared;
   hipStream_t st = static_cast<hipStream_t>(stream);
-  hipError_t e;
-  {
-    ProfScope ps(L, PW_PH_GATEUP, st);
-    e = wl.path == GemmPath::kTiled    ? pw::launch_tgemm(a, true, st)
-        : wl.path == GemmPath::kStream ? pw::launch_sgemm(a, true, st)
-                                       : pw::launch_gateup(a, st);
+  hipError_t e = hipSuccess;
+  // routed experts, then shared experts: each range with its own kernels
+  auto for_range = [&](const RangePlan& r) {
+    a.e0 = r.e0;
+    a.ne = r.ne;
+    a.s_range = static_cast<int>(r.S);
+    a.nsplit = r.nsplit;
+    a.kb_per_split = r.kb_per_split;
+    a.mtb = r.mtb;
+  };
+  for (int pass = 0; pass < 2 && e == hipSuccess; ++pass) {
+    const bool gateup = pass == 0;
+    for (const RangePlan& r : wl.r) {
+      if (r.ne <= 0) continue;
+      for_range(r);
+      ProfScope ps(L, gateup ? PW_PH_GATEUP : PW_PH_DOWN, st);
+      e = r.path == GemmPath::kTiled    ? pw::launch_tgemm(a, gateup, st)
+          : r.path == GemmPath::kStream ? pw::launch_sgemm(a, gateup, st)
+          : gateup                      ? pw::launch_gateup(a, st)
+                                        : pw::launch_down(a, st);
+      if (e != hipSuccess) break;
+    }
+    if (e != hipSuccess) return hip_fail(e, gateup ? "gate/up launch" : "down launch");
   }
-  if (e != hipSuccess) return hip_fail(e, "gate/up launch");
-  {
-    ProfScope ps(L, PW_PH_DOWN, st);
-    e = wl.path == GemmPath::kTiled    ? pw::launch_tgemm(a, false, st)
-        : wl.path == GemmPath::kStream ? pw::launch_sgemm(a, false, st)
-                                       : pw::launch_down(a, st);
-  }
-  if (e != hipSuccess) return hip_fail(e, "down launch");
+  a.nsplit = wl.r[0].nsplit;
+  a.nsplit_sh = wl.r[1].nsplit;
   {
     ProfScope ps(L, PW_PH_COMBINE, st);
     e = pw::launch_combine(a, st);
@@ -526,9 +582,10 @@ pw_status pw_moe_paged_gemm_noalloc(const pw_layer* L, const void* x, int T, int
                                     void* y, int out_fp32, void* stream) {
   if (!L) return fail(PW_EINVAL, "null layer");
   if (T < 0 || K < 1 || K > L->st.desc.E) return fail(PW_EINVAL, "need T >= 0 and 1 <= K <= E");
+  if (L->n_shared > 0 && K <= L->n_shared) return fail(PW_EINVAL, "K must exceed the shared experts");
   if (T == 0) return PW_OK;
   if (static_cast<int64_t>(T) * K >= (int64_t(1) << 31)) return fail(PW_EINVAL, "T*K too large");
-  const size_t need = ws_layout(L->st.desc, T, K, L->st.n_apl > 0).total;
+  const size_t need = ws_layout(L->st.desc, T, K, L->st.n_apl > 0, L->n_shared).total;
   if (need > pw::kStaticScratchBytes)
     return fail(PW_ENOMEM, "the call needs " + std::to_string(need) + " bytes of workspace, more than the " +
                                std::to_string(pw::kStaticScratchBytes) +

@@ -532,7 +532,7 @@ __global__ __launch_bounds__(64 * NW) void k_gateup(const GemmArgs a) {
   constexpr int GU = gu_rows<RT, NW>();
   __shared__ __attribute__((aligned(16))) uint8_t lds[gu_lds_bytes<NTMAX, RT, NW>()];
   const int upe = a.F / GU;
-  const int e = blockIdx.x / upe, unit = blockIdx.x % upe;
+  const int e = a.e0 + static_cast<int>(blockIdx.x) / upe, unit = blockIdx.x % upe;
   const int off_e = clampi(a.offsets[e], 0, a.S);
   const int n_e = clampi(a.offsets[e + 1], off_e, a.S) - off_e;
   if (n_e <= 0) return;
@@ -617,7 +617,7 @@ __global__ __launch_bounds__(64 * NW) void k_down(const GemmArgs a) {
   const int upe = a.H / DN;
   const int split = blockIdx.x % a.nsplit;
   const int rest = blockIdx.x / a.nsplit;
-  const int e = rest / upe, unit = rest % upe;
+  const int e = a.e0 + rest / upe, unit = rest % upe;
   const int off_e = clampi(a.offsets[e], 0, a.S);
   const int n_e = clampi(a.offsets[e + 1], off_e, a.S) - off_e;
   if (n_e <= 0) return;
@@ -647,9 +647,9 @@ void gemm_launch_nw(const GemmArgs& a, bool gateup, hipStream_t st) {
   constexpr int RT = row_tiles<NTMAX>();
   const dim3 block(64 * NW);
   if (gateup)
-    hipLaunchKernelGGL((k_gateup<ACT, SDT, NTMAX, GK, NW>), dim3(a.E * (a.F / gu_rows<RT, NW>())), block, 0, st, a);
+    hipLaunchKernelGGL((k_gateup<ACT, SDT, NTMAX, GK, NW>), dim3(a.ne * (a.F / gu_rows<RT, NW>())), block, 0, st, a);
   else
-    hipLaunchKernelGGL((k_down<ACT, SDT, NTMAX, GK, NW>), dim3(a.E * (a.H / dn_rows<RT, NW>()) * a.nsplit), block, 0,
+    hipLaunchKernelGGL((k_down<ACT, SDT, NTMAX, GK, NW>), dim3(a.ne * (a.H / dn_rows<RT, NW>()) * a.nsplit), block, 0,
                        st, a);
 }
 
@@ -679,6 +679,7 @@ void gemm_dispatch_g(const GemmArgs& a, bool gateup, hipStream_t st) {
 
 hipError_t gemm_dispatch(const GemmArgs& a, bool gateup, hipStream_t st) {
   if (a.mtb != 1 && a.mtb != 2 && a.mtb != 4) return hipErrorInvalidValue;
+  if (a.ne <= 0) return hipSuccess;
   if (a.act == PW_BF16) {
     if (a.sdt == PW_BF16) gemm_dispatch_g<PW_BF16, PW_BF16>(a, gateup, st);
     else gemm_dispatch_g<PW_BF16, PW_F16>(a, gateup, st);

@@ -81,10 +81,19 @@ struct GemmArgs {
   int act, sdt;
   int mtb;                    // M tiles (of 16 slots) per pass: 1, 2 or 4
   int apl;                    // the layer holds nested bit-plane pages
+  // experts [e0, e0 + ne) are the ones a GEMM launch covers, holding about
+  // s_range of the S slots (routed and shared experts run as separate launches)
+  int e0, ne, s_range;
+  // combine: the last n_shared of the topk columns are shared-expert slots,
+  // whose down projection ran with nsplit_sh K splits
+  int n_shared, nsplit_sh;
 };
 
-hipError_t launch_route_topk(const float* logits, int T, int E, int K, int renorm,
-                             int32_t* ids, float* w, hipStream_t st);
+// Routed top-K of E logits per token, then n_shared shared-expert columns
+// (experts E .. E + n_shared - 1, weight shared_gate[t][j] or 1): rows of
+// K + n_shared ids and weights.
+hipError_t launch_route_topk(const float* logits, int T, int E, int K, int renorm, int n_shared,
+                             const float* shared_gate, int32_t* ids, float* w, hipStream_t st);
 hipError_t launch_permute(const int32_t* ids, int T, int K, int E, int32_t* offsets,
                           int32_t* sorted_slot, int32_t* slot_pos, hipStream_t st);
 hipError_t launch_qjobs(const QJobBatch& b, hipStream_t st);

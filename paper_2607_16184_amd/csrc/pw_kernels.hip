@@ -23,8 +23,11 @@ constexpr int kRouteLogitsPerLane = 4;            // E <= 256
 // next expert each. The weights use the same fp32 arithmetic as a serial
 // loop: m = the largest selected logit, a_k = exp(l_k - m), w_k = a_k / sum,
 // with the sum taken in k order (renorm) or in expert order over all E.
+// Rows of ids and w hold K + n_shared columns: the routed experts, then the
+// shared experts E + j with weight gate[t n_shared + j] (1 without a gate).
 __global__ __launch_bounds__(256) void k_route_topk(const float* __restrict__ logits, int T, int E,
-                                                    int K, int renorm, int32_t* __restrict__ ids,
+                                                    int K, int renorm, int n_shared,
+                                                    const float* __restrict__ gate, int32_t* __restrict__ ids,
                                                     float* __restrict__ w) {
   const int t = blockIdx.x * 4 + static_cast<int>(threadIdx.x >> 6);
   if (t >= T) return;   // wave-uniform
@@ -77,12 +80,17 @@ __global__ __launch_bounds__(256) void k_route_topk(const float* __restrict__ lo
   } else {
     for (int e = 0; e < E; ++e) sum += expf(l[e] - m);
   }
+  const int Kt = K + n_shared;
 #pragma unroll
   for (int k = 0; k < kMaxTopK; ++k) {
     if (k < K) {
-      ids[static_cast<size_t>(t) * K + k] = se[k];
-      w[static_cast<size_t>(t) * K + k] = expf(sv[k] - m) / sum;
+      ids[static_cast<size_t>(t) * Kt + k] = se[k];
+      w[static_cast<size_t>(t) * Kt + k] = expf(sv[k] - m) / sum;
     }
+  }
+  for (int j = 0; j < n_shared; ++j) {
+    ids[static_cast<size_t>(t) * Kt + K + j] = E + j;
+    w[static_cast<size_t>(t) * Kt + K + j] = gate ? gate[static_cast<size_t>(t) * n_shared + j] : 1.0f;
   }
 }
 
@@ -560,6 +568,8 @@ __global__ void k_clear_table(pw_page_entry* table, size_t n) {
 
 // ---------------------------------------------------------------------------
 // combine: y[t] = sum_k w[t,k] * sum_split opart[split][slot_pos[t,k]]
+// (k ascending; the last n_shared columns are shared-expert slots, whose
+// down projection has nsplit_sh K splits)
 // ---------------------------------------------------------------------------
 
 __global__ __launch_bounds__(256) void k_combine(const GemmArgs a) {
@@ -569,8 +579,9 @@ __global__ __launch_bounds__(256) void k_combine(const GemmArgs a) {
   f32x4 y = {0.f, 0.f, 0.f, 0.f};
   for (int k = 0; k < a.topk; ++k) {
     const int pos = clampi(a.slot_pos[static_cast<size_t>(t) * a.topk + k], 0, a.S - 1);
+    const int nsp = k < a.topk - a.n_shared ? a.nsplit : a.nsplit_sh;
     f32x4 o = {0.f, 0.f, 0.f, 0.f};
-    for (int sp = 0; sp < a.nsplit; ++sp)
+    for (int sp = 0; sp < nsp; ++sp)
       o += *reinterpret_cast<const f32x4*>(a.opart + (static_cast<size_t>(sp) * a.S + pos) * a.H + n);
     const float wk = a.topk_w[static_cast<size_t>(t) * a.topk + k];
     y += wk * o;
@@ -860,10 +871,12 @@ __global__ __launch_bounds__(256) void k_expert_stats(const double* norm2, int b
 // launchers
 // ---------------------------------------------------------------------------
 
-hipError_t launch_route_topk(const float* logits, int T, int E, int K, int renorm, int32_t* ids,
-                             float* w, hipStream_t st) {
+hipError_t launch_route_topk(const float* logits, int T, int E, int K, int renorm, int n_shared,
+                             const float* shared_gate, int32_t* ids, float* w, hipStream_t st) {
   if (T <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_route_topk, dim3((T + 3) / 4), dim3(256), 0, st, logits, T, E, K, renorm, ids, w);
+  if (K > kMaxTopK || E > 64 * kRouteLogitsPerLane) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_route_topk, dim3((T + 3) / 4), dim3(256), 0, st, logits, T, E, K, renorm, n_shared,
+                     shared_gate, ids, w);
   return hipGetLastError();
 }
 

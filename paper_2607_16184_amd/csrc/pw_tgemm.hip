@@ -313,7 +313,7 @@ __device__ __forceinline__ void tile_loop(uint8_t* lds, const uint8_t* tile0, co
 
 // Maps a tile index to (expert, first slot) from the routing offsets.
 __device__ __forceinline__ bool tile_expert(const GemmArgs& a, int mt, int* e_out, int* off_e, int* n_e, int* m0) {
-  for (int e = 0; e < a.E; ++e) {
+  for (int e = a.e0; e < a.e0 + a.ne; ++e) {
     const int o = clampi(a.offsets[e], 0, a.S);
     const int n = clampi(a.offsets[e + 1], o, a.S) - o;
     const int cnt = (n + kTM - 1) / kTM;
@@ -581,7 +581,7 @@ __global__ __launch_bounds__(256) void k_sgemm(const GemmArgs a, int nblk, int m
   {
     int rest = mt;
     bool found = false;
-    for (int x = 0; x < a.E && !found; ++x) {
+    for (int x = a.e0; x < a.e0 + a.ne && !found; ++x) {
       const int o = clampi(a.offsets[x], 0, a.S);
       const int n = clampi(a.offsets[x + 1], o, a.S) - o;
       const int cnt = (n + MT - 1) / MT;
@@ -711,7 +711,7 @@ __global__ __launch_bounds__(256) void k_sgemm(const GemmArgs a, int nblk, int m
 template <int ACT, int SDT, int MT>
 void sgemm_go(const GemmArgs& a, bool gateup, hipStream_t st) {
   const int nblk = gateup ? a.F / 64 : a.H / 128;
-  const int mtmax = (a.S + MT - 1) / MT + a.E;
+  const int mtmax = (a.s_range + MT - 1) / MT + a.ne;
   const int n = ((nblk + kGN - 1) / kGN * kGN * mtmax + 7) / 8 * 8 * (gateup ? 1 : a.nsplit);
   if (a.apl) {
     if (gateup)
@@ -731,7 +731,7 @@ void sgemm_go(const GemmArgs& a, bool gateup, hipStream_t st) {
 // twice per CU.
 template <int ACT, int SDT>
 void sgemm_mt(const GemmArgs& a, bool gateup, hipStream_t st) {
-  const int expect = (a.S + a.E - 1) / a.E;
+  const int expect = (a.s_range + a.ne - 1) / a.ne;
   if (a.apl && expect <= 24) sgemm_go<ACT, SDT, 32>(a, gateup, st);
   else sgemm_go<ACT, SDT, 64>(a, gateup, st);
 }
@@ -750,8 +750,9 @@ void tgemm_go(const GemmArgs& a, bool gateup, int n, int nblk, int mtmax, hipStr
 int tgemm_mtmax(int S, int E) { return (S + kTM - 1) / kTM + E; }
 
 hipError_t launch_tgemm(const GemmArgs& a, bool gateup, hipStream_t st) {
+  if (a.ne <= 0) return hipSuccess;
   const int nblk = gateup ? a.F / 128 : a.H / 256;
-  const int mtmax = tgemm_mtmax(a.S, a.E);
+  const int mtmax = tgemm_mtmax(a.s_range, a.ne);
   const int n = ((nblk + kGN - 1) / kGN * kGN * mtmax + 7) / 8 * 8;
   if (a.act == PW_BF16) {
     if (a.sdt == PW_BF16) tgemm_go<PW_BF16, PW_BF16>(a, gateup, n, nblk, mtmax, st);
@@ -766,6 +767,7 @@ hipError_t launch_tgemm(const GemmArgs& a, bool gateup, hipStream_t st) {
 // Streaming path (64-slot tiles): per-expert slot counts between the decode
 // kernels' range and the large-tile kernel's.
 hipError_t launch_sgemm(const GemmArgs& a, bool gateup, hipStream_t st) {
+  if (a.ne <= 0) return hipSuccess;
   if (a.act == PW_BF16) {
     if (a.sdt == PW_BF16) sgemm_mt<PW_BF16, PW_BF16>(a, gateup, st);
     else sgemm_mt<PW_BF16, PW_F16>(a, gateup, st);

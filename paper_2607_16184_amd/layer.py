@@ -114,6 +114,24 @@ class PagedLayer:
                          offsets.data_ptr(), ss.data_ptr(), sp.data_ptr(), _stream(stream))
         return ids, w, offsets, ss, sp
 
+    def set_shared_experts(self, n_shared: int):
+        """Declare the layer's last n_shared experts as shared experts."""
+        pw.pw_layer_set_shared_experts(self.handle, n_shared)
+        self.n_shared = n_shared
+
+    def route_shared(self, logits: torch.Tensor, K: int, n_shared: int, gate: torch.Tensor = None,
+                     renorm: int = 1, stream=None, out=None):
+        """Routed top-K over logits [T, E_routed] plus n_shared shared columns
+        (weights from gate [T, n_shared] fp32, or 1): [T, K + n_shared] routing."""
+        T, E = logits.shape
+        Kt = K + n_shared
+        ids, w, offsets, ss, sp = out if out is not None else self.routing_buffers(T, E + n_shared, Kt,
+                                                                                   logits.device)
+        pw.pw_route_topk_shared(logits.data_ptr(), T, E, K, renorm, n_shared,
+                                gate.data_ptr() if gate is not None else 0, ids.data_ptr(), w.data_ptr(),
+                                offsets.data_ptr(), ss.data_ptr(), sp.data_ptr(), _stream(stream))
+        return ids, w, offsets, ss, sp
+
     def workspace(self, T: int, K: int) -> Tuple[int, int]:
         need = pw.pw_workspace_bytes(self.handle, T, K)
         if need > self._ws_bytes:

@@ -92,6 +92,8 @@ def _load():
         "pw_probe_mfma": (i32, [i32, i32, vp, vp]),
         "pw_workspace_bytes": (i32, [vp, i32, i32, P(sz)]),
         "pw_moe_paged_gemm": (i32, [vp, vp, i32, i32, vp, vp, vp, vp, vp, i32, vp, sz, vp]),
+        "pw_layer_set_shared_experts": (i32, [vp, i32]),
+        "pw_route_topk_shared": (i32, [vp, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp]),
         "pw_moe_paged_gemm_noalloc": (i32, [vp, vp, i32, i32, vp, vp, vp, vp, vp, i32, vp]),
         "pw_requant_block": (i32, [vp, i32, i32, i32, i32, vp, P(sz)]),
         "pw_requant_blocks": (i32, [vp, i32, P(i32), P(i32), P(i32), P(i32), vp, P(sz)]),
@@ -204,6 +206,17 @@ def pw_moe_paged_gemm(layer: int, x_ptr: int, T: int, K: int, w_ptr: int, offset
                       ws_ptr: int, ws_bytes: int, stream: int):
     _check(_lib.pw_moe_paged_gemm(layer, x_ptr, T, K, w_ptr, offsets_ptr, sorted_slot_ptr,
                                   slot_pos_ptr, y_ptr, out_fp32, ws_ptr, ws_bytes, stream))
+
+
+def pw_layer_set_shared_experts(layer: int, n_shared: int):
+    _check(_lib.pw_layer_set_shared_experts(layer, n_shared))
+
+
+def pw_route_topk_shared(logits_ptr: int, T: int, E: int, K: int, renorm: int, n_shared: int, gate_ptr: int,
+                         ids_ptr: int, w_ptr: int, offsets_ptr: int, sorted_slot_ptr: int, slot_pos_ptr: int,
+                         stream: int):
+    _check(_lib.pw_route_topk_shared(logits_ptr, T, E, K, renorm, n_shared, gate_ptr or None, ids_ptr, w_ptr,
+                                     offsets_ptr, sorted_slot_ptr, slot_pos_ptr, stream))
 
 
 def pw_moe_paged_gemm_noalloc(layer: int, x_ptr: int, T: int, K: int, w_ptr: int, offsets_ptr: int,

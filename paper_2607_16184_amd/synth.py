@@ -11,8 +11,9 @@ used; every tensor here is drawn from a seeded normal distribution.
 
 Seeds: ``np.random.default_rng(1000 * cfg_id + stream)`` with streams
 0 logits, 1 per-expert logit bias, 2 activations, 3/4/5 gate/up/down weights,
-6 bitwidth map, 7 pool order, 8 downshift page selection, and 100 + s for the
-logits and activations of decode step s in the downshift workload.
+6 bitwidth map, 7 pool order, 8 downshift page selection, 9 shared-expert
+gates, and 100 + s for the logits and activations of decode step s in the
+downshift workload.
 
 16-bit values are produced by round-to-nearest-even from fp32 draws and are
 returned as raw uint16 bit patterns; no consumer re-rounds them.
@@ -35,8 +36,8 @@ class LayerConfig:
 
     cfg_id: int
     name: str
-    E: int                  # routed experts
-    K: int                  # top-k
+    E: int                  # experts of the layer (routed, then n_shared shared)
+    K: int                  # routed top-k
     H: int                  # hidden size
     F: int                  # expert FFN size
     T: int                  # tokens per step
@@ -52,10 +53,16 @@ class LayerConfig:
     downshift_frac: float = 0.0
     downshift_bits: int = 4
     downshift_chunks: int = 0
+    # shared experts: the last n_shared of the E experts, used by every token
+    n_shared: int = 0
 
     @property
     def S(self) -> int:
-        return self.T * self.K
+        return self.T * (self.K + self.n_shared)
+
+    @property
+    def E_routed(self) -> int:
+        return self.E - self.n_shared
 
     def nrb(self, proj: int) -> int:
         """Row-blocks (pages) per expert for a projection."""
@@ -96,6 +103,15 @@ CONFIGS: Dict[str, LayerConfig] = {
                       T=64, R=128, G=128, act=BF16, sdt=BF16,
                       mix=(0.5, 0.25, 0.25), steps=32, downshift_frac=0.25,
                       downshift_bits=4, downshift_chunks=8),
+    # shared experts, shaped like Qwen1.5-MoE's layer (Table 1: 60 routed +
+    # 4 shared experts, top-4; hidden 2048, expert FFN 1408): 128 decode
+    # tokens, 64-row pages 25/25/50, a per-token gate per shared expert
+    "qwen_shared": _cfg(cfg_id=6, name="qwen_shared", E=64, K=4, H=2048, F=1408,
+                        T=128, R=64, G=128, act=BF16, sdt=BF16,
+                        mix=(0.25, 0.25, 0.5), n_shared=4),
+    # tiny layer with 8 routed + 2 shared experts (parity cases)
+    "tiny_shared": _cfg(cfg_id=7, name="tiny_shared", E=10, K=2, H=256, F=512, T=16, R=64, G=64,
+                        act=F16, sdt=F16, mix=None, n_shared=2),
 }
 
 
@@ -121,13 +137,20 @@ def from16(bits: np.ndarray, fmt: int) -> np.ndarray:
 
 
 def logits(cfg: LayerConfig, stream: int = 0, T: Optional[int] = None) -> np.ndarray:
-    """Router logits [T, E] fp32 ~ N(0,1), plus a per-expert N(0, bias_sd) bias."""
+    """Router logits [T, E_routed] fp32 ~ N(0,1), plus a per-expert N(0, bias_sd) bias."""
     T = cfg.T if T is None else T
-    lg = rng(cfg, stream).standard_normal((T, cfg.E), dtype=np.float32)
+    lg = rng(cfg, stream).standard_normal((T, cfg.E_routed), dtype=np.float32)
     if cfg.bias_sd > 0:
-        b = rng(cfg, 1).standard_normal(cfg.E, dtype=np.float32) * np.float32(cfg.bias_sd)
+        b = rng(cfg, 1).standard_normal(cfg.E_routed, dtype=np.float32) * np.float32(cfg.bias_sd)
         lg = (lg + b[None, :]).astype(np.float32)
     return np.ascontiguousarray(lg)
+
+
+def shared_gate(cfg: LayerConfig, T: Optional[int] = None) -> np.ndarray:
+    """Per-token gates of the shared experts [T, n_shared] fp32 ~ U(0, 1) (the
+    range of a sigmoid gate), drawn from stream 9."""
+    T = cfg.T if T is None else T
+    return np.ascontiguousarray(rng(cfg, 9).uniform(0.0, 1.0, (T, cfg.n_shared)).astype(np.float32))
 
 
 def activations(cfg: LayerConfig, T: Optional[int] = None) -> np.ndarray:
