@@ -45,8 +45,10 @@ def kernel_hash():
 
 def describe(cfg):
     mix = "iid{16,8,4}" if cfg.mix is None else "%d/%d/%d%% 16-bit/int8/int4" % tuple(round(100 * m) for m in cfg.mix)
-    return ("%s: %d experts top-%d, H=%d, F=%d, %d tokens %s, %d-row pages %s, G=%d, shuffled pool"
-            % (cfg.name, cfg.E, cfg.K, cfg.H, cfg.F, cfg.T, "bf16" if cfg.act else "fp16", cfg.R, mix, cfg.G))
+    experts = ("%d experts" % cfg.E if not cfg.n_shared
+               else "%d routed + %d shared (gated) experts" % (cfg.E_routed, cfg.n_shared))
+    return ("%s: %s top-%d, H=%d, F=%d, %d tokens %s, %d-row pages %s, G=%d, shuffled pool"
+            % (cfg.name, experts, cfg.K, cfg.H, cfg.F, cfg.T, "bf16" if cfg.act else "fp16", cfg.R, mix, cfg.G))
 
 
 def page_bytes_active(cfg, bits, counts):
@@ -90,12 +92,21 @@ def time_steps(L, cfg, x, logits, steps, warmup):
     from paper_2607_16184_amd import pw
     from paper_2607_16184_amd.layer import PagedLayer
     Ls = L if isinstance(L, (list, tuple)) else [L]
-    rbuf = PagedLayer.routing_buffers(cfg.T, cfg.E, cfg.K)
+    rbuf = PagedLayer.routing_buffers(cfg.T, cfg.E, cfg.K + cfg.n_shared)
     y = torch.empty((cfg.T, cfg.H), dtype=torch.int16, device="cuda")
+    gate = None
+    if cfg.n_shared:
+        from paper_2607_16184_amd import synth
+        gate = torch.from_numpy(synth.shared_gate(cfg)).cuda()
+        for Li in Ls:
+            Li.set_shared_experts(cfg.n_shared)
 
     def step(i):
         Li = Ls[i % len(Ls)]
-        routing = Li.route(logits, cfg.K, out=rbuf)
+        if cfg.n_shared:
+            routing = Li.route_shared(logits, cfg.K, cfg.n_shared, gate=gate, out=rbuf)
+        else:
+            routing = Li.route(logits, cfg.K, out=rbuf)
         Li.forward(x, routing, y=y)
 
     for i in range(max(warmup, len(Ls))):
@@ -122,7 +133,8 @@ def time_steps(L, cfg, x, logits, steps, warmup):
         for k in range(4):
             ms[k] += m[k]
             cnt[k] += c[k]
-    per_kernel = {name: (ms[i] / cnt[i] if cnt[i] else None)
+    # per step (a layer with shared experts launches each GEMM phase twice)
+    per_kernel = {name: (ms[i] / steps if cnt[i] else None)
                   for i, name in enumerate(("gateup", "down", "combine", "requant"))}
     counts = (rbuf[2][1:] - rbuf[2][:-1]).cpu().numpy()
     out = {"wall_ms": (t1 - t0) * 1e3 / steps, "eager_ms": ev0.elapsed_time(ev1) / steps,
@@ -178,28 +190,132 @@ def traffic_for(kernel, workload, algo_bytes):
     return rec.get("bytes_per_launch")
 
 
-def cpu_baseline(cfg, w16, bits, logits_np, x16, weight_bytes, budget_s=20.0):
-    """The oracle, timed on this host on a bounded sample of the step's tokens."""
-    import numpy as np
-    import oracle
-    t0 = time.time()
-    O = oracle.OracleLayer(cfg.E, cfg.H, cfg.F, cfg.R, cfg.G, cfg.act, cfg.sdt, w16, bits)
-    log("oracle layer built in %.1f s" % (time.time() - t0))
-    ids, w = oracle.route(logits_np, cfg.K)
-    done, spent = 0, 0.0
-    chunk = 1
-    while done < cfg.T and spent < budget_s:
-        toks = list(range(done, min(cfg.T, done + chunk)))
+def cpu_model():
+    """The host CPU's model name (from /proc/cpuinfo)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _median3(fn):
+    ts = []
+    for _ in range(3):
+        t = time.perf_counter()
+        fn()
+        ts.append(time.perf_counter() - t)
+    return sorted(ts)[1]
+
+
+def _oracle_step_s(O, x16, ids, w, T, budget_s):
+    """Seconds of one whole oracle step: the median of 3 full steps when one
+    fits a quarter of the budget, else a growing sample of tokens scaled to
+    T. Returns (seconds, tokens timed, description)."""
+    t = time.perf_counter()
+    O.forward(x16, ids, w, tokens=[0])
+    one = time.perf_counter() - t
+    if one * T <= budget_s / 4:
+        return _median3(lambda: O.forward(x16, ids, w)), T, "median of 3 full steps"
+    done, spent, chunk = 1, one, 1
+    while done < T and spent < budget_s:
+        toks = list(range(done, min(T, done + chunk)))
         t = time.perf_counter()
         O.forward(x16, ids, w, tokens=toks)
         spent += time.perf_counter() - t
         done += len(toks)
         chunk = min(chunk * 2, 8)
-    step_s = spent * cfg.T / done
-    return {"value": weight_bytes / step_s / 1e9, "unit": "GB/s", "cores": oracle.threads(),
-            "kind": "oracle",
-            "sample": "oracle forward (fp64, OpenMP) of %d of the %d tokens of one step, scaled to "
-                      "the full step (%.2f s measured, %.1f s per step)" % (done, cfg.T, spent, step_s)}
+    if done == T:
+        return spent, done, "all %d tokens once, in growing chunks" % T
+    return spent * T / done, done, "%d of %d tokens, scaled to %d" % (done, T, T)
+
+
+def cpu_baseline(cfg, w16, bits, logits_np, x16, weight_bytes, budget_s=12.0):
+    """The oracle (plain C, fp64 FFN, OpenMP over output rows), timed on this
+    host: the benchmark's decode step with every thread (median of 3 steps)
+    and on one thread (a sample of tokens, scaled), routing alone, and the
+    other workloads' steps, each bounded, with what was sampled stated."""
+    import numpy as np
+    import oracle
+    from paper_2607_16184_amd import synth
+    threads = oracle.threads()
+    t0 = time.time()
+    O = oracle.OracleLayer(cfg.E, cfg.H, cfg.F, cfg.R, cfg.G, cfg.act, cfg.sdt, w16, bits)
+    log("oracle layer built in %.1f s" % (time.time() - t0))
+    route_s = _median3(lambda: oracle.route(logits_np, cfg.K))
+    ids, w = oracle.route(logits_np, cfg.K)
+    step_s, done, how = _oracle_step_s(O, x16, ids, w, cfg.T, budget_s)
+    # one thread: a sample of tokens, scaled to the step
+    oracle.set_threads(1)
+    try:
+        st_s, st_done, st_how = _oracle_step_s(O, x16, ids, w, cfg.T, budget_s / 2)
+    finally:
+        oracle.set_threads(threads)
+    out = {"value": weight_bytes / step_s / 1e9, "unit": "GB/s", "cores": threads,
+           "kind": "oracle", "cpu_model": cpu_model(),
+           "sample": "oracle step (routing + fp64 forward of every routed slot, OpenMP over %d threads) "
+                     "of the %s layer: %s, %.3f s per step" % (threads, cfg.name, how, step_s),
+           "step_s": round(step_s, 4), "routing_ms": round(route_s * 1e3, 4),
+           "single_thread": {"value": weight_bytes / st_s / 1e9, "unit": "GB/s", "step_s": round(st_s, 3),
+                             "sample": st_how}}
+    configs = {}
+    # tiny layer: whole steps, every thread and one thread
+    c1 = synth.CONFIGS["tiny"]
+    w1 = [synth.expert_weights(c1, p) for p in range(3)]
+    O1 = oracle.OracleLayer(c1.E, c1.H, c1.F, c1.R, c1.G, c1.act, c1.sdt, w1, synth.bitmap(c1))
+    lg1, x1 = synth.logits(c1), synth.activations(c1)
+    ids1, w1r = oracle.route(lg1, c1.K)
+    mt = _median3(lambda: O1.forward(x1, ids1, w1r))
+    oracle.set_threads(1)
+    try:
+        s1 = _median3(lambda: O1.forward(x1, ids1, w1r))
+    finally:
+        oracle.set_threads(threads)
+    configs["tiny"] = {"step_ms": round(mt * 1e3, 3), "step_ms_single_thread": round(s1 * 1e3, 3),
+                       "routing_ms": round(_median3(lambda: oracle.route(lg1, c1.K)) * 1e3, 4),
+                       "sample": "median of 3 full steps"}
+    # prefill: its routing over all 4096 tokens; the forward of a 64-token
+    # slice (per-token cost depends on the shapes and the bitwidth mix only,
+    # which the decode layer's pages share), one run, scaled to 4096 tokens
+    c3 = synth.CONFIGS["mixtral_prefill"]
+    lg3, x3 = synth.logits(c3), synth.activations(c3)
+    t = time.perf_counter()
+    ids3, w3 = oracle.route(lg3, c3.K)
+    r3 = time.perf_counter() - t
+    t = time.perf_counter()
+    O.forward(x3, ids3, w3, tokens=list(range(64)))
+    f3 = (time.perf_counter() - t) * c3.T / 64
+    configs["mixtral_prefill"] = {"step_s_scaled": round(f3, 2), "routing_ms": round(r3 * 1e3, 3),
+                                  "gflops_per_s": round(6.0 * c3.S * c3.H * c3.F / f3 / 1e9, 2),
+                                  "sample": "one run of a 64-token slice scaled to 4096 tokens (labelled "
+                                            "scaled), on the decode layer's pages (same shapes and mix)"}
+    # fine-grained layer: whole steps
+    c4 = synth.CONFIGS["finegrained"]
+    w4 = [synth.expert_weights(c4, p) for p in range(3)]
+    b4 = synth.bitmap(c4)
+    O4 = oracle.OracleLayer(c4.E, c4.H, c4.F, c4.R, c4.G, c4.act, c4.sdt, w4, b4)
+    lg4, x4 = synth.logits(c4), synth.activations(c4)
+    ids4, w4r = oracle.route(lg4, c4.K)
+    s4, _, how4 = _oracle_step_s(O4, x4, ids4, w4r, c4.T, budget_s)
+    configs["finegrained"] = {"step_s": round(s4, 3), "routing_ms": round(_median3(lambda: oracle.route(lg4, c4.K)) * 1e3, 4),
+                              "gflops_per_s": round(6.0 * c4.S * c4.H * c4.F / s4 / 1e9, 2), "sample": how4}
+    del O4, w4
+    # runtime downshift: the requant of the 256 plan pages (16 -> int4)
+    c5 = synth.CONFIGS["downshift"]
+    plan = [blk for ch in synth.downshift_plan(c5, bits) for blk in ch]
+    rows = [w16[p][e, rb * cfg.R:(rb + 1) * cfg.R] for (e, p, rb) in plan]
+    rq = _median3(lambda: [oracle.quantize_page16(r, cfg.act, cfg.G, 4, cfg.sdt) for r in rows])
+    moved = sum(oracle.page_bytes(cfg.R, cfg.kdim(p), cfg.G, 16) + oracle.page_bytes(cfg.R, cfg.kdim(p), cfg.G, 4)
+                for (_, p, _) in plan)
+    configs["downshift_requant"] = {"pages": len(plan), "requant_s": round(rq, 3),
+                                    "GBps": round(moved / rq / 1e9, 3),
+                                    "sample": "median of 3 runs of the oracle quantizer over the 256 pages "
+                                              "(single-threaded per page), on the decode layer's weights"}
+    out["configs"] = configs
+    return out
 
 
 def leg_layer(name, steps, warmup, pools=1):
@@ -222,7 +338,7 @@ def leg_layer(name, steps, warmup, pools=1):
     wb = per[0] + per[1] + per[2]
     km = r["kernel_ms"]
     gemm_ms = km["gateup"] + km["down"]
-    flops = 6.0 * cfg.T * cfg.K * cfg.H * cfg.F
+    flops = 6.0 * cfg.S * cfg.H * cfg.F
     for Li in Ls:
         Li.close()
     return {"workload": describe(cfg), "steps": steps, "ms_per_step": round(r["event_ms"], 4),
@@ -693,7 +809,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="mixtral_decode")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--extras", default="ceilings,bitwidths,prefill,finegrained,downshift,offload,planner,apl",
+    ap.add_argument("--extras", default="ceilings,bitwidths,prefill,finegrained,shared,downshift,offload,planner,apl",
                     help="comma list of extra legs on the same JSON line ('' for none)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after the timed steps, run one device copy of this many MiB "
@@ -790,6 +906,11 @@ def main():
             # 0.57 GB of weights: three pools in turn, so no step reads the
             # previous step's weights from the 256 MB last-level cache
             extras["finegrained"] = leg_layer("finegrained", steps=51, warmup=3, pools=3)
+        elif leg == "shared":
+            # Qwen-shaped layer with 60 routed + 4 shared experts: routed
+            # experts on the decode kernels, shared ones on the tiled kernel;
+            # 0.57 GB of weights, so three pools in turn as above
+            extras["shared"] = leg_layer("qwen_shared", steps=51, warmup=3, pools=3)
         elif leg == "downshift":
             extras["downshift"] = leg_downshift()
         elif leg == "offload":

@@ -85,6 +85,7 @@ def lib():
         + [_c_u16p, _c_i32p, _c_u8p, _c_u16p, _c_u16p] * 3
         + [ctypes.c_int, ctypes.c_int, _c_i32p, ctypes.c_int, _c_f64p])
     L.or_threads.restype = ctypes.c_int
+    L.or_set_threads.argtypes = [ctypes.c_int]
     L.or_init()
     _lib = L
     return L
@@ -280,6 +281,11 @@ def permute(ids: np.ndarray, E: int):
 def threads() -> int:
     """OpenMP threads the oracle's parallel loops use."""
     return int(lib().or_threads())
+
+
+def set_threads(n: int) -> None:
+    """Threads for the oracle's later parallel loops (for timing the oracle)."""
+    lib().or_set_threads(int(n))
 
 
 def routing_mass(ids: np.ndarray, w: np.ndarray, E: int) -> np.ndarray:

@@ -158,6 +158,15 @@ int or_threads(void) {
 #endif
 }
 
+/* Set the threads later OpenMP regions of the oracle use (timing only). */
+void or_set_threads(int n) {
+#ifdef _OPENMP
+    if (n > 0) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
 /* Build the lookup tables of both formats (call once before any threads). */
 void or_init(void) {
     build_tab(FMT_F16);
