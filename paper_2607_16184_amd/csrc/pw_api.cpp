@@ -110,16 +110,23 @@ struct WsLayout {
 // S / ne: up to 48, the decode kernels (weights streamed in registers, exact
 // code-domain arithmetic, up to four 16-slot tiles per pass); up to 127, the
 // streaming kernel with 64-slot tiles; from 128, the LDS-tiled 256 x 256
-// kernel. The last two need 32/64-row staging inside one page, 128-row down
-// blocks and 32-bit activation row offsets (and the tiled kernel 256-row down
-// blocks).
-GemmPath pick_path(const pw_layer_desc& d, size_t S, size_t S_all, int ne, bool apl) {
+// kernel. The shared experts of a decode-sized batch are a few experts with a
+// few hundred slots each: where the tiled kernel's tiles would not give every
+// CU a workgroup, the streaming kernel's smaller tiles spread their work. The
+// last two need 32/64-row staging inside one page, 128-row down blocks and
+// 32-bit activation row offsets (and the tiled kernel 256-row down blocks).
+constexpr size_t kCUs = 256;
+
+GemmPath pick_path(const pw_layer_desc& d, size_t S, size_t S_all, int ne, bool apl, bool shared) {
   const size_t expect = (S + ne - 1) / ne;
   const bool fits = S_all * d.F * 2 < (size_t(1) << 32) && S_all * d.H * 2 < (size_t(1) << 32);
   const bool tiles = fits && d.G >= 64 && d.R % 64 == 0 && d.F % 128 == 0;
   // nested bit-plane pages are read by the streaming kernel only
   if (apl) return GemmPath::kStream;
-  if (expect >= 128 && tiles && d.H % 256 == 0) return GemmPath::kTiled;
+  if (expect >= 128 && tiles && d.H % 256 == 0) {
+    const size_t tiled_wgs = static_cast<size_t>(ne) * ((expect + 255) / 256) * (d.F / 128);
+    return shared && tiled_wgs < kCUs ? GemmPath::kStream : GemmPath::kTiled;
+  }
   if (expect > 48 && tiles && d.H % 128 == 0) return GemmPath::kStream;
   return GemmPath::kDecode;
 }
@@ -137,7 +144,7 @@ RangePlan plan_range(const pw_layer_desc& d, int e0, int ne, size_t S, size_t S_
   }
   const int nkbF = d.F / 128;
   const int expect = static_cast<int>((S + ne - 1) / ne);
-  r.path = pick_path(d, S, S_all, ne, apl);
+  r.path = pick_path(d, S, S_all, ne, apl, e0 > 0);
   // The decode kernels split the down projection's K = F when too few
   // (expert, row-block) units exist to fill the chip; deterministic in
   // (desc, T, K).
@@ -420,6 +427,12 @@ pw_status pw_route_topk_shared(const float* logits, int T, int E, int K, int ren
   if (!offsets || (T > 0 && (!logits || !ids || !w || !sorted_slot || !slot_pos)))
     return fail(PW_EINVAL, "null argument");
   hipStream_t st = static_cast<hipStream_t>(stream);
+  if (pw::route_permute_fits(T, E, K, n_shared)) {
+    // small batches: one launch routes and permutes
+    hipError_t e = pw::launch_route_permute(logits, T, E, K, renorm, n_shared, shared_gate, ids, w, offsets,
+                                            sorted_slot, slot_pos, st);
+    return e == hipSuccess ? PW_OK : hip_fail(e, "router launch");
+  }
   hipError_t e = pw::launch_route_topk(logits, T, E, K, renorm, n_shared, shared_gate, ids, w, st);
   if (e != hipSuccess) return hip_fail(e, "router launch");
   e = pw::launch_permute(ids, T, Kt, E + n_shared, offsets, sorted_slot, slot_pos, st);

@@ -94,6 +94,11 @@ struct GemmArgs {
 // K + n_shared ids and weights.
 hipError_t launch_route_topk(const float* logits, int T, int E, int K, int renorm, int n_shared,
                              const float* shared_gate, int32_t* ids, float* w, hipStream_t st);
+// Both in one single-workgroup launch, for batches route_permute_fits admits.
+bool route_permute_fits(int T, int E, int K, int n_shared);
+hipError_t launch_route_permute(const float* logits, int T, int E, int K, int renorm, int n_shared,
+                                const float* shared_gate, int32_t* ids, float* w, int32_t* offsets,
+                                int32_t* sorted_slot, int32_t* slot_pos, hipStream_t st);
 hipError_t launch_permute(const int32_t* ids, int T, int K, int E, int32_t* offsets,
                           int32_t* sorted_slot, int32_t* slot_pos, hipStream_t st);
 hipError_t launch_qjobs(const QJobBatch& b, hipStream_t st);

@@ -25,12 +25,10 @@ constexpr int kRouteLogitsPerLane = 4;            // E <= 256
 // with the sum taken in k order (renorm) or in expert order over all E.
 // Rows of ids and w hold K + n_shared columns: the routed experts, then the
 // shared experts E + j with weight gate[t n_shared + j] (1 without a gate).
-__global__ __launch_bounds__(256) void k_route_topk(const float* __restrict__ logits, int T, int E,
-                                                    int K, int renorm, int n_shared,
-                                                    const float* __restrict__ gate, int32_t* __restrict__ ids,
-                                                    float* __restrict__ w) {
-  const int t = blockIdx.x * 4 + static_cast<int>(threadIdx.x >> 6);
-  if (t >= T) return;   // wave-uniform
+// lds_ids (may be null): the token's row of ids also goes there.
+__device__ __forceinline__ void route_token(const float* __restrict__ logits, int t, int E, int K, int renorm,
+                                            int n_shared, const float* __restrict__ gate,
+                                            int32_t* __restrict__ ids, float* __restrict__ w, int* lds_ids) {
   const int lane = lane_id();
   const float* l = logits + static_cast<size_t>(t) * E;
   float v[kRouteLogitsPerLane];
@@ -81,17 +79,29 @@ __global__ __launch_bounds__(256) void k_route_topk(const float* __restrict__ lo
     for (int e = 0; e < E; ++e) sum += expf(l[e] - m);
   }
   const int Kt = K + n_shared;
+  const size_t row = static_cast<size_t>(t) * Kt;
 #pragma unroll
   for (int k = 0; k < kMaxTopK; ++k) {
     if (k < K) {
-      ids[static_cast<size_t>(t) * Kt + k] = se[k];
-      w[static_cast<size_t>(t) * Kt + k] = expf(sv[k] - m) / sum;
+      ids[row + k] = se[k];
+      w[row + k] = expf(sv[k] - m) / sum;
+      if (lds_ids) lds_ids[row + k] = se[k];
     }
   }
   for (int j = 0; j < n_shared; ++j) {
-    ids[static_cast<size_t>(t) * Kt + K + j] = E + j;
-    w[static_cast<size_t>(t) * Kt + K + j] = gate ? gate[static_cast<size_t>(t) * n_shared + j] : 1.0f;
+    ids[row + K + j] = E + j;
+    w[row + K + j] = gate ? gate[static_cast<size_t>(t) * n_shared + j] : 1.0f;
+    if (lds_ids) lds_ids[row + K + j] = E + j;
   }
+}
+
+__global__ __launch_bounds__(256) void k_route_topk(const float* __restrict__ logits, int T, int E,
+                                                    int K, int renorm, int n_shared,
+                                                    const float* __restrict__ gate, int32_t* __restrict__ ids,
+                                                    float* __restrict__ w) {
+  const int t = blockIdx.x * 4 + static_cast<int>(threadIdx.x >> 6);
+  if (t >= T) return;   // wave-uniform
+  route_token(logits, t, E, K, renorm, n_shared, gate, ids, w, nullptr);
 }
 
 // Token permutation, one workgroup per expert e. Each workgroup builds the
@@ -163,6 +173,147 @@ __global__ __launch_bounds__(kPermThreads) void k_permute(const int32_t* __restr
     sorted_slot[base + r] = s;
     slot_pos[s] = base + r;
   });
+}
+
+// Small batches (T (K + n_shared) <= kFusedMaxSlots, T E <= kFusedMaxLogits):
+// routing and permutation in one workgroup, so one launch does both.
+//  1. the batch's logits are staged in LDS (coalesced loads);
+//  2. thread t selects token t's top K by a serial pass over its logits in
+//     expert order, carrying each logit down a fixed K-entry list kept in
+//     (value descending, index ascending) order (the order of the wave
+//     arg-max), then forms the weights with the same fp32 arithmetic as
+//     route_token;
+//  3. wave c ranks the slots of chunk c (64 slots) among the chunk's slots of
+//     the same expert (one ballot per distinct expert in the chunk) and
+//     counts them per expert;
+//  4. per expert the chunk counts become absolute starts (offsets plus the
+//     earlier chunks), so slot s lands at start[chunk][expert] + rank: slots
+//     of an expert in increasing s, as in the two-launch path.
+constexpr int kFusedThreads = 1024;
+constexpr int kFusedMaxSlots = 1024;
+constexpr int kFusedChunks = kFusedMaxSlots / 64;
+constexpr int kFusedMaxLogits = 8192;
+
+template <int KL>
+__device__ __forceinline__ void route_token_serial(const float* l, int t, int E, int K, int renorm, int n_shared,
+                                                   const float* __restrict__ gate, int32_t* __restrict__ ids,
+                                                   float* __restrict__ w, int* lds_ids) {
+  float sv[KL];
+  int se[KL];
+#pragma unroll
+  for (int k = 0; k < KL; ++k) {
+    sv[k] = -__builtin_inff();
+    se[k] = -1;
+  }
+  for (int e = 0; e < E; ++e) {
+    float v = l[e];
+    int x = e;
+#pragma unroll
+    for (int k = 0; k < KL; ++k) {
+      // (value descending, index ascending): a new logit has the highest
+      // index so far, a displaced entry may precede an equal one below it
+      if (k < K && (se[k] < 0 || v > sv[k] || (v == sv[k] && x < se[k]))) {
+        const float tv = sv[k];
+        const int tx = se[k];
+        sv[k] = v;
+        se[k] = x;
+        v = tv;
+        x = tx;
+      }
+    }
+  }
+  const float m = sv[0];
+  float sum = 0.0f;
+  if (renorm) {
+#pragma unroll
+    for (int k = 0; k < KL; ++k)
+      if (k < K) sum += expf(sv[k] - m);
+  } else {
+    for (int e = 0; e < E; ++e) sum += expf(l[e] - m);
+  }
+  const int Kt = K + n_shared;
+  const size_t row = static_cast<size_t>(t) * Kt;
+#pragma unroll
+  for (int k = 0; k < KL; ++k) {
+    if (k < K) {
+      ids[row + k] = se[k];
+      w[row + k] = expf(sv[k] - m) / sum;
+      lds_ids[row + k] = se[k];
+    }
+  }
+  for (int j = 0; j < n_shared; ++j) {
+    ids[row + K + j] = E + j;
+    w[row + K + j] = gate ? gate[static_cast<size_t>(t) * n_shared + j] : 1.0f;
+    lds_ids[row + K + j] = E + j;
+  }
+}
+
+// KL: the list length of the top-K selection (a power of two, at least K)
+template <int KL>
+__global__ __launch_bounds__(kFusedThreads) void k_route_permute(const float* __restrict__ logits, int T, int E,
+                                                                 int K, int renorm, int n_shared,
+                                                                 const float* __restrict__ gate,
+                                                                 int32_t* __restrict__ ids, float* __restrict__ w,
+                                                                 int32_t* __restrict__ offsets,
+                                                                 int32_t* __restrict__ sorted_slot,
+                                                                 int32_t* __restrict__ slot_pos) {
+  __shared__ float s_lg[kFusedMaxLogits];
+  __shared__ int s_ids[kFusedMaxSlots];
+  __shared__ int s_rank[kFusedMaxSlots];
+  __shared__ int cc[kFusedChunks][kMaxExperts];   // per chunk: count, then absolute start
+  __shared__ int tot[kMaxExperts];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = lane_id();
+  const int Et = E + n_shared, S = T * (K + n_shared);
+  const int nchunk = (S + 63) / 64;
+  for (int i = tid; i < T * E; i += kFusedThreads) s_lg[i] = logits[i];
+  for (int i = tid; i < kFusedChunks * kMaxExperts; i += kFusedThreads) cc[i / kMaxExperts][i % kMaxExperts] = 0;
+  __syncthreads();
+  if (tid < T)
+    route_token_serial<KL>(s_lg + static_cast<size_t>(tid) * E, tid, E, K, renorm, n_shared, gate, ids, w, s_ids);
+  __syncthreads();
+  if (wave < nchunk) {
+    const int s = wave * 64 + lane;
+    const bool live = s < S;
+    const int id = live ? s_ids[s] : -1;
+    unsigned long long todo = __ballot(live);
+    int rank = 0;
+    while (todo) {
+      const int first = __ffsll(static_cast<long long>(todo)) - 1;
+      const int e0 = __shfl(id, first);
+      const unsigned long long m = __ballot(id == e0);
+      if (id == e0) {
+        rank = static_cast<int>(__builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(m >> 32),
+                                                          __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(m), 0u)));
+      }
+      if (lane == first) cc[wave][e0] = __popcll(m);
+      todo &= ~m;
+    }
+    if (live) s_rank[s] = rank;
+  }
+  __syncthreads();
+  if (tid < Et) {
+    int n = 0;
+    for (int c = 0; c < nchunk; ++c) n += cc[c][tid];
+    tot[tid] = n;
+  }
+  __syncthreads();
+  if (tid < Et) {
+    int start = 0;
+    for (int x = 0; x < tid; ++x) start += tot[x];
+    offsets[tid] = start;
+    if (tid == Et - 1) offsets[Et] = start + tot[tid];
+    for (int c = 0; c < nchunk; ++c) {
+      const int n = cc[c][tid];
+      cc[c][tid] = start;
+      start += n;
+    }
+  }
+  __syncthreads();
+  for (int s = tid; s < S; s += kFusedThreads) {
+    const int pos = cc[s >> 6][s_ids[s]] + s_rank[s];
+    sorted_slot[pos] = s;
+    slot_pos[s] = pos;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -572,19 +723,38 @@ __global__ void k_clear_table(pw_page_entry* table, size_t n) {
 // down projection has nsplit_sh K splits)
 // ---------------------------------------------------------------------------
 
+// Columns are taken four at a time: their positions, weights and partial
+// rows are all loaded before any is summed, so the loads of a thread overlap;
+// the sums themselves keep the order (splits ascending per column, columns
+// ascending into y).
+constexpr int kCombineCols = 4;
+
 __global__ __launch_bounds__(256) void k_combine(const GemmArgs a) {
   const int t = blockIdx.x;
   const int n = (blockIdx.y * 256 + threadIdx.x) * 4;
   if (n >= a.H) return;
   f32x4 y = {0.f, 0.f, 0.f, 0.f};
-  for (int k = 0; k < a.topk; ++k) {
-    const int pos = clampi(a.slot_pos[static_cast<size_t>(t) * a.topk + k], 0, a.S - 1);
-    const int nsp = k < a.topk - a.n_shared ? a.nsplit : a.nsplit_sh;
-    f32x4 o = {0.f, 0.f, 0.f, 0.f};
-    for (int sp = 0; sp < nsp; ++sp)
-      o += *reinterpret_cast<const f32x4*>(a.opart + (static_cast<size_t>(sp) * a.S + pos) * a.H + n);
-    const float wk = a.topk_w[static_cast<size_t>(t) * a.topk + k];
-    y += wk * o;
+  const size_t row = static_cast<size_t>(t) * a.topk;
+  for (int k0 = 0; k0 < a.topk; k0 += kCombineCols) {
+    int pos[kCombineCols], nsp[kCombineCols];
+    float wk[kCombineCols];
+#pragma unroll
+    for (int j = 0; j < kCombineCols; ++j) {
+      const int k = min(k0 + j, a.topk - 1);
+      pos[j] = clampi(a.slot_pos[row + k], 0, a.S - 1);
+      wk[j] = a.topk_w[row + k];
+      nsp[j] = k0 + j >= a.topk ? 0 : k < a.topk - a.n_shared ? a.nsplit : a.nsplit_sh;
+    }
+    f32x4 o[kCombineCols];
+#pragma unroll
+    for (int j = 0; j < kCombineCols; ++j) {
+      o[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int sp = 0; sp < nsp[j]; ++sp)
+        o[j] += *reinterpret_cast<const f32x4*>(a.opart + (static_cast<size_t>(sp) * a.S + pos[j]) * a.H + n);
+    }
+#pragma unroll
+    for (int j = 0; j < kCombineCols; ++j)
+      if (k0 + j < a.topk) y += wk[j] * o[j];
   }
   if (a.out_fp32) {
     *reinterpret_cast<f32x4*>(static_cast<float*>(a.y) + static_cast<size_t>(t) * a.H + n) = y;
@@ -877,6 +1047,37 @@ hipError_t launch_route_topk(const float* logits, int T, int E, int K, int renor
   if (K > kMaxTopK || E > 64 * kRouteLogitsPerLane) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_route_topk, dim3((T + 3) / 4), dim3(256), 0, st, logits, T, E, K, renorm, n_shared,
                      shared_gate, ids, w);
+  return hipGetLastError();
+}
+
+// The single-workgroup path's serial selection and per-expert prefixes grow
+// with the expert count: measured at 4.9 us against about 6 us for the two
+// launches with 8 experts and 64 tokens, but 29.5 us with 60 experts and 128
+// tokens, so it serves layers of at most kFusedMaxExperts experts.
+constexpr int kFusedMaxExperts = 32;
+
+bool route_permute_fits(int T, int E, int K, int n_shared) {
+  return T >= 1 && T * (K + n_shared) <= kFusedMaxSlots && T * E <= kFusedMaxLogits &&
+         E + n_shared <= kFusedMaxExperts && K <= kMaxTopK;
+}
+
+hipError_t launch_route_permute(const float* logits, int T, int E, int K, int renorm, int n_shared,
+                                const float* shared_gate, int32_t* ids, float* w, int32_t* offsets,
+                                int32_t* sorted_slot, int32_t* slot_pos, hipStream_t st) {
+  if (!route_permute_fits(T, E, K, n_shared)) return hipErrorInvalidValue;
+  const dim3 g(1), b(kFusedThreads);
+  if (K <= 2)
+    hipLaunchKernelGGL(k_route_permute<2>, g, b, 0, st, logits, T, E, K, renorm, n_shared, shared_gate, ids, w,
+                       offsets, sorted_slot, slot_pos);
+  else if (K <= 4)
+    hipLaunchKernelGGL(k_route_permute<4>, g, b, 0, st, logits, T, E, K, renorm, n_shared, shared_gate, ids, w,
+                       offsets, sorted_slot, slot_pos);
+  else if (K <= 8)
+    hipLaunchKernelGGL(k_route_permute<8>, g, b, 0, st, logits, T, E, K, renorm, n_shared, shared_gate, ids, w,
+                       offsets, sorted_slot, slot_pos);
+  else
+    hipLaunchKernelGGL(k_route_permute<16>, g, b, 0, st, logits, T, E, K, renorm, n_shared, shared_gate, ids, w,
+                       offsets, sorted_slot, slot_pos);
   return hipGetLastError();
 }
 

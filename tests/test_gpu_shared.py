@@ -62,7 +62,10 @@ def _check(L, O, cfg, T, with_gate, tokens=None):
 
 # T = 16: both ranges on the decode kernels; T = 100: routed on the decode
 # kernels (25 slots per expert), shared on the streaming kernel (100);
-# T = 300: routed on the streaming kernel (75), shared on the tiled one (300)
+# T = 300: routed and shared on the streaming kernel (75 and 300 slots per
+# expert; two shared experts fill too few 256 x 256 tiles for the tiled one,
+# so the tiled kernel runs the shared range only where the tiles fill the
+# chip, as in test_shared_experts_tiled)
 @pytest.mark.parametrize("T", [16, 100, 300])
 @pytest.mark.parametrize("with_gate", [False, True])
 def test_tiny_shared_experts(T, with_gate):
@@ -73,6 +76,19 @@ def test_tiny_shared_experts(T, with_gate):
     O = oracle_layer(cfg, w16, bits)
     e16, e32 = _check(L, O, cfg, T, with_gate)
     assert e16 <= TOL16 and e32 <= TOL32, (T, e16, e32)
+    L.close()
+
+
+def test_shared_experts_tiled():
+    """Shared experts on the tiled kernel: 4 shared experts of a tiny layer
+    with F = 4096 at T = 600 fill 4 x 3 x 32 = 384 tiles of 256 x 256."""
+    cfg, w16, bits, order = case("tiny_shared", F=4096, n_shared=4, E=12, T=600)
+    say("shared experts: tiled shared range, T=600")
+    L = gpu_layer(cfg, w16, bits, order)
+    L.set_shared_experts(cfg.n_shared)
+    O = oracle_layer(cfg, w16, bits)
+    e16, e32 = _check(L, O, cfg, cfg.T, True, tokens=list(range(0, 600, 7)) + [599])
+    assert e16 <= TOL16 and e32 <= TOL32, (e16, e32)
     L.close()
 
 
@@ -125,7 +141,8 @@ def test_qwen_shared_full():
     """Qwen1.5-MoE-shaped layer (60 routed + 4 shared experts, top-4, 2048 /
     1408, 128 tokens, gated shared experts): every page byte and every token
     of the output. The routed experts run the decode kernels (9 slots per
-    expert), the shared ones the tiled kernel (128 each)."""
+    expert), the shared ones the streaming kernel (128 each: four experts
+    would fill only 44 of the tiled kernel's 256 x 256 tiles)."""
     cfg, w16, bits, order = case("qwen_shared")
     say("shared experts: Qwen-shaped layer, build (%d pages)" % len(order))
     L = gpu_layer(cfg, w16, bits, order)
