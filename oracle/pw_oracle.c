@@ -464,6 +464,7 @@ typedef struct {
     const uint16_t* s;
     const uint16_t* z;
     int rows, cols;
+    uint16_t* wr;   /* w_round: each quantized weight rounded once, or NULL */
 } or_proj;
 
 /* dot(row n of expert e's projection, v) with the weight read at its page's
@@ -471,6 +472,20 @@ typedef struct {
  * w_round=1 a quantized weight is instead first rounded to fp32 and then to
  * the activation format (round to nearest even both times): the value a
  * kernel feeds to a 16-bit matrix unit after dequantizing in fp32.         */
+/* The weight of row n, column j of a quantized page: z + c*s (exact in fp64). */
+static double quant_weight(const or_proj* P, int e, int n, int j, int G, const double* dsdt) {
+    int ng = P->cols / G;
+    size_t base = ((size_t)e * P->rows + n) * P->cols;
+    size_t sb = ((size_t)e * P->rows + n) * ng;
+    return dsdt[P->z[sb + j / G]] + (double)P->codes[base + j] * dsdt[P->s[sb + j / G]];
+}
+
+/* The w_round reading of a quantized weight: rounded to fp32, then to the
+ * activation format (round to nearest even both times), as a bit pattern. */
+static uint16_t rounded_weight(const or_proj* P, int e, int n, int j, int G, const double* dsdt, int act) {
+    return or_round_nearest16((double)(float)quant_weight(P, e, n, j, G, dsdt), act);
+}
+
 static double proj_row_dot(const or_proj* P, int e, int n, const double* v, int R, int G,
                            const double* d16, const double* dsdt, int w_round, int act) {
     int b = P->bits[(size_t)e * (P->rows / R) + n / R];
@@ -479,18 +494,36 @@ static double proj_row_dot(const or_proj* P, int e, int n, const double* v, int 
     if (b == 16) {
         const uint16_t* w = P->w16 + base;
         for (int j = 0; j < P->cols; ++j) acc += d16[w[j]] * v[j];
+    } else if (w_round && P->wr) {
+        const uint16_t* w = P->wr + base;
+        for (int j = 0; j < P->cols; ++j) acc += d16[w[j]] * v[j];
     } else {
-        int ng = P->cols / G;
-        const uint8_t* c = P->codes + base;
-        const uint16_t* s = P->s + ((size_t)e * P->rows + n) * ng;
-        const uint16_t* z = P->z + ((size_t)e * P->rows + n) * ng;
         for (int j = 0; j < P->cols; ++j) {
-            double wv = dsdt[z[j / G]] + (double)c[j] * dsdt[s[j / G]];
-            if (w_round) wv = or_decode16(or_round_nearest16((double)(float)wv, act), act);
+            double wv = quant_weight(P, e, n, j, G, dsdt);
+            if (w_round) wv = or_decode16(rounded_weight(P, e, n, j, G, dsdt, act), act);
             acc += wv * v[j];
         }
     }
     return acc;
+}
+
+/* w_round: every quantized weight of the experts in `used` rounded once up
+ * front (the same values proj_row_dot would round per token), or NULL when
+ * the memory is not there (proj_row_dot then rounds as it goes).           */
+static uint16_t* round_all(const or_proj* P, const unsigned char* used, int E, int R, int G,
+                           const double* dsdt, int act) {
+    uint16_t* wr = (uint16_t*)malloc(sizeof(uint16_t) * (size_t)E * P->rows * P->cols);
+    if (!wr) return NULL;
+    for (int e = 0; e < E; ++e) {
+        if (!used[e]) continue;
+#pragma omp parallel for schedule(static)
+        for (int n = 0; n < P->rows; ++n) {
+            if (P->bits[(size_t)e * (P->rows / R) + n / R] == 16) continue;
+            uint16_t* w = wr + ((size_t)e * P->rows + n) * P->cols;
+            for (int j = 0; j < P->cols; ++j) w[j] = rounded_weight(P, e, n, j, G, dsdt, act);
+        }
+    }
+    return wr;
 }
 
 /* y[t] = sum_k w[t,k] * down_e( silu(gate_e(x_t)) * up_e(x_t) ), e = ids[t,k],
@@ -508,13 +541,23 @@ void or_moe_forward(const uint16_t* x16, int T, int H, int F, int E, int K, int 
                     const uint16_t* ds, const uint16_t* dz,
                     int h_round, int w_round, const int32_t* tok, int n_tok, double* y) {
     (void)T;
-    (void)E;
     or_init();
     const double* d16 = dec_table(act);
     const double* dsdt = dec_table(sdt);
-    or_proj PG = {g16, gbits, gcodes, gs, gz, F, H};
-    or_proj PU = {u16, ubits, ucodes, us, uz, F, H};
-    or_proj PD = {d16w, dbits, dcodes, ds, dz, H, F};
+    or_proj PG = {g16, gbits, gcodes, gs, gz, F, H, NULL};
+    or_proj PU = {u16, ubits, ucodes, us, uz, F, H, NULL};
+    or_proj PD = {d16w, dbits, dcodes, ds, dz, H, F, NULL};
+    if (w_round) {
+        unsigned char* used = (unsigned char*)calloc((size_t)E, 1);
+        if (used) {
+            for (int ti = 0; ti < n_tok; ++ti)
+                for (int k = 0; k < K; ++k) used[ids[(size_t)tok[ti] * K + k]] = 1;
+            PG.wr = round_all(&PG, used, E, R, G, dsdt, act);
+            PU.wr = round_all(&PU, used, E, R, G, dsdt, act);
+            PD.wr = round_all(&PD, used, E, R, G, dsdt, act);
+            free(used);
+        }
+    }
     double* xv = (double*)malloc(sizeof(double) * H);
     double* h = (double*)malloc(sizeof(double) * F);
     double* o = (double*)malloc(sizeof(double) * H);
@@ -542,4 +585,7 @@ void or_moe_forward(const uint16_t* x16, int T, int H, int F, int E, int K, int 
     free(xv);
     free(h);
     free(o);
+    free(PG.wr);
+    free(PU.wr);
+    free(PD.wr);
 }
