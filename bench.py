@@ -380,26 +380,43 @@ def leg_downshift(steps_before=8, steps_after=8):
     Lw.close()
     del Lw
     need = sum(pw.pw_page_bytes(cfg, p, 16) + pw.pw_page_bytes(cfg, p, 4) for (_, p, _) in pages)
-    Li = PagedLayer(cfg, int(need * 1.05) + (1 << 20))
-    Li.load_pages(w16, bits, pages)
-    torch.cuda.synchronize()
-    evi = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in plan]
-    pw.pw_profile_read(Li.handle, reset=True)
-    pw.pw_profile_enable(Li.handle, True)
-    for k, chunk in enumerate(plan):
-        evi[k][0].record()
-        Li.requant(chunk, 4)
-        evi[k][1].record()
-        Li.commit()
-        Li.reclaim()
-    torch.cuda.synchronize()
-    pw.pw_profile_enable(Li.handle, False)
-    alone_kernel_ms = pw.pw_profile_read(Li.handle, reset=True)[0][pw.PW_PH_REQUANT]
-    alone_ms = [a.elapsed_time(b) for a, b in evi]
-    log("requant alone, call ms per chunk: %s" % " ".join("%.3f" % m for m in alone_ms))
-    alone_moved = sum(pw.pw_page_bytes(cfg, p, 16) + pw.pw_page_bytes(cfg, p, 4) for (_, p, _) in pages)
-    Li.close()
-    del Li
+    alone_moved = need
+
+    def alone(chunks, head_start):
+        """Requant of the plan's pages on an idle GPU, one call per chunk:
+        (kernel ms summed over the launches, call ms per chunk, launches).
+        head_start: a bounded spin (torch.cuda._sleep) occupies the stream
+        before each call, so the call's launches are queued before the GPU
+        reaches them and the kernel events hold no host submission time."""
+        Li = PagedLayer(cfg, int(need * 1.05) + (1 << 20))
+        Li.load_pages(w16, bits, pages)
+        torch.cuda.synchronize()
+        evi = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in chunks]
+        pw.pw_profile_read(Li.handle, reset=True)
+        pw.pw_profile_enable(Li.handle, True)
+        for k, chunk in enumerate(chunks):
+            if head_start:
+                torch.cuda._sleep(2_000_000)
+            evi[k][0].record()
+            Li.requant(chunk, 4)
+            evi[k][1].record()
+            Li.commit()
+            Li.reclaim()
+        torch.cuda.synchronize()
+        pw.pw_profile_enable(Li.handle, False)
+        ms, cnt = pw.pw_profile_read(Li.handle, reset=True)
+        Li.close()
+        return ms[pw.PW_PH_REQUANT], [a.elapsed_time(b) for a, b in evi], cnt[pw.PW_PH_REQUANT]
+
+    # the whole plan in one call (launches of up to 448 pages per bitwidth
+    # pair), then the plan's chunks one call each (one launch per chunk);
+    # the call time of the one call is also taken without the head start
+    alone_kernel_ms, gpu_call_ms, alone_launches = alone([pages], True)
+    chunk_kernel_ms, chunk_ms, _ = alone(plan, True)
+    _, alone_ms, _ = alone([pages], False)
+    log("requant alone: one call %.3f ms with host submission, %.3f ms queued ahead (%d launches, kernels "
+        "%.4f ms); per chunk call ms: %s" % (alone_ms[0], gpu_call_ms[0], alone_launches, alone_kernel_ms,
+                                           " ".join("%.3f" % m for m in chunk_ms)))
     L = PagedLayer(cfg, PagedLayer.pool_bytes_for(cfg, bits, slack=0.1))
     L.load_pages(w16, bits, synth.pool_order(cfg))
     del w16
@@ -455,8 +472,13 @@ def leg_downshift(steps_before=8, steps_after=8):
             "step_ms_before": round(before, 4), "step_ms_during": round(during, 4),
             "step_ms_after": round(after, 4), "decode_slowdown": round(during / before - 1.0, 4),
             "requant_alone_GBps": round(alone_moved / (alone_kernel_ms * 1e-3) / 1e9, 1),
-            "requant_alone_kernel_ms_all_chunks": round(alone_kernel_ms, 4),
-            "requant_alone_call_ms_all_chunks": round(sum(alone_ms), 4),
+            "requant_alone_kernel_ms": round(alone_kernel_ms, 4),
+            "requant_alone_launches": alone_launches,
+            "requant_alone_call_ms": round(alone_ms[0], 4),
+            "requant_alone_call_ms_queued_ahead": round(gpu_call_ms[0], 4),
+            "requant_alone_chunked_GBps": round(alone_moved / (chunk_kernel_ms * 1e-3) / 1e9, 1),
+            "requant_alone_chunked_kernel_ms_all_chunks": round(chunk_kernel_ms, 4),
+            "requant_alone_chunked_call_ms_all_chunks": round(sum(chunk_ms), 4),
             "requant_during_decode_GBps": round(moved / (rq_ms * 1e-3) / 1e9, 1) if rq_ms else None,
             "requant_ms_per_launch_during_decode": round(rq_ms / max(cnt[pw.PW_PH_REQUANT], 1), 4),
             "bytes_freed": int(freed), "post_switch_weight_GBps": round(post_bytes / (after * 1e-3) / 1e9, 1)}

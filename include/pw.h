@@ -118,10 +118,12 @@ pw_status pw_page_bytes(const pw_layer_desc* desc, int proj, int bits, size_t* b
 
 /* Sec. 3.1 (weight page table: one row per block with its committed
  * bitwidth and memory size). Create a layer over a caller-owned pool
- * [pool_dev, pool_dev + pool_bytes) (256-byte aligned) and device table
- * table_dev (pw_table_entries entries, 8-byte aligned). The table is cleared
- * to absent entries on the null stream, which is synchronized.
- *   bad shape (see pw_layer_desc), null or misaligned pointers: PW_EINVAL.
+ * [pool_dev, pool_dev + pool_bytes) (256-byte aligned, at most 2^40 bytes)
+ * and device table table_dev (pw_table_entries entries, 8-byte aligned). The
+ * table is cleared to absent entries on the null stream, which is
+ * synchronized.
+ *   bad shape (see pw_layer_desc), null or misaligned pointers, a pool
+ *   above 2^40 bytes: PW_EINVAL.
  *   clearing the table failed: PW_EHIP (no handle is returned).            */
 pw_status pw_layer_create(const pw_layer_desc* desc, void* pool_dev, size_t pool_bytes,
                           pw_page_entry* table_dev, pw_layer** out);
@@ -234,8 +236,9 @@ pw_status pw_moe_paged_gemm_noalloc(const pw_layer* layer, const void* x, int T,
 pw_status pw_requant_block(pw_layer* layer, int e, int proj, int rb, int new_bits,
                            void* side_stream, size_t* delta_bytes);
 
-/* Batched form of pw_requant_block over n blocks (one kernel launch per 32
- * blocks). On error no block of the batch is left pending.
+/* Batched form of pw_requant_block over n blocks (one kernel launch per 448
+ * blocks of one (old, new) bitwidth pair, pages of every projection
+ * together). On error no block of the batch is left pending.
  * Ordering: the kernels read the source pages on side_stream; the caller
  * orders side_stream after the stream that loaded or last wrote them (the
  * library itself waits only for host-copy transfers of those pages).     */

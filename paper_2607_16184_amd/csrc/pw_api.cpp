@@ -87,6 +87,9 @@ struct ProfScope {
 
 bool mult_of_256(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 255u) == 0; }
 
+// Pool offsets travel to the requant kernel as 32-bit counts of 256 bytes.
+constexpr uint64_t kMaxPoolBytes = uint64_t(1) << 40;
+
 // Device workspace layout of pw_moe_paged_gemm.
 enum class GemmPath { kDecode, kStream, kTiled };
 
@@ -223,6 +226,57 @@ pw_status run_qjobs(pw_layer* L, const std::vector<pw::QJob>& jobs, hipStream_t 
   return PW_OK;
 }
 
+// Requant of pool pages, grouped by (source, destination) bitwidths in the
+// plan's order, kMaxRqJobs pages per launch. The kernel finds a page's
+// scale/zero block right after its codes (the slot layout of the allocator).
+struct RqPlanned {
+  pw_page_entry src, dst;
+  int proj;
+};
+pw_status run_requant(pw_layer* L, const std::vector<RqPlanned>& jobs, hipStream_t st) {
+  const pw_layer_desc& d = L->st.desc;
+  static const int kPairs[3][2] = {{16, 8}, {16, 4}, {8, 4}};
+  for (const RqPlanned& j : jobs) {
+    bool known = false;
+    for (const auto& pr : kPairs) known = known || (j.src.bits == pr[0] && j.dst.bits == pr[1]);
+    if (!known) return fail(PW_EUNSUPPORTED, "requant supports 16 -> 8, 16 -> 4 and 8 -> 4 only");
+    const bool sz_follows = (j.src.bits == 16 || j.src.sz_off == j.src.data_off + L->st.code_bytes(j.proj, j.src.bits)) &&
+                            j.dst.sz_off == j.dst.data_off + L->st.code_bytes(j.proj, j.dst.bits);
+    if (!sz_follows || (j.src.data_off | j.dst.data_off) % 256 != 0)
+      return fail(PW_EINVAL, "requant: a slot is not laid out as codes then scale/zero words on a 256-byte boundary");
+  }
+  for (const auto& pr : kPairs) {
+    pw::RqBatch b{};
+    b.pool = L->pool;
+    b.R = d.R;
+    b.G = d.G;
+    b.kb[0] = static_cast<uint16_t>(d.H / 128);
+    b.kb[1] = static_cast<uint16_t>(d.F / 128);
+    auto flush = [&]() -> pw_status {
+      if (b.n_jobs == 0) return PW_OK;
+      ProfScope ps(L, PW_PH_REQUANT, st);
+      hipError_t e = pw::launch_requant(b, pr[0], pr[1], d.act, d.sdt, st);
+      b.n_jobs = 0;
+      for (uint32_t& w : b.kbit) w = 0u;
+      return e == hipSuccess ? PW_OK : hip_fail(e, "requant launch");
+    };
+    for (const RqPlanned& j : jobs) {
+      if (j.src.bits != pr[0] || j.dst.bits != pr[1]) continue;
+      const int n = b.n_jobs++;
+      b.src[n] = static_cast<uint32_t>(j.src.data_off / 256);
+      b.dst[n] = static_cast<uint32_t>(j.dst.data_off / 256);
+      if (j.proj == PW_DOWN) b.kbit[n >> 5] |= 1u << (n & 31);
+      if (b.n_jobs == pw::kMaxRqJobs) {
+        pw_status s = flush();
+        if (s != PW_OK) return s;
+      }
+    }
+    pw_status s = flush();
+    if (s != PW_OK) return s;
+  }
+  return PW_OK;
+}
+
 pw_status write_entries(pw_layer* L, const std::vector<std::pair<size_t, pw_page_entry>>& w,
                         hipStream_t st) {
   for (size_t base = 0; base < w.size(); base += pw::kMaxEntryWrites) {
@@ -281,6 +335,7 @@ pw_status pw_layer_create(const pw_layer_desc* d, void* pool_dev, size_t pool_by
   *out = nullptr;
   if (!pw::LayerState::valid_desc(*d, &err)) return fail(PW_EINVAL, err);
   if (!mult_of_256(pool_dev)) return fail(PW_EINVAL, "pool must be 256-byte aligned");
+  if (static_cast<uint64_t>(pool_bytes) > kMaxPoolBytes) return fail(PW_EINVAL, "pool larger than 2^40 bytes");
   if (reinterpret_cast<uintptr_t>(table_dev) & 7u) return fail(PW_EINVAL, "table must be 8-byte aligned");
   pw_layer* L = new pw_layer(*d, pool_dev, pool_bytes, table_dev);
   hipError_t e = pw::launch_clear_table(table_dev, L->st.n_entries, nullptr);
@@ -667,22 +722,14 @@ pw_status pw_requant_blocks(pw_layer* L, int n, const int* e, const int* proj, c
       return hip_fail(he, "hipStreamWaitEvent");
     }
   }
-  // one launch for the whole plan (jobs of every projection, each with its K)
-  std::vector<pw::QJob> jobs;
+  // launches of up to kMaxRqJobs pages per bitwidth pair (pages of every
+  // projection together, each with its K)
+  std::vector<RqPlanned> jobs;
   for (const Planned& p : plan) {
     if (p.dst.rsv & pw::LayerState::kInPlace) continue;   // a bit-plane drop needs no kernel
-    pw::QJob j{};
-    j.src = L->pool + p.src.data_off;
-    j.src_sz = p.src.bits == 16 ? nullptr : L->pool + p.src.sz_off;
-    j.dst = L->pool + p.dst.data_off;
-    j.dst_sz = L->pool + p.dst.sz_off;
-    j.K = L->st.kdim(p.proj);
-    j.src_bits = p.src.bits;
-    j.dst_bits = p.dst.bits;
-    j.src_plain = 0;
-    jobs.push_back(j);
+    jobs.push_back(RqPlanned{p.src, p.dst, p.proj});
   }
-  pw_status rs = run_qjobs(L, jobs, st);
+  pw_status rs = run_requant(L, jobs, st);
   if (rs != PW_OK) {
     drain(st);
     rollback();

@@ -33,6 +33,23 @@ struct QJobBatch {
   uint32_t total_items;
 };
 
+// Pages of one requant launch, all of one (source, destination) bitwidth
+// pair. A page's slot and its scale/zero block (right after the codes) are
+// at pool + 256 src[j] and pool + 256 dst[j]; bit j of kbit selects its K
+// (kb[0] = H / 128 for gate/up pages, kb[1] = F / 128 for down pages). The
+// whole batch travels as the kernel argument (under 4 KiB).
+constexpr int kMaxRqJobs = 448;
+struct RqBatch {
+  uint8_t* pool;
+  int n_jobs;
+  int R, G;
+  uint16_t kb[2];
+  uint32_t kbit[kMaxRqJobs / 32];
+  uint32_t src[kMaxRqJobs];
+  uint32_t dst[kMaxRqJobs];
+};
+static_assert(sizeof(RqBatch) <= 4000, "requant batch must fit a 4 KiB kernel argument");
+
 // Nested bit-plane quantization of whole blocks (one thread per row).
 constexpr int kMaxAplJobs = 32;
 // per-row float64 scratch: centroids of levels 4..8 (16 + 32 + 64 + 128 + 256),
@@ -102,6 +119,9 @@ hipError_t launch_route_permute(const float* logits, int T, int E, int K, int re
 hipError_t launch_permute(const int32_t* ids, int T, int K, int E, int32_t* offsets,
                           int32_t* sorted_slot, int32_t* slot_pos, hipStream_t st);
 hipError_t launch_qjobs(const QJobBatch& b, hipStream_t st);
+// Requant of pool pages (16 -> 8, 16 -> 4 or 8 -> 4, every page of the batch
+// the same pair); hipErrorInvalidValue for a batch the kernel cannot take.
+hipError_t launch_requant(const RqBatch& b, int src_bits, int dst_bits, int act, int sdt, hipStream_t st);
 hipError_t launch_entry_writes(pw_page_entry* table, const EntryWrites& w, hipStream_t st);
 hipError_t launch_clear_table(pw_page_entry* table, size_t n, hipStream_t st);
 hipError_t launch_gateup(const GemmArgs& a, hipStream_t st);

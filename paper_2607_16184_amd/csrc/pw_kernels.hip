@@ -706,6 +706,166 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void k
   qjobs_item<ACT, SDT, kQG128>(b);
 }
 
+// ---------------------------------------------------------------------------
+// Requantization of pool pages to fewer bits (16 -> 8, 16 -> 4, 8 -> 4).
+//
+// A launch covers up to kMaxRqJobs pages of one (source, destination) pair
+// of bitwidths. The grid is (spans / 4, row tiles, pages): the wave of span
+// 4 blockIdx.x + w of row tile blockIdx.y of page blockIdx.z codes that
+// 16-row x max(G, 128)-value piece, so it finds its work from its indices
+// with no search. Waves past a page's last span exit at once. The bitwidths
+// are template parameters: every wave runs one straight path, the kernel
+// stays under 64 VGPRs and eight waves per SIMD keep their loads in flight.
+// Pool addresses are formed in the global address space, so the loads and
+// stores are plain global (not flat) accesses; source blocks and codes are
+// touched once, so both move as nontemporal (streaming) accesses.
+// ---------------------------------------------------------------------------
+
+#define PW_GLOBAL __attribute__((address_space(1)))
+typedef const PW_GLOBAL uint8_t* gsrc_t;
+typedef PW_GLOBAL uint8_t* gdst_t;
+
+template <int SRC, int GK>
+__device__ __forceinline__ void rq_load(gsrc_t src, gsrc_t src_sz, size_t tile, int R, int G, int blk, int r,
+                                        QRaw& raw) {
+  const int lane = lane_id();
+  if constexpr (SRC == 16) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      raw.w[i] = __builtin_nontemporal_load(reinterpret_cast<const PW_GLOBAL u32x4*>(src + tile * 4096 + 1024 * i + 16 * lane));
+  } else {
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+      raw.w[u] = __builtin_nontemporal_load(reinterpret_cast<const PW_GLOBAL u32x4*>(src + tile * 2048 + 1024 * u + 16 * lane));
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int g = GK == kQG64 ? 2 * blk + (i >> 1) : GK == kQG128 ? blk : (blk * 128) / G;
+      raw.sz[i] = *reinterpret_cast<const PW_GLOBAL uint32_t*>(src_sz + (static_cast<size_t>(g) * R + r) * 4);
+    }
+  }
+}
+
+// The code of v as an integer-valued float (q_code without the conversion).
+__device__ __forceinline__ float q_codef(float v, const QGroup& g, float Qf) {
+  const float d = v - g.z;
+  const float qa = d * g.rs;
+  float c = rintf(qa);
+  if (!g.fast || fabsf(qa - c) > 0.5f - 0x1p-12f) c = rintf(d / g.s);
+  return __builtin_amdgcn_fmed3f(c, 0.0f, Qf);
+}
+
+// Codes of one block in the destination tile layout. A code is an integer in
+// [0, Q], so the byte conversion of cvt_pk_u8_f32 is exact; each call places
+// one code in a chosen byte of a word. 4-bit word of k-step i: nibble t holds
+// code 8i + 2t and nibble 4 + t code 8i + 2t + 1, i.e. bytes [c0 c4 c1 c5]
+// in the low nibbles and [c2 c6 c3 c7] in the high ones.
+template <int DST, typename CF>
+__device__ __forceinline__ void rq_store_codes(gdst_t dst, size_t tile, CF cf) {
+  const int lane = lane_id();
+  if constexpr (DST == 8) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      u32x4 o;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const int e = 16 * u + 4 * w;
+        uint32_t x = __builtin_amdgcn_cvt_pk_u8_f32(cf(e), 0, 0u);
+        x = __builtin_amdgcn_cvt_pk_u8_f32(cf(e + 1), 1, x);
+        x = __builtin_amdgcn_cvt_pk_u8_f32(cf(e + 2), 2, x);
+        o[w] = __builtin_amdgcn_cvt_pk_u8_f32(cf(e + 3), 3, x);
+      }
+      __builtin_nontemporal_store(o, reinterpret_cast<PW_GLOBAL u32x4*>(dst + tile * 2048 + 1024 * u + 16 * lane));
+    }
+  } else {
+    u32x4 o;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int e = 8 * i;
+      uint32_t a = __builtin_amdgcn_cvt_pk_u8_f32(cf(e), 0, 0u);
+      a = __builtin_amdgcn_cvt_pk_u8_f32(cf(e + 4), 1, a);
+      a = __builtin_amdgcn_cvt_pk_u8_f32(cf(e + 1), 2, a);
+      a = __builtin_amdgcn_cvt_pk_u8_f32(cf(e + 5), 3, a);
+      uint32_t c = __builtin_amdgcn_cvt_pk_u8_f32(cf(e + 2), 0, 0u);
+      c = __builtin_amdgcn_cvt_pk_u8_f32(cf(e + 6), 1, c);
+      c = __builtin_amdgcn_cvt_pk_u8_f32(cf(e + 3), 2, c);
+      c = __builtin_amdgcn_cvt_pk_u8_f32(cf(e + 7), 3, c);
+      o[i] = a | (c << 4);
+    }
+    __builtin_nontemporal_store(o, reinterpret_cast<PW_GLOBAL u32x4*>(dst + tile * 1024 + 16 * lane));
+  }
+}
+
+template <int ACT, int SDT, int GK, int SRC, int DST>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void k_requant(const RqBatch b) {
+  const int j = blockIdx.z;
+  const int nkb = ((b.kbit[j >> 5] >> (j & 31)) & 1u) ? b.kb[1] : b.kb[0];
+  const int span = GK == kQGBig ? b.G / 128 : 1;   // blocks per wave
+  const int sp = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (sp * span >= nkb) return;
+  const int lane = lane_id(), lc = lane & 15, lg = lane >> 4;
+  const int R = b.R, tau = blockIdx.y, r = tau * 16 + lc;
+  constexpr float Qf = static_cast<float>((1 << DST) - 1);
+  const size_t rk = static_cast<size_t>(R) * nkb * 128;   // values of the page
+  gsrc_t src = (gsrc_t)b.pool + static_cast<size_t>(b.src[j]) * 256;   // generic to global: C-style casts
+  gsrc_t src_sz = src + rk * SRC / 8;
+  gdst_t dst = (gdst_t)b.pool + static_cast<size_t>(b.dst[j]) * 256;
+  gdst_t dst_sz = dst + rk * DST / 8;
+  const size_t row0 = static_cast<size_t>(tau) * nkb;   // first tile of the row tile
+  float lo0 = __builtin_inff(), hi0 = -__builtin_inff(), lo1 = lo0, hi1 = hi0;
+  if constexpr (GK != kQGBig) {
+    QRaw raw;
+    rq_load<SRC, GK>(src, src_sz, row0 + sp, R, b.G, sp, r, raw);
+#pragma unroll
+    for (int e = 0; e < 32; ++e) {
+      const float v = q_elem<ACT, SDT, SRC>(raw, e);
+      if (GK == kQG64 && e >= 16) {
+        lo1 = fminf(lo1, v);
+        hi1 = fmaxf(hi1, v);
+      } else {
+        lo0 = fminf(lo0, v);
+        hi0 = fmaxf(hi0, v);
+      }
+    }
+    q_rowreduce(lo0, hi0, lo1, hi1);
+    uint32_t sb0, zb0, sb1 = 0u, zb1 = 0u;
+    q_params<SDT>(lo0, hi0, static_cast<int>(Qf), &sb0, &zb0);
+    if (GK == kQG64) q_params<SDT>(lo1, hi1, static_cast<int>(Qf), &sb1, &zb1);
+    const QGroup g0 = q_group<SDT>(sb0, zb0), g1 = q_group<SDT>(sb1, zb1);
+    rq_store_codes<DST>(dst, row0 + sp, [&](int e) {
+      return q_codef(q_elem<ACT, SDT, SRC>(raw, e), (GK == kQG64 && e >= 16) ? g1 : g0, Qf);
+    });
+    if (lg == 0) {
+      const int gi = GK == kQG64 ? 2 * sp : sp;
+      *reinterpret_cast<PW_GLOBAL uint32_t*>(dst_sz + (static_cast<size_t>(gi) * R + r) * 4) = sb0 | (zb0 << 16);
+      if (GK == kQG64)
+        *reinterpret_cast<PW_GLOBAL uint32_t*>(dst_sz + (static_cast<size_t>(gi + 1) * R + r) * 4) = sb1 | (zb1 << 16);
+    }
+  } else {
+    // G > 128: the group spans `span` blocks; its extremes first, then the
+    // codes, each pass reading the blocks again
+    for (int blk = sp * span; blk < (sp + 1) * span; ++blk) {
+      QRaw raw;
+      rq_load<SRC, GK>(src, src_sz, row0 + blk, R, b.G, blk, r, raw);
+#pragma unroll
+      for (int e = 0; e < 32; ++e) {
+        const float v = q_elem<ACT, SDT, SRC>(raw, e);
+        lo0 = fminf(lo0, v);
+        hi0 = fmaxf(hi0, v);
+      }
+    }
+    q_rowreduce(lo0, hi0, lo1, hi1);
+    uint32_t sb0, zb0;
+    q_params<SDT>(lo0, hi0, static_cast<int>(Qf), &sb0, &zb0);
+    const QGroup g0 = q_group<SDT>(sb0, zb0);
+    for (int blk = sp * span; blk < (sp + 1) * span; ++blk) {
+      QRaw raw;
+      rq_load<SRC, GK>(src, src_sz, row0 + blk, R, b.G, blk, r, raw);
+      rq_store_codes<DST>(dst, row0 + blk, [&](int e) { return q_codef(q_elem<ACT, SDT, SRC>(raw, e), g0, Qf); });
+    }
+    if (lg == 0) *reinterpret_cast<PW_GLOBAL uint32_t*>(dst_sz + (static_cast<size_t>(sp) * R + r) * 4) = sb0 | (zb0 << 16);
+  }
+}
+
 __global__ void k_entry_writes(pw_page_entry* table, const EntryWrites w) {
   const int i = threadIdx.x;
   if (i < w.n) table[w.idx[i]] = w.ent[i];
@@ -1104,6 +1264,48 @@ hipError_t launch_qjobs(const QJobBatch& b, hipStream_t st) {
   } else {
     if (b.sdt == PW_BF16) qjobs_go<PW_F16, PW_BF16>(b, st);
     else qjobs_go<PW_F16, PW_F16>(b, st);
+  }
+  return hipGetLastError();
+}
+
+template <int ACT, int SDT, int GK>
+static void requant_go(const RqBatch& b, int src_bits, int dst_bits, dim3 grid, hipStream_t st) {
+  const dim3 block(256);
+  if (src_bits == 16 && dst_bits == 8)
+    hipLaunchKernelGGL((k_requant<ACT, SDT, GK, 16, 8>), grid, block, 0, st, b);
+  else if (src_bits == 16)
+    hipLaunchKernelGGL((k_requant<ACT, SDT, GK, 16, 4>), grid, block, 0, st, b);
+  else
+    hipLaunchKernelGGL((k_requant<ACT, SDT, GK, 8, 4>), grid, block, 0, st, b);
+}
+
+template <int ACT, int SDT>
+static void requant_g(const RqBatch& b, int src_bits, int dst_bits, dim3 grid, hipStream_t st) {
+  if (b.G == 64) requant_go<ACT, SDT, kQG64>(b, src_bits, dst_bits, grid, st);
+  else if (b.G == 128) requant_go<ACT, SDT, kQG128>(b, src_bits, dst_bits, grid, st);
+  else requant_go<ACT, SDT, kQGBig>(b, src_bits, dst_bits, grid, st);
+}
+
+hipError_t launch_requant(const RqBatch& b, int src_bits, int dst_bits, int act, int sdt, hipStream_t st) {
+  if (b.n_jobs == 0) return hipSuccess;
+  const bool pair_ok = (src_bits == 16 && (dst_bits == 8 || dst_bits == 4)) || (src_bits == 8 && dst_bits == 4);
+  if (!pair_ok || b.n_jobs < 0 || b.n_jobs > kMaxRqJobs || b.R <= 0 || b.R % 16 != 0 ||
+      (b.G != 64 && b.G != 128 && b.G != 256 && b.G != 512))
+    return hipErrorInvalidValue;
+  const int span = b.G > 128 ? b.G / 128 : 1;
+  uint32_t max_spans = 0;
+  for (int j = 0; j < b.n_jobs; ++j) {
+    const uint32_t kb = ((b.kbit[j >> 5] >> (j & 31)) & 1u) ? b.kb[1] : b.kb[0];
+    if (kb == 0 || kb % span != 0) return hipErrorInvalidValue;
+    max_spans = std::max<uint32_t>(max_spans, kb / span);
+  }
+  const dim3 grid((max_spans + 3) / 4, b.R / 16, b.n_jobs);
+  if (act == PW_BF16) {
+    if (sdt == PW_BF16) requant_g<PW_BF16, PW_BF16>(b, src_bits, dst_bits, grid, st);
+    else requant_g<PW_BF16, PW_F16>(b, src_bits, dst_bits, grid, st);
+  } else {
+    if (sdt == PW_BF16) requant_g<PW_F16, PW_BF16>(b, src_bits, dst_bits, grid, st);
+    else requant_g<PW_F16, PW_F16>(b, src_bits, dst_bits, grid, st);
   }
   return hipGetLastError();
 }

@@ -87,16 +87,20 @@ def test_tiny_quantized_pages_bit_exact():
     L.close()
 
 
-# G = 64 (fp16) runs the generic requant kernel, G = 128 the one-group-per-
-# block kernel, here also with bf16 activations and scales.
+# Every bitwidth pair at G = 64 (two groups per 128-value block), 128 (one)
+# and 256 / 512 (a group over two or four blocks, coded in two passes), with
+# fp16 and bf16 activations and scales.
 @pytest.mark.parametrize("src,dst,G,act,sdt", [
     (16, 8, 64, synth.F16, synth.F16), (16, 4, 64, synth.F16, synth.F16), (8, 4, 64, synth.F16, synth.F16),
     (16, 8, 128, synth.BF16, synth.BF16), (16, 4, 128, synth.BF16, synth.BF16), (8, 4, 128, synth.BF16, synth.BF16),
     (8, 4, 128, synth.F16, synth.BF16),
+    (16, 8, 256, synth.BF16, synth.F16), (16, 4, 256, synth.F16, synth.BF16), (8, 4, 256, synth.BF16, synth.BF16),
+    (16, 4, 512, synth.BF16, synth.F16), (8, 4, 512, synth.F16, synth.F16),
 ])
 def test_tiny_requant_bit_exact(src, dst, G, act, sdt):
     import torch
-    cfg, w16, _, order = case("tiny", G=G, act=act, sdt=sdt)
+    extra = dict(H=512, F=1024) if G == 512 else {}
+    cfg, w16, _, order = case("tiny", G=G, act=act, sdt=sdt, **extra)
     bits = [np.full((cfg.E, cfg.nrb(p)), src, np.int32) for p in range(3)]
     say("tiny requant %d->%d G=%d act=%d sdt=%d" % (src, dst, G, act, sdt))
     L = gpu_layer(cfg, w16, bits, order, slack=1.0)
@@ -107,6 +111,41 @@ def test_tiny_requant_bit_exact(src, dst, G, act, sdt):
     want = 0
     for (e, p, rb) in blocks:
         want += O.requant(p, e, rb, dst)
+    assert delta == want
+    assert L.commit() == len(blocks)
+    torch.cuda.synchronize()
+    _check_pages(L, O, order)
+    assert L.reclaim() > 0
+    L.close()
+
+
+def test_requant_mixed_pairs_several_launches():
+    """One requant call over 600 pages of a 32-expert layer, mixing the three
+    bitwidth pairs (16 -> 8, 16 -> 4, 8 -> 4) and both K (gate/up and down
+    pages): the 16 -> 4 pages take two launches of at most 448 pages. Every
+    page of the layer is compared byte for byte afterwards."""
+    import torch
+    from paper_2607_16184_amd import pw
+    cfg, w16, _, order = case("tiny", E=32)
+    rng = np.random.default_rng(11)
+    bits = [np.where(rng.random((cfg.E, cfg.nrb(p))) < 0.2, 8, 16).astype(np.int32) for p in range(3)]
+    say("requant: 32-expert tiny layer, mixed pairs over %d pages" % len(order))
+    L = gpu_layer(cfg, w16, bits, order, slack=1.0)
+    O = oracle_layer(cfg, w16, bits)
+    blocks, new = [], []
+    for (e, p, rb) in order:
+        b = int(bits[p][e, rb])
+        nb = 4 if b == 8 else (8 if rng.random() < 0.1 else 4)
+        blocks.append((e, p, rb))
+        new.append(nb)
+    pairs = [(int(bits[p][e, rb]), nb) for (e, p, rb), nb in zip(blocks, new)]
+    assert set(pairs) == {(16, 8), (16, 4), (8, 4)}
+    assert pairs.count((16, 4)) > 448          # 449 here: a second launch of one page
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    es, ps, rbs = zip(*blocks)
+    delta = pw.pw_requant_blocks(L.handle, list(es), list(ps), list(rbs), new, side.cuda_stream)
+    want = sum(O.requant(p, e, rb, nb) for (e, p, rb), nb in zip(blocks, new))
     assert delta == want
     assert L.commit() == len(blocks)
     torch.cuda.synchronize()
