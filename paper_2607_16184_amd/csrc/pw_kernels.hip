@@ -964,15 +964,12 @@ __device__ __forceinline__ int apl_nearest16(const double (&c)[16], double x) {
   return jb;
 }
 
+// The whole row r of job J in one thread, in the oracle's order of steps
+// (the reference form, used for rows whose sums could round).
 template <int ACT>
-__global__ __launch_bounds__(64) void k_apl_quant(const AplBatch b) {
+__device__ void apl_quant_row_seq(const AplJob& J, int r, int R) {
 #pragma clang fp contract(off)
-  const uint32_t g = blockIdx.x * 64u + threadIdx.x;
-  if (g >= b.total_rows) return;
-  int jb = 0;
-  while (jb + 1 < b.n_jobs && b.job[jb + 1].row_base <= g) ++jb;
-  const AplJob& J = b.job[jb];
-  const int r = static_cast<int>(g - J.row_base), K = J.K, R = b.R;
+  const int K = J.K;
   const uint16_t* v = J.src + static_cast<size_t>(r) * K;
   uint8_t* code = J.codes + static_cast<size_t>(r) * K;
   double* cent = reinterpret_cast<double*>(J.scratch + static_cast<size_t>(r) * kAplScratchRow);
@@ -1082,6 +1079,240 @@ __global__ __launch_bounds__(64) void k_apl_quant(const AplBatch b) {
   uint16_t* lut8 = reinterpret_cast<uint16_t*>(J.page + 8 * rk8 + 32 * static_cast<size_t>(R)) +
                    static_cast<size_t>(r) * 256;
   for (int j = 0; j < 256; ++j) lut8[j] = static_cast<uint16_t>(rne16_d(cp[j], ACT));
+}
+
+// ---------------------------------------------------------------------------
+// The same quantizer with one 256-thread workgroup per row. Every float64 sum
+// of the algorithm adds 16-bit values, which are integer multiples of the
+// smallest value's unit (2^(e - 7) for bf16, 2^(e - 10) for fp16); when the
+// row's largest magnitude times K stays within 2^53 of that unit, every
+// partial sum of every subset is exact, so the sums come out bit-identical in
+// any order: the workgroup accumulates them with LDS atomics. Minima and
+// maxima do not depend on order either, and every other step (assignments,
+// means, child centroids, LUT rounding) is per value or per cluster, so the
+// row's codes and LUTs equal the one-thread form's bit for bit. A row that
+// fails the bound (or has K > 16384) runs the one-thread form in thread 0.
+// ---------------------------------------------------------------------------
+
+constexpr int kAplThreads = 256;
+constexpr int kAplPerThread = 64;                 // values per thread: K <= 16384
+
+// Unit and magnitude exponents of a nonzero 16-bit value: x is a multiple of
+// 2^unit and |x| < 2^(mag + 1). Non-finite values give mag = 4096 (no bound).
+template <int ACT>
+__device__ __forceinline__ void apl_exps(uint32_t h, int& unit, int& mag) {
+  if constexpr (ACT == PW_BF16) {
+    const int E = (h >> 7) & 0xFF;
+    if (E == 0xFF) { unit = -4096; mag = 4096; return; }
+    unit = E == 0 ? -133 : E - 134;
+    mag = E == 0 ? -127 : E - 127;
+  } else {
+    const int E = (h >> 10) & 0x1F;
+    if (E == 0x1F) { unit = -4096; mag = 4096; return; }
+    unit = E == 0 ? -24 : E - 25;
+    mag = E == 0 ? -15 : E - 15;
+  }
+}
+
+// order-preserving 64-bit keys of doubles (for LDS integer min / max)
+__device__ __forceinline__ unsigned long long apl_key(double x) {
+  const unsigned long long u = static_cast<unsigned long long>(__double_as_longlong(x));
+  return (u >> 63) ? ~u : (u | 0x8000000000000000ull);
+}
+__device__ __forceinline__ double apl_unkey(unsigned long long k) {
+  const unsigned long long u = (k >> 63) ? (k & 0x7FFFFFFFFFFFFFFFull) : ~k;
+  return __longlong_as_double(static_cast<long long>(u));
+}
+
+template <int ACT>
+__global__ __launch_bounds__(kAplThreads) void k_apl_quant(const AplBatch b) {
+#pragma clang fp contract(off)
+  const uint32_t g = blockIdx.x;                   // the row of the batch
+  if (g >= b.total_rows) return;
+  int jb = 0;
+  while (jb + 1 < b.n_jobs && b.job[jb + 1].row_base <= g) ++jb;
+  const AplJob& J = b.job[jb];
+  const int r = static_cast<int>(g - J.row_base), K = J.K, R = b.R, tid = threadIdx.x;
+  __shared__ double s_sum[256];
+  __shared__ int s_cnt[256];
+  __shared__ unsigned long long s_min[128], s_max[128];
+  __shared__ double s_cp[128], s_cc[256];
+  __shared__ int s_unit, s_mag;
+  const uint16_t* v = J.src + static_cast<size_t>(r) * K;
+  const bool fits = K <= kAplThreads * kAplPerThread;
+  // this thread's values k = tid + 256 i, held as 16-bit patterns
+  uint32_t vh[kAplPerThread / 2];
+  int umin = 4096, mmax = -4096;
+  double lo = __builtin_inf(), hi = -__builtin_inf();
+#pragma unroll
+  for (int i = 0; i < kAplPerThread; ++i) {
+    const int k = tid + kAplThreads * i;
+    const uint32_t h = (fits && k < K) ? v[k] : 0u;
+    if (i & 1) vh[i >> 1] |= h << 16;
+    else vh[i >> 1] = h;
+    if (fits && k < K) {
+      const double x = val16(h, ACT);
+      lo = x < lo ? x : lo;
+      hi = x > hi ? x : hi;
+      if ((h & 0x7FFFu) != 0u) {
+        int u, m;
+        apl_exps<ACT>(h, u, m);
+        umin = min(umin, u);
+        mmax = max(mmax, m);
+      }
+    }
+  }
+  if (tid == 0) {
+    s_unit = 4096;
+    s_mag = -4096;
+    s_min[0] = ~0ull;
+    s_max[0] = 0ull;
+  }
+  __syncthreads();
+  atomicMin(&s_unit, umin);
+  atomicMax(&s_mag, mmax);
+  if (fits && tid < K) {
+    atomicMin(&s_min[0], apl_key(lo));
+    atomicMax(&s_max[0], apl_key(hi));
+  }
+  __syncthreads();
+  int klog = 0;
+  while ((1 << klog) < K) ++klog;
+  // all values zero: every sum is +0.0, exact
+  const bool exact = fits && (s_mag == -4096 || (s_mag + 1) - s_unit + klog <= 53);
+  if (!exact) {
+    if (tid == 0) apl_quant_row_seq<ACT>(J, r, R);
+    return;
+  }
+  auto val = [&](int i) { return val16((vh[i >> 1] >> (16 * (i & 1))) & 0xFFFFu, ACT); };
+  auto live = [&](int i) { return tid + kAplThreads * i < K; };
+  lo = apl_unkey(s_min[0]);
+  hi = apl_unkey(s_max[0]);
+  // 4-bit seed: centroids in registers (every thread computes the same)
+  double c[16];
+#pragma unroll
+  for (int j = 0; j < 16; ++j) c[j] = lo + (hi - lo) * ((2.0 * j + 1.0) / 32.0);
+  uint32_t cw[kAplPerThread / 4];                  // this thread's codes, 8 bits each
+  for (int it = 0; it < 8; ++it) {
+    double S[16];
+    int N[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      S[j] = 0.0;
+      N[j] = 0;
+    }
+#pragma unroll
+    for (int i = 0; i < kAplPerThread; ++i) {
+      if (!live(i)) continue;
+      const double x = val(i);
+      const int a = apl_nearest16(c, x);
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        S[j] += j == a ? x : 0.0;
+        N[j] += j == a ? 1 : 0;
+      }
+    }
+    if (tid < 16) {
+      s_sum[tid] = 0.0;
+      s_cnt[tid] = 0;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      if (N[j] == 0) continue;
+      atomicAdd(&s_sum[j], S[j]);
+      atomicAdd(&s_cnt[j], N[j]);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < 16; ++j)
+      if (s_cnt[j] > 0) c[j] = s_sum[j] / s_cnt[j];
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < kAplPerThread; ++i) {
+    const uint32_t a = live(i) ? static_cast<uint32_t>(apl_nearest16(c, val(i))) : 0u;
+    if ((i & 3) == 0) cw[i >> 2] = a;
+    else cw[i >> 2] |= a << (8 * (i & 3));
+  }
+  auto code_of = [&](int i) { return static_cast<int>((cw[i >> 2] >> (8 * (i & 3))) & 0xFFu); };
+  const size_t rk8 = static_cast<size_t>(R) * K / 8;
+  uint16_t* lut4 = reinterpret_cast<uint16_t*>(J.page + 4 * rk8) + static_cast<size_t>(r) * 16;
+  if (tid < 16) lut4[tid] = static_cast<uint16_t>(rne16_d(c[tid], ACT));
+  uint8_t* code = J.codes + static_cast<size_t>(r) * K;
+  if (J.bits != 8) {
+#pragma unroll
+    for (int i = 0; i < kAplPerThread; ++i)
+      if (live(i)) code[tid + kAplThreads * i] = static_cast<uint8_t>(code_of(i) << 4);
+    return;
+  }
+  if (tid < 16) s_cp[tid] = c[tid];
+  // one-bit splits to 8 bits
+  for (int P = 16; P <= 128; P *= 2) {
+    if (tid < P) {
+      s_cnt[tid] = 0;
+      s_sum[tid] = 0.0;
+      s_min[tid] = ~0ull;
+      s_max[tid] = 0ull;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < kAplPerThread; ++i) {
+      if (!live(i)) continue;
+      const double x = val(i);
+      const int p = code_of(i);
+      atomicAdd(&s_cnt[p], 1);
+      atomicAdd(&s_sum[p], x);
+      atomicMin(&s_min[p], apl_key(x));
+      atomicMax(&s_max[p], apl_key(x));
+    }
+    __syncthreads();
+    if (tid < P) {
+      const int n = s_cnt[tid];
+      if (n > 0) {
+        const double m = s_sum[tid] / n;
+        s_cc[2 * tid] = (apl_unkey(s_min[tid]) + m) / 2.0;
+        s_cc[2 * tid + 1] = (m + apl_unkey(s_max[tid])) / 2.0;
+      } else {
+        s_cc[2 * tid] = s_cp[tid];
+        s_cc[2 * tid + 1] = s_cp[tid];
+      }
+    }
+    __syncthreads();
+    for (int it = 0; it < 4; ++it) {
+      s_cnt[tid] = 0;                              // 2P <= 256 children
+      s_sum[tid] = 0.0;
+      __syncthreads();
+#pragma unroll
+      for (int i = 0; i < kAplPerThread; ++i) {
+        if (!live(i)) continue;
+        const double x = val(i);
+        const int p = code_of(i);
+        const int q = 2 * p + (fabs(x - s_cc[2 * p + 1]) < fabs(x - s_cc[2 * p]) ? 1 : 0);
+        atomicAdd(&s_cnt[q], 1);
+        atomicAdd(&s_sum[q], x);
+      }
+      __syncthreads();
+      if (tid < 2 * P && s_cnt[tid] > 0) s_cc[tid] = s_sum[tid] / s_cnt[tid];
+      __syncthreads();
+    }
+#pragma unroll
+    for (int i = 0; i < kAplPerThread; ++i) {
+      if (!live(i)) continue;
+      const double x = val(i);
+      const int p = code_of(i);
+      const uint32_t q = static_cast<uint32_t>(2 * p + (fabs(x - s_cc[2 * p + 1]) < fabs(x - s_cc[2 * p]) ? 1 : 0));
+      cw[i >> 2] = (cw[i >> 2] & ~(0xFFu << (8 * (i & 3)))) | (q << (8 * (i & 3)));
+    }
+    if (tid < 2 * P && P < 128) s_cp[tid] = s_cc[tid];
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < kAplPerThread; ++i)
+    if (live(i)) code[tid + kAplThreads * i] = static_cast<uint8_t>(code_of(i));
+  uint16_t* lut8 = reinterpret_cast<uint16_t*>(J.page + 8 * rk8 + 32 * static_cast<size_t>(R)) +
+                   static_cast<size_t>(r) * 256;
+  lut8[tid] = static_cast<uint16_t>(rne16_d(s_cc[tid], ACT));
 }
 
 // One thread per (job, plane, tile, lane) word: bit 8 i + q of lane l's word
@@ -1331,11 +1562,12 @@ hipError_t launch_combine(const GemmArgs& a, hipStream_t st) {
 }
 
 hipError_t launch_apl_quant(const AplBatch& b, hipStream_t st) {
-  const dim3 grid((b.total_rows + 63) / 64);
+  if (b.total_rows == 0) return hipSuccess;
+  const dim3 grid(b.total_rows), block(kAplThreads);   // one workgroup per row
   if (b.act == PW_BF16)
-    hipLaunchKernelGGL(k_apl_quant<PW_BF16>, grid, dim3(64), 0, st, b);
+    hipLaunchKernelGGL(k_apl_quant<PW_BF16>, grid, block, 0, st, b);
   else
-    hipLaunchKernelGGL(k_apl_quant<PW_F16>, grid, dim3(64), 0, st, b);
+    hipLaunchKernelGGL(k_apl_quant<PW_F16>, grid, block, 0, st, b);
   return hipGetLastError();
 }
 

@@ -220,6 +220,47 @@ def test_apl_load_errors():
     L.close()
 
 
+def test_apl_wide_range_and_degenerate_rows():
+    """The quantizer sums a row's values in any order when every partial sum
+    is exact (the row's largest magnitude times K within 2^53 of its
+    smallest value's unit); rows beyond that bound take the one-thread form,
+    which sums in order of k. Here, in bf16 blocks of each projection: rows
+    holding 2^-100-sized values beside ordinary weights (beyond the bound),
+    a row of zeros, a constant row, and a row of two values. Every page is
+    byte-identical to the oracle's, in both precisions."""
+    cfg, w16, bits, _ = case("tiny", act=synth.BF16, sdt=synth.BF16)
+    w16 = [np.array(w, copy=True) for w in w16]
+    rng = np.random.default_rng(3)
+    enc = lambda x: oracle.round_nearest16(float(x), synth.BF16)
+    touched = []
+    for p in range(3):
+        for b in (8, 4):
+            e, rb = next((e, rb) for e in range(cfg.E) for rb in range(cfg.nrb(p)) if bits[p][e, rb] == b)
+            r0 = rb * cfg.R
+            K = w16[p].shape[2]
+            tiny = [enc(x) for x in rng.choice([1e-30, -3e-31, 7e-29], size=K // 8)]
+            cols = rng.choice(K, size=K // 8, replace=False)
+            w16[p][e, r0, cols] = tiny                          # beyond the exact-sum bound
+            w16[p][e, r0 + 1, :] = 0                            # zeros
+            w16[p][e, r0 + 2, :] = enc(0.25)                    # constant
+            w16[p][e, r0 + 3, :] = np.where(np.arange(K) % 3 == 0, enc(-0.5), enc(0.125))   # two values
+            touched.append((e, p, rb))
+    say("bit-plane pages with wide-range and degenerate rows: %d blocks" % len(touched))
+    L = _layer(cfg, w16, bits)
+    pages = _oracle_pages(cfg, w16, bits)
+    for (e, p, rb), (buf, _, _, _) in pages.items():
+        got = L.page_image(e, p, rb)
+        want = buf[:got.size]
+        if not np.array_equal(got, want):
+            K = cfg.F if p == 2 else cfg.H
+            b = int(bits[p][e, rb])
+            gc, gl = apl.decode_page(got, cfg.R, K, b)
+            wc, wl = apl.decode_page(want, cfg.R, K, b)
+            raise AssertionError("page %s: %d code and %d LUT mismatches" % ((e, p, rb), (gc != wc).sum(),
+                                                                          (gl != wl).sum()))
+    L.close()
+
+
 def test_apl_mixtral_sampled_pages():
     """The Mixtral-shaped decode layer with its quantized pages as bit-plane
     pages (the configuration the benchmark times): sampled pages of every
