@@ -53,10 +53,13 @@ template <> struct WStage<4> { u32x2 v[2]; uint32_t sz[2]; };  // tile t: one wo
 // Nested bit-plane pages (format codes 108 and 104: 8 and 4 planes). Per row
 // tile and 128-value block, lane l holds one 32-bit word per plane covering
 // its four k-steps; `lut` points at the wave's 32 LUT rows staged in LDS.
+// The LUT pointer is held in the LDS address space, so lookups are LDS reads
+// with 32-bit addresses (a generic pointer would make them flat loads).
 constexpr int kApl8 = 108, kApl4 = 104;
 template <int B> constexpr int apl_planes() { return B == kApl8 ? 8 : 4; }
-template <> struct WStage<kApl8> { uint32_t p[2][8]; int hh; const uint16_t* lut; };
-template <> struct WStage<kApl4> { uint32_t p[2][4]; int hh; const uint16_t* lut; };
+typedef const __attribute__((address_space(3))) uint16_t* lds_lut_t;
+template <> struct WStage<kApl8> { uint32_t p[2][8]; int hh; lds_lut_t lut; };
+template <> struct WStage<kApl4> { uint32_t p[2][4]; int hh; lds_lut_t lut; };
 
 // A wave's activation share: slot tiles 2 * wave + j / 2, k-step j mod 2.
 struct XStage {
@@ -81,7 +84,7 @@ __device__ __forceinline__ void w_fetch(WStage<B>& w, const uint8_t* tile0, cons
                                                        4 * lane);
     }
     w.hh = hh;
-    w.lut = reinterpret_cast<const uint16_t*>(szrow);
+    w.lut = (lds_lut_t)szrow;   // szrow points into LDS for these pages (generic to LDS: a C-style cast)
     (void)g;
   } else {
 #pragma unroll
@@ -140,7 +143,7 @@ __device__ __forceinline__ u32x4 w_piece(const WStage<B>& w, int f) {
     y = (x ^ (x >> 28)) & 0x00000000F0F0F0F0ull;
     x = x ^ y ^ (y << 28);
     constexpr int nl = B == kApl8 ? 256 : 16;
-    const uint16_t* lut = w.lut + (16 * t + (lane_id() & 15)) * nl;
+    const lds_lut_t lut = w.lut + (16 * t + (lane_id() & 15)) * nl;
     u32x4 o;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
