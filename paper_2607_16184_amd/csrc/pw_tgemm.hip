@@ -130,12 +130,19 @@ __device__ __forceinline__ u32x4 pack8(const float (&v)[8]) {
 template <int ACT, int SDT, int B>
 __device__ __forceinline__ u32x4 w_piece(const WStage<B>& w, int f) {
   if constexpr (B == kApl8 || B == kApl4) {
-    // plane j's eight bits of this k-step go to byte 7 - j; an 8 x 8 bit
-    // transpose leaves element q's code in byte q (plane 0 in the top bit)
-    const int t = f >> 1, sh = 8 * (2 * w.hh + (f & 1));
-    uint64_t x = 0;
-#pragma unroll
-    for (int j = 0; j < apl_planes<B>(); ++j) x |= static_cast<uint64_t>((w.p[t][j] >> sh) & 0xFFu) << (8 * (7 - j));
+    // plane j's eight bits of this k-step (byte bs of its word) go to byte
+    // 7 - j, gathered with byte permutes; an 8 x 8 bit transpose then leaves
+    // element q's code in byte q (plane 0 in the top bit)
+    const int t = f >> 1;
+    const uint32_t bs = static_cast<uint32_t>(2 * w.hh + (f & 1));
+    const uint32_t pair = 0x0C0C0000u | ((4u + bs) << 8) | bs;   // (S0.byte bs, S1.byte bs) -> bytes 1, 0
+    const uint32_t hi = __builtin_amdgcn_perm(__builtin_amdgcn_perm(w.p[t][0], w.p[t][1], pair),
+                                              __builtin_amdgcn_perm(w.p[t][2], w.p[t][3], pair), 0x05040100u);
+    uint32_t lo = 0u;
+    if constexpr (B == kApl8)
+      lo = __builtin_amdgcn_perm(__builtin_amdgcn_perm(w.p[t][4], w.p[t][5], pair),
+                                 __builtin_amdgcn_perm(w.p[t][6], w.p[t][7], pair), 0x05040100u);
+    uint64_t x = (static_cast<uint64_t>(hi) << 32) | lo;
     uint64_t y = (x ^ (x >> 7)) & 0x00AA00AA00AA00AAull;
     x = x ^ y ^ (y << 7);
     y = (x ^ (x >> 14)) & 0x0000CCCC0000CCCCull;
