@@ -77,3 +77,68 @@ def test_downshift_under_decode():
     assert torch.equal(ya, yb)
     L.close()
     L2.close()
+
+
+
+def _fwd_ref(O, cfg, lg, x16):
+    ids, w = oracle.route(lg, cfg.K)
+    return O.forward(x16, ids, w, h_round=True)
+
+
+@pytest.mark.parametrize("delay_side", [True, False])
+def test_commit_order_with_widened_race_window(delay_side):
+    """Sec. 3.1 offload order and Sec. 3.3 safe boundaries under a widened
+    race window. A bounded spin (torch.cuda._sleep: a fixed cycle budget
+    that always ends) holds back either the side stream ahead of the
+    requant, so the commit is enqueued long before the new pages exist, or
+    the main stream ahead of the steps, so the new pages are written while
+    the old ones are still to be read. In three rounds (16 -> 8, 8 -> 4 and
+    16 -> 4, over different blocks) the step enqueued before the commit must
+    match the oracle of the old table and the step after it the new one;
+    reclaim, called while the spun stream is still behind the commit, frees
+    nothing, and frees the old slots once it has passed. Every page is
+    byte-identical at the end and the pool gains exactly the sum of Eq. 3's
+    deltas."""
+    import torch
+    cfg, w16, bits, order = case("tiny", T=16)
+    bits = [np.full_like(b, 16) for b in bits]
+    say("commit order, widened window on the %s stream" % ("side" if delay_side else "main"))
+    L = gpu_layer(cfg, w16, bits, order, slack=1.0)
+    O = oracle_layer(cfg, w16, bits)
+    side = torch.cuda.Stream()
+    main = torch.cuda.current_stream()
+    blocks = list(order)
+    rounds = [(blocks[0::4], 8), (blocks[0::4], 4), (blocks[1::4], 4)]
+    spin = 50_000_000                                   # cycles of the bounded spin
+    warm = [_step(L, cfg, 99)[0] for _ in range(2)]     # the allocator holds blocks of every size used below
+    torch.cuda.synchronize()
+    del warm
+    free0 = L.stats()[1]
+    total = 0
+    for r, (chunk, nb) in enumerate(rounds):
+        # inputs go to the device first: a host-to-device copy from pageable
+        # memory waits for its stream, which would let the spin drain
+        (lg0, x0), (lg1, x1) = synth.step_inputs(cfg, 100 + 2 * r), synth.step_inputs(cfg, 101 + 2 * r)
+        d0, d1 = (to_dev(lg0), to_dev16(x0)), (to_dev(lg1), to_dev16(x1))
+        torch.cuda.synchronize()
+        side.wait_stream(main)
+        if delay_side:
+            with torch.cuda.stream(side):
+                torch.cuda._sleep(spin)
+        total += L.requant(chunk, nb, stream=side)
+        if not delay_side:
+            torch.cuda._sleep(spin)                     # the main stream falls behind
+        y0 = L.forward(d0[1], L.route(d0[0], cfg.K), out_fp32=True)
+        assert L.commit() == len(chunk)
+        y1 = L.forward(d1[1], L.route(d1[0], cfg.K), out_fp32=True)
+        assert L.reclaim() == 0, r                      # main has not passed the commit yet
+        torch.cuda.synchronize()
+        e0 = rel_err(y0.cpu().numpy(), _fwd_ref(O, cfg, lg0, x0))
+        for (e, p, rb) in chunk:
+            O.requant(p, e, rb, nb)
+        e1 = rel_err(y1.cpu().numpy(), _fwd_ref(O, cfg, lg1, x1))
+        assert e0 <= 1e-3 and e1 <= 1e-3, (r, e0, e1)
+        assert L.reclaim() > 0, r
+    assert L.stats()[1] - free0 == total                # Eq. 3, exactly
+    assert assert_all_pages_equal(L, O, cfg) == len(order)
+    L.close()
