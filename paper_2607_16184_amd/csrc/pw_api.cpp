@@ -200,8 +200,9 @@ pw_status check_hip_last(const char* what) {
   return e == hipSuccess ? PW_OK : hip_fail(e, what);
 }
 
-// Launch quantize / requant jobs that all share one projection kind.
-// Quantize / requantize jobs (each with its own K), up to kMaxQJobs per launch.
+// Load-time quantization (or 16-bit layout) of pages from 16-bit values, each
+// job with its own K, up to kMaxQJobs per launch (profiled with the requant
+// phase).
 pw_status run_qjobs(pw_layer* L, const std::vector<pw::QJob>& jobs, hipStream_t st) {
   const pw_layer_desc& d = L->st.desc;
   const int span = d.G > 128 ? d.G / 128 : 1;
@@ -221,7 +222,7 @@ pw_status run_qjobs(pw_layer* L, const std::vector<pw::QJob>& jobs, hipStream_t 
     b.total_items = items;
     ProfScope ps(L, PW_PH_REQUANT, st);
     hipError_t e = pw::launch_qjobs(b, st);
-    if (e != hipSuccess) return hip_fail(e, "requant launch");
+    if (e != hipSuccess) return hip_fail(e, "page quantization launch");
   }
   return PW_OK;
 }
@@ -371,10 +372,8 @@ pw_status pw_layer_load_page(pw_layer* L, int e, int proj, int rb, int bits, con
   pw::QJob j{};
   j.K = L->st.kdim(proj);
   j.src = static_cast<const uint8_t*>(rows16);
-  j.src_sz = nullptr;
   j.dst = L->pool + ent.data_off;
   j.dst_sz = bits == 16 ? nullptr : L->pool + ent.sz_off;
-  j.src_bits = 16;
   j.dst_bits = static_cast<uint8_t>(bits);
   j.src_plain = 1;
   s = run_qjobs(L, {j}, st);

@@ -10,17 +10,17 @@
 
 namespace pw {
 
-// One page transformation for the quantize / requant kernel.
+// One page quantized at load time from 16-bit values (or laid out as a
+// 16-bit page) by the load-time kernel.
 struct QJob {
-  const uint8_t* src;      // source values (16-bit) or code block
-  const uint8_t* src_sz;   // source scale/zero block (quantized sources)
-  uint8_t* dst;            // destination code block
+  const uint8_t* src;      // source 16-bit values
+  uint8_t* dst;            // destination values or code block
   uint8_t* dst_sz;         // destination scale/zero block
   uint32_t item_base;      // first work item of this job
   int K;                   // reduction length of the page's rows (H or F)
-  uint8_t src_bits, dst_bits;
+  uint8_t dst_bits;        // 16, 8 or 4
   uint8_t src_plain;       // 1: src is R x K row-major 16-bit values (not a pool page)
-  uint8_t rsv;
+  uint8_t rsv[2];
 };
 constexpr int kMaxQJobs = 32;
 // A job has (R / 16) tiles x (K / max(G, 128)) work items; job j's items

@@ -317,7 +317,9 @@ __global__ __launch_bounds__(kFusedThreads) void k_route_permute(const float* __
 }
 
 // ---------------------------------------------------------------------------
-// Group-wise RTN quantize / requantize / 16-bit layout transform.
+// Group-wise RTN: quantization of 16-bit rows into a page at load time (or a
+// 16-bit page's layout transform), and requantization of pool pages to fewer
+// bits (k_requant, below).
 //
 // Page layout: tiles of 16 rows x 128 values stored tile after tile (row tile
 // major); inside a tile, lane l = 16 lg + lc (row lc, k-run lg) of k-step i
@@ -331,91 +333,46 @@ __global__ __launch_bounds__(kFusedThreads) void k_route_permute(const float* __
 // Group layout along K: G = 64 (two groups per 128-block), G = 128 (one),
 // G = 256 or 512 (one group spans 2 or 4 blocks). The activation dtype ACT,
 // the scale dtype SDT and the group layout GK are template parameters of the
-// kernel; source and destination bitwidths vary per job.
+// kernels; the load-time kernel's destination bitwidth varies per job.
 enum { kQG64 = 0, kQG128 = 1, kQGBig = 2 };
 
 // The raw 16-byte pieces lane l holds of one 128-value block of a row tile,
 // for every source format (16-bit: four pieces; 8-bit: two; 4-bit: one), plus
-// the (scale, zero) word of each k-step's group for quantized sources.
+// the (scale, zero) word of each k-step's group for quantized sources (the
+// load-time kernel reads 16-bit sources only; k_requant all three).
 struct QRaw {
   u32x4 w[4];
   uint32_t sz[4];
 };
 
-template <int GK>
-__device__ __forceinline__ void q_load(const QJob& job, const QJobBatch& b, int tau, int blk, QRaw& raw) {
+// The lane's four 16-byte pieces of 16-bit block blk of row tile tau: from a
+// 16-bit pool page (tile layout) or from R x K row-major rows (src_plain).
+__device__ __forceinline__ void q_load(const QJob& job, int tau, int blk, QRaw& raw) {
   const int lane = lane_id(), lc = lane & 15, lg = lane >> 4;
   const int K = job.K, nkb = K / 128;
   const size_t tile = static_cast<size_t>(tau) * nkb + blk;
-  if (job.src_bits == 16) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const uint8_t* src = job.src_plain
-          ? job.src + (static_cast<size_t>(tau * 16 + lc) * K + blk * 128 + 32 * i + 8 * lg) * 2
-          : job.src + tile * 4096 + 1024 * i + 16 * lane;
-      raw.w[i] = *reinterpret_cast<const u32x4*>(src);
-    }
-    return;
-  }
-  if (job.src_bits == 8) {
-#pragma unroll
-    for (int u = 0; u < 2; ++u) raw.w[u] = *reinterpret_cast<const u32x4*>(job.src + tile * 2048 + 1024 * u + 16 * lane);
-  } else {
-    raw.w[0] = *reinterpret_cast<const u32x4*>(job.src + tile * 1024 + 16 * lane);
-  }
-  const int r = tau * 16 + lc;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const int g = GK == kQG64 ? 2 * blk + (i >> 1) : GK == kQG128 ? blk : (blk * 128) / b.G;
-    raw.sz[i] = *reinterpret_cast<const uint32_t*>(job.src_sz + (static_cast<size_t>(g) * b.R + r) * 4);
+    const uint8_t* src = job.src_plain
+        ? job.src + (static_cast<size_t>(tau * 16 + lc) * K + blk * 128 + 32 * i + 8 * lg) * 2
+        : job.src + tile * 4096 + 1024 * i + 16 * lane;
+    raw.w[i] = *reinterpret_cast<const u32x4*>(src);
   }
 }
 
 // The 32 values (k-steps i = 0..3, 8 values each) lane l holds of the block,
-// widened to fp32: 16-bit values, or quantized codes dequantized as
-// fl32(z + c s) (c s is exact in fp32).
-template <int ACT, int SDT>
-__device__ __forceinline__ void q_widen(const QJob& job, const QRaw& raw, float (&v)[32]) {
-  if (job.src_bits == 16) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        v[8 * i + 2 * q] = val16(raw.w[i][q], ACT);
-        v[8 * i + 2 * q + 1] = val16(raw.w[i][q] >> 16, ACT);
-      }
-    return;
-  }
-  uint32_t c[32];
-  if (job.src_bits == 8) {
-#pragma unroll
-    for (int u = 0; u < 2; ++u)
-#pragma unroll
-      for (int w = 0; w < 4; ++w)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) c[16 * u + 4 * w + q] = (raw.w[u][w] >> (8 * q)) & 0xFFu;
-  } else {
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        c[8 * i + 2 * t] = (raw.w[0][i] >> (4 * t)) & 15u;
-        c[8 * i + 2 * t + 1] = (raw.w[0][i] >> (16 + 4 * t)) & 15u;
-      }
-  }
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const float s = val16(raw.sz[i], SDT), z = val16(raw.sz[i] >> 16, SDT);
-#pragma unroll
-    for (int q = 0; q < 8; ++q) v[8 * i + q] = z + static_cast<float>(c[8 * i + q]) * s;   // c*s exact
-  }
-}
-
-template <int ACT, int SDT, int GK>
-__device__ __forceinline__ void q_read(const QJob& job, const QJobBatch& b, int tau, int blk, float (&v)[32]) {
+// widened to fp32 (exactly).
+template <int ACT>
+__device__ __forceinline__ void q_read(const QJob& job, int tau, int blk, float (&v)[32]) {
   QRaw raw;
-  q_load<GK>(job, b, tau, blk, raw);
-  q_widen<ACT, SDT>(job, raw, v);
+  q_load(job, tau, blk, raw);
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      v[8 * i + 2 * q] = val16(raw.w[i][q], ACT);
+      v[8 * i + 2 * q + 1] = val16(raw.w[i][q] >> 16, ACT);
+    }
 }
 
 // (scale, zero) bit patterns of a group from its extremes (the quantizer's steps).
@@ -563,9 +520,11 @@ __device__ __forceinline__ float q_elem(const QRaw& raw, int e) {
   }
 }
 
-template <int ACT, int SDT, int GK, int SRC>
+// One 16-bit block quantized to the job's destination (16: layout transform).
+template <int ACT, int SDT, int GK>
 __device__ __forceinline__ void q_block(const QJob& job, const QJobBatch& b, const QRaw& raw, int tau, int blk, int lg,
                                         int r, int Q) {
+  constexpr int SRC = 16;
   const int lane = lane_id();
   const size_t tile = static_cast<size_t>(tau) * (job.K / 128) + blk;
   if (job.dst_bits == 16) {          // layout transform of a 16-bit page
@@ -662,30 +621,28 @@ __device__ __forceinline__ void qjobs_item(const QJobBatch& b) {
   const int Q = (1 << job.dst_bits) - 1;
   if constexpr (GK != kQGBig) {
     QRaw raw;
-    q_load<GK>(job, b, tau, sp, raw);
-    if (job.src_bits == 16) q_block<ACT, SDT, GK, 16>(job, b, raw, tau, sp, lg, r, Q);
-    else if (job.src_bits == 8) q_block<ACT, SDT, GK, 8>(job, b, raw, tau, sp, lg, r, Q);
-    else q_block<ACT, SDT, GK, 4>(job, b, raw, tau, sp, lg, r, Q);
+    q_load(job, tau, sp, raw);
+    q_block<ACT, SDT, GK>(job, b, raw, tau, sp, lg, r, Q);
     (void)R;
   } else {
     float v[32];
     if (job.dst_bits == 16) {
       for (int blk = sp * span; blk < (sp + 1) * span; ++blk) {
-        q_read<ACT, SDT, GK>(job, b, tau, blk, v);
+        q_read<ACT>(job, tau, blk, v);
         q_store16<ACT>(job, tau, blk, v);
       }
       return;
     }
     float lo0 = __builtin_inff(), hi0 = -__builtin_inff(), lo1 = lo0, hi1 = hi0;
     for (int blk = sp * span; blk < (sp + 1) * span; ++blk) {
-      q_read<ACT, SDT, GK>(job, b, tau, blk, v);
+      q_read<ACT>(job, tau, blk, v);
       q_extremes<GK>(v, lo0, hi0, lo1, hi1);
     }
     q_rowreduce(lo0, hi0, lo1, hi1);
     uint32_t sb0, zb0;
     q_params<SDT>(lo0, hi0, Q, &sb0, &zb0);
     for (int blk = sp * span; blk < (sp + 1) * span; ++blk) {
-      q_read<ACT, SDT, GK>(job, b, tau, blk, v);
+      q_read<ACT>(job, tau, blk, v);
       q_store_codes<SDT, GK>(job, tau, blk, v, sb0, zb0, 0u, 0u, Q);
     }
     if (lg == 0) *reinterpret_cast<uint32_t*>(job.dst_sz + (static_cast<size_t>(sp) * R + r) * 4) = sb0 | (zb0 << 16);
@@ -698,9 +655,7 @@ __global__ __launch_bounds__(256) void k_qjobs(const QJobBatch b) {
 }
 
 // G = 128 (one group per block): the one-block path fits in 64 VGPRs, so
-// eight waves per SIMD and 32 blocks per CU are in flight. A requant wave is
-// latency-bound (it loads one 4 KiB block, then computes and stores), so the
-// bytes in flight set the rate.
+// eight waves per SIMD and 32 blocks per CU are in flight.
 template <int ACT, int SDT>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void k_qjobs_g128(const QJobBatch b) {
   qjobs_item<ACT, SDT, kQG128>(b);
