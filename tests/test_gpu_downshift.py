@@ -80,6 +80,32 @@ def test_downshift_under_decode():
 
 
 
+def test_downshift_plan_in_one_call():
+    """The whole 256-page plan of the Mixtral-shaped layer requantized to int4
+    in one call (one launch, as the benchmark's requant-alone figure runs it):
+    every page byte-identical to the oracle and the pool gains exactly
+    Eq. 3's 258,736,128 bytes."""
+    import torch
+    cfg, w16, bits, order = case("downshift")
+    plan = synth.downshift_plan(cfg, list(bits))
+    pages = [pg for chunk in plan for pg in chunk]
+    say("downshift: the 256-page plan in one call")
+    L = gpu_layer(cfg, w16, bits, order, slack=0.1)
+    O = oracle_layer(cfg, w16, bits)
+    free0 = L.stats()[1]
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    delta = L.requant(pages, 4, stream=side)
+    assert L.commit() == len(pages)
+    torch.cuda.synchronize()
+    L.reclaim()
+    want = sum(O.requant(p, e, rb, 4) for (e, p, rb) in pages)
+    assert delta == want == 258_736_128
+    assert L.stats()[1] - free0 == want
+    assert assert_all_pages_equal(L, O, cfg, pages) == 256
+    L.close()
+
+
 def _fwd_ref(O, cfg, lg, x16):
     ids, w = oracle.route(lg, cfg.K)
     return O.forward(x16, ids, w, h_round=True)
