@@ -237,6 +237,8 @@ struct RqPlanned {
 pw_status run_requant(pw_layer* L, const std::vector<RqPlanned>& jobs, hipStream_t st) {
   const pw_layer_desc& d = L->st.desc;
   static const int kPairs[3][2] = {{16, 8}, {16, 4}, {8, 4}};
+  if (d.H / 128 > 65535 || d.F / 128 > 65535)
+    return fail(PW_EUNSUPPORTED, "requant: H and F must stay below 2^23 (16-bit block counts)");
   for (const RqPlanned& j : jobs) {
     bool known = false;
     for (const auto& pr : kPairs) known = known || (j.src.bits == pr[0] && j.dst.bits == pr[1]);
