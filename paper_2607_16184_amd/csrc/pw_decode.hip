@@ -524,6 +524,18 @@ __device__ __forceinline__ void gateup_any(int code, const GemmArgs& a, uint8_t*
   }
 }
 
+// Workgroups are dealt to the eight XCDs in turn (blockIdx mod 8), each XCD
+// with its own L2. With many experts, the down projection gives all `per_e`
+// workgroups of one expert to one XCD (XCD x runs experts x, x + 8, x + 16,
+// ... in order), so the expert's h rows, which no other expert reads, are
+// fetched into one L2 instead of eight (the gate/up activations are token
+// rows that every XCD reads anyway). The grid holds ne * per_e workgroups.
+__device__ __forceinline__ int xcd_expert_order(int b, int per_e, int ne) {
+  if (ne < 32 || ne % 8 != 0) return b;
+  const int x = b & 7, j = b >> 3;
+  return (x + 8 * (j / per_e)) * per_e + j % per_e;
+}
+
 // NTMAX slot tiles per pass (1, 2 or 4); experts with fewer slots take fewer
 // (at NTMAX = 4 also three).
 template <int ACT, int SDT, int NTMAX, int GK, int NW>
@@ -615,8 +627,9 @@ __global__ __launch_bounds__(64 * NW) void k_down(const GemmArgs a) {
   constexpr int DN = dn_rows<RT, NW>();
   __shared__ __attribute__((aligned(16))) uint8_t lds[lds_x_bytes<NTMAX>()];
   const int upe = a.H / DN;
-  const int split = blockIdx.x % a.nsplit;
-  const int rest = blockIdx.x / a.nsplit;
+  const int wg = xcd_expert_order(static_cast<int>(blockIdx.x), upe * a.nsplit, a.ne);
+  const int split = wg % a.nsplit;
+  const int rest = wg / a.nsplit;
   const int e = a.e0 + rest / upe, unit = rest % upe;
   const int off_e = clampi(a.offsets[e], 0, a.S);
   const int n_e = clampi(a.offsets[e + 1], off_e, a.S) - off_e;
