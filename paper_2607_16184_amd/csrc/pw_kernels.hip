@@ -838,38 +838,49 @@ __global__ void k_clear_table(pw_page_entry* table, size_t n) {
 // down projection has nsplit_sh K splits)
 // ---------------------------------------------------------------------------
 
-// Columns are taken four at a time: their positions, weights and partial
-// rows are all loaded before any is summed, so the loads of a thread overlap;
-// the sums themselves keep the order (splits ascending per column, columns
-// ascending into y).
-constexpr int kCombineCols = 4;
-
+// A thread holds four outputs of token t. Columns are taken C at a time (C
+// of 2, 4, 8: the column count rounded up, at most 16 / NSP; NSP: the largest
+// split count rounded up to 1, 2, 4 or 8): the partial rows of every split
+// of those columns are all loaded before any is summed, so up to 16 loads of
+// a thread are in flight together; the sums keep the order (splits ascending
+// per column, columns ascending into y).
+template <int NSP, int C>
 __global__ __launch_bounds__(256) void k_combine(const GemmArgs a) {
   const int t = blockIdx.x;
   const int n = (blockIdx.y * 256 + threadIdx.x) * 4;
   if (n >= a.H) return;
   f32x4 y = {0.f, 0.f, 0.f, 0.f};
   const size_t row = static_cast<size_t>(t) * a.topk;
-  for (int k0 = 0; k0 < a.topk; k0 += kCombineCols) {
-    int pos[kCombineCols], nsp[kCombineCols];
-    float wk[kCombineCols];
+  for (int k0 = 0; k0 < a.topk; k0 += C) {
+    int pos[C], nsp[C];
+    float wk[C];
 #pragma unroll
-    for (int j = 0; j < kCombineCols; ++j) {
+    for (int j = 0; j < C; ++j) {
       const int k = min(k0 + j, a.topk - 1);
       pos[j] = clampi(a.slot_pos[row + k], 0, a.S - 1);
       wk[j] = a.topk_w[row + k];
       nsp[j] = k0 + j >= a.topk ? 0 : k < a.topk - a.n_shared ? a.nsplit : a.nsplit_sh;
     }
-    f32x4 o[kCombineCols];
+    // unconditional loads (a split past the column's count reloads one of its
+    // own rows and is not summed): no branch separates them from each other
+    f32x4 part[C][NSP];
 #pragma unroll
-    for (int j = 0; j < kCombineCols; ++j) {
-      o[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-      for (int sp = 0; sp < nsp[j]; ++sp)
-        o[j] += *reinterpret_cast<const f32x4*>(a.opart + (static_cast<size_t>(sp) * a.S + pos[j]) * a.H + n);
+    for (int j = 0; j < C; ++j)
+#pragma unroll
+      for (int sp = 0; sp < NSP; ++sp) {
+        const int spc = min(sp, max(nsp[j] - 1, 0));
+        part[j][sp] = *reinterpret_cast<const f32x4*>(a.opart + (static_cast<size_t>(spc) * a.S + pos[j]) * a.H + n);
+      }
+#pragma unroll
+    for (int j = 0; j < C; ++j) {
+      if (k0 + j < a.topk) {
+        f32x4 o = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int sp = 0; sp < NSP; ++sp)
+          if (sp < nsp[j]) o += part[j][sp];
+        y += wk[j] * o;
+      }
     }
-#pragma unroll
-    for (int j = 0; j < kCombineCols; ++j)
-      if (k0 + j < a.topk) y += wk[j] * o[j];
   }
   if (a.out_fp32) {
     *reinterpret_cast<f32x4*>(static_cast<float*>(a.y) + static_cast<size_t>(t) * a.H + n) = y;
@@ -1511,8 +1522,22 @@ hipError_t launch_clear_table(pw_page_entry* table, size_t n, hipStream_t st) {
 
 hipError_t launch_combine(const GemmArgs& a, hipStream_t st) {
   if (a.T <= 0) return hipSuccess;
+  const int nmax = a.n_shared > 0 && a.nsplit_sh > a.nsplit ? a.nsplit_sh : a.nsplit;
+  if (nmax < 1 || nmax > 8) return hipErrorInvalidValue;
+  const int nsp = nmax == 1 ? 1 : nmax == 2 ? 2 : nmax <= 4 ? 4 : 8;
+  const int cols = std::min(a.topk <= 2 ? 2 : a.topk <= 4 ? 4 : 8, 16 / nsp);
   const dim3 grid(a.T, (a.H / 4 + 255) / 256), block(256);
-  hipLaunchKernelGGL(k_combine, grid, block, 0, st, a);
+  switch (nsp * 16 + cols) {
+    case 16 + 2: hipLaunchKernelGGL((k_combine<1, 2>), grid, block, 0, st, a); break;
+    case 16 + 4: hipLaunchKernelGGL((k_combine<1, 4>), grid, block, 0, st, a); break;
+    case 16 + 8: hipLaunchKernelGGL((k_combine<1, 8>), grid, block, 0, st, a); break;
+    case 32 + 2: hipLaunchKernelGGL((k_combine<2, 2>), grid, block, 0, st, a); break;
+    case 32 + 4: hipLaunchKernelGGL((k_combine<2, 4>), grid, block, 0, st, a); break;
+    case 32 + 8: hipLaunchKernelGGL((k_combine<2, 8>), grid, block, 0, st, a); break;
+    case 64 + 2: hipLaunchKernelGGL((k_combine<4, 2>), grid, block, 0, st, a); break;
+    case 64 + 4: hipLaunchKernelGGL((k_combine<4, 4>), grid, block, 0, st, a); break;
+    default: hipLaunchKernelGGL((k_combine<8, 2>), grid, block, 0, st, a); break;
+  }
   return hipGetLastError();
 }
 
