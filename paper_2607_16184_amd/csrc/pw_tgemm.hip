@@ -131,36 +131,48 @@ template <int ACT, int SDT, int B>
 __device__ __forceinline__ u32x4 w_piece(const WStage<B>& w, int f) {
   if constexpr (B == kApl8 || B == kApl4) {
     // plane j's eight bits of this k-step (byte bs of its word) go to byte
-    // 7 - j, gathered with byte permutes; an 8 x 8 bit transpose then leaves
-    // element q's code in byte q (plane 0 in the top bit)
+    // 7 - j of a 64-bit word (8-bit pages; 4-bit pages: byte 3 - j of a
+    // 32-bit word), gathered with byte permutes; a bit transpose then brings
+    // each element's plane bits together (plane 0 the most significant)
     const int t = f >> 1;
     const uint32_t bs = static_cast<uint32_t>(2 * w.hh + (f & 1));
     const uint32_t pair = 0x0C0C0000u | ((4u + bs) << 8) | bs;   // (S0.byte bs, S1.byte bs) -> bytes 1, 0
     const uint32_t hi = __builtin_amdgcn_perm(__builtin_amdgcn_perm(w.p[t][0], w.p[t][1], pair),
                                               __builtin_amdgcn_perm(w.p[t][2], w.p[t][3], pair), 0x05040100u);
-    uint32_t lo = 0u;
-    if constexpr (B == kApl8)
-      lo = __builtin_amdgcn_perm(__builtin_amdgcn_perm(w.p[t][4], w.p[t][5], pair),
-                                 __builtin_amdgcn_perm(w.p[t][6], w.p[t][7], pair), 0x05040100u);
-    uint64_t x = (static_cast<uint64_t>(hi) << 32) | lo;
-    uint64_t y = (x ^ (x >> 7)) & 0x00AA00AA00AA00AAull;
-    x = x ^ y ^ (y << 7);
-    y = (x ^ (x >> 14)) & 0x0000CCCC0000CCCCull;
-    x = x ^ y ^ (y << 14);
-    y = (x ^ (x >> 28)) & 0x00000000F0F0F0F0ull;
-    x = x ^ y ^ (y << 28);
     constexpr int nl = B == kApl8 ? 256 : 16;
     const lds_lut_t lut = w.lut + (16 * t + (lane_id() & 15)) * nl;
+    uint32_t idx[8];
+    if constexpr (B == kApl8) {
+      const uint32_t lo = __builtin_amdgcn_perm(__builtin_amdgcn_perm(w.p[t][4], w.p[t][5], pair),
+                                                __builtin_amdgcn_perm(w.p[t][6], w.p[t][7], pair), 0x05040100u);
+      // 8 x 8 transpose (three delta swaps): element e's code in byte e
+      uint64_t x = (static_cast<uint64_t>(hi) << 32) | lo;
+      uint64_t y = (x ^ (x >> 7)) & 0x00AA00AA00AA00AAull;
+      x = x ^ y ^ (y << 7);
+      y = (x ^ (x >> 14)) & 0x0000CCCC0000CCCCull;
+      x = x ^ y ^ (y << 14);
+      y = (x ^ (x >> 28)) & 0x00000000F0F0F0F0ull;
+      x = x ^ y ^ (y << 28);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) idx[e] = static_cast<uint32_t>(x >> (8 * e)) & 0xFFu;
+    } else {
+      // 4 x 8 transpose: bit 8 r + e (row r = byte r, element e) goes to bit
+      // 4 n + r with n = 4 e1 + 2 e0 + e2 (the bits of e rotated), which two
+      // delta swaps of index bits (0 with 3, 1 with 4) do: element e's 4-bit
+      // code in nibble n
+      uint32_t x = hi;
+      uint32_t y = (x ^ (x >> 7)) & 0x00AA00AAu;
+      x = x ^ y ^ (y << 7);
+      y = (x ^ (x >> 14)) & 0x0000CCCCu;
+      x = x ^ y ^ (y << 14);
+      constexpr int nib[8] = {0, 2, 4, 6, 1, 3, 5, 7};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) idx[e] = (x >> (4 * nib[e])) & 0xFu;
+    }
     u32x4 o;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      uint32_t i0 = static_cast<uint32_t>(x >> (16 * q)) & 0xFFu, i1 = static_cast<uint32_t>(x >> (16 * q + 8)) & 0xFFu;
-      if constexpr (B == kApl4) {
-        i0 >>= 4;
-        i1 >>= 4;
-      }
-      o[q] = static_cast<uint32_t>(lut[i0]) | (static_cast<uint32_t>(lut[i1]) << 16);
-    }
+    for (int q = 0; q < 4; ++q)
+      o[q] = static_cast<uint32_t>(lut[idx[2 * q]]) | (static_cast<uint32_t>(lut[idx[2 * q + 1]]) << 16);
     return o;
   } else if constexpr (B == 16) {
     return w.v[f];
