@@ -171,8 +171,13 @@ pw_status pw_route_topk(const float* logits, int T, int E, int K, int renorm,
  * token's last n_shared columns must be the shared experts (in order), its
  * first columns routed experts only. The GEMM runs the routed and the shared
  * experts as separate launches, each with the kernels suited to its slots
- * per expert (a shared expert has T). No GPU work; takes effect for the
- * next GEMM call.                                                          */
+ * per expert (a shared expert has T); the shared experts' launches go to a
+ * stream of the layer's own, forked from the caller's stream and joined back
+ * before the combine, so that they run beside the routed ones (under graph
+ * capture: two branches). The first call with n_shared > 0 creates that
+ * stream (default priority) and its two events on the pool's device
+ * (PW_EHIP if that fails); pw_layer_destroy releases them. Takes effect
+ * for the next GEMM call.                                                  */
 pw_status pw_layer_set_shared_experts(pw_layer* layer, int n_shared);
 
 /* Router with shared experts: the top-K of pw_route_topk over the E routed

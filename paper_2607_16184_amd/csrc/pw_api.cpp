@@ -56,6 +56,10 @@ struct pw_layer {
   pw_page_entry* table;
   uint8_t* host_pool = nullptr;   // caller's pinned host memory for page copies
   int n_shared = 0;               // the last n_shared experts are shared experts
+  // layers with shared experts: a stream of the layer's device on which the
+  // shared experts' GEMMs run beside the routed ones, and its fork/join events
+  hipStream_t side = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
   bool prof = false;
   std::vector<ProfRec> recs;
   double tot_ms[PW_NPHASE] = {0, 0, 0, 0};
@@ -358,6 +362,12 @@ pw_status pw_layer_destroy(pw_layer* L) {
     (void)hipEventDestroy(r.a);
     (void)hipEventDestroy(r.b);
   }
+  if (L->side) {
+    (void)hipStreamSynchronize(L->side);
+    (void)hipStreamDestroy(L->side);
+  }
+  if (L->fork) (void)hipEventDestroy(L->fork);
+  if (L->join) (void)hipEventDestroy(L->join);
   delete L;
   return PW_OK;
 }
@@ -507,6 +517,27 @@ pw_status pw_layer_set_shared_experts(pw_layer* L, int n_shared) {
   if (!L) return fail(PW_EINVAL, "null layer");
   if (n_shared < 0 || n_shared >= L->st.desc.E)
     return fail(PW_EINVAL, "need 0 <= n_shared < E (at least one routed expert)");
+  if (n_shared > 0 && !L->side) {
+    // created on the pool's device (default priority, no implicit
+    // synchronization with the null stream: the fork/join events order it)
+    hipPointerAttribute_t attr{};
+    hipError_t e = hipPointerGetAttributes(&attr, L->pool);
+    int cur = -1;
+    if (e == hipSuccess) e = hipGetDevice(&cur);
+    if (e == hipSuccess && attr.device != cur) e = hipSetDevice(attr.device);
+    if (e == hipSuccess) e = hipStreamCreateWithFlags(&L->side, hipStreamNonBlocking);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&L->fork, hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&L->join, hipEventDisableTiming);
+    if (cur >= 0 && attr.device != cur) (void)hipSetDevice(cur);
+    if (e != hipSuccess) {
+      if (L->side) (void)hipStreamDestroy(L->side);
+      if (L->fork) (void)hipEventDestroy(L->fork);
+      if (L->join) (void)hipEventDestroy(L->join);
+      L->side = nullptr;
+      L->fork = L->join = nullptr;
+      return hip_fail(e, "creating the shared experts' stream");
+    }
+  }
   L->n_shared = n_shared;
   return PW_OK;
 }
@@ -613,7 +644,17 @@ pw_status pw_moe_paged_gemm(const pw_layer* Lc, const void* x, int T, int K, con
   a.n_shared = L->n_shared;
   hipStream_t st = static_cast<hipStream_t>(stream);
   hipError_t e = hipSuccess;
-  // routed experts, then shared experts: each range with its own kernels
+  // routed experts, then shared experts: each range with its own kernels.
+  // With both present, the shared experts' GEMMs run on the layer's own
+  // stream, forked from `stream` and joined back before the combine: their
+  // few workgroups share the chip with the routed ones instead of running
+  // alone after them. (They write disjoint rows of h and of the partials.)
+  const bool fork = wl.r[0].ne > 0 && wl.r[1].ne > 0 && L->side;
+  if (fork) {
+    e = hipEventRecord(L->fork, st);
+    if (e == hipSuccess) e = hipStreamWaitEvent(L->side, L->fork, 0);
+    if (e != hipSuccess) return hip_fail(e, "forking the shared experts' stream");
+  }
   auto for_range = [&](const RangePlan& r) {
     a.e0 = r.e0;
     a.ne = r.ne;
@@ -622,20 +663,33 @@ pw_status pw_moe_paged_gemm(const pw_layer* Lc, const void* x, int T, int K, con
     a.kb_per_split = r.kb_per_split;
     a.mtb = r.mtb;
   };
+  const char* what = nullptr;
   for (int pass = 0; pass < 2 && e == hipSuccess; ++pass) {
     const bool gateup = pass == 0;
-    for (const RangePlan& r : wl.r) {
+    for (int ri = 0; ri < 2 && e == hipSuccess; ++ri) {
+      const RangePlan& r = wl.r[ri];
       if (r.ne <= 0) continue;
       for_range(r);
-      ProfScope ps(L, gateup ? PW_PH_GATEUP : PW_PH_DOWN, st);
-      e = r.path == GemmPath::kTiled    ? pw::launch_tgemm(a, gateup, st)
-          : r.path == GemmPath::kStream ? pw::launch_sgemm(a, gateup, st)
-          : gateup                      ? pw::launch_gateup(a, st)
-                                        : pw::launch_down(a, st);
-      if (e != hipSuccess) break;
+      hipStream_t rs = fork && ri == 1 ? L->side : st;
+      ProfScope ps(L, gateup ? PW_PH_GATEUP : PW_PH_DOWN, rs);
+      e = r.path == GemmPath::kTiled    ? pw::launch_tgemm(a, gateup, rs)
+          : r.path == GemmPath::kStream ? pw::launch_sgemm(a, gateup, rs)
+          : gateup                      ? pw::launch_gateup(a, rs)
+                                        : pw::launch_down(a, rs);
+      if (e != hipSuccess) what = gateup ? "gate/up launch" : "down launch";
     }
-    if (e != hipSuccess) return hip_fail(e, gateup ? "gate/up launch" : "down launch");
   }
+  if (fork) {
+    // joined even after a failed launch, so that `stream` never waits on a
+    // branch that was left open
+    hipError_t ej = hipEventRecord(L->join, L->side);
+    if (ej == hipSuccess) ej = hipStreamWaitEvent(st, L->join, 0);
+    if (e == hipSuccess && ej != hipSuccess) {
+      e = ej;
+      what = "joining the shared experts' stream";
+    }
+  }
+  if (e != hipSuccess) return hip_fail(e, what);
   a.nsplit = wl.r[0].nsplit;
   a.nsplit_sh = wl.r[1].nsplit;
   {
