@@ -121,10 +121,13 @@ pw_status pw_page_bytes(const pw_layer_desc* desc, int proj, int bits, size_t* b
  * [pool_dev, pool_dev + pool_bytes) (256-byte aligned, at most 2^40 bytes)
  * and device table table_dev (pw_table_entries entries, 8-byte aligned). The
  * table is cleared to absent entries on the null stream, which is
- * synchronized.
+ * synchronized. The layer also creates, on the pool's device, a stream of
+ * its own (default priority) and two events, for the GEMM's concurrent
+ * chains (pw_layer_set_chains) and shared experts.
  *   bad shape (see pw_layer_desc), null or misaligned pointers, a pool
  *   above 2^40 bytes: PW_EINVAL.
- *   clearing the table failed: PW_EHIP (no handle is returned).            */
+ *   clearing the table or creating the stream failed: PW_EHIP (no handle
+ *   is returned).                                                          */
 pw_status pw_layer_create(const pw_layer_desc* desc, void* pool_dev, size_t pool_bytes,
                           pw_page_entry* table_dev, pw_layer** out);
 
@@ -174,11 +177,28 @@ pw_status pw_route_topk(const float* logits, int T, int E, int K, int renorm,
  * per expert (a shared expert has T); the shared experts' launches go to a
  * stream of the layer's own, forked from the caller's stream and joined back
  * before the combine, so that they run beside the routed ones (under graph
- * capture: two branches). The first call with n_shared > 0 creates that
- * stream (default priority) and its two events on the pool's device
- * (PW_EHIP if that fails); pw_layer_destroy releases them. Takes effect
- * for the next GEMM call.                                                  */
+ * capture: two branches; with pw_layer_set_chains(layer, 1), on the
+ * caller's stream after them). That stream (default priority) and its two
+ * events live on the pool's device
+ * (created with the layer by pw_layer_create); pw_layer_destroy releases
+ * them. Takes effect for the next GEMM call.                               */
 pw_status pw_layer_set_shared_experts(pw_layer* layer, int n_shared);
+
+/* Concurrent expert chains (Sec. 3.3: the MoE forward as a GPU-side
+ * pipeline; here the boundary between its gate/up and down phases). With
+ * chains = 2 (the default), when a call's experts run on the decode kernels
+ * and the layer has no shared experts, they are split into two halves, each
+ * a chain of gate/up then down: the first on the caller's stream, the
+ * second on the layer's own stream (forked from the caller's and joined
+ * back before the combine; under graph capture, two branches), so that the
+ * phase boundary of one chain overlaps the other's GEMMs; a layer with
+ * shared experts runs those on the layer's stream instead (see
+ * pw_layer_set_shared_experts). chains = 1 launches everything on the
+ * caller's stream, one launch after another (each kernel alone on the GPU,
+ * as a per-kernel timing needs). Results are identical either way (each
+ * expert's rows are computed by the same kernels). PW_EINVAL unless chains
+ * is 1 or 2. No GPU work; takes effect for the next GEMM call.            */
+pw_status pw_layer_set_chains(pw_layer* layer, int chains);
 
 /* Router with shared experts: the top-K of pw_route_topk over the E routed
  * experts' logits ([T,E] fp32), and for every token n_shared more columns,
@@ -329,10 +349,14 @@ pw_status pw_pool_stats(const pw_layer* layer, size_t* used, size_t* free_bytes,
                         size_t* largest_free);
 
 /* Per-kernel timing with HIP events recorded on the kernels' own streams.
- * Phases: 0 gate/up GEMM, 1 down GEMM, 2 combine, 3 requant.
+ * Phases: 0 gate/up GEMM, 1 down GEMM, 2 combine, 3 requant (one record per
+ * launch), 4 the GEMM phases of a pw_moe_paged_gemm call as a whole (one
+ * record per call, on the caller's stream, from before its first GEMM launch
+ * to after the last one, every chain joined: with concurrent chains the
+ * per-launch records of phases 0 and 1 overlap, this one does not).
  * pw_profile_read waits for the recorded events and returns the summed
- * milliseconds and launch counts per phase; reset != 0 clears them.        */
-enum { PW_PH_GATEUP = 0, PW_PH_DOWN = 1, PW_PH_COMBINE = 2, PW_PH_REQUANT = 3, PW_NPHASE = 4 };
+ * milliseconds and counts per phase; reset != 0 clears them.              */
+enum { PW_PH_GATEUP = 0, PW_PH_DOWN = 1, PW_PH_COMBINE = 2, PW_PH_REQUANT = 3, PW_PH_GEMM = 4, PW_NPHASE = 5 };
 pw_status pw_profile_enable(pw_layer* layer, int on);
 pw_status pw_profile_read(pw_layer* layer, double* total_ms, int64_t* count, int reset);
 

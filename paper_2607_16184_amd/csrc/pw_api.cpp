@@ -56,14 +56,15 @@ struct pw_layer {
   pw_page_entry* table;
   uint8_t* host_pool = nullptr;   // caller's pinned host memory for page copies
   int n_shared = 0;               // the last n_shared experts are shared experts
-  // layers with shared experts: a stream of the layer's device on which the
-  // shared experts' GEMMs run beside the routed ones, and its fork/join events
+  // a stream of the layer's device on which the second expert chain or the
+  // shared experts' GEMMs run beside the others, and its fork/join events
   hipStream_t side = nullptr;
   hipEvent_t fork = nullptr, join = nullptr;
   bool prof = false;
   std::vector<ProfRec> recs;
-  double tot_ms[PW_NPHASE] = {0, 0, 0, 0};
-  int64_t cnt[PW_NPHASE] = {0, 0, 0, 0};
+  double tot_ms[PW_NPHASE] = {};
+  int64_t cnt[PW_NPHASE] = {};
+  int chains = 2;                 // concurrent expert chains of a decode-sized GEMM call
 
   pw_layer(const pw_layer_desc& d, void* p, size_t bytes, pw_page_entry* t)
       : st(d, bytes, &evops), pool(static_cast<uint8_t*>(p)), table(t) {}
@@ -299,6 +300,32 @@ pw_status write_entries(pw_layer* L, const std::vector<std::pair<size_t, pw_page
   return PW_OK;
 }
 
+// The layer's own stream and its fork/join events, on the pool's device.
+hipError_t ensure_side(pw_layer* L) {
+  if (L->side) return hipSuccess;
+  {
+    // created on the pool's device (default priority, no implicit
+    // synchronization with the null stream: the fork/join events order it)
+    hipPointerAttribute_t attr{};
+    hipError_t e = hipPointerGetAttributes(&attr, L->pool);
+    int cur = -1;
+    if (e == hipSuccess) e = hipGetDevice(&cur);
+    if (e == hipSuccess && attr.device != cur) e = hipSetDevice(attr.device);
+    if (e == hipSuccess) e = hipStreamCreateWithFlags(&L->side, hipStreamNonBlocking);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&L->fork, hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&L->join, hipEventDisableTiming);
+    if (cur >= 0 && attr.device != cur) (void)hipSetDevice(cur);
+    if (e != hipSuccess) {
+      if (L->side) (void)hipStreamDestroy(L->side);
+      if (L->fork) (void)hipEventDestroy(L->fork);
+      if (L->join) (void)hipEventDestroy(L->join);
+      L->side = nullptr;
+      L->fork = L->join = nullptr;
+    }
+    return e;
+  }
+}
+
 }  // namespace
 
 extern "C" {
@@ -350,6 +377,11 @@ pw_status pw_layer_create(const pw_layer_desc* d, void* pool_dev, size_t pool_by
   if (e != hipSuccess) {
     delete L;
     return hip_fail(e, "clearing the page table");
+  }
+  e = ensure_side(L);
+  if (e != hipSuccess) {
+    delete L;
+    return hip_fail(e, "creating the layer's stream");
   }
   *out = L;
   return PW_OK;
@@ -513,30 +545,21 @@ pw_status pw_route_topk(const float* logits, int T, int E, int K, int renorm, in
                               stream);
 }
 
+
+pw_status pw_layer_set_chains(pw_layer* L, int chains) {
+  if (!L) return fail(PW_EINVAL, "null layer");
+  if (chains != 1 && chains != 2) return fail(PW_EINVAL, "chains must be 1 or 2");
+  L->chains = chains;
+  return PW_OK;
+}
+
 pw_status pw_layer_set_shared_experts(pw_layer* L, int n_shared) {
   if (!L) return fail(PW_EINVAL, "null layer");
   if (n_shared < 0 || n_shared >= L->st.desc.E)
     return fail(PW_EINVAL, "need 0 <= n_shared < E (at least one routed expert)");
-  if (n_shared > 0 && !L->side) {
-    // created on the pool's device (default priority, no implicit
-    // synchronization with the null stream: the fork/join events order it)
-    hipPointerAttribute_t attr{};
-    hipError_t e = hipPointerGetAttributes(&attr, L->pool);
-    int cur = -1;
-    if (e == hipSuccess) e = hipGetDevice(&cur);
-    if (e == hipSuccess && attr.device != cur) e = hipSetDevice(attr.device);
-    if (e == hipSuccess) e = hipStreamCreateWithFlags(&L->side, hipStreamNonBlocking);
-    if (e == hipSuccess) e = hipEventCreateWithFlags(&L->fork, hipEventDisableTiming);
-    if (e == hipSuccess) e = hipEventCreateWithFlags(&L->join, hipEventDisableTiming);
-    if (cur >= 0 && attr.device != cur) (void)hipSetDevice(cur);
-    if (e != hipSuccess) {
-      if (L->side) (void)hipStreamDestroy(L->side);
-      if (L->fork) (void)hipEventDestroy(L->fork);
-      if (L->join) (void)hipEventDestroy(L->join);
-      L->side = nullptr;
-      L->fork = L->join = nullptr;
-      return hip_fail(e, "creating the shared experts' stream");
-    }
+  if (n_shared > 0) {
+    const hipError_t e = ensure_side(L);
+    if (e != hipSuccess) return hip_fail(e, "creating the shared experts' stream");
   }
   L->n_shared = n_shared;
   return PW_OK;
@@ -644,17 +667,36 @@ pw_status pw_moe_paged_gemm(const pw_layer* Lc, const void* x, int T, int K, con
   a.n_shared = L->n_shared;
   hipStream_t st = static_cast<hipStream_t>(stream);
   hipError_t e = hipSuccess;
-  // routed experts, then shared experts: each range with its own kernels.
-  // With both present, the shared experts' GEMMs run on the layer's own
-  // stream, forked from `stream` and joined back before the combine: their
-  // few workgroups share the chip with the routed ones instead of running
-  // alone after them. (They write disjoint rows of h and of the partials.)
-  const bool fork = wl.r[0].ne > 0 && wl.r[1].ne > 0 && L->side;
-  if (fork) {
-    e = hipEventRecord(L->fork, st);
-    if (e == hipSuccess) e = hipStreamWaitEvent(L->side, L->fork, 0);
-    if (e != hipSuccess) return hip_fail(e, "forking the shared experts' stream");
+  // Routed experts, then shared experts: each range with its own kernels.
+  // Launch units: with shared experts, the shared range runs on the layer's
+  // own stream beside the routed one (its few workgroups share the chip with
+  // the routed ones instead of running alone after them); without, a
+  // decode-sized routed range runs as two chains of gate/up then down over
+  // the two halves of its experts, the second on the layer's stream, so that
+  // the boundary between one chain's phases overlaps the other's GEMMs. The
+  // layer's stream is forked from `stream` and joined back before the
+  // combine. Units write disjoint rows of h and of the partials.
+  struct Unit {
+    RangePlan r;
+    hipStream_t s;
+  };
+  Unit units[2];
+  int nu = 0;
+  const bool shared_fork = L->chains == 2 && L->side && wl.r[0].ne > 0 && wl.r[1].ne > 0;
+  const bool split_routed =
+      L->chains == 2 && L->side && wl.r[1].ne <= 0 && wl.r[0].path == GemmPath::kDecode && wl.r[0].ne >= 2;
+  if (split_routed) {
+    units[0] = Unit{wl.r[0], st};
+    units[0].r.ne = wl.r[0].ne / 2;
+    units[1] = Unit{wl.r[0], L->side};
+    units[1].r.e0 = wl.r[0].e0 + units[0].r.ne;
+    units[1].r.ne = wl.r[0].ne - units[0].r.ne;
+    nu = 2;
+  } else {
+    for (int ri = 0; ri < 2; ++ri)
+      if (wl.r[ri].ne > 0) units[nu++] = Unit{wl.r[ri], shared_fork && ri == 1 ? L->side : st};
   }
+  const bool fork = shared_fork || split_routed;
   auto for_range = [&](const RangePlan& r) {
     a.e0 = r.e0;
     a.ne = r.ne;
@@ -664,29 +706,36 @@ pw_status pw_moe_paged_gemm(const pw_layer* Lc, const void* x, int T, int K, con
     a.mtb = r.mtb;
   };
   const char* what = nullptr;
-  for (int pass = 0; pass < 2 && e == hipSuccess; ++pass) {
-    const bool gateup = pass == 0;
-    for (int ri = 0; ri < 2 && e == hipSuccess; ++ri) {
-      const RangePlan& r = wl.r[ri];
-      if (r.ne <= 0) continue;
-      for_range(r);
-      hipStream_t rs = fork && ri == 1 ? L->side : st;
-      ProfScope ps(L, gateup ? PW_PH_GATEUP : PW_PH_DOWN, rs);
-      e = r.path == GemmPath::kTiled    ? pw::launch_tgemm(a, gateup, rs)
-          : r.path == GemmPath::kStream ? pw::launch_sgemm(a, gateup, rs)
-          : gateup                      ? pw::launch_gateup(a, rs)
-                                        : pw::launch_down(a, rs);
-      if (e != hipSuccess) what = gateup ? "gate/up launch" : "down launch";
+  {
+    ProfScope span(L, PW_PH_GEMM, st);
+    if (fork) {
+      e = hipEventRecord(L->fork, st);
+      if (e == hipSuccess) e = hipStreamWaitEvent(L->side, L->fork, 0);
+      if (e != hipSuccess) return hip_fail(e, "forking the layer's stream");
     }
-  }
-  if (fork) {
-    // joined even after a failed launch, so that `stream` never waits on a
-    // branch that was left open
-    hipError_t ej = hipEventRecord(L->join, L->side);
-    if (ej == hipSuccess) ej = hipStreamWaitEvent(st, L->join, 0);
-    if (e == hipSuccess && ej != hipSuccess) {
-      e = ej;
-      what = "joining the shared experts' stream";
+    for (int pass = 0; pass < 2 && e == hipSuccess; ++pass) {
+      const bool gateup = pass == 0;
+      for (int ui = 0; ui < nu && e == hipSuccess; ++ui) {
+        const RangePlan& r = units[ui].r;
+        for_range(r);
+        hipStream_t rs = units[ui].s;
+        ProfScope ps(L, gateup ? PW_PH_GATEUP : PW_PH_DOWN, rs);
+        e = r.path == GemmPath::kTiled    ? pw::launch_tgemm(a, gateup, rs)
+            : r.path == GemmPath::kStream ? pw::launch_sgemm(a, gateup, rs)
+            : gateup                      ? pw::launch_gateup(a, rs)
+                                          : pw::launch_down(a, rs);
+        if (e != hipSuccess) what = gateup ? "gate/up launch" : "down launch";
+      }
+    }
+    if (fork) {
+      // joined even after a failed launch, so that `stream` never waits on a
+      // branch that was left open
+      hipError_t ej = hipEventRecord(L->join, L->side);
+      if (ej == hipSuccess) ej = hipStreamWaitEvent(st, L->join, 0);
+      if (e == hipSuccess && ej != hipSuccess) {
+        e = ej;
+        what = "joining the layer's stream";
+      }
     }
   }
   if (e != hipSuccess) return hip_fail(e, what);

@@ -119,6 +119,10 @@ class PagedLayer:
         pw.pw_layer_set_shared_experts(self.handle, n_shared)
         self.n_shared = n_shared
 
+    def set_chains(self, chains: int):
+        """1 or 2 concurrent expert chains for decode-sized GEMM calls."""
+        pw.pw_layer_set_chains(self.handle, chains)
+
     def route_shared(self, logits: torch.Tensor, K: int, n_shared: int, gate: torch.Tensor = None,
                      renorm: int = 1, stream=None, out=None):
         """Routed top-K over logits [T, E_routed] plus n_shared shared columns

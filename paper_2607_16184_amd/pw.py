@@ -24,7 +24,7 @@ PW_OK, PW_EINVAL, PW_ENOMEM, PW_EBUSY, PW_EUNSUPPORTED, PW_EHIP, PW_ESTATE = ran
 PW_F16, PW_BF16 = 0, 1
 PW_GATE, PW_UP, PW_DOWN = 0, 1, 2
 PW_PAGE_ABSENT, PW_PAGE_RESIDENT, PW_PAGE_REQUANT_PENDING, PW_PAGE_RELOAD_PENDING = 0, 1, 2, 3
-PW_PH_GATEUP, PW_PH_DOWN, PW_PH_COMBINE, PW_PH_REQUANT, PW_NPHASE = 0, 1, 2, 3, 4
+PW_PH_GATEUP, PW_PH_DOWN, PW_PH_COMBINE, PW_PH_REQUANT, PW_PH_GEMM, PW_NPHASE = 0, 1, 2, 3, 4, 5
 
 
 class pw_page_entry(ctypes.Structure):
@@ -93,6 +93,7 @@ def _load():
         "pw_workspace_bytes": (i32, [vp, i32, i32, P(sz)]),
         "pw_moe_paged_gemm": (i32, [vp, vp, i32, i32, vp, vp, vp, vp, vp, i32, vp, sz, vp]),
         "pw_layer_set_shared_experts": (i32, [vp, i32]),
+        "pw_layer_set_chains": (i32, [vp, i32]),
         "pw_route_topk_shared": (i32, [vp, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp]),
         "pw_moe_paged_gemm_noalloc": (i32, [vp, vp, i32, i32, vp, vp, vp, vp, vp, i32, vp]),
         "pw_requant_block": (i32, [vp, i32, i32, i32, i32, vp, P(sz)]),
@@ -210,6 +211,10 @@ def pw_moe_paged_gemm(layer: int, x_ptr: int, T: int, K: int, w_ptr: int, offset
 
 def pw_layer_set_shared_experts(layer: int, n_shared: int):
     _check(_lib.pw_layer_set_shared_experts(layer, n_shared))
+
+
+def pw_layer_set_chains(layer: int, chains: int):
+    _check(_lib.pw_layer_set_chains(layer, chains))
 
 
 def pw_route_topk_shared(logits_ptr: int, T: int, E: int, K: int, renorm: int, n_shared: int, gate_ptr: int,

@@ -92,3 +92,22 @@ def test_graph_replay_shared_experts(T):
         torch.cuda.synchronize()
         assert torch.equal(other, want), r
     L.close()
+
+
+@pytest.mark.parametrize("T", [16, 40, 100])
+def test_chains_bit_identical(T):
+    """The routed experts as one chain or as two concurrent chains (the
+    second on the layer's stream) give the same bits, 16-bit and fp32 out."""
+    import torch
+    cfg, w16, bits, order = case("tiny", T=T)
+    say("one chain vs two chains, tiny T=%d" % T)
+    L = gpu_layer(cfg, w16, bits, order)
+    logits, x = to_dev(synth.logits(cfg)), to_dev16(synth.activations(cfg))
+    routing = L.route(logits, cfg.K)
+    out = {}
+    for chains in (1, 2):
+        L.set_chains(chains)
+        out[chains] = (L.forward(x, routing).clone(), L.forward(x, routing, out_fp32=True).clone())
+    torch.cuda.synchronize()
+    assert torch.equal(out[1][0], out[2][0]) and torch.equal(out[1][1], out[2][1])
+    L.close()
