@@ -81,9 +81,12 @@ def build_layer(cfg, w16=None, bits=None):
 
 
 def time_steps(L, cfg, x, logits, steps, warmup):
-    """Warm up; time `steps` eager steps with per-kernel HIP-event profiling;
-    then capture one step (route + paged GEMMs + combine) in a HIP graph and
-    time exactly `steps` replays of it, which is the step time reported. Every
+    """Warm up; time `steps` eager steps with per-kernel HIP-event profiling,
+    with the routed experts in one chain (each GEMM launch alone: the
+    per-kernel durations), then `steps` eager steps with the layers' default
+    two chains; then capture one step (route + paged GEMMs + combine) in a
+    HIP graph and time exactly `steps` replays of it, which is the step time
+    reported (and the same with one chain, for comparison). Every
     replay's output is checked bit-exact against the eager step. L may be a
     list of layers holding the same pages in separate pools: step i then runs
     on layer i mod len(L), so that no step finds another's weights in a cache."""
@@ -113,34 +116,54 @@ def time_steps(L, cfg, x, logits, steps, warmup):
         step(i)
     torch.cuda.synchronize()
     y_eager = y.clone()
-    for Li in Ls:
-        pw.pw_profile_read(Li.handle, reset=True)
-        pw.pw_profile_enable(Li.handle, True)
-    ev0 = torch.cuda.Event(enable_timing=True)
-    ev1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    ev0.record()
-    for i in range(steps):
-        step(i)
-    ev1.record()
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    ms, cnt = [0.0] * 4, [0] * 4
-    for Li in Ls:
-        pw.pw_profile_enable(Li.handle, False)
-        m, c = pw.pw_profile_read(Li.handle, reset=True)
-        for k in range(4):
-            ms[k] += m[k]
-            cnt[k] += c[k]
+
+    def profiled(chains):
+        """`steps` eager steps with the layers' launch profiling on; per-phase
+        milliseconds and counts summed over the layers, wall and event ms."""
+        for Li in Ls:
+            pw.pw_layer_set_chains(Li.handle, chains)
+            pw.pw_profile_read(Li.handle, reset=True)
+            pw.pw_profile_enable(Li.handle, True)
+        ev0 = torch.cuda.Event(enable_timing=True)
+        ev1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        ev0.record()
+        for i in range(steps):
+            step(i)
+        ev1.record()
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        ms, cnt = [0.0] * pw.PW_NPHASE, [0] * pw.PW_NPHASE
+        for Li in Ls:
+            pw.pw_profile_enable(Li.handle, False)
+            m, c = pw.pw_profile_read(Li.handle, reset=True)
+            for k in range(pw.PW_NPHASE):
+                ms[k] += m[k]
+                cnt[k] += c[k]
+        if not torch.equal(y, y_eager):
+            raise RuntimeError("the %d-chain step differs from the first eager step" % chains)
+        return ms, cnt, (t1 - t0) * 1e3 / steps, ev0.elapsed_time(ev1) / steps
+
+    # per-kernel durations with the experts in one chain (each GEMM launch
+    # alone on the GPU); then the eager step with the layers' default two
+    # chains
+    ms1, cnt1, _, _ = profiled(1)
+    _, _, wall_ms, eager_ms = profiled(2)
     # per step (a layer with shared experts launches each GEMM phase twice)
-    per_kernel = {name: (ms[i] / steps if cnt[i] else None)
+    per_kernel = {name: (ms1[i] / steps if cnt1[i] else None)
                   for i, name in enumerate(("gateup", "down", "combine", "requant"))}
     counts = (rbuf[2][1:] - rbuf[2][:-1]).cpu().numpy()
-    out = {"wall_ms": (t1 - t0) * 1e3 / steps, "eager_ms": ev0.elapsed_time(ev1) / steps,
+    out = {"wall_ms": wall_ms, "eager_ms": eager_ms,
            "kernel_ms": per_kernel, "counts": counts, "graph": False, "layers": len(Ls)}
     out["event_ms"] = out["eager_ms"]
-    try:
+
+    def graph_steps(chains):
+        """Capture one step per layer with `chains` expert chains, check
+        replays bit-exact, time exactly `steps` replays: (ms per step, the
+        per-step p10/p50/p90)."""
+        for Li in Ls:
+            pw.pw_layer_set_chains(Li.handle, chains)
         graphs = []
         side = torch.cuda.Stream()
         for i in range(len(Ls)):
@@ -159,6 +182,10 @@ def time_steps(L, cfg, x, logits, steps, warmup):
             torch.cuda.synchronize()
             if not torch.equal(y, y_eager):
                 raise RuntimeError("graph replay differs from the eager step")
+        # an untimed run of `steps` back-to-back replays first: the first such
+        # run of a process measures a few per cent slow
+        for i in range(steps):
+            graphs[i % len(graphs)].replay()
         torch.cuda.synchronize()
         evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
         evs[0].record()
@@ -168,12 +195,20 @@ def time_steps(L, cfg, x, logits, steps, warmup):
         torch.cuda.synchronize()
         if not torch.equal(y, y_eager):
             raise RuntimeError("graph replay differs from the eager step")
-        out["event_ms"] = evs[0].elapsed_time(evs[-1]) / steps
         per = sorted(evs[i].elapsed_time(evs[i + 1]) for i in range(steps))
-        out["step_ms_p10_p50_p90"] = [round(float(np.percentile(per, q)), 4) for q in (10, 50, 90)]
+        return evs[0].elapsed_time(evs[-1]) / steps, [round(float(np.percentile(per, q)), 4) for q in (10, 50, 90)]
+
+    try:
+        # the step as reported (the layers' default two chains), then the
+        # same step with one chain, for comparison
+        out["event_ms"], out["step_ms_p10_p50_p90"] = graph_steps(2)
+        out["event_ms_one_chain"], _ = graph_steps(1)
         out["graph"] = True
     except Exception as exc:                          # report eager timing instead
         log("graph timing unavailable (%s); reporting eager steps" % exc)
+    finally:
+        for Li in Ls:
+            pw.pw_layer_set_chains(Li.handle, 2)
     return out
 
 
@@ -349,6 +384,7 @@ def leg_layer(name, steps, warmup, pools=1):
             "weight_GBps_per_step": round(wb / (r["event_ms"] * 1e-3) / 1e9, 1),
             "gateup_ms": round(km["gateup"], 4), "down_ms": round(km["down"], 4),
             "combine_ms": round(km["combine"], 4),
+            "ms_per_step_one_chain": round(r["event_ms_one_chain"], 4) if r.get("event_ms_one_chain") else None,
             "mfma_frac_gemm": round(flops / (gemm_ms * 1e-3) / MFMA_PEAK_BF16, 4),
             "mfma_frac_step": round(flops / (r["event_ms"] * 1e-3) / MFMA_PEAK_BF16, 4),
             "tflops_gemm": round(flops / (gemm_ms * 1e-3) / 1e12, 1)}
@@ -898,12 +934,18 @@ def main():
                      "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": traffic_for("gateup", cfg.name, gu_bytes),
                      "kernel": "k_gateup (paged gate/up GEMM + SwiGLU)",
-                     "algorithmic_bytes_per_launch": int(gu_bytes), "avg_launch_ms": round(gu_ms, 4)},
+                     "algorithmic_bytes_per_launch": int(gu_bytes), "avg_launch_ms": round(gu_ms, 4),
+                     "launched": "alone: one launch over all routed experts per step, in eager profiled "
+                                 "steps (the timed graph step runs the experts as two concurrent chains "
+                                 "of gate/up then down)"},
         "kernels": {
             "gateup_ms": round(gu_ms, 4), "down_ms": round(dn_ms, 4),
             "combine_ms": round(r["kernel_ms"]["combine"], 4),
             "down_GBps": round(dn_bytes / (dn_ms * 1e-3) / 1e9, 1),
             "gemm_weight_GBps": round((per[0] + per[1] + per[2]) / ((gu_ms + dn_ms) * 1e-3) / 1e9, 1),
+            "kernel_timing": "gateup_ms, down_ms, combine_ms: HIP events around each launch, launched "
+                             "alone (the routed experts in one chain), eager profiled steps",
+            "step_ms_one_chain": round(r["event_ms_one_chain"], 4) if r.get("event_ms_one_chain") else None,
             "mfma_frac": round(flops / ((gu_ms + dn_ms) * 1e-3) / MFMA_PEAK_BF16, 5),
             "wall_ms_per_step_eager": round(r["wall_ms"], 4),
             "eager_ms_per_step": round(r["eager_ms"], 4),
