@@ -226,6 +226,11 @@ pw_status pw_workspace_bytes(const pw_layer* layer, int T, int K, size_t* gemm_w
  * Requires every page of the layer to be present (PW_ESTATE otherwise).
  * Sizes: T*K < 2^31, and T*K*max(F, H)*2 < 2^32 (32-bit row offsets in the
  * kernels; PW_EUNSUPPORTED otherwise: split the batch).
+ * Streams: the work is ordered after what `stream` already holds and y is
+ * complete when `stream` passes the call; part of it may run on the layer's
+ * own stream in between (pw_layer_set_chains), forked from and joined back
+ * into `stream`, so the caller orders nothing else. The workspace is in use
+ * until `stream` passes the call.
  * Deterministic: no floating-point atomics; a fixed summation order.      */
 pw_status pw_moe_paged_gemm(const pw_layer* layer, const void* x, int T, int K,
                             const float* topk_w, const int32_t* offsets,
