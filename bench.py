@@ -187,16 +187,26 @@ def time_steps(L, cfg, x, logits, steps, warmup):
         for i in range(steps):
             graphs[i % len(graphs)].replay()
         torch.cuda.synchronize()
+        # the timed run: events before the first and after the last replay only
+        # (an event after every replay costs about 1.5 % per step)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for i in range(steps):
+            graphs[i % len(graphs)].replay()
+        e1.record()
+        torch.cuda.synchronize()
+        if not torch.equal(y, y_eager):
+            raise RuntimeError("graph replay differs from the eager step")
+        ms = e0.elapsed_time(e1) / steps
+        # then as many replays with an event after each, for the spread
         evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
         evs[0].record()
         for i in range(steps):
             graphs[i % len(graphs)].replay()
             evs[i + 1].record()
         torch.cuda.synchronize()
-        if not torch.equal(y, y_eager):
-            raise RuntimeError("graph replay differs from the eager step")
         per = sorted(evs[i].elapsed_time(evs[i + 1]) for i in range(steps))
-        return evs[0].elapsed_time(evs[-1]) / steps, [round(float(np.percentile(per, q)), 4) for q in (10, 50, 90)]
+        return ms, [round(float(np.percentile(per, q)), 4) for q in (10, 50, 90)]
 
     try:
         # the step as reported (the layers' default two chains), then the
