@@ -18,6 +18,46 @@ namespace {
 constexpr int kMaxTopK = 16;
 constexpr int kRouteLogitsPerLane = 4;            // E <= 256
 
+// Selection key of logit v of expert e: larger key = earlier in (value
+// descending, expert ascending) order. The float's bits are mapped to an
+// order-preserving unsigned value (-0 taken as +0, so the two tie like equal
+// values), the expert index complemented below them; 0 is below every key.
+__device__ __forceinline__ uint64_t route_key(float v, int e) {
+  uint32_t u = __float_as_uint(v);
+  if (u == 0x80000000u) u = 0u;
+  u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return (static_cast<uint64_t>(u) << 32) | (0xFFFFFFFFu - static_cast<uint32_t>(e));
+}
+
+template <int CTRL>
+__device__ __forceinline__ uint64_t dpp_u64(uint64_t x) {
+  const uint32_t lo = static_cast<uint32_t>(
+      __builtin_amdgcn_update_dpp(0, static_cast<int>(static_cast<uint32_t>(x)), CTRL, 0xF, 0xF, false));
+  const uint32_t hi = static_cast<uint32_t>(
+      __builtin_amdgcn_update_dpp(0, static_cast<int>(static_cast<uint32_t>(x >> 32)), CTRL, 0xF, 0xF, false));
+  return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
+__device__ __forceinline__ uint64_t max_u64(uint64_t a, uint64_t b) { return a > b ? a : b; }
+
+// Largest key of the wave, the same in every lane: within each row of 16
+// lanes by DPP exchanges (pairs, quads, half-row and row mirrors), then over
+// the four rows' results read out as wave-uniform values.
+__device__ __forceinline__ uint64_t wave_max_key(uint64_t k) {
+  k = max_u64(k, dpp_u64<0xB1>(k));    // quad_perm 1,0,3,2
+  k = max_u64(k, dpp_u64<0x4E>(k));    // quad_perm 2,3,0,1
+  k = max_u64(k, dpp_u64<0x141>(k));   // row_half_mirror
+  k = max_u64(k, dpp_u64<0x140>(k));   // row_mirror
+  uint64_t best = 0;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const uint32_t lo = __builtin_amdgcn_readlane(static_cast<uint32_t>(k), 16 * r);
+    const uint32_t hi = __builtin_amdgcn_readlane(static_cast<uint32_t>(k >> 32), 16 * r);
+    best = max_u64(best, (static_cast<uint64_t>(hi) << 32) | lo);
+  }
+  return best;
+}
+
 // One wave per token: lane l holds logits l, l + 64, ...; K rounds of a
 // wave-wide arg-max in (value descending, index ascending) order take the
 // next expert each. The weights use the same fp32 arithmetic as a serial
@@ -31,43 +71,28 @@ __device__ __forceinline__ void route_token(const float* __restrict__ logits, in
                                             int32_t* __restrict__ ids, float* __restrict__ w, int* lds_ids) {
   const int lane = lane_id();
   const float* l = logits + static_cast<size_t>(t) * E;
-  float v[kRouteLogitsPerLane];
-  bool live[kRouteLogitsPerLane];
+  uint64_t key[kRouteLogitsPerLane];
 #pragma unroll
   for (int q = 0; q < kRouteLogitsPerLane; ++q) {
     const int e = lane + 64 * q;
-    live[q] = e < E;
-    v[q] = live[q] ? l[e] : 0.0f;
+    key[q] = e < E ? route_key(l[e], e) : 0ull;
   }
   float sv[kMaxTopK];
   int se[kMaxTopK];
 #pragma unroll
   for (int k = 0; k < kMaxTopK; ++k) {
     if (k < K) {
-      float bv = 0.0f;
-      int be = 0x7fffffff;
+      uint64_t mine = key[0];
 #pragma unroll
-      for (int q = 0; q < kRouteLogitsPerLane; ++q) {
-        const int e = lane + 64 * q;
-        if (live[q] && (be == 0x7fffffff || v[q] > bv || (v[q] == bv && e < be))) {
-          bv = v[q];
-          be = e;
-        }
-      }
-#pragma unroll
-      for (int off = 32; off >= 1; off >>= 1) {
-        const float ov = __shfl_xor(bv, off);
-        const int oe = __shfl_xor(be, off);
-        if (oe != 0x7fffffff && (be == 0x7fffffff || ov > bv || (ov == bv && oe < be))) {
-          bv = ov;
-          be = oe;
-        }
-      }
-      sv[k] = bv;
+      for (int q = 1; q < kRouteLogitsPerLane; ++q) mine = max_u64(mine, key[q]);
+      const uint64_t best = wave_max_key(mine);
+      const int be = static_cast<int>(0xFFFFFFFFu - static_cast<uint32_t>(best));
+      const uint32_t u = static_cast<uint32_t>(best >> 32);
       se[k] = be;
+      sv[k] = __uint_as_float((u & 0x80000000u) ? (u & 0x7FFFFFFFu) : ~u);   // the logit (-0 read as +0)
 #pragma unroll
       for (int q = 0; q < kRouteLogitsPerLane; ++q)
-        if (lane + 64 * q == be) live[q] = false;
+        if (lane + 64 * q == be) key[q] = 0ull;
     }
   }
   if (lane != 0) return;

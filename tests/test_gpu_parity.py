@@ -62,6 +62,15 @@ def test_route_edge_cases():
     _route_check(np.zeros((5, 16), np.float32), 3)
     _route_check(rng.standard_normal((1, 64)).astype(np.float32), 6)
     _route_check(rng.standard_normal((3000, 256)).astype(np.float32), 16)   # several permute chunks
+    # one wave per token (more than 32 experts): ties, +0 and -0 (equal
+    # values: the lower index first), all-negative rows
+    lg = -np.abs(rng.standard_normal((200, 64))).astype(np.float32) - 1.0
+    lg[:50, 10:20] = 0.5
+    lg[50:100, 7] = -0.0
+    lg[50:100, 3] = 0.0
+    lg[50:100, 40] = -0.0
+    _route_check(lg, 6)
+    _route_check(lg, 6, renorm=0)
 
 
 def _check_pages(L, O, pages):
