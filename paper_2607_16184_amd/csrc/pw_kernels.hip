@@ -174,9 +174,17 @@ __global__ __launch_bounds__(kPermThreads) void k_permute(const int32_t* __restr
   const int e = blockIdx.x, tid = threadIdx.x, wave = tid >> 6, lane = lane_id();
   for (int i = tid; i < E; i += kPermThreads) cnt[i] = 0;
   __syncthreads();
-  for (int s = tid; s < S; s += kPermThreads) {
-    const int id = ids[s];
-    if (id >= 0 && id < E) atomicAdd(&cnt[id], 1);
+  // eight ids per thread in flight before their counts are added
+  for (int s0 = tid; s0 < S; s0 += 8 * kPermThreads) {
+    int id[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int s = s0 + j * kPermThreads;
+      id[j] = s < S ? ids[s] : -1;
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      if (id[j] >= 0 && id[j] < E) atomicAdd(&cnt[id[j]], 1);
   }
   const int per = ((S + 3) / 4 + 63) / 64 * 64;
   const int q0 = min(S, wave * per), q1 = min(S, q0 + per);
