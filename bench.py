@@ -182,9 +182,10 @@ def time_steps(L, cfg, x, logits, steps, warmup):
             torch.cuda.synchronize()
             if not torch.equal(y, y_eager):
                 raise RuntimeError("graph replay differs from the eager step")
-        # an untimed run of `steps` back-to-back replays first: the first such
-        # run of a process measures a few per cent slow
-        for i in range(steps):
+        # an untimed run of back-to-back replays first, at least `steps` of
+        # them and about 50 ms (by the eager step time): the first such run
+        # of a process measures a few per cent slow
+        for i in range(max(steps, int(50.0 / max(eager_ms, 1e-3)) + 1)):
             graphs[i % len(graphs)].replay()
         torch.cuda.synchronize()
         # the timed run: events before the first and after the last replay only
