@@ -287,7 +287,7 @@ __device__ __forceinline__ void lds_sync() {
 template <int ACT, int SDT, int B>
 __device__ __forceinline__ void tile_loop(uint8_t* lds, const uint8_t* tile0, const uint8_t* szrow,
                                           const uint8_t* const (&xrow)[2], int nkb, int R, int G, int wave,
-                                          int wn, int wm, f32x16 (&acc)[4][2]) {
+                                          int wn, int wm, bool live, f32x16 (&acc)[4][2]) {
 #pragma unroll
   for (int r = 0; r < 4; ++r)
 #pragma unroll
@@ -307,12 +307,12 @@ __device__ __forceinline__ void tile_loop(uint8_t* lds, const uint8_t* tile0, co
     x_fetch(xs, xrow, kTK);
   }
   lds_sync();
-  ops_read(op, lds, wn, wm, 0);
+  if (live) ops_read(op, lds, wn, wm, 0);
   if (wn == 1) lds_sync();
   for (int st = 0; st < nstage; ++st) {
     const uint8_t* cur = lds + (st & 1) * kSB;
     uint8_t* nxt = lds + ((st + 1) & 1) * kSB;
-    ops_mma<ACT>(op, acc);
+    if (live) ops_mma<ACT>(op, acc);
     lds_sync();
     if (st + 1 < nstage) {
       stage_store<ACT, SDT, B>(ws, xs, nxt, wave);
@@ -322,11 +322,11 @@ __device__ __forceinline__ void tile_loop(uint8_t* lds, const uint8_t* tile0, co
         x_fetch(xs, xrow, s2 * kTK);
       }
     }
-    ops_read(op, cur, wn, wm, 1);
+    if (live) ops_read(op, cur, wn, wm, 1);
     lds_sync();
-    ops_mma<ACT>(op, acc);
+    if (live) ops_mma<ACT>(op, acc);
     lds_sync();
-    if (st + 1 < nstage) ops_read(op, nxt, wn, wm, 0);
+    if (live && st + 1 < nstage) ops_read(op, nxt, wn, wm, 0);
     lds_sync();
   }
   if (wn == 0) lds_sync();
@@ -429,9 +429,13 @@ __global__ __launch_bounds__(kThreads) void k_tgemm(const GemmArgs a, int nblk, 
   // gate/up kernel would not, and keeps the VGPR form.
   if constexpr (!GATEUP) asm volatile("" ::: "a0");
   const int nkb = K / 128;
-  if (bits == 16) tile_loop<ACT, SDT, 16>(lds, tile0, szrow, xrow, nkb, R, a.G, wave, wn, wm, acc);
-  else if (bits == 8) tile_loop<ACT, SDT, 8>(lds, tile0, szrow, xrow, nkb, R, a.G, wave, wn, wm, acc);
-  else tile_loop<ACT, SDT, 4>(lds, tile0, szrow, xrow, nkb, R, a.G, wave, wn, wm, acc);
+  // In an expert's ragged last tile, waves whose 64 slots all lie past the
+  // expert's slots still stage their share and pass every barrier, but read
+  // no operands and issue no MFMAs (their LDS bandwidth goes to the others).
+  const bool live = m0 + wm * 64 < n_e;
+  if (bits == 16) tile_loop<ACT, SDT, 16>(lds, tile0, szrow, xrow, nkb, R, a.G, wave, wn, wm, live, acc);
+  else if (bits == 8) tile_loop<ACT, SDT, 8>(lds, tile0, szrow, xrow, nkb, R, a.G, wave, wn, wm, live, acc);
+  else tile_loop<ACT, SDT, 4>(lds, tile0, szrow, xrow, nkb, R, a.G, wave, wn, wm, live, acc);
 
   // Accumulator element 4 q + r of tile (rt, ct) is row 32 rt + 8 q + 4 (lane / 32)
   // + r of the wave's 128 rows, slot 32 ct + lane mod 32 of its 64 slots.
