@@ -872,7 +872,7 @@ __global__ void k_clear_table(pw_page_entry* table, size_t n) {
 // ---------------------------------------------------------------------------
 
 // A thread holds four outputs of token t. Columns are taken C at a time (C
-// of 2, 4, 8: the column count rounded up, at most 16 / NSP; NSP: the largest
+// of 2, 4, 6, 8: the column count rounded up, at most 16 / NSP; NSP: the largest
 // split count rounded up to 1, 2, 4 or 8): the partial rows of every split
 // of those columns are all loaded before any is summed, so up to 16 loads of
 // a thread are in flight together; the sums keep the order (splits ascending
@@ -1558,14 +1558,16 @@ hipError_t launch_combine(const GemmArgs& a, hipStream_t st) {
   const int nmax = a.n_shared > 0 && a.nsplit_sh > a.nsplit ? a.nsplit_sh : a.nsplit;
   if (nmax < 1 || nmax > 8) return hipErrorInvalidValue;
   const int nsp = nmax == 1 ? 1 : nmax == 2 ? 2 : nmax <= 4 ? 4 : 8;
-  const int cols = std::min(a.topk <= 2 ? 2 : a.topk <= 4 ? 4 : 8, 16 / nsp);
+  const int cols = std::min(a.topk <= 2 ? 2 : a.topk <= 4 ? 4 : a.topk <= 6 ? 6 : 8, 16 / nsp);
   const dim3 grid(a.T, (a.H / 4 + 255) / 256), block(256);
   switch (nsp * 16 + cols) {
     case 16 + 2: hipLaunchKernelGGL((k_combine<1, 2>), grid, block, 0, st, a); break;
     case 16 + 4: hipLaunchKernelGGL((k_combine<1, 4>), grid, block, 0, st, a); break;
+    case 16 + 6: hipLaunchKernelGGL((k_combine<1, 6>), grid, block, 0, st, a); break;
     case 16 + 8: hipLaunchKernelGGL((k_combine<1, 8>), grid, block, 0, st, a); break;
     case 32 + 2: hipLaunchKernelGGL((k_combine<2, 2>), grid, block, 0, st, a); break;
     case 32 + 4: hipLaunchKernelGGL((k_combine<2, 4>), grid, block, 0, st, a); break;
+    case 32 + 6: hipLaunchKernelGGL((k_combine<2, 6>), grid, block, 0, st, a); break;
     case 32 + 8: hipLaunchKernelGGL((k_combine<2, 8>), grid, block, 0, st, a); break;
     case 64 + 2: hipLaunchKernelGGL((k_combine<4, 2>), grid, block, 0, st, a); break;
     case 64 + 4: hipLaunchKernelGGL((k_combine<4, 4>), grid, block, 0, st, a); break;
