@@ -184,8 +184,9 @@ pw_status pw_route_topk(const float* logits, int T, int E, int K, int renorm,
  * them. Takes effect for the next GEMM call.                               */
 pw_status pw_layer_set_shared_experts(pw_layer* layer, int n_shared);
 
-/* Concurrent expert chains (Sec. 3.3: the MoE forward as a GPU-side
- * pipeline; here the boundary between its gate/up and down phases). With
+/* Concurrent expert chains (Sec. 3.3 runs the MoE forward as one fused
+ * kernel; here its gate/up and down phases are separate launches, and this
+ * setting overlaps the boundary between them). With
  * chains = 2 (the default), when a call's experts run on the decode kernels
  * and the layer has no shared experts, they are split into two halves, each
  * a chain of gate/up then down: the first on the caller's stream, the
