@@ -110,4 +110,9 @@ def test_chains_bit_identical(T):
         out[chains] = (L.forward(x, routing).clone(), L.forward(x, routing, out_fp32=True).clone())
     torch.cuda.synchronize()
     assert torch.equal(out[1][0], out[2][0]) and torch.equal(out[1][1], out[2][1])
+    from paper_2607_16184_amd import pw
+    for bad in (0, 3):
+        with pytest.raises(pw.PWError) as ei:
+            L.set_chains(bad)
+        assert ei.value.status == pw.PW_EINVAL
     L.close()
