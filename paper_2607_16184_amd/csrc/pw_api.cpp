@@ -169,6 +169,14 @@ RangePlan plan_range(const pw_layer_desc& d, int e0, int ne, size_t S, size_t S_
     const size_t units = active * (d.H / 128);
     nsplit = static_cast<int>(std::max<size_t>(1, std::min<size_t>(8, 1024 / std::max<size_t>(units, 1))));
   }
+  // and the tiled kernel in two when its down tiles (256 rows x 256 slots,
+  // one workgroup per CU) would run fewer than three rounds on the chip (the
+  // last, partly filled round then weighs less; three or four splits add
+  // more partial-sum traffic than they save)
+  if (r.path == GemmPath::kTiled) {
+    const size_t tiles = (S / 256 + static_cast<size_t>(ne)) * (d.H / 256);
+    nsplit = tiles < 3 * kCUs ? 2 : 1;
+  }
   nsplit = std::min(nsplit, nkbF);
   // a split holds whole quantization groups (G = 256, 512 span 2, 4 blocks)
   const int bpg = d.G > 128 ? d.G / 128 : 1;

@@ -286,25 +286,28 @@ __device__ __forceinline__ void lds_sync() {
 // after its last write.
 template <int ACT, int SDT, int B>
 __device__ __forceinline__ void tile_loop(uint8_t* lds, const uint8_t* tile0, const uint8_t* szrow,
-                                          const uint8_t* const (&xrow)[2], int nkb, int R, int G, int wave,
-                                          int wn, int wm, bool live, f32x16 (&acc)[4][2]) {
+                                          const uint8_t* const (&xrow)[2], int nkb, int kb0, int kb1, int R,
+                                          int G, int wave, int wn, int wm, bool live, f32x16 (&acc)[4][2]) {
 #pragma unroll
   for (int r = 0; r < 4; ++r)
 #pragma unroll
     for (int c = 0; c < 2; ++c)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[r][c][e] = 0.0f;
-  const int nstage = nkb * 128 / kTK;
+  // stages of 64 values over the 128-blocks [kb0, kb1); stage s of the row
+  // is s0 + st
+  const int nstage = (kb1 - kb0) * 128 / kTK;
+  const int s0 = kb0 * 128 / kTK;
   auto group_of = [&](int st) { return G == 64 ? st : (st * kTK) / G; };
   WStage<B> ws;
   XStage xs;
   Ops op;
-  w_fetch<B>(ws, tile0, szrow, 0, 0, group_of(0), nkb, R);
-  x_fetch(xs, xrow, 0);
+  w_fetch<B>(ws, tile0, szrow, s0 >> 1, s0 & 1, group_of(s0), nkb, R);
+  x_fetch(xs, xrow, s0 * kTK);
   stage_store<ACT, SDT, B>(ws, xs, lds, wave);
   if (nstage > 1) {
-    w_fetch<B>(ws, tile0, szrow, 0, 1, group_of(1), nkb, R);
-    x_fetch(xs, xrow, kTK);
+    w_fetch<B>(ws, tile0, szrow, (s0 + 1) >> 1, (s0 + 1) & 1, group_of(s0 + 1), nkb, R);
+    x_fetch(xs, xrow, (s0 + 1) * kTK);
   }
   lds_sync();
   if (live) ops_read(op, lds, wn, wm, 0);
@@ -317,7 +320,7 @@ __device__ __forceinline__ void tile_loop(uint8_t* lds, const uint8_t* tile0, co
     if (st + 1 < nstage) {
       stage_store<ACT, SDT, B>(ws, xs, nxt, wave);
       if (st + 2 < nstage) {
-        const int s2 = st + 2;
+        const int s2 = s0 + st + 2;
         w_fetch<B>(ws, tile0, szrow, s2 >> 1, s2 & 1, group_of(s2), nkb, R);
         x_fetch(xs, xrow, s2 * kTK);
       }
@@ -363,6 +366,7 @@ __global__ __launch_bounds__(kThreads) void k_tgemm(const GemmArgs a, int nblk, 
   const int band = logical / (kGN * mtmax), inb = logical % (kGN * mtmax);
   const int nb = band * kGN + inb % kGN, mt = inb / kGN;
   if (nb >= nblk) return;
+  if (!GATEUP && static_cast<int>(blockIdx.y) * a.kb_per_split >= a.F / 128) return;   // an empty K split
   int e, off_e, n_e, m0;
   if (!tile_expert(a, mt, &e, &off_e, &n_e, &m0)) return;
 
@@ -429,13 +433,17 @@ __global__ __launch_bounds__(kThreads) void k_tgemm(const GemmArgs a, int nblk, 
   // gate/up kernel would not, and keeps the VGPR form.
   if constexpr (!GATEUP) asm volatile("" ::: "a0");
   const int nkb = K / 128;
+  // the down projection may split K = F (grid y: the split; fp32 partials)
+  const int split = GATEUP ? 0 : static_cast<int>(blockIdx.y);
+  const int kb0 = GATEUP ? 0 : split * a.kb_per_split;
+  const int kb1 = GATEUP ? nkb : min(nkb, kb0 + a.kb_per_split);
   // In an expert's ragged last tile, waves whose 64 slots all lie past the
   // expert's slots still stage their share and pass every barrier, but read
   // no operands and issue no MFMAs (their LDS bandwidth goes to the others).
   const bool live = m0 + wm * 64 < n_e;
-  if (bits == 16) tile_loop<ACT, SDT, 16>(lds, tile0, szrow, xrow, nkb, R, a.G, wave, wn, wm, live, acc);
-  else if (bits == 8) tile_loop<ACT, SDT, 8>(lds, tile0, szrow, xrow, nkb, R, a.G, wave, wn, wm, live, acc);
-  else tile_loop<ACT, SDT, 4>(lds, tile0, szrow, xrow, nkb, R, a.G, wave, wn, wm, live, acc);
+  if (bits == 16) tile_loop<ACT, SDT, 16>(lds, tile0, szrow, xrow, nkb, kb0, kb1, R, a.G, wave, wn, wm, live, acc);
+  else if (bits == 8) tile_loop<ACT, SDT, 8>(lds, tile0, szrow, xrow, nkb, kb0, kb1, R, a.G, wave, wn, wm, live, acc);
+  else tile_loop<ACT, SDT, 4>(lds, tile0, szrow, xrow, nkb, kb0, kb1, R, a.G, wave, wn, wm, live, acc);
 
   // Accumulator element 4 q + r of tile (rt, ct) is row 32 rt + 8 q + 4 (lane / 32)
   // + r of the wave's 128 rows, slot 32 ct + lane mod 32 of its 64 slots.
@@ -486,7 +494,7 @@ __global__ __launch_bounds__(kThreads) void k_tgemm(const GemmArgs a, int nblk, 
         for (int rt = 0; rt < 4; ++rt)
 #pragma unroll
           for (int q = 0; q < 4; ++q)
-            *reinterpret_cast<f32x4*>(a.opart + static_cast<size_t>(off_e + m) * a.H + nb * 256 + wn * 128 +
+            *reinterpret_cast<f32x4*>(a.opart + (static_cast<size_t>(split) * a.S + off_e + m) * a.H + nb * 256 + wn * 128 +
                                       rt * 32 + q * 8 + rsub) =
                 f32x4{acc[rt][ct][4 * q], acc[rt][ct][4 * q + 1], acc[rt][ct][4 * q + 2], acc[rt][ct][4 * q + 3]};
       }
@@ -767,7 +775,7 @@ void tgemm_go(const GemmArgs& a, bool gateup, int n, int nblk, int mtmax, hipStr
   if (gateup)
     hipLaunchKernelGGL((k_tgemm<ACT, SDT, true>), dim3(n), dim3(kThreads), 0, st, a, nblk, mtmax);
   else
-    hipLaunchKernelGGL((k_tgemm<ACT, SDT, false>), dim3(n), dim3(kThreads), 0, st, a, nblk, mtmax);
+    hipLaunchKernelGGL((k_tgemm<ACT, SDT, false>), dim3(n, a.nsplit), dim3(kThreads), 0, st, a, nblk, mtmax);
 }
 
 }  // namespace
