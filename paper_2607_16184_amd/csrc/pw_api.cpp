@@ -308,30 +308,28 @@ pw_status write_entries(pw_layer* L, const std::vector<std::pair<size_t, pw_page
   return PW_OK;
 }
 
-// The layer's own stream and its fork/join events, on the pool's device.
+// The layer's own stream and its fork/join events, created on the pool's
+// device (default priority; no implicit synchronization with the null
+// stream: the fork/join events order it).
 hipError_t ensure_side(pw_layer* L) {
   if (L->side) return hipSuccess;
-  {
-    // created on the pool's device (default priority, no implicit
-    // synchronization with the null stream: the fork/join events order it)
-    hipPointerAttribute_t attr{};
-    hipError_t e = hipPointerGetAttributes(&attr, L->pool);
-    int cur = -1;
-    if (e == hipSuccess) e = hipGetDevice(&cur);
-    if (e == hipSuccess && attr.device != cur) e = hipSetDevice(attr.device);
-    if (e == hipSuccess) e = hipStreamCreateWithFlags(&L->side, hipStreamNonBlocking);
-    if (e == hipSuccess) e = hipEventCreateWithFlags(&L->fork, hipEventDisableTiming);
-    if (e == hipSuccess) e = hipEventCreateWithFlags(&L->join, hipEventDisableTiming);
-    if (cur >= 0 && attr.device != cur) (void)hipSetDevice(cur);
-    if (e != hipSuccess) {
-      if (L->side) (void)hipStreamDestroy(L->side);
-      if (L->fork) (void)hipEventDestroy(L->fork);
-      if (L->join) (void)hipEventDestroy(L->join);
-      L->side = nullptr;
-      L->fork = L->join = nullptr;
-    }
-    return e;
+  hipPointerAttribute_t attr{};
+  hipError_t e = hipPointerGetAttributes(&attr, L->pool);
+  int cur = -1;
+  if (e == hipSuccess) e = hipGetDevice(&cur);
+  if (e == hipSuccess && attr.device != cur) e = hipSetDevice(attr.device);
+  if (e == hipSuccess) e = hipStreamCreateWithFlags(&L->side, hipStreamNonBlocking);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&L->fork, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&L->join, hipEventDisableTiming);
+  if (cur >= 0 && attr.device != cur) (void)hipSetDevice(cur);
+  if (e != hipSuccess) {
+    if (L->side) (void)hipStreamDestroy(L->side);
+    if (L->fork) (void)hipEventDestroy(L->fork);
+    if (L->join) (void)hipEventDestroy(L->join);
+    L->side = nullptr;
+    L->fork = L->join = nullptr;
   }
+  return e;
 }
 
 }  // namespace
@@ -565,10 +563,6 @@ pw_status pw_layer_set_shared_experts(pw_layer* L, int n_shared) {
   if (!L) return fail(PW_EINVAL, "null layer");
   if (n_shared < 0 || n_shared >= L->st.desc.E)
     return fail(PW_EINVAL, "need 0 <= n_shared < E (at least one routed expert)");
-  if (n_shared > 0) {
-    const hipError_t e = ensure_side(L);
-    if (e != hipSuccess) return hip_fail(e, "creating the shared experts' stream");
-  }
   L->n_shared = n_shared;
   return PW_OK;
 }
