@@ -179,9 +179,9 @@ pw_status pw_route_topk(const float* logits, int T, int E, int K, int renorm,
  * before the combine, so that they run beside the routed ones (under graph
  * capture: two branches; with pw_layer_set_chains(layer, 1), on the
  * caller's stream after them). That stream (default priority) and its two
- * events live on the pool's device
- * (created with the layer by pw_layer_create); pw_layer_destroy releases
- * them. Takes effect for the next GEMM call.                               */
+ * events live on the pool's device (created with the layer by
+ * pw_layer_create; pw_layer_destroy releases them). No GPU work; takes
+ * effect for the next GEMM call.                                           */
 pw_status pw_layer_set_shared_experts(pw_layer* layer, int n_shared);
 
 /* Concurrent expert chains (Sec. 3.3 runs the MoE forward as one fused
