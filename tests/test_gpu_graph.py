@@ -116,3 +116,26 @@ def test_chains_bit_identical(T):
             L.set_chains(bad)
         assert ei.value.status == pw.PW_EINVAL
     L.close()
+
+
+@pytest.mark.parametrize("T,kw", [(16, {}), (100, {}), (600, dict(F=4096, n_shared=4, E=12))])
+def test_chains_bit_identical_shared(T, kw):
+    """With shared experts the shared range runs on the layer's stream beside
+    the routed one (two chains) or after it (one chain): same bits. T = 100
+    puts the shared range on the streaming kernel, T = 600 (4 shared experts
+    of F = 4096) on the tiled one."""
+    import torch
+    cfg, w16, bits, order = case("tiny_shared", T=T, **kw)
+    say("one chain vs two chains with shared experts, T=%d" % T)
+    L = gpu_layer(cfg, w16, bits, order)
+    L.set_shared_experts(cfg.n_shared)
+    logits, x = to_dev(synth.logits(cfg, T=T)), to_dev16(synth.activations(cfg, T=T))
+    gate = to_dev(synth.shared_gate(cfg, T=T))
+    routing = L.route_shared(logits, cfg.K, cfg.n_shared, gate=gate)
+    out = {}
+    for chains in (1, 2):
+        L.set_chains(chains)
+        out[chains] = (L.forward(x, routing).clone(), L.forward(x, routing, out_fp32=True).clone())
+    torch.cuda.synchronize()
+    assert torch.equal(out[1][0], out[2][0]) and torch.equal(out[1][1], out[2][1])
+    L.close()
