@@ -154,8 +154,10 @@ RangePlan plan_range(const pw_layer_desc& d, int e0, int ne, size_t S, size_t S_
   const int expect = static_cast<int>((S + ne - 1) / ne);
   r.path = pick_path(d, S, S_all, ne, apl, e0 > 0);
   // The decode kernels split the down projection's K = F when too few
-  // (expert, row-block) units exist to fill the chip; deterministic in
-  // (desc, T, K).
+  // (expert, 64-row block) units exist to fill the chip; deterministic in
+  // (desc, T, K). At four slot tiles a workgroup covers 256 rows, so fewer
+  // workgroups result, and that is kept: with that many slots per expert the
+  // fp32 partials of a split cost more than the fuller chip gains.
   int nsplit = 1;
   if (r.path == GemmPath::kDecode && S <= 4096) {
     const size_t active = std::min<size_t>(ne, S);
