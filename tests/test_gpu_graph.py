@@ -11,13 +11,15 @@ from paper_2607_16184_amd import synth
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("T", [16, 300, 1000])
-def test_graph_replay_matches_eager(T):
+@pytest.mark.parametrize("T,chains", [(16, 2), (16, 1), (300, 2), (1000, 2)])
+def test_graph_replay_matches_eager(T, chains):
+    """Captured with two chains (two graph branches at decode sizes) or one."""
     import torch
     from paper_2607_16184_amd.layer import PagedLayer
     cfg, w16, bits, order = case("tiny", T=T)
-    say("graph replay tiny T=%d" % T)
+    say("graph replay tiny T=%d chains=%d" % (T, chains))
     L = gpu_layer(cfg, w16, bits, order)
+    L.set_chains(chains)
     logits, x = to_dev(synth.logits(cfg)), to_dev16(synth.activations(cfg))
     rbuf = PagedLayer.routing_buffers(cfg.T, cfg.E, cfg.K)
     y = torch.empty((cfg.T, cfg.H), dtype=torch.float32, device="cuda")
