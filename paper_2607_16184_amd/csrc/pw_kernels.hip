@@ -62,7 +62,9 @@ __device__ __forceinline__ uint64_t wave_max_key(uint64_t k) {
 // wave-wide arg-max in (value descending, index ascending) order take the
 // next expert each. The weights use the same fp32 arithmetic as a serial
 // loop: m = the largest selected logit, a_k = exp(l_k - m), w_k = a_k / sum,
-// with the sum taken in k order (renorm) or in expert order over all E.
+// with the sum taken in k order (renorm) or in expert order over all E (each
+// lane computes the exponentials of its own logits, and the terms are added
+// one lane after another: the serial loop's operations in its order).
 // Rows of ids and w hold K + n_shared columns: the routed experts, then the
 // shared experts E + j with weight gate[t n_shared + j] (1 without a gate).
 // lds_ids (may be null): the token's row of ids also goes there.
@@ -72,10 +74,12 @@ __device__ __forceinline__ void route_token(const float* __restrict__ logits, in
   const int lane = lane_id();
   const float* l = logits + static_cast<size_t>(t) * E;
   uint64_t key[kRouteLogitsPerLane];
+  float lv[kRouteLogitsPerLane];
 #pragma unroll
   for (int q = 0; q < kRouteLogitsPerLane; ++q) {
     const int e = lane + 64 * q;
-    key[q] = e < E ? route_key(l[e], e) : 0ull;
+    lv[q] = e < E ? l[e] : 0.0f;
+    key[q] = e < E ? route_key(lv[q], e) : 0ull;
   }
   float sv[kMaxTopK];
   int se[kMaxTopK];
@@ -95,13 +99,22 @@ __device__ __forceinline__ void route_token(const float* __restrict__ logits, in
         if (lane + 64 * q == be) key[q] = 0ull;
     }
   }
-  if (lane != 0) return;
   const float m = sv[0];
   float sum = 0.0f;
   if (renorm) {
+    if (lane != 0) return;
     for (int k = 0; k < K; ++k) sum += expf(sv[k] - m);
   } else {
-    for (int e = 0; e < E; ++e) sum += expf(l[e] - m);
+    // terms past E are +0 and leave the (positive) sum unchanged
+#pragma unroll
+    for (int q = 0; q < kRouteLogitsPerLane; ++q) {
+      if (64 * q < E) {
+        const int ex = __float_as_int(lane + 64 * q < E ? expf(lv[q] - m) : 0.0f);
+#pragma unroll
+        for (int j = 0; j < 64; ++j) sum += __int_as_float(__builtin_amdgcn_readlane(ex, j));
+      }
+    }
+    if (lane != 0) return;
   }
   const int Kt = K + n_shared;
   const size_t row = static_cast<size_t>(t) * Kt;

@@ -71,6 +71,10 @@ def test_route_edge_cases():
     lg[50:100, 40] = -0.0
     _route_check(lg, 6)
     _route_check(lg, 6, renorm=0)
+    # unrenormalised weights on the one-wave-per-token path: a partly filled
+    # block of 64 lanes (E = 60) and four logits per lane (E = 256)
+    _route_check(rng.standard_normal((500, 60)).astype(np.float32), 4, renorm=0)
+    _route_check(rng.standard_normal((500, 256)).astype(np.float32), 8, renorm=0)
 
 
 def _check_pages(L, O, pages):
