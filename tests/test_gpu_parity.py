@@ -364,9 +364,11 @@ def test_tiny_group_sizes_and_scale_dtypes(act, sdt, G, H, F, T):
 
 
 # Edge shapes on the decode path: a single token, every expert selected
-# (K = E), unrenormalised routing weights, a 64-expert top-6 layer with few
-# tokens (most experts empty), and no tokens at all.
-@pytest.mark.parametrize("T,K,E,renorm", [(1, 2, 8, 1), (3, 8, 8, 1), (7, 2, 8, 0), (5, 6, 64, 1)])
+# (K = E), unrenormalised routing weights (through the fused router at 8
+# experts and the one-wave-per-token router at 64), a 64-expert top-6 layer
+# with few tokens (most experts empty), and no tokens at all.
+@pytest.mark.parametrize("T,K,E,renorm", [(1, 2, 8, 1), (3, 8, 8, 1), (7, 2, 8, 0), (5, 6, 64, 1),
+                                          (40, 6, 64, 0)])
 def test_tiny_edge_shapes(T, K, E, renorm):
     import torch
     cfg, w16, bits, order = case("tiny", T=T, K=K, E=E)
